@@ -1,0 +1,201 @@
+"""Plausible mistakes planted in the oracle (CPU only) to show that its pins
+catch them.  ``tests/conftest.py`` applies one of these when the environment
+variable ORACLE_MUTATION names it; ``test_oracle_mutations.py`` runs the pin
+suites under each and expects a failure."""
+
+import numpy as np
+
+import oracle.accept as oa
+import oracle.decode as od
+import oracle.model as om
+import oracle.verify as ov
+
+_MODULES = (om, ov, od, oa)
+
+
+def _patch(name, fn):
+    for mod in _MODULES:
+        if hasattr(mod, name):
+            setattr(mod, name, fn)
+
+
+def rope_sign():
+    def rope(x, pos, base):
+        dh = x.shape[-1]
+        half = dh // 2
+        ang = np.asarray(pos, dtype=np.float64)[..., None] * om.rope_inv_freq(dh, base)
+        c, s = np.cos(ang), np.sin(ang)
+        x1, x2 = x[..., :half], x[..., half:]
+        return np.concatenate([x1 * c + x2 * s, x2 * c - x1 * s], axis=-1)
+    _patch("rope", rope)
+
+
+def rope_interleaved():
+    def rope(x, pos, base):
+        dh = x.shape[-1]
+        ang = np.asarray(pos, dtype=np.float64)[..., None] * om.rope_inv_freq(dh, base)
+        c, s = np.cos(ang), np.sin(ang)
+        x1, x2 = x[..., 0::2], x[..., 1::2]
+        out = np.empty_like(x)
+        out[..., 0::2] = x1 * c - x2 * s
+        out[..., 1::2] = x2 * c + x1 * s
+        return out
+    _patch("rope", rope)
+
+
+def rope_freq_exponent():
+    _orig = om.rope_inv_freq
+    om.rope_inv_freq = lambda dh, base: base ** (-np.arange(dh // 2, dtype=np.float64) / dh)
+
+
+def rmsnorm_eps_outside():
+    _patch("rmsnorm", lambda x, g, eps: x / (np.sqrt(np.mean(x * x, axis=-1, keepdims=True)) + eps) * g)
+
+
+def attention_unscaled():
+    def tree_attention(q, k, v, Kp, Vp, visible):
+        T, Hq, dh = q.shape
+        group = Hq // k.shape[1]
+        o = np.zeros((T, Hq, dh))
+        for hq in range(Hq):
+            hk = hq // group
+            keys = np.concatenate([Kp[hk], k[:, hk, :]], axis=0)
+            vals = np.concatenate([Vp[hk], v[:, hk, :]], axis=0)
+            s = np.where(visible, q[:, hq, :] @ keys.T, -np.inf)
+            o[:, hq, :] = om.softmax(s, axis=-1) @ vals
+        return o
+    _patch("tree_attention", tree_attention)
+
+
+def gqa_modulo():
+    def tree_attention(q, k, v, Kp, Vp, visible):
+        T, Hq, dh = q.shape
+        Hkv = k.shape[1]
+        o = np.zeros((T, Hq, dh))
+        for hq in range(Hq):
+            hk = hq % Hkv
+            keys = np.concatenate([Kp[hk], k[:, hk, :]], axis=0)
+            vals = np.concatenate([Vp[hk], v[:, hk, :]], axis=0)
+            s = np.where(visible, q[:, hq, :] @ keys.T / np.sqrt(dh), -np.inf)
+            o[:, hq, :] = om.softmax(s, axis=-1) @ vals
+        return o
+    _patch("tree_attention", tree_attention)
+
+
+def no_ancestor_mask():
+    _patch("ancestor_matrix", lambda parents: np.tril(np.ones((len(parents), len(parents)), dtype=bool)))
+
+
+def position_by_node_id():
+    from workloads import gen
+    gen.Tree.depths = lambda self: np.arange(self.n, dtype=np.int32)
+
+
+def drop_attention_residual():
+    orig = ov.tree_attention
+
+    def verify_tree(ow, prefix_kv, tree, prefix_len):
+        m = ow.shape
+        T, P = tree.n, prefix_len
+        pos = P + tree.depths()
+        visible = np.concatenate([np.ones((T, P), dtype=bool), ov.ancestor_matrix(tree.parents)], axis=1)
+        x = ow.embed(tree.tokens)
+        ks, vs = [], []
+        for l in range(m.n_layers):
+            L = ow.layer(l)
+            q, k, v = om.split_qkv(om.rmsnorm(x, L["attn_norm"], m.rms_eps), L["w_qkv"], m)
+            q, k = om.rope(q, pos[:, None], m.rope_base), om.rope(k, pos[:, None], m.rope_base)
+            ks.append(k)
+            vs.append(v)
+            Kp, Vp = prefix_kv(l)
+            x = orig(q, k, v, Kp, Vp, visible).reshape(T, -1) @ L["w_o"].T
+            x = x + om.mlp(om.rmsnorm(x, L["mlp_norm"], m.rms_eps), L, m)[0]
+        logits = om.rmsnorm(x, ow.final_norm, m.rms_eps) @ ow.lm_head().T
+        return ov.VerifyResult(logits, x, ks, vs, None)
+    ov.verify_tree = verify_tree
+    import oracle
+    oracle.verify_tree = verify_tree
+
+
+def swiglu_swapped():
+    def swiglu(h, w_gate_up, w_down):
+        f = w_down.shape[1]
+        return (om.silu(h @ w_gate_up[f:].T) * (h @ w_gate_up[:f].T)) @ w_down.T
+    _patch("swiglu", swiglu)
+
+
+def moe_unnormalised():
+    def moe(h, L, top_k):
+        logits = h @ L["w_router"].T
+        p = om.softmax(logits, axis=-1)
+        out = np.zeros_like(h)
+        for r in range(h.shape[0]):
+            for e in np.argsort(-p[r], kind="stable")[:top_k]:
+                out[r] += p[r, e] * om.swiglu(h[r:r + 1], L["w_gate_up"][e], L["w_down"][e])[0]
+        return out, logits
+    _patch("moe", moe)
+
+
+def qkv_kv_swapped():
+    def split_qkv(h, w_qkv, m):
+        Hq, Hkv, dh = m.n_q_heads, m.n_kv_heads, m.head_dim
+        y = h @ w_qkv.T
+        q = y[:, : Hq * dh].reshape(-1, Hq, dh)
+        v = y[:, Hq * dh: (Hq + Hkv) * dh].reshape(-1, Hkv, dh)
+        k = y[:, (Hq + Hkv) * dh:].reshape(-1, Hkv, dh)
+        return q, k, v
+    _patch("split_qkv", split_qkv)
+
+
+def accept_no_bonus():
+    orig = oa.accept_dfs
+
+    def accept_dfs(tree, pred):
+        r = orig(tree, pred)
+        return oa.AcceptResult(r.length, r.tokens[:-1], r.path)
+    _patch("accept_dfs", accept_dfs)
+    import oracle
+    oracle.accept_dfs = accept_dfs
+
+
+def accept_first_child_only():
+    def accept_dfs(tree, pred):
+        node, path = 0, []
+        while True:
+            kids = [c for c in range(1, tree.n) if tree.parents[c] == node]
+            if not kids or int(tree.tokens[kids[0]]) != int(pred[node]):
+                break
+            node = kids[0]
+            path.append(node)
+        return oa.AcceptResult(len(path), [int(tree.tokens[i]) for i in path] + [int(pred[node])], path)
+    _patch("accept_dfs", accept_dfs)
+    import oracle
+    oracle.accept_dfs = accept_dfs
+
+
+def argmax_last_on_ties():
+    def argmax_first(logits):
+        rev = np.flip(logits, axis=-1)
+        return logits.shape[-1] - 1 - np.argmax(rev, axis=-1)
+    _patch("argmax_first", argmax_first)
+    import oracle
+    oracle.argmax_first = argmax_first
+
+
+def latency_missing_depth():
+    import oracle.latency as ol
+    ol.speedup_ratio = lambda t, t_bar, d, tau: t / (t + t_bar) * tau
+    import oracle
+    oracle.speedup_ratio = ol.speedup_ratio
+
+
+MUTATIONS = {f.__name__: f for f in [
+    rope_sign, rope_interleaved, rope_freq_exponent, rmsnorm_eps_outside, attention_unscaled,
+    gqa_modulo, no_ancestor_mask, position_by_node_id, drop_attention_residual, swiglu_swapped,
+    moe_unnormalised, qkv_kv_swapped, accept_no_bonus, accept_first_child_only,
+    argmax_last_on_ties, latency_missing_depth,
+]}
+
+
+def apply(name: str) -> None:
+    MUTATIONS[name]()
