@@ -1,0 +1,252 @@
+#!/usr/bin/env python3
+"""Benchmark of one GRIFFIN-style tree-verification step on one MI355X.
+
+A step is one full verify pass over one batch: host tree preparation, the
+target forward over every draft-tree node (all layers, LM head), the vocab
+argmax and the acceptance walk, plus the copy of the acceptance result to the
+host.  Inputs (random-init weights, the prefix KV cache and a pool of seeded
+draft trees) are resident in HBM before timing starts.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload llama3-8b]
+
+Prints one JSON line (rank 0).  Multi-GPU runs are not part of this build.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBS = 8000.0   # MI355X HBM3E spec sheet
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def algorithmic_bytes(w, experts_touched=None):
+    """Bytes a verify step must move: every weight once, the prefix KV read,
+    the tree K/V written (SURVEY-style accounting; activations excluded)."""
+    m = w.model
+    weights = m.weight_bytes(experts_touched) + 2 * w.tree_nodes * w.batch * m.d_model  # + embedding rows
+    kv_read = w.batch * w.prefix_len * m.kv_bytes_per_position()
+    kv_write = w.batch * w.tree_nodes * m.kv_bytes_per_position()
+    return weights + kv_read + kv_write, dict(weights=weights, kv_read=kv_read, kv_write=kv_write)
+
+
+def class_bytes_per_launch(w):
+    """Algorithmic HBM bytes of one launch of each GEMM class (weights streamed once)."""
+    m = w.model
+    d, f = m.d_model, m.d_ff
+    e = m.n_experts
+    return {
+        "qkv_gemm": 2 * m.qkv_rows * d,
+        "o_gemm": 2 * d * m.n_q_heads * m.head_dim,
+        "gate_up_gemm": 2 * e * 2 * f * d,
+        "down_gemm": 2 * e * d * f,
+        "lm_head_gemm": 2 * m.vocab * d,
+        "tree_attention": w.batch * w.prefix_len * m.kv_bytes_per_position() // m.n_layers,
+    }
+
+
+def cpu_baseline(w, weights_gpu, n_layers_sample=2):
+    """Time the fp64 oracle on a bounded sample of the same step: embedding +
+    LM head + n_layers_sample layers of one tree, the per-layer time
+    extrapolated to the full depth."""
+    import numpy as np
+    import torch
+    from threadpoolctl import threadpool_info
+
+    import oracle
+    from workloads import gen
+    from workloads.configs import with_layers
+
+    m = w.model
+    k = min(n_layers_sample, m.n_layers)
+    tree, _ = gen.workload_tree(w, 0, 0)
+
+    def sample_weights(nl):
+        layers = [{kk: (None if v is None else v.to("cpu")) for kk, v in weights_gpu.layers[l].items()}
+                  for l in range(nl)]
+        shp = with_layers(w, nl).model
+        return oracle.OracleWeights(gen.ModelWeights(shp, weights_gpu.embed.to("cpu"), weights_gpu.lm_head.to("cpu"),
+                                                     weights_gpu.final_norm.to("cpu"), layers), cache=False)
+
+    kv = []
+    for l in range(k):
+        kk, vv = gen.synthetic_kv(m, l, 0, w.prefix_len, w.weight_seed, "cpu")
+        kv.append((kk.to(torch.float64).numpy(), vv.to(torch.float64).numpy()))
+    ow0 = sample_weights(0)
+    t0 = time.perf_counter()
+    oracle.verify_tree(ow0, lambda l: kv[l], tree, w.prefix_len)
+    t_head = time.perf_counter() - t0
+    owk = sample_weights(k)
+    t0 = time.perf_counter()
+    oracle.verify_tree(owk, lambda l: kv[l], tree, w.prefix_len)
+    t_k = time.perf_counter() - t0
+    per_layer = max(t_k - t_head, 0.0) / k
+    t_full = t_head + per_layer * m.n_layers
+    threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    return {
+        "value": round(1.0 / t_full, 6),
+        "unit": "verify_steps/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": (f"fp64 oracle, one {w.tree_nodes}-node tree at prefix {w.prefix_len}: embedding + LM head "
+                   f"({t_head:.1f} s) and {k} of {m.n_layers} layers ({t_k - t_head:.1f} s), per-layer time "
+                   f"extrapolated to {m.n_layers} layers = {t_full:.1f} s per step"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="llama3-8b")
+    ap.add_argument("--pool", type=int, default=16)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-profile", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on exactly one GPU; --gpus {args.gpus} is not supported", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2502_11018_amd as P
+    from workloads import gen
+    from workloads.configs import get_workload
+
+    w = get_workload(args.workload)
+    m = w.model
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    t0 = time.time()
+    weights = gen.make_weights(m, w.weight_seed, device=dev)
+    torch.cuda.synchronize()
+    log(f"weights {weights.nbytes() / 1e9:.2f} GB generated in {time.time() - t0:.1f} s")
+    max_tree = 64
+    v = P.TreeVerifier(m, weights, max_batch=w.batch, max_tree=max_tree, max_depth=w.depth,
+                       kv_capacity=w.kv_capacity())
+    for l in range(m.n_layers):
+        for b in range(w.batch):
+            k, vv = gen.synthetic_kv(m, l, b, w.prefix_len, w.weight_seed, dev)
+            v.write_prefix(l, b, k, vv)
+    torch.cuda.synchronize()
+    log(f"prefix KV written ({w.batch} x {w.prefix_len} positions)")
+
+    # pool of draft trees; planted paths use the target's greedy continuation,
+    # obtained from the verify path itself on chain trees
+    pool = []
+    for i in range(args.pool):
+        trees, paths = zip(*[gen.workload_tree(w, i, b) for b in range(w.batch)])
+        trees = list(trees)
+        need = max(len(p) for p in paths)
+        if need:
+            chains = [[int(t.tokens[0])] for t in trees]
+            for _ in range(need):
+                v.step([w.prefix_len] * w.batch, [gen.chain_tree(c[0], c[1:]) for c in chains])
+                v.accept()
+                pred = v.predictions()
+                for b, c in enumerate(chains):
+                    c.append(int(pred[b, len(c) - 1]))
+            trees = [gen.apply_plant(t, p, chains[b][1:]) for b, (t, p) in enumerate(zip(trees, paths))]
+        pool.append(trees)
+    log(f"tree pool of {len(pool)} ready")
+
+    prefix = [w.prefix_len] * w.batch
+    packed = [P.pack_trees(t, max_tree) for t in pool]
+    accepted = []
+
+    def one_step(i):
+        n, tok, par = packed[i % len(packed)]
+        v.step_arrays(prefix, n, tok, par)
+        return v.accept()
+
+    for i in range(args.warmup):
+        one_step(i)
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    start.record(v.stream)
+    for i in range(args.steps):
+        r = one_step(i)
+        accepted.extend(int(x) for x in r.length)
+    stop.record(v.stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall * 1e3 / args.steps
+    ev_ms = start.elapsed_time(stop) / args.steps
+    steps_per_s = 1e3 / ms_per_step
+    total_bytes, parts = algorithmic_bytes(w)
+    log(f"{ms_per_step:.3f} ms/step (events {ev_ms:.3f}), {steps_per_s:.1f} steps/s")
+
+    # per kernel class timing (separate pass: event records between launches)
+    kernels, roofline = {}, None
+    if not args.no_profile:
+        v.profile_enable()
+        nprof = min(args.steps, 20)
+        for i in range(nprof):
+            one_step(i)
+        prof = v.profile_read()
+        v.profile_enable(0)
+        per_launch = class_bytes_per_launch(w)
+        for name, (ms, n) in prof.items():
+            if n == 0:
+                continue
+            ent = {"ms_per_step": round(ms / nprof, 4), "launches_per_step": n // nprof,
+                   "avg_launch_us": round(1e3 * ms / n, 2)}
+            if name in per_launch:
+                ent["bytes_per_launch"] = per_launch[name]
+                ent["achieved_GBs"] = round(per_launch[name] / (ms / n * 1e-3) / 1e9, 1)
+            kernels[name] = ent
+        dom = max((k for k in kernels if k in per_launch), key=lambda k: kernels[k]["ms_per_step"])
+        ach = kernels[dom]["achieved_GBs"]
+        roofline = {"bound": "hbm", "kernel": dom, "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                    "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
+                    "bytes_per_launch": kernels[dom]["bytes_per_launch"],
+                    "avg_launch_us": kernels[dom]["avg_launch_us"]}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("timing the fp64 oracle on a bounded sample")
+        cpu = cpu_baseline(w, weights)
+
+    out = {
+        "metric": "verify steps/sec & draft-tree tokens/sec at 1 GPU; achieved HBM GB/s vs peak",
+        "value": round(steps_per_s * 1.0, 3),
+        "unit": "verify_steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (random-init weights, seeded prefix KV and draft trees)",
+        "config": {"workload": w.name, "model_shape": m.name, "batch": w.batch, "prefix_len": w.prefix_len,
+                   "tree_nodes": w.tree_nodes, "draft_tokens": w.n_draft, "depth": w.depth},
+        "draft_tree_tokens_per_s": round(steps_per_s * w.batch * w.n_draft, 1),
+        "algorithmic_bytes_per_step": total_bytes,
+        "step_hbm_GBs": round(total_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+        "step_hbm_frac": round(total_bytes / (ms_per_step * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        "synthetic_mean_accept_len": round(float(np.mean(accepted)) + 1.0, 3) if accepted else None,
+        "roofline": roofline,
+        "kernels": kernels,
+        "cpu_baseline": cpu,
+    }
+    v.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,206 @@
+/*
+ * griffin_verify.h - tree verification for GRIFFIN-style speculative decoding
+ * on one AMD Instinct MI355X (gfx950).
+ *
+ * What the library computes.  In each draft-and-verify cycle the target model
+ * scores every draft token in a single forward pass (paper, Sec. 3).  The draft
+ * tokens form a tree because several top-k candidates are kept per position
+ * (Sec. 4.1), and a draft token counts only if the target's own greedy
+ * prediction at its parent equals it, a rejection discarding everything below
+ * it (Sec. 4.1); decoding is greedy at temperature 0 (Sec. 5).  The library
+ * therefore takes a prefix KV cache plus a draft tree per sequence and returns
+ * the greedy acceptance length and the accepted tokens: the deepest node whose
+ * whole root path is accepted, then the target's prediction at that node (the
+ * extra token the paper's acceptance length counts, Sec. 5).  Trees follow the
+ * paper's appendix "Draft Tree Structure" (up to 64 nodes here; the paper uses
+ * 60 draft tokens at depth 6).
+ *
+ * Conventions shared by every entry point.
+ *  - A tree has n nodes; node 0 is the root: the last accepted token, which is
+ *    not yet in the KV cache.  parents[0] = -1 and 0 <= parents[i] < i.
+ *  - Node i sits at sequence position prefix_len + depth(i) (rotary position)
+ *    and its K/V go to cache slot prefix_len + i.  Slots [prefix_len,
+ *    prefix_len + n) are scratch: each step overwrites them.  For a chain
+ *    (parents[i] = i - 1) slot and position coincide, so committing a chain is
+ *    just prefix_len += n.
+ *  - The model is a LLaMA-family decoder (RMSNorm, rotate-half rotary
+ *    embedding, grouped-query attention with contiguous groups, SwiGLU MLP) or
+ *    its Mixtral mixture-of-experts variant (softmax router, top-k experts,
+ *    kept probabilities renormalised); these are the targets of Sec. 5.
+ *  - Greedy argmax ties go to the lowest token id; among equally deep accepted
+ *    nodes the one with the smallest id is reported.
+ *  - bf16 means IEEE bfloat16 bit patterns (uint16).  All device pointers are
+ *    borrowed: the caller allocates them, keeps them alive while the context
+ *    lives, and frees them.  Device pointers must be 16-byte aligned.
+ *  - Every function returns GRIFFIN_OK (0) or a negative status; argument and
+ *    tree validation happens before any device work, so on a validation error
+ *    nothing is launched and nothing (KV cache included) is written.
+ *  - A context is not thread-safe.  Several contexts may borrow the same
+ *    weights; two contexts must not share a KV cache region they both write.
+ */
+#ifndef GRIFFIN_VERIFY_H
+#define GRIFFIN_VERIFY_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GRIFFIN_OK 0
+#define GRIFFIN_EINVAL (-1)    /* null or inconsistent argument */
+#define GRIFFIN_ESHAPE (-2)    /* model shape the kernels do not support */
+#define GRIFFIN_ETREE (-3)     /* malformed tree: parents[0] != -1, parent not in [0,i), n out of [1,max_tree], depth > max_depth */
+#define GRIFFIN_ETOKEN (-4)    /* token id outside [0, vocab) */
+#define GRIFFIN_ECAPACITY (-5) /* prefix_len < 0 or prefix_len + n > kv_capacity */
+#define GRIFFIN_EORDER (-6)    /* griffin_accept / griffin_read_predictions before any step */
+#define GRIFFIN_ENOMEM (-7)    /* device or pinned host allocation failed */
+#define GRIFFIN_EHIP (-8)      /* a HIP runtime call failed; griffin_last_error has the text */
+#define GRIFFIN_ENUMERIC (-9)  /* a NaN appeared in the logits of a valid tree node */
+
+/* Model shape and limits.  Supported: head_dim 64 or 128; n_q_heads a
+ * multiple of n_kv_heads; d_model, n_q_heads*head_dim and d_ff multiples of 8;
+ * n_experts in [1, 64] with top_k in [1, min(n_experts, 4)] when n_experts > 1;
+ * max_tree in [1, 64]; max_depth in [0, max_tree - 1]; kv_capacity a positive
+ * multiple of 32. */
+typedef struct griffin_model_desc {
+  int32_t n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ff, vocab;
+  int32_t n_experts; /* 1 = dense SwiGLU MLP */
+  int32_t top_k;     /* experts per token when n_experts > 1 (ignored otherwise) */
+  float rms_eps;
+  double rope_base;
+  int32_t max_batch;   /* sequences per step */
+  int32_t max_tree;    /* nodes per tree, root included (<= 64) */
+  int32_t max_depth;   /* deepest node depth accepted by the validator */
+  int32_t kv_capacity; /* cache slots per (layer, sequence, KV head) */
+} griffin_model_desc;
+
+/* Device weights, bf16, row-major, borrowed.  Per-layer fields point to host
+ * arrays of n_layers device pointers (the host arrays are copied at init).
+ *   embed       [vocab][d_model]
+ *   lm_head     [vocab][d_model]          (untied)
+ *   final_norm  [d_model]
+ *   attn_norm   [d_model]                 RMSNorm gain before attention
+ *   w_qkv       [(Hq + 2*Hkv)*head_dim][d_model]; rows are all query heads,
+ *               then all key heads, then all value heads (head-major)
+ *   w_o         [d_model][Hq*head_dim]
+ *   mlp_norm    [d_model]
+ *   w_gate_up   dense: [2*d_ff][d_model] (gate rows, then up rows)
+ *               MoE:   [n_experts][2*d_ff][d_model]
+ *   w_down      dense: [d_model][d_ff];  MoE: [n_experts][d_model][d_ff]
+ *   w_router    MoE: [n_experts][d_model]; NULL (the array itself) for dense */
+typedef struct griffin_weights {
+  const void *embed, *lm_head, *final_norm;
+  const void *const *attn_norm, *const *w_qkv, *const *w_o, *const *mlp_norm;
+  const void *const *w_gate_up, *const *w_down, *const *w_router;
+} griffin_weights;
+
+typedef struct griffin_ctx griffin_ctx;
+
+/* Bytes of one of the two KV cache buffers for this shape:
+ * n_layers * max_batch * n_kv_heads * kv_capacity * head_dim * 2. */
+size_t griffin_kv_cache_bytes(const griffin_model_desc *desc);
+
+/* Create a context.
+ * k_cache: device bf16 [n_layers][max_batch][n_kv_heads][kv_capacity][head_dim],
+ *          keys after rotation.
+ * v_cache: device bf16 [n_layers][max_batch][n_kv_heads][head_dim][kv_capacity]
+ *          (values stored transposed: one row per head dimension).
+ * hip_stream: the hipStream_t every launch is enqueued on (NULL = default).
+ * The context allocates its own workspace (activations, partial sums,
+ * metadata, pinned staging) and frees it in griffin_verify_free.
+ * Errors: EINVAL (null pointer, misaligned pointer), ESHAPE, ENOMEM, EHIP. */
+int griffin_verify_init(const griffin_model_desc *desc, const griffin_weights *weights,
+                        void *k_cache, void *v_cache, void *hip_stream, griffin_ctx **out);
+
+/* Enqueue one verification pass over `batch` trees (asynchronous).
+ * Host arrays, row b of each describes sequence b (cache row b):
+ *   prefix_len [batch]            cached positions of sequence b
+ *   n_nodes    [batch]            tree size, root included
+ *   tokens     [batch][max_tree]  token of node i (entries >= n_nodes ignored)
+ *   parents    [batch][max_tree]  parent of node i; parents[b][0] = -1
+ * logits_out: optional device fp32 [batch*max_tree][vocab]; row b*max_tree+i
+ *   receives node i's logits (rows of absent nodes are left untouched).
+ * The pass writes the trees' K/V into cache slots [prefix_len, prefix_len+n)
+ * of each sequence, then runs the acceptance walk on the device.  The host
+ * arrays may be reused as soon as the call returns.
+ * Errors: EINVAL, ETREE, ETOKEN, ECAPACITY (nothing launched), EHIP. */
+int griffin_verify_step(griffin_ctx *ctx, int32_t batch, const int32_t *prefix_len,
+                        const int32_t *n_nodes, const int32_t *tokens, const int32_t *parents,
+                        float *logits_out);
+
+/* Wait for the last step and copy its acceptance result to host arrays:
+ *   accept_len [batch]                 accepted draft tokens L in [0, max_depth]
+ *   tokens_out [batch][max_depth + 1]  L accepted tokens, then the target's
+ *                                      prediction at the last accepted node;
+ *                                      remaining entries -1
+ *   path_nodes [batch][max_depth]      node ids of the accepted tokens, -1 padded
+ * Any output pointer may be NULL.  The paper's acceptance length is L + 1.
+ * Errors: EORDER (no step yet), EHIP, ENUMERIC (a NaN logit in a valid node;
+ * the outputs are still written). */
+int griffin_accept(griffin_ctx *ctx, int32_t *accept_len, int32_t *tokens_out, int32_t *path_nodes);
+
+/* Wait for the last step and copy the target's greedy prediction (argmax of
+ * the logits) of every node: pred [batch][max_tree] host, -1 for absent nodes.
+ * Errors: EORDER, EHIP. */
+int griffin_read_predictions(griffin_ctx *ctx, int32_t *pred);
+
+/* Release the context (waits for its stream first).  NULL is a no-op. */
+void griffin_verify_free(griffin_ctx *ctx);
+
+/* Static text for a status code. */
+const char *griffin_status_str(int code);
+
+/* Text of the last error recorded on ctx ("" if none). */
+const char *griffin_last_error(const griffin_ctx *ctx);
+
+/* Host-only tree validation and metadata (no device work, no context).
+ * For one tree of n nodes: checks it like griffin_verify_step does against
+ * (max_tree, max_depth, vocab, kv_capacity) and fills, when non-NULL,
+ *   depth [n]    node depth (root 0)
+ *   pos   [n]    prefix_len + depth (rotary position)
+ *   anc   [n]    bit j set iff node j is node i or one of its ancestors
+ * Errors: EINVAL, ETREE, ETOKEN, ECAPACITY. */
+int griffin_tree_prepare(int32_t n, const int32_t *tokens, const int32_t *parents, int32_t prefix_len,
+                         int32_t max_tree, int32_t max_depth, int32_t vocab, int32_t kv_capacity,
+                         int32_t *depth, int32_t *pos, uint64_t *anc);
+
+/* Run only the device acceptance walk on given predictions (no model, no
+ * context): for `batch` trees (host arrays laid out as in griffin_verify_step)
+ * and host pred [batch][max_tree] (the target's prediction per node), fill the
+ * same outputs as griffin_accept.  Allocates and frees its own device buffers
+ * and synchronises hip_stream.  Errors: EINVAL, ETREE, ETOKEN, ENOMEM, EHIP. */
+int griffin_accept_walk(void *hip_stream, int32_t batch, int32_t max_tree, int32_t max_depth,
+                        int32_t vocab, const int32_t *n_nodes, const int32_t *tokens,
+                        const int32_t *parents, const int32_t *pred, int32_t *accept_len,
+                        int32_t *tokens_out, int32_t *path_nodes);
+
+/* Kernel classes of one verification pass, for griffin_profile_*. */
+#define GRIFFIN_KC_QKV 0     /* QKV projection GEMM */
+#define GRIFFIN_KC_ROPE 1    /* rotary embedding + tree K/V write */
+#define GRIFFIN_KC_ATTN 2    /* tree-masked attention and split merge */
+#define GRIFFIN_KC_O 3       /* output projection GEMM */
+#define GRIFFIN_KC_NORM 4    /* residual update + RMSNorm (and embedding) */
+#define GRIFFIN_KC_GATE_UP 5 /* gate/up GEMM with SwiGLU (MoE: routed experts) */
+#define GRIFFIN_KC_DOWN 6    /* down GEMM (MoE: routed experts) */
+#define GRIFFIN_KC_LM_HEAD 7 /* LM head GEMM with per-tile argmax */
+#define GRIFFIN_KC_OTHER 8   /* argmax reduction, acceptance walk, MoE routing */
+#define GRIFFIN_KC_COUNT 9
+
+/* Per-class timing with HIP events recorded on the context's stream around
+ * every launch of the classes in `class_mask` (bit k = class k); 0 disables.
+ * Timing adds two event records per launch, so time the pass without it. */
+int griffin_profile_enable(griffin_ctx *ctx, uint32_t class_mask);
+
+/* Wait for the stream, then return per class the summed launch durations in
+ * milliseconds (ms[GRIFFIN_KC_COUNT]) and the number of launches timed
+ * (launches[GRIFFIN_KC_COUNT]) since the last read or enable; resets both.
+ * Errors: EINVAL, EHIP. */
+int griffin_profile_read(griffin_ctx *ctx, double *ms, int64_t *launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GRIFFIN_VERIFY_H */

@@ -1,0 +1,351 @@
+// Row-wise kernels of the verify pass: embedding gather, residual update +
+// RMSNorm, rotary embedding + tree K/V write, vocab argmax reduction, the
+// acceptance walk and the MoE router.  All reductions use fixed orders, so
+// repeated runs give identical bits.
+
+#include "device_common.h"
+#include "griffin_internal.h"
+
+namespace griffin {
+
+// ------------------------------------------------------------- embedding ----
+// x[r][:] = E[token[r]][:] as fp32; one workgroup per row.
+__global__ __launch_bounds__(256) void embed_kernel(const uint16_t* __restrict__ E, const int32_t* token,
+                                                    int d, float* __restrict__ x) {
+  const int r = blockIdx.x;
+  const uint16_t* src = E + (long long)token[r] * d;
+  float* dst = x + (long long)r * d;
+  for (int j = threadIdx.x * 4; j < d; j += blockDim.x * 4) {
+    const uint2 v = *reinterpret_cast<const uint2*>(src + j);
+    *reinterpret_cast<float4*>(dst + j) =
+        make_float4(bf16_to_f32(v.x & 0xffff), bf16_to_f32(v.x >> 16), bf16_to_f32(v.y & 0xffff),
+                    bf16_to_f32(v.y >> 16));
+  }
+}
+
+hipError_t launch_embed(const uint16_t* embed, const int32_t* token, int rows, int d, float* x, hipStream_t s) {
+  hipLaunchKernelGGL(embed_kernel, dim3(rows), dim3(256), 0, s, embed, token, d, x);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------ residual update + RMSNorm ----
+// x[r] += (split partial sums | weighted MoE expert outputs); then
+// xn[r] = bf16(x[r] * rsqrt(mean(x[r]^2) + eps) * gain).
+// 256 threads, each owning up to RN_MAX float4 groups of the row in registers.
+constexpr int RN_THREADS = 256;
+constexpr int RN_MAX = 8;  // d <= 8192
+
+__global__ __launch_bounds__(RN_THREADS) void residual_rmsnorm_kernel(float* __restrict__ x, ResidualAdd add,
+                                                                      const uint16_t* __restrict__ gain,
+                                                                      float eps, int d,
+                                                                      uint16_t* __restrict__ xn) {
+  __shared__ float red[16];
+  const int r = blockIdx.x;
+  float* xr = x + (long long)r * d;
+  const int groups = d >> 2;
+  float4 v[RN_MAX];
+  float ss = 0.f;
+  const bool upd = add.parts != nullptr;
+#pragma unroll
+  for (int u = 0; u < RN_MAX; ++u) {
+    const int gi = threadIdx.x + u * RN_THREADS;
+    if (gi < groups) {
+      float4 a = reinterpret_cast<const float4*>(xr)[gi];
+      if (upd) {
+        if (add.slot == nullptr) {
+          for (int s = 0; s < add.n_parts; ++s) {
+            const float4 p = reinterpret_cast<const float4*>(add.parts + s * add.part_stride + (long long)r * d)[gi];
+            a.x += p.x; a.y += p.y; a.z += p.z; a.w += p.w;
+          }
+        } else {
+          for (int k = 0; k < add.top_k; ++k) {
+            const int sl = add.slot[r * add.top_k + k];
+            if (sl < 0) continue;
+            const float w = add.slot_w[r * add.top_k + k];
+            const float4 p = reinterpret_cast<const float4*>(add.parts + (long long)sl * d)[gi];
+            a.x += w * p.x; a.y += w * p.y; a.z += w * p.z; a.w += w * p.w;
+          }
+        }
+        reinterpret_cast<float4*>(xr)[gi] = a;
+      }
+      v[u] = a;
+      ss += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
+    }
+  }
+  const float tot = block_sum(ss, red);
+  const float rs = rsqrtf(tot / (float)d + eps);
+  uint16_t* xo = xn + (long long)r * d;
+#pragma unroll
+  for (int u = 0; u < RN_MAX; ++u) {
+    const int gi = threadIdx.x + u * RN_THREADS;
+    if (gi < groups) {
+      const uint2 gg = *reinterpret_cast<const uint2*>(gain + 4 * gi);
+      const float4 a = v[u];
+      uint2 o;
+      o.x = pack_bf16x2(a.x * rs * bf16_to_f32(gg.x & 0xffff), a.y * rs * bf16_to_f32(gg.x >> 16));
+      o.y = pack_bf16x2(a.z * rs * bf16_to_f32(gg.y & 0xffff), a.w * rs * bf16_to_f32(gg.y >> 16));
+      *reinterpret_cast<uint2*>(xo + 4 * gi) = o;
+    }
+  }
+}
+
+hipError_t launch_residual_rmsnorm(float* x, const ResidualAdd& add, const uint16_t* gain, float eps, int rows,
+                                   int d, uint16_t* xn, hipStream_t s) {
+  if (d % 4 != 0 || d > 4 * RN_THREADS * RN_MAX) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(residual_rmsnorm_kernel, dim3(rows), dim3(RN_THREADS), 0, s, x, add, gain, eps, d, xn);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------ rotary + tree K/V write ----
+// For a valid tree row r = b*max_tree + i: sum the K-split partials of its
+// QKV projection, rotate q and k (rotate-half pairing j <-> j + dh/2) at the
+// node's position, write q (bf16) for attention, and k / v into cache slot
+// prefix_len[b] + i (k row-major per slot, v transposed: one row per dim).
+__global__ __launch_bounds__(256) void qkv_rope_kernel(const float* __restrict__ parts, int n_parts,
+                                                       long long part_stride, StepMeta meta,
+                                                       const float* __restrict__ rcos,
+                                                       const float* __restrict__ rsin, int Hq, int Hkv,
+                                                       int dh, int max_tree, int kv_cap,
+                                                       uint16_t* __restrict__ q_out,
+                                                       uint16_t* __restrict__ kc, uint16_t* __restrict__ vc) {
+  const int r = blockIdx.x;
+  const int b = r / max_tree, i = r % max_tree;
+  if (i >= meta.n_nodes[b]) return;
+  const int half = dh >> 1;
+  const int heads = Hq + 2 * Hkv;
+  const int width = heads * dh;
+  const int pos = meta.pos[r];
+  const int slot = meta.prefix_len[b] + i;
+  const float* row = parts + (long long)r * width;
+  for (int t = threadIdx.x; t < heads * half; t += blockDim.x) {
+    const int h = t / half, j = t % half;
+    const int c1 = h * dh + j, c2 = c1 + half;
+    float x1 = 0.f, x2 = 0.f;
+    for (int s = 0; s < n_parts; ++s) {
+      x1 += row[s * part_stride + c1];
+      x2 += row[s * part_stride + c2];
+    }
+    if (h < Hq + Hkv) {
+      const float c = rcos[(long long)pos * half + j], sn = rsin[(long long)pos * half + j];
+      const float y1 = x1 * c - x2 * sn;
+      const float y2 = x2 * c + x1 * sn;
+      if (h < Hq) {
+        uint16_t* q = q_out + ((long long)r * Hq + h) * dh;
+        q[j] = f32_to_bf16(y1);
+        q[j + half] = f32_to_bf16(y2);
+      } else {
+        uint16_t* k = kc + (((long long)b * Hkv + (h - Hq)) * kv_cap + slot) * dh;
+        k[j] = f32_to_bf16(y1);
+        k[j + half] = f32_to_bf16(y2);
+      }
+    } else {
+      uint16_t* v = vc + ((long long)b * Hkv + (h - Hq - Hkv)) * dh * kv_cap;
+      v[(long long)j * kv_cap + slot] = f32_to_bf16(x1);
+      v[(long long)(j + half) * kv_cap + slot] = f32_to_bf16(x2);
+    }
+  }
+}
+
+hipError_t launch_qkv_rope(const float* qkv_parts, int n_parts, long long part_stride, StepMeta meta,
+                           const float* rope_cos, const float* rope_sin, int Hq, int Hkv, int dh, int max_tree,
+                           int batch, int kv_cap, uint16_t* q_out, uint16_t* k_cache_l, uint16_t* v_cache_l,
+                           hipStream_t s) {
+  hipLaunchKernelGGL(qkv_rope_kernel, dim3(batch * max_tree), dim3(256), 0, s, qkv_parts, n_parts, part_stride,
+                     meta, rope_cos, rope_sin, Hq, Hkv, dh, max_tree, kv_cap, q_out, k_cache_l, v_cache_l);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------ argmax reduction ----
+// pred[r] = argmax over the LM-head tiles' partial maxima (ascending tile
+// order, strict comparison, so ties keep the lowest token id).
+__global__ __launch_bounds__(64) void argmax_reduce_kernel(const float* __restrict__ pmax,
+                                                           const int32_t* __restrict__ pidx,
+                                                           const int32_t* __restrict__ pnan, int n_tiles,
+                                                           int ld_part, int32_t* pred, int32_t* nan_row) {
+  const int r = blockIdx.x;
+  const int lane = threadIdx.x;
+  float best = -INFINITY;
+  int bidx = 0x7fffffff;
+  int nan_cnt = 0;
+  for (int t = lane; t < n_tiles; t += 64) {
+    const float v = pmax[(long long)r * ld_part + t];
+    const int id = pidx[(long long)r * ld_part + t];
+    nan_cnt += pnan[(long long)r * ld_part + t];
+    if (v > best || (v == best && id < bidx)) { best = v; bidx = id; }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const float ob = __shfl_xor(best, o, 64);
+    const int oi = __shfl_xor(bidx, o, 64);
+    nan_cnt += __shfl_xor(nan_cnt, o, 64);
+    if (ob > best || (ob == best && oi < bidx)) { best = ob; bidx = oi; }
+  }
+  if (lane == 0) {
+    pred[r] = bidx;
+    nan_row[r] = nan_cnt;
+  }
+}
+
+hipError_t launch_argmax_reduce(const float* pmax, const int32_t* pidx, const int32_t* pnan, int n_tiles,
+                                int ld_part, int rows, int32_t* pred, int32_t* nan_row, hipStream_t s) {
+  hipLaunchKernelGGL(argmax_reduce_kernel, dim3(rows), dim3(64), 0, s, pmax, pidx, pnan, n_tiles, ld_part, pred,
+                     nan_row);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------- acceptance walk ----
+// One wavefront per sequence, one lane per tree node.  Node i (i >= 1) matches
+// when its token equals the prediction at its parent; it is accepted when every
+// node on its root path matches (its ancestor mask, root excluded, lies inside
+// the match ballot).  The deepest accepted node wins, smallest id on ties.
+__global__ __launch_bounds__(64) void accept_kernel(StepMeta meta, const int32_t* __restrict__ pred,
+                                                    const int32_t* __restrict__ nan_row, int max_tree,
+                                                    int max_depth, int32_t* __restrict__ result) {
+  const int b = blockIdx.x;
+  const int i = threadIdx.x;
+  const int n = meta.n_nodes[b];
+  const int r = b * max_tree + i;
+  const bool live = i < n;
+  bool match = false;
+  int depth = 0;
+  uint64_t anc = 0;
+  if (live) {
+    depth = meta.depth[r];
+    anc = meta.anc[r];
+    match = (i == 0) || (meta.token[r] == pred[b * max_tree + meta.parent[r]]);
+  }
+  const uint64_t matched = __ballot(match);
+  const bool ok = live && ((anc & ~matched) == 0);
+  // key: deeper first, then smaller id
+  int key = ok ? (depth << 8) | (255 - i) : -1;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) key = max(key, __shfl_xor(key, o, 64));
+  const int best = 255 - (key & 255);
+  const int L = key >> 8;
+  const uint64_t best_anc = __shfl(anc, best, 64);
+  const int nan_any = __any(live && nan_row[r] != 0);
+  int32_t* res = result + (long long)b * result_stride(max_depth);
+  int32_t* tokens_out = res + 2;
+  int32_t* path = res + 3 + max_depth;
+  if (live && i != 0 && ((best_anc >> i) & 1ull)) {
+    path[depth - 1] = i;
+    tokens_out[depth - 1] = meta.token[r];
+  }
+  if (i >= L && i < max_depth) path[i] = -1;
+  if (i > L && i <= max_depth) tokens_out[i] = -1;
+  if (i == 0) {
+    res[0] = L;
+    res[1] = nan_any ? 1 : 0;
+    tokens_out[L] = pred[b * max_tree + best];
+  }
+}
+
+hipError_t launch_accept(StepMeta meta, const int32_t* pred, const int32_t* nan_row, int batch, int max_tree,
+                         int max_depth, int32_t* result, hipStream_t s) {
+  hipLaunchKernelGGL(accept_kernel, dim3(batch), dim3(64), 0, s, meta, pred, nan_row, max_tree, max_depth, result);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------ MoE router ----
+// For a valid row: h = RMSNorm(x) (fp32, from the fp32 residual), router
+// logits h . w_e in fp32, softmax, keep the top_k experts (ties to the lower
+// id), renormalise their probabilities.  Absent rows get expert id -1.
+__global__ __launch_bounds__(256) void moe_route_kernel(const float* __restrict__ x,
+                                                        const uint16_t* __restrict__ gain, float eps,
+                                                        const uint16_t* __restrict__ wr, int d, int n_experts,
+                                                        int top_k, const int32_t* n_nodes, int max_tree,
+                                                        int32_t* route_ids, float* route_w) {
+  __shared__ float red[16];
+  __shared__ float logit[64];
+  const int r = blockIdx.x;
+  const int b = r / max_tree, i = r % max_tree;
+  if (i >= n_nodes[b]) {
+    if (threadIdx.x < top_k) {
+      route_ids[r * top_k + threadIdx.x] = -1;
+      route_w[r * top_k + threadIdx.x] = 0.f;
+    }
+    return;
+  }
+  const float* xr = x + (long long)r * d;
+  float ss = 0.f;
+  for (int j = threadIdx.x; j < d; j += blockDim.x) ss += xr[j] * xr[j];
+  const float rs = rsqrtf(block_sum(ss, red) / (float)d + eps);
+  for (int e = 0; e < n_experts; ++e) {
+    const uint16_t* w = wr + (long long)e * d;
+    float acc = 0.f;
+    for (int j = threadIdx.x; j < d; j += blockDim.x) acc += xr[j] * rs * bf16_to_f32(gain[j]) * bf16_to_f32(w[j]);
+    const float t = block_sum(acc, red);
+    if (threadIdx.x == 0) logit[e] = t;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float mx = -INFINITY;
+    for (int e = 0; e < n_experts; ++e) mx = fmaxf(mx, logit[e]);
+    float* p = logit;  // probabilities (unnormalised) in place
+    for (int e = 0; e < n_experts; ++e) p[e] = __expf(logit[e] - mx);
+    int chosen[4];
+    float ps[4], tot = 0.f;
+    for (int k = 0; k < top_k; ++k) {
+      int best = -1;
+      for (int e = 0; e < n_experts; ++e) {
+        bool used = false;
+        for (int q = 0; q < k; ++q) used |= chosen[q] == e;
+        if (!used && (best < 0 || p[e] > p[best])) best = e;
+      }
+      chosen[k] = best;
+      ps[k] = p[best];
+      tot += p[best];
+    }
+    for (int k = 0; k < top_k; ++k) {
+      route_ids[r * top_k + k] = chosen[k];
+      route_w[r * top_k + k] = ps[k] / tot;
+    }
+  }
+}
+
+hipError_t launch_moe_route(const float* x, const uint16_t* gain, float eps, const uint16_t* w_router, int rows,
+                            int d, int n_experts, int top_k, const int32_t* n_nodes, int max_tree,
+                            int32_t* route_ids, float* route_w, hipStream_t s) {
+  if (n_experts > 64 || top_k > 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(moe_route_kernel, dim3(rows), dim3(256), 0, s, x, gain, eps, w_router, d, n_experts, top_k,
+                     n_nodes, max_tree, route_ids, route_w);
+  return hipGetLastError();
+}
+
+// Per-expert row lists in ascending row order (deterministic): gather[e][c]
+// is the c-th row routed to expert e, slot[r][k] = e * cap + c for the k-th
+// kept expert of row r (-1 for absent rows, including padding rows).
+__global__ __launch_bounds__(64) void moe_lists_kernel(const int32_t* __restrict__ route_ids, int rows,
+                                                       int padded_rows, int n_experts, int top_k, int cap,
+                                                       int32_t* gather, int32_t* count, int32_t* slot) {
+  const int e = threadIdx.x;
+  for (int r = e; r < padded_rows; r += blockDim.x)
+    if (r >= rows)
+      for (int k = 0; k < top_k; ++k) slot[r * top_k + k] = -1;
+  if (e >= n_experts) return;
+  int c = 0;
+  for (int r = 0; r < rows; ++r)
+    for (int k = 0; k < top_k; ++k) {
+      const int id = route_ids[r * top_k + k];
+      if (id < 0) {
+        if (e == 0) slot[r * top_k + k] = -1;
+      } else if (id == e) {
+        gather[e * cap + c] = r;
+        slot[r * top_k + k] = e * cap + c;
+        ++c;
+      }
+    }
+  count[e] = c;
+}
+
+hipError_t launch_moe_lists(const int32_t* route_ids, int rows, const int32_t* n_nodes, int max_tree,
+                            int n_experts, int top_k, int cap, int32_t* gather, int32_t* count, int32_t* slot,
+                            hipStream_t s) {
+  (void)n_nodes;
+  (void)max_tree;
+  hipLaunchKernelGGL(moe_lists_kernel, dim3(1), dim3(64), 0, s, route_ids, rows, cap, n_experts, top_k, cap,
+                     gather, count, slot);
+  return hipGetLastError();
+}
+
+}  // namespace griffin

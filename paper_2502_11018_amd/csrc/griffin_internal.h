@@ -1,0 +1,112 @@
+// Internal interfaces between the host library (host.cpp) and the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace griffin {
+
+// Per-step metadata, device resident, one row per (sequence, node slot):
+// row r = b * max_tree + i.  Built on the host from the trees and uploaded in
+// one copy per step.
+struct StepMeta {
+  const int32_t* prefix_len;  // [B]
+  const int32_t* n_nodes;     // [B]
+  const int32_t* token;       // [R] token id (0 for absent nodes)
+  const int32_t* pos;         // [R] rotary position prefix_len + depth
+  const int32_t* parent;      // [R]
+  const int32_t* depth;       // [R]
+  const uint64_t* anc;        // [R] ancestor-or-self bitmask over node ids
+};
+
+// GEMM with a bf16 activation operand X [rows][K] and a bf16 weight W [N][K]
+// (out = X W^T), fp32 accumulation.  See gemm.hip for the tiling.
+enum GemmEpilogue : int {
+  EPI_STORE = 0,    // fp32 out[s][row][n] (s = K-split index)
+  EPI_SWIGLU = 1,   // bf16 out[row][n] = silu(gate) * up; W rows: gate [0,N), up [N,2N)
+  EPI_ARGMAX = 2,   // per (row, 32-column tile) max/argmax/NaN count; optional fp32 logits
+};
+
+struct GemmArgs {
+  const uint16_t* X;         // activations, bf16
+  int ldx;                   // row stride of X (elements)
+  const int32_t* gather;     // optional [E][cap] X row of each (expert, tile row); NULL = identity
+  const int32_t* count;      // optional [E] valid rows per expert; NULL = m_tiles*64
+  int cap;                   // rows per expert in gather space
+  int x_erows;               // without gather: X row = e * x_erows + tile row
+  int o_erows;               // output row = e * o_erows + tile row
+  const uint16_t* W;         // weights, bf16 [N or 2N][K] (+ e * w_estride)
+  long long w_estride;       // elements between experts' weights
+  int N, K;
+  int m_tiles;               // 64-row tiles
+  int splits;                // K split across workgroups (EPI_STORE only)
+  // EPI_STORE
+  float* out;                // [splits][out_rows][ldo]
+  long long out_split_stride;
+  int ldo;
+  // EPI_SWIGLU
+  uint16_t* act;             // bf16 [rows][lda]
+  int lda;
+  // EPI_ARGMAX
+  float* pmax;               // [rows][ld_part]
+  int32_t* pidx;
+  int32_t* pnan;
+  int ld_part;
+  float* logits;             // optional fp32 [rows][ld_logits], rows < logit_rows
+  long long ld_logits;
+  int logit_rows;
+};
+
+// Residual update folded into the normalisation kernel:
+// x[r] += sum_s parts[s][r]           (dense, K-split partial sums), or
+// x[r] += sum_k w[r][k] * parts[slot[r][k]]   (MoE expert outputs)
+struct ResidualAdd {
+  const float* parts;
+  int n_parts;
+  long long part_stride;     // elements between splits
+  const int32_t* slot;       // MoE: [rows][top_k] slot of each kept expert output, NULL for dense
+  const float* slot_w;       // MoE: [rows][top_k] renormalised router weights
+  int top_k;
+};
+
+struct AttnArgs {
+  const uint16_t* q;         // bf16 [R][Hq][dh]
+  const uint16_t* k_cache;   // this layer: [max_batch][Hkv][cap][dh]
+  const uint16_t* v_cache;   // this layer: [max_batch][Hkv][dh][cap]
+  float* part_o;             // [B][Hq][S][qrows][dh]
+  float* part_ml;            // [B][Hq][S][qrows][2]
+  StepMeta meta;
+  int Hq, Hkv, dh, kv_cap, max_tree, qblocks, splits;
+  float scale_log2;          // log2(e) / sqrt(dh)
+};
+
+// launchers (return hipGetLastError())
+hipError_t launch_gemm(int epi, int nb, int kw, const GemmArgs& a, int experts, hipStream_t s);
+hipError_t launch_embed(const uint16_t* embed, const int32_t* token, int rows, int d, float* x, hipStream_t s);
+hipError_t launch_residual_rmsnorm(float* x, const ResidualAdd& add, const uint16_t* gain, float eps,
+                                   int rows, int d, uint16_t* xn, hipStream_t s);
+hipError_t launch_qkv_rope(const float* qkv_parts, int n_parts, long long part_stride, StepMeta meta,
+                           const float* rope_cos, const float* rope_sin, int Hq, int Hkv, int dh,
+                           int max_tree, int batch, int kv_cap, uint16_t* q_out, uint16_t* k_cache_l,
+                           uint16_t* v_cache_l, hipStream_t s);
+hipError_t launch_attention(const AttnArgs& a, int batch, hipStream_t s);
+hipError_t launch_attn_combine(const float* part_o, const float* part_ml, StepMeta meta, int Hq, int dh,
+                               int splits, int qrows, int max_tree, int batch, uint16_t* o_out,
+                               hipStream_t s);
+hipError_t launch_argmax_reduce(const float* pmax, const int32_t* pidx, const int32_t* pnan, int n_tiles,
+                                int ld_part, int rows, int32_t* pred, int32_t* nan_row, hipStream_t s);
+hipError_t launch_accept(StepMeta meta, const int32_t* pred, const int32_t* nan_row, int batch,
+                         int max_tree, int max_depth, int32_t* result, hipStream_t s);
+hipError_t launch_moe_route(const float* x, const uint16_t* gain, float eps, const uint16_t* w_router,
+                            int rows, int d, int n_experts, int top_k, const int32_t* n_nodes,
+                            int max_tree, int32_t* route_ids, float* route_w, hipStream_t s);
+hipError_t launch_moe_lists(const int32_t* route_ids, int rows, const int32_t* n_nodes, int max_tree,
+                            int n_experts, int top_k, int cap, int32_t* gather, int32_t* count,
+                            int32_t* slot, hipStream_t s);
+
+// Result block written by the acceptance kernel, per sequence b:
+// [0] accept_len, [1] nan flag, [2 .. 2+max_depth] tokens_out (max_depth+1),
+// [3+max_depth .. 3+2*max_depth) path.
+__host__ __device__ inline int result_stride(int max_depth) { return 3 + 2 * max_depth; }
+
+}  // namespace griffin

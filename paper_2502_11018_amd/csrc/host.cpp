@@ -1,0 +1,770 @@
+// Host side of the C ABI declared in include/griffin_verify.h: argument and
+// tree validation, per-step metadata, workspace ownership and the launch
+// sequence of one verification pass.
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "griffin_internal.h"
+#include "griffin_verify.h"
+
+using namespace griffin;
+
+namespace {
+
+constexpr int kMaxTree = 64;
+
+int round_up(int x, int m) { return (x + m - 1) / m * m; }
+int cdiv(int x, int m) { return (x + m - 1) / m; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Validate one tree and, optionally, fill depth / position / ancestor masks.
+int prepare_tree(int32_t n, const int32_t* tokens, const int32_t* parents, int32_t prefix_len, int32_t max_tree,
+                 int32_t max_depth, int32_t vocab, int32_t kv_capacity, int32_t* depth, int32_t* pos,
+                 uint64_t* anc, std::string* why) {
+  auto fail = [&](int code, const char* fmt, long a = 0, long b = 0) {
+    if (why) {
+      char buf[256];
+      snprintf(buf, sizeof buf, fmt, a, b);
+      *why = buf;
+    }
+    return code;
+  };
+  if (!tokens || !parents) return fail(GRIFFIN_EINVAL, "null tree array");
+  if (n < 1 || n > max_tree || n > kMaxTree) return fail(GRIFFIN_ETREE, "tree size %ld outside [1, %ld]", n, max_tree);
+  if (prefix_len < 0 || (long)prefix_len + n > kv_capacity)
+    return fail(GRIFFIN_ECAPACITY, "prefix_len %ld + nodes %ld exceeds kv_capacity", prefix_len, n);
+  if (parents[0] != -1) return fail(GRIFFIN_ETREE, "parents[0] = %ld, must be -1", parents[0]);
+  int32_t dep[kMaxTree];
+  uint64_t an[kMaxTree];
+  dep[0] = 0;
+  an[0] = 1ull;
+  for (int i = 0; i < n; ++i) {
+    if (tokens[i] < 0 || tokens[i] >= vocab) return fail(GRIFFIN_ETOKEN, "token %ld of node %ld out of range", tokens[i], i);
+    if (i == 0) continue;
+    const int p = parents[i];
+    if (p < 0 || p >= i) return fail(GRIFFIN_ETREE, "parent %ld of node %ld not in [0, i)", p, i);
+    dep[i] = dep[p] + 1;
+    if (dep[i] > max_depth) return fail(GRIFFIN_ETREE, "node %ld has depth %ld > max_depth", i, dep[i]);
+    an[i] = an[p] | (1ull << i);
+  }
+  for (int i = 0; i < n; ++i) {
+    if (depth) depth[i] = dep[i];
+    if (pos) pos[i] = prefix_len + dep[i];
+    if (anc) anc[i] = an[i];
+  }
+  return GRIFFIN_OK;
+}
+
+int validate_desc(const griffin_model_desc* d, std::string* why) {
+  auto bad = [&](const char* m) {
+    if (why) *why = m;
+    return GRIFFIN_ESHAPE;
+  };
+  if (d->n_layers < 1 || d->d_model < 8 || d->vocab < 2 || d->d_ff < 8) return bad("non-positive dimension");
+  if (d->head_dim != 64 && d->head_dim != 128) return bad("head_dim must be 64 or 128");
+  if (d->n_kv_heads < 1 || d->n_q_heads < 1 || d->n_q_heads % d->n_kv_heads) return bad("n_q_heads must be a multiple of n_kv_heads");
+  if (d->d_model % 8 || d->d_ff % 8 || (d->n_q_heads * d->head_dim) % 8) return bad("d_model, d_ff, n_q_heads*head_dim must be multiples of 8");
+  if (d->d_model > 8192) return bad("d_model above 8192");
+  if (d->n_experts < 1 || d->n_experts > 64) return bad("n_experts must be in [1, 64]");
+  if (d->n_experts > 1 && (d->top_k < 1 || d->top_k > 4 || d->top_k > d->n_experts)) return bad("top_k must be in [1, min(n_experts, 4)]");
+  if (d->max_batch < 1) return bad("max_batch < 1");
+  if (d->max_tree < 1 || d->max_tree > kMaxTree) return bad("max_tree must be in [1, 64]");
+  if (d->max_depth < 0 || d->max_depth >= d->max_tree) return bad("max_depth must be in [0, max_tree - 1]");
+  if (d->kv_capacity < 32 || d->kv_capacity % 32) return bad("kv_capacity must be a positive multiple of 32");
+  if (!(d->rms_eps > 0.f) || !(d->rope_base > 1.0)) return bad("rms_eps must be > 0 and rope_base > 1");
+  return GRIFFIN_OK;
+}
+
+}  // namespace
+
+struct griffin_ctx {
+  griffin_model_desc d{};
+  const uint16_t *embed = nullptr, *lm_head = nullptr, *final_norm = nullptr;
+  std::vector<const uint16_t*> attn_norm, w_qkv, w_o, mlp_norm, w_gu, w_down, w_router;
+  uint16_t *k_cache = nullptr, *v_cache = nullptr;
+  hipStream_t stream = nullptr;
+
+  int R = 0, Mpad = 0, qkv_n = 0, attn_w = 0, lm_tiles = 0, attn_splits = 1, qblocks = 1;
+  int E = 1, topk = 1;
+  long long parts_elems = 0;
+
+  std::vector<void*> allocs;
+  float *x = nullptr, *parts = nullptr, *attn_po = nullptr, *attn_pml = nullptr;
+  float *rope_cos = nullptr, *rope_sin = nullptr, *pmax = nullptr, *route_w = nullptr, *yslots = nullptr;
+  uint16_t *xn = nullptr, *q = nullptr, *o = nullptr, *act = nullptr;
+  int32_t *pidx = nullptr, *pnan = nullptr, *pred = nullptr, *nan_row = nullptr, *result = nullptr;
+  int32_t *route_ids = nullptr, *gather = nullptr, *count = nullptr, *slot = nullptr;
+
+  // metadata: one device buffer, double-buffered pinned staging
+  char* meta_dev = nullptr;
+  char* meta_host[2] = {nullptr, nullptr};
+  hipEvent_t meta_ev[2] = {nullptr, nullptr};
+  size_t meta_bytes = 0;
+  size_t off_prefix = 0, off_nodes = 0, off_token = 0, off_pos = 0, off_parent = 0, off_depth = 0, off_anc = 0;
+  int meta_cur = 0;
+  StepMeta meta{};
+
+  int32_t* result_host = nullptr;
+  int32_t* pred_host = nullptr;
+  // per-class launch timing (griffin_profile_*)
+  uint32_t prof_mask = 0;
+  std::vector<hipEvent_t> prof_ev;     // pairs: start, stop
+  std::vector<int> prof_cls;           // class of each pair
+  size_t prof_used = 0;                // pairs recorded since the last read
+  int batch = 0;
+  bool stepped = false;
+  std::string err;
+};
+
+namespace {
+
+int set_err(griffin_ctx* c, int code, const std::string& msg) {
+  if (c) c->err = msg;
+  return code;
+}
+
+int hip_err(griffin_ctx* c, const char* what, hipError_t e) {
+  return set_err(c, GRIFFIN_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define HIP_TRY(ctx, call)                                          \
+  do {                                                              \
+    hipError_t e_ = (call);                                         \
+    if (e_ != hipSuccess) return hip_err((ctx), #call, e_);         \
+  } while (0)
+
+template <typename T>
+int dev_alloc(griffin_ctx* c, T** p, size_t count) {
+  void* raw = nullptr;
+  const size_t bytes = std::max<size_t>(count * sizeof(T), 256);
+  hipError_t e = hipMalloc(&raw, bytes);
+  if (e != hipSuccess) return set_err(c, GRIFFIN_ENOMEM, std::string("hipMalloc: ") + hipGetErrorString(e));
+  c->allocs.push_back(raw);
+  e = hipMemset(raw, 0, bytes);
+  if (e != hipSuccess) return hip_err(c, "hipMemset", e);
+  *p = static_cast<T*>(raw);
+  return GRIFFIN_OK;
+}
+
+#define TRY(expr)                   \
+  do {                              \
+    int rc_ = (expr);               \
+    if (rc_ != GRIFFIN_OK) return rc_; \
+  } while (0)
+
+// K-split count for a streaming GEMM: aim at ~512 workgroups, keep >= 4
+// 64-wide K steps per wave.
+int choose_splits(int tiles, int K, int kw) {
+  const int steps = cdiv(K, 64);
+  const int max_split = std::max(1, steps / (kw * 4));
+  return std::max(1, std::min(cdiv(512, tiles), max_split));
+}
+
+struct Plan {
+  int qkv_splits, o_splits, down_splits;
+};
+
+Plan make_plan(const griffin_ctx* c, int m_tiles) {
+  Plan p{};
+  p.qkv_splits = choose_splits(cdiv(c->qkv_n, 32) * m_tiles, c->d.d_model, 4);
+  p.o_splits = choose_splits(cdiv(c->d.d_model, 32) * m_tiles, c->attn_w, 4);
+  p.down_splits = choose_splits(cdiv(c->d.d_model, 32) * m_tiles, c->d.d_ff, 4);
+  return p;
+}
+
+GemmArgs gemm_base(const uint16_t* X, int ldx, const uint16_t* W, int N, int K, int m_tiles) {
+  GemmArgs a{};
+  a.X = X;
+  a.ldx = ldx;
+  a.W = W;
+  a.N = N;
+  a.K = K;
+  a.m_tiles = m_tiles;
+  a.splits = 1;
+  return a;
+}
+
+// Event pair for one timed launch (grown on demand, reused after each read).
+int prof_pair(griffin_ctx* c, int cls, hipEvent_t* a, hipEvent_t* b) {
+  if (c->prof_used * 2 + 2 > c->prof_ev.size()) {
+    for (int k = 0; k < 2; ++k) {
+      hipEvent_t e;
+      HIP_TRY(c, hipEventCreate(&e));
+      c->prof_ev.push_back(e);
+    }
+    c->prof_cls.push_back(0);
+  }
+  c->prof_cls[c->prof_used] = cls;
+  *a = c->prof_ev[2 * c->prof_used];
+  *b = c->prof_ev[2 * c->prof_used + 1];
+  ++c->prof_used;
+  return GRIFFIN_OK;
+}
+
+#define LAUNCH(cls, call)                                                   \
+  do {                                                                      \
+    hipEvent_t ev0_ = nullptr, ev1_ = nullptr;                              \
+    const bool prof_ = (c->prof_mask >> (cls)) & 1u;                        \
+    if (prof_) {                                                            \
+      TRY(prof_pair(c, (cls), &ev0_, &ev1_));                               \
+      HIP_TRY(c, hipEventRecord(ev0_, c->stream));                          \
+    }                                                                       \
+    HIP_TRY(c, call);                                                       \
+    if (prof_) HIP_TRY(c, hipEventRecord(ev1_, c->stream));                 \
+  } while (0)
+
+int enqueue_pass(griffin_ctx* c, float* logits_out) {
+  const griffin_model_desc& d = c->d;
+  const int B = c->batch;
+  const int rows = B * d.max_tree;
+  const int Mpad = round_up(rows, 64);
+  const int m_tiles = Mpad / 64;
+  const Plan plan = make_plan(c, m_tiles);
+  const long long ps = (long long)Mpad;  // rows per split slice of `parts`
+  hipStream_t s = c->stream;
+  const size_t layer_kv = (size_t)d.max_batch * d.n_kv_heads * d.kv_capacity * d.head_dim;
+
+  LAUNCH(GRIFFIN_KC_NORM, launch_embed(c->embed, c->meta.token, Mpad, d.d_model, c->x, s));
+  ResidualAdd none{};
+  ResidualAdd add_down{};
+  for (int l = 0; l < d.n_layers; ++l) {
+    // ---- attention block
+    LAUNCH(GRIFFIN_KC_NORM, launch_residual_rmsnorm(c->x, l == 0 ? none : add_down, c->attn_norm[l], d.rms_eps, Mpad,
+                                       d.d_model, c->xn, s));
+    {
+      GemmArgs a = gemm_base(c->xn, d.d_model, c->w_qkv[l], c->qkv_n, d.d_model, m_tiles);
+      a.splits = plan.qkv_splits;
+      a.out = c->parts;
+      a.ldo = c->qkv_n;
+      a.out_split_stride = ps * c->qkv_n;
+      LAUNCH(GRIFFIN_KC_QKV, launch_gemm(EPI_STORE, 1, 4, a, 1, s));
+    }
+    uint16_t* kc = c->k_cache + (size_t)l * layer_kv;
+    uint16_t* vc = c->v_cache + (size_t)l * layer_kv;
+    LAUNCH(GRIFFIN_KC_ROPE, launch_qkv_rope(c->parts, plan.qkv_splits, ps * c->qkv_n, c->meta, c->rope_cos, c->rope_sin,
+                               d.n_q_heads, d.n_kv_heads, d.head_dim, d.max_tree, B, d.kv_capacity, c->q, kc, vc,
+                               s));
+    {
+      AttnArgs a{};
+      a.q = c->q;
+      a.k_cache = kc;
+      a.v_cache = vc;
+      a.part_o = c->attn_po;
+      a.part_ml = c->attn_pml;
+      a.meta = c->meta;
+      a.Hq = d.n_q_heads;
+      a.Hkv = d.n_kv_heads;
+      a.dh = d.head_dim;
+      a.kv_cap = d.kv_capacity;
+      a.max_tree = d.max_tree;
+      a.qblocks = c->qblocks;
+      a.splits = c->attn_splits;
+      a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.head_dim));
+      LAUNCH(GRIFFIN_KC_ATTN, launch_attention(a, B, s));
+    }
+    LAUNCH(GRIFFIN_KC_ATTN, launch_attn_combine(c->attn_po, c->attn_pml, c->meta, d.n_q_heads, d.head_dim, c->attn_splits,
+                                   c->qblocks * 32, d.max_tree, B, c->o, s));
+    {
+      GemmArgs a = gemm_base(c->o, c->attn_w, c->w_o[l], d.d_model, c->attn_w, m_tiles);
+      a.splits = plan.o_splits;
+      a.out = c->parts;
+      a.ldo = d.d_model;
+      a.out_split_stride = ps * d.d_model;
+      LAUNCH(GRIFFIN_KC_O, launch_gemm(EPI_STORE, 1, 4, a, 1, s));
+    }
+    ResidualAdd add_o{};
+    add_o.parts = c->parts;
+    add_o.n_parts = plan.o_splits;
+    add_o.part_stride = ps * d.d_model;
+    LAUNCH(GRIFFIN_KC_NORM, launch_residual_rmsnorm(c->x, add_o, c->mlp_norm[l], d.rms_eps, Mpad, d.d_model, c->xn, s));
+
+    // ---- MLP block
+    if (c->E == 1) {
+      GemmArgs g = gemm_base(c->xn, d.d_model, c->w_gu[l], d.d_ff, d.d_model, m_tiles);
+      g.act = c->act;
+      g.lda = d.d_ff;
+      LAUNCH(GRIFFIN_KC_GATE_UP, launch_gemm(EPI_SWIGLU, 2, 4, g, 1, s));
+      GemmArgs dn = gemm_base(c->act, d.d_ff, c->w_down[l], d.d_model, d.d_ff, m_tiles);
+      dn.splits = plan.down_splits;
+      dn.out = c->parts;
+      dn.ldo = d.d_model;
+      dn.out_split_stride = ps * d.d_model;
+      LAUNCH(GRIFFIN_KC_DOWN, launch_gemm(EPI_STORE, 1, 4, dn, 1, s));
+      add_down = ResidualAdd{};
+      add_down.parts = c->parts;
+      add_down.n_parts = plan.down_splits;
+      add_down.part_stride = ps * d.d_model;
+    } else {
+      LAUNCH(GRIFFIN_KC_OTHER, launch_moe_route(c->x, c->mlp_norm[l], d.rms_eps, c->w_router[l], rows, d.d_model, c->E, c->topk,
+                                  c->meta.n_nodes, d.max_tree, c->route_ids, c->route_w, s));
+      LAUNCH(GRIFFIN_KC_OTHER, launch_moe_lists(c->route_ids, rows, c->meta.n_nodes, d.max_tree, c->E, c->topk, Mpad, c->gather,
+                                  c->count, c->slot, s));
+      GemmArgs g = gemm_base(c->xn, d.d_model, c->w_gu[l], d.d_ff, d.d_model, m_tiles);
+      g.gather = c->gather;
+      g.count = c->count;
+      g.cap = Mpad;
+      g.o_erows = Mpad;
+      g.w_estride = 2LL * d.d_ff * d.d_model;
+      g.act = c->act;
+      g.lda = d.d_ff;
+      LAUNCH(GRIFFIN_KC_GATE_UP, launch_gemm(EPI_SWIGLU, 2, 4, g, c->E, s));
+      GemmArgs dn = gemm_base(c->act, d.d_ff, c->w_down[l], d.d_model, d.d_ff, m_tiles);
+      dn.count = c->count;
+      dn.cap = Mpad;
+      dn.x_erows = Mpad;
+      dn.o_erows = Mpad;
+      dn.w_estride = (long long)d.d_model * d.d_ff;
+      dn.out = c->yslots;
+      dn.ldo = d.d_model;
+      LAUNCH(GRIFFIN_KC_DOWN, launch_gemm(EPI_STORE, 1, 4, dn, c->E, s));
+      add_down = ResidualAdd{};
+      add_down.parts = c->yslots;
+      add_down.slot = c->slot;
+      add_down.slot_w = c->route_w;
+      add_down.top_k = c->topk;
+      add_down.n_parts = 1;
+    }
+  }
+  // ---- final norm, LM head with fused per-tile argmax, reduction, acceptance
+  LAUNCH(GRIFFIN_KC_NORM, launch_residual_rmsnorm(c->x, add_down, c->final_norm, d.rms_eps, Mpad, d.d_model, c->xn, s));
+  {
+    GemmArgs a = gemm_base(c->xn, d.d_model, c->lm_head, d.vocab, d.d_model, m_tiles);
+    a.pmax = c->pmax;
+    a.pidx = c->pidx;
+    a.pnan = c->pnan;
+    a.ld_part = c->lm_tiles;
+    a.logits = logits_out;
+    a.ld_logits = d.vocab;
+    a.logit_rows = rows;
+    LAUNCH(GRIFFIN_KC_LM_HEAD, launch_gemm(EPI_ARGMAX, 1, 4, a, 1, s));
+  }
+  LAUNCH(GRIFFIN_KC_OTHER, launch_argmax_reduce(c->pmax, c->pidx, c->pnan, c->lm_tiles, c->lm_tiles, rows, c->pred, c->nan_row, s));
+  LAUNCH(GRIFFIN_KC_OTHER, launch_accept(c->meta, c->pred, c->nan_row, B, d.max_tree, d.max_depth, c->result, s));
+  return GRIFFIN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t griffin_kv_cache_bytes(const griffin_model_desc* d) {
+  if (!d) return 0;
+  return (size_t)d->n_layers * d->max_batch * d->n_kv_heads * d->kv_capacity * d->head_dim * 2;
+}
+
+const char* griffin_status_str(int code) {
+  switch (code) {
+    case GRIFFIN_OK: return "ok";
+    case GRIFFIN_EINVAL: return "invalid argument";
+    case GRIFFIN_ESHAPE: return "unsupported model shape";
+    case GRIFFIN_ETREE: return "malformed draft tree";
+    case GRIFFIN_ETOKEN: return "token id out of range";
+    case GRIFFIN_ECAPACITY: return "KV cache capacity exceeded";
+    case GRIFFIN_EORDER: return "accept called before any step";
+    case GRIFFIN_ENOMEM: return "out of memory";
+    case GRIFFIN_EHIP: return "HIP runtime error";
+    case GRIFFIN_ENUMERIC: return "NaN in logits";
+    default: return "unknown status";
+  }
+}
+
+const char* griffin_last_error(const griffin_ctx* ctx) { return ctx ? ctx->err.c_str() : ""; }
+
+int griffin_tree_prepare(int32_t n, const int32_t* tokens, const int32_t* parents, int32_t prefix_len,
+                         int32_t max_tree, int32_t max_depth, int32_t vocab, int32_t kv_capacity, int32_t* depth,
+                         int32_t* pos, uint64_t* anc) {
+  if (max_tree < 1 || max_tree > kMaxTree || vocab < 1 || max_depth < 0) return GRIFFIN_EINVAL;
+  return prepare_tree(n, tokens, parents, prefix_len, max_tree, max_depth, vocab, kv_capacity, depth, pos, anc,
+                      nullptr);
+}
+
+void griffin_verify_free(griffin_ctx* c) {
+  if (!c) return;
+  hipStreamSynchronize(c->stream);
+  for (void* p : c->allocs) hipFree(p);
+  for (int k = 0; k < 2; ++k) {
+    if (c->meta_host[k]) hipHostFree(c->meta_host[k]);
+    if (c->meta_ev[k]) hipEventDestroy(c->meta_ev[k]);
+  }
+  for (hipEvent_t e : c->prof_ev) hipEventDestroy(e);
+  if (c->result_host) hipHostFree(c->result_host);
+  if (c->pred_host) hipHostFree(c->pred_host);
+  delete c;
+}
+
+int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w, void* k_cache, void* v_cache,
+                        void* hip_stream, griffin_ctx** out) {
+  if (!out) return GRIFFIN_EINVAL;
+  *out = nullptr;
+  if (!desc || !w || !k_cache || !v_cache) return GRIFFIN_EINVAL;
+  std::string why;
+  int rc = validate_desc(desc, &why);
+  if (rc != GRIFFIN_OK) return rc;
+  const griffin_model_desc& d = *desc;
+  const bool moe = d.n_experts > 1;
+  if (!w->embed || !w->lm_head || !w->final_norm || !w->attn_norm || !w->w_qkv || !w->w_o || !w->mlp_norm ||
+      !w->w_gate_up || !w->w_down || (moe && !w->w_router))
+    return GRIFFIN_EINVAL;
+  if (!aligned16(w->embed) || !aligned16(w->lm_head) || !aligned16(k_cache) || !aligned16(v_cache))
+    return GRIFFIN_EINVAL;
+  for (int l = 0; l < d.n_layers; ++l) {
+    const void* ps[] = {w->attn_norm[l], w->w_qkv[l], w->w_o[l], w->mlp_norm[l], w->w_gate_up[l], w->w_down[l],
+                        moe ? w->w_router[l] : w->w_qkv[l]};
+    for (const void* p : ps)
+      if (!p || !aligned16(p)) return GRIFFIN_EINVAL;
+  }
+
+  griffin_ctx* c = new (std::nothrow) griffin_ctx();
+  if (!c) return GRIFFIN_ENOMEM;
+  c->d = d;
+  c->embed = static_cast<const uint16_t*>(w->embed);
+  c->lm_head = static_cast<const uint16_t*>(w->lm_head);
+  c->final_norm = static_cast<const uint16_t*>(w->final_norm);
+  for (int l = 0; l < d.n_layers; ++l) {
+    c->attn_norm.push_back(static_cast<const uint16_t*>(w->attn_norm[l]));
+    c->w_qkv.push_back(static_cast<const uint16_t*>(w->w_qkv[l]));
+    c->w_o.push_back(static_cast<const uint16_t*>(w->w_o[l]));
+    c->mlp_norm.push_back(static_cast<const uint16_t*>(w->mlp_norm[l]));
+    c->w_gu.push_back(static_cast<const uint16_t*>(w->w_gate_up[l]));
+    c->w_down.push_back(static_cast<const uint16_t*>(w->w_down[l]));
+    c->w_router.push_back(moe ? static_cast<const uint16_t*>(w->w_router[l]) : nullptr);
+  }
+  c->k_cache = static_cast<uint16_t*>(k_cache);
+  c->v_cache = static_cast<uint16_t*>(v_cache);
+  c->stream = static_cast<hipStream_t>(hip_stream);
+  c->E = moe ? d.n_experts : 1;
+  c->topk = moe ? d.top_k : 1;
+
+  c->R = d.max_batch * d.max_tree;
+  c->Mpad = round_up(c->R, 64);
+  c->qkv_n = (d.n_q_heads + 2 * d.n_kv_heads) * d.head_dim;
+  c->attn_w = d.n_q_heads * d.head_dim;
+  c->lm_tiles = cdiv(d.vocab, 32);
+  c->qblocks = cdiv(d.max_tree, 32);
+  {
+    const int by_len = cdiv(d.kv_capacity, 256);
+    const int by_par = std::max(1, cdiv(2048, d.max_batch * d.n_q_heads * c->qblocks));
+    c->attn_splits = std::max(1, std::min(std::min(by_len, by_par), 64));
+  }
+  const long long Mp = c->Mpad;
+  // the split plan depends on the batch of each step: size for the largest
+  for (int mt = 1; mt <= c->Mpad / 64; ++mt) {
+    const Plan plan = make_plan(c, mt);
+    c->parts_elems = std::max(c->parts_elems,
+                              64LL * mt * std::max({(long long)plan.qkv_splits * c->qkv_n,
+                                                    (long long)plan.o_splits * d.d_model,
+                                                    (long long)plan.down_splits * d.d_model}));
+  }
+  const int qrows = c->qblocks * 32;
+
+#define ALLOC(ptr, n)                          \
+  do {                                         \
+    int rc_ = dev_alloc(c, &(ptr), (size_t)(n)); \
+    if (rc_ != GRIFFIN_OK) {                   \
+      griffin_verify_free(c);                  \
+      return rc_;                              \
+    }                                          \
+  } while (0)
+
+  ALLOC(c->x, Mp * d.d_model);
+  ALLOC(c->xn, Mp * d.d_model);
+  ALLOC(c->parts, c->parts_elems);
+  ALLOC(c->q, Mp * c->attn_w);
+  ALLOC(c->o, Mp * c->attn_w);
+  ALLOC(c->attn_po, (long long)d.max_batch * d.n_q_heads * c->attn_splits * qrows * d.head_dim);
+  ALLOC(c->attn_pml, (long long)d.max_batch * d.n_q_heads * c->attn_splits * qrows * 2);
+  ALLOC(c->act, (long long)c->E * Mp * d.d_ff);
+  ALLOC(c->pmax, Mp * c->lm_tiles);
+  ALLOC(c->pidx, Mp * c->lm_tiles);
+  ALLOC(c->pnan, Mp * c->lm_tiles);
+  ALLOC(c->pred, Mp);
+  ALLOC(c->nan_row, Mp);
+  ALLOC(c->result, (long long)d.max_batch * result_stride(d.max_depth));
+  ALLOC(c->rope_cos, (long long)d.kv_capacity * (d.head_dim / 2));
+  ALLOC(c->rope_sin, (long long)d.kv_capacity * (d.head_dim / 2));
+  if (moe) {
+    ALLOC(c->route_ids, Mp * c->topk);
+    ALLOC(c->route_w, Mp * c->topk);
+    ALLOC(c->gather, (long long)c->E * Mp);
+    ALLOC(c->count, c->E);
+    ALLOC(c->slot, Mp * c->topk);
+    ALLOC(c->yslots, (long long)c->E * Mp * d.d_model);
+  }
+#undef ALLOC
+
+  // rotary tables: angle pos * base^(-2j/dh) evaluated in double, stored fp32
+  {
+    const int half = d.head_dim / 2;
+    std::vector<float> cs((size_t)d.kv_capacity * half), sn((size_t)d.kv_capacity * half);
+    for (int j = 0; j < half; ++j) {
+      const double inv = std::pow(d.rope_base, -2.0 * j / d.head_dim);
+      for (int p = 0; p < d.kv_capacity; ++p) {
+        const double ang = (double)p * inv;
+        cs[(size_t)p * half + j] = (float)std::cos(ang);
+        sn[(size_t)p * half + j] = (float)std::sin(ang);
+      }
+    }
+    hipError_t e = hipMemcpy(c->rope_cos, cs.data(), cs.size() * sizeof(float), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(c->rope_sin, sn.data(), sn.size() * sizeof(float), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+      griffin_verify_free(c);
+      return GRIFFIN_EHIP;
+    }
+  }
+
+  // metadata layout (8-byte aligned sections)
+  {
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+      const size_t o = off;
+      off += (bytes + 255) / 256 * 256;
+      return o;
+    };
+    c->off_anc = take(sizeof(uint64_t) * Mp);
+    c->off_prefix = take(sizeof(int32_t) * d.max_batch);
+    c->off_nodes = take(sizeof(int32_t) * d.max_batch);
+    c->off_token = take(sizeof(int32_t) * Mp);
+    c->off_pos = take(sizeof(int32_t) * Mp);
+    c->off_parent = take(sizeof(int32_t) * Mp);
+    c->off_depth = take(sizeof(int32_t) * Mp);
+    c->meta_bytes = off;
+    hipError_t e = hipMalloc((void**)&c->meta_dev, c->meta_bytes);
+    if (e != hipSuccess) {
+      griffin_verify_free(c);
+      return GRIFFIN_ENOMEM;
+    }
+    c->allocs.push_back(c->meta_dev);
+    hipMemset(c->meta_dev, 0, c->meta_bytes);
+    for (int k = 0; k < 2; ++k) {
+      if (hipHostMalloc((void**)&c->meta_host[k], c->meta_bytes, hipHostMallocDefault) != hipSuccess ||
+          hipEventCreateWithFlags(&c->meta_ev[k], hipEventDisableTiming) != hipSuccess) {
+        griffin_verify_free(c);
+        return GRIFFIN_ENOMEM;
+      }
+      memset(c->meta_host[k], 0, c->meta_bytes);
+    }
+    c->meta.anc = reinterpret_cast<const uint64_t*>(c->meta_dev + c->off_anc);
+    c->meta.prefix_len = reinterpret_cast<const int32_t*>(c->meta_dev + c->off_prefix);
+    c->meta.n_nodes = reinterpret_cast<const int32_t*>(c->meta_dev + c->off_nodes);
+    c->meta.token = reinterpret_cast<const int32_t*>(c->meta_dev + c->off_token);
+    c->meta.pos = reinterpret_cast<const int32_t*>(c->meta_dev + c->off_pos);
+    c->meta.parent = reinterpret_cast<const int32_t*>(c->meta_dev + c->off_parent);
+    c->meta.depth = reinterpret_cast<const int32_t*>(c->meta_dev + c->off_depth);
+  }
+  if (hipHostMalloc((void**)&c->result_host, sizeof(int32_t) * d.max_batch * result_stride(d.max_depth),
+                    hipHostMallocDefault) != hipSuccess ||
+      hipHostMalloc((void**)&c->pred_host, sizeof(int32_t) * Mp, hipHostMallocDefault) != hipSuccess) {
+    griffin_verify_free(c);
+    return GRIFFIN_ENOMEM;
+  }
+  hipError_t e = hipDeviceSynchronize();
+  if (e != hipSuccess) {
+    griffin_verify_free(c);
+    return GRIFFIN_EHIP;
+  }
+  *out = c;
+  return GRIFFIN_OK;
+}
+
+int griffin_verify_step(griffin_ctx* c, int32_t batch, const int32_t* prefix_len, const int32_t* n_nodes,
+                        const int32_t* tokens, const int32_t* parents, float* logits_out) {
+  if (!c) return GRIFFIN_EINVAL;
+  const griffin_model_desc& d = c->d;
+  if (batch < 1 || batch > d.max_batch || !prefix_len || !n_nodes || !tokens || !parents)
+    return set_err(c, GRIFFIN_EINVAL, "bad batch or null host array");
+  if (logits_out && !aligned16(logits_out)) return set_err(c, GRIFFIN_EINVAL, "logits_out not 16-byte aligned");
+  // validate everything before touching any buffer
+  for (int b = 0; b < batch; ++b) {
+    std::string why;
+    const int rc = prepare_tree(n_nodes[b], tokens + (size_t)b * d.max_tree, parents + (size_t)b * d.max_tree,
+                                prefix_len[b], d.max_tree, d.max_depth, d.vocab, d.kv_capacity, nullptr, nullptr,
+                                nullptr, &why);
+    if (rc != GRIFFIN_OK) return set_err(c, rc, "sequence " + std::to_string(b) + ": " + why);
+  }
+  // fill the staging buffer not used by the previous step's copy
+  const int k = c->meta_cur ^ 1;
+  HIP_TRY(c, hipEventSynchronize(c->meta_ev[k]));
+  char* h = c->meta_host[k];
+  memset(h, 0, c->meta_bytes);
+  auto* h_anc = reinterpret_cast<uint64_t*>(h + c->off_anc);
+  auto* h_prefix = reinterpret_cast<int32_t*>(h + c->off_prefix);
+  auto* h_nodes = reinterpret_cast<int32_t*>(h + c->off_nodes);
+  auto* h_token = reinterpret_cast<int32_t*>(h + c->off_token);
+  auto* h_pos = reinterpret_cast<int32_t*>(h + c->off_pos);
+  auto* h_parent = reinterpret_cast<int32_t*>(h + c->off_parent);
+  auto* h_depth = reinterpret_cast<int32_t*>(h + c->off_depth);
+  for (int b = 0; b < batch; ++b) {
+    const int n = n_nodes[b];
+    const size_t r0 = (size_t)b * d.max_tree;
+    h_prefix[b] = prefix_len[b];
+    h_nodes[b] = n;
+    prepare_tree(n, tokens + r0, parents + r0, prefix_len[b], d.max_tree, d.max_depth, d.vocab, d.kv_capacity,
+                 h_depth + r0, h_pos + r0, h_anc + r0, nullptr);
+    for (int i = 0; i < n; ++i) {
+      h_token[r0 + i] = tokens[r0 + i];
+      h_parent[r0 + i] = i == 0 ? 0 : parents[r0 + i];
+    }
+  }
+  HIP_TRY(c, hipMemcpyAsync(c->meta_dev, h, c->meta_bytes, hipMemcpyHostToDevice, c->stream));
+  HIP_TRY(c, hipEventRecord(c->meta_ev[k], c->stream));
+  c->meta_cur = k;
+  c->batch = batch;
+  c->stepped = false;
+  const int rc = enqueue_pass(c, logits_out);
+  if (rc != GRIFFIN_OK) return rc;
+  c->stepped = true;
+  return GRIFFIN_OK;
+}
+
+int griffin_accept(griffin_ctx* c, int32_t* accept_len, int32_t* tokens_out, int32_t* path_nodes) {
+  if (!c) return GRIFFIN_EINVAL;
+  if (!c->stepped) return set_err(c, GRIFFIN_EORDER, "no verification step has been enqueued");
+  const griffin_model_desc& d = c->d;
+  const int st = result_stride(d.max_depth);
+  HIP_TRY(c, hipMemcpyAsync(c->result_host, c->result, sizeof(int32_t) * c->batch * st, hipMemcpyDeviceToHost,
+                            c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  bool nan = false;
+  for (int b = 0; b < c->batch; ++b) {
+    const int32_t* r = c->result_host + (size_t)b * st;
+    if (accept_len) accept_len[b] = r[0];
+    nan |= r[1] != 0;
+    if (tokens_out) memcpy(tokens_out + (size_t)b * (d.max_depth + 1), r + 2, sizeof(int32_t) * (d.max_depth + 1));
+    if (path_nodes && d.max_depth > 0)
+      memcpy(path_nodes + (size_t)b * d.max_depth, r + 3 + d.max_depth, sizeof(int32_t) * d.max_depth);
+  }
+  if (nan) return set_err(c, GRIFFIN_ENUMERIC, "NaN in the logits of a tree node");
+  return GRIFFIN_OK;
+}
+
+int griffin_read_predictions(griffin_ctx* c, int32_t* pred) {
+  if (!c || !pred) return GRIFFIN_EINVAL;
+  if (!c->stepped) return set_err(c, GRIFFIN_EORDER, "no verification step has been enqueued");
+  const int rows = c->batch * c->d.max_tree;
+  HIP_TRY(c, hipMemcpyAsync(c->pred_host, c->pred, sizeof(int32_t) * rows, hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  const int32_t* nodes = reinterpret_cast<const int32_t*>(c->meta_host[c->meta_cur] + c->off_nodes);
+  for (int r = 0; r < rows; ++r) {
+    const int b = r / c->d.max_tree, i = r % c->d.max_tree;
+    pred[r] = i < nodes[b] ? c->pred_host[r] : -1;
+  }
+  return GRIFFIN_OK;
+}
+
+int griffin_profile_enable(griffin_ctx* c, uint32_t class_mask) {
+  if (!c) return GRIFFIN_EINVAL;
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  c->prof_mask = class_mask & ((1u << GRIFFIN_KC_COUNT) - 1);
+  c->prof_used = 0;
+  return GRIFFIN_OK;
+}
+
+int griffin_profile_read(griffin_ctx* c, double* ms, int64_t* launches) {
+  if (!c || !ms || !launches) return GRIFFIN_EINVAL;
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  for (int k = 0; k < GRIFFIN_KC_COUNT; ++k) {
+    ms[k] = 0.0;
+    launches[k] = 0;
+  }
+  for (size_t i = 0; i < c->prof_used; ++i) {
+    float t = 0.f;
+    HIP_TRY(c, hipEventElapsedTime(&t, c->prof_ev[2 * i], c->prof_ev[2 * i + 1]));
+    ms[c->prof_cls[i]] += t;
+    launches[c->prof_cls[i]] += 1;
+  }
+  c->prof_used = 0;
+  return GRIFFIN_OK;
+}
+
+int griffin_accept_walk(void* hip_stream, int32_t batch, int32_t max_tree, int32_t max_depth, int32_t vocab,
+                        const int32_t* n_nodes, const int32_t* tokens, const int32_t* parents, const int32_t* pred,
+                        int32_t* accept_len, int32_t* tokens_out, int32_t* path_nodes) {
+  if (batch < 1 || max_tree < 1 || max_tree > kMaxTree || max_depth < 0 || max_depth >= max_tree || vocab < 1 ||
+      !n_nodes || !tokens || !parents || !pred)
+    return GRIFFIN_EINVAL;
+  const int rows = batch * max_tree;
+  std::vector<uint64_t> anc(rows, 0);
+  std::vector<int32_t> tok(rows, 0), par(rows, 0), dep(rows, 0), pos(rows, 0), nodes(batch), zero(batch, 0);
+  for (int b = 0; b < batch; ++b) {
+    const size_t r0 = (size_t)b * max_tree;
+    const int rc = prepare_tree(n_nodes[b], tokens + r0, parents + r0, 0, max_tree, max_depth, vocab,
+                                1 << 30, dep.data() + r0, pos.data() + r0, anc.data() + r0, nullptr);
+    if (rc != GRIFFIN_OK) return rc;
+    nodes[b] = n_nodes[b];
+    for (int i = 0; i < n_nodes[b]; ++i) {
+      tok[r0 + i] = tokens[r0 + i];
+      par[r0 + i] = i == 0 ? 0 : parents[r0 + i];
+      if (pred[r0 + i] < 0 || pred[r0 + i] >= vocab) return GRIFFIN_ETOKEN;
+    }
+  }
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  const int st = result_stride(max_depth);
+  char* dev = nullptr;
+  const size_t n_anc = sizeof(uint64_t) * rows, n_int = sizeof(int32_t) * rows;
+  const size_t total = n_anc + 6 * n_int + sizeof(int32_t) * 2 * batch + sizeof(int32_t) * batch * st + 1024;
+  if (hipMalloc((void**)&dev, total) != hipSuccess) return GRIFFIN_ENOMEM;
+  char* p = dev;
+  auto carve = [&](size_t bytes) {
+    char* q = p;
+    p += (bytes + 255) / 256 * 256;
+    return q;
+  };
+  StepMeta m{};
+  uint64_t* d_anc = reinterpret_cast<uint64_t*>(carve(n_anc));
+  int32_t* d_tok = reinterpret_cast<int32_t*>(carve(n_int));
+  int32_t* d_par = reinterpret_cast<int32_t*>(carve(n_int));
+  int32_t* d_dep = reinterpret_cast<int32_t*>(carve(n_int));
+  int32_t* d_pred = reinterpret_cast<int32_t*>(carve(n_int));
+  int32_t* d_nan = reinterpret_cast<int32_t*>(carve(n_int));
+  int32_t* d_nodes = reinterpret_cast<int32_t*>(carve(sizeof(int32_t) * batch));
+  int32_t* d_res = reinterpret_cast<int32_t*>(carve(sizeof(int32_t) * batch * st));
+  int rc = GRIFFIN_OK;
+  std::vector<int32_t> res((size_t)batch * st);
+  hipError_t e = hipSuccess;
+  if (p > dev + total) {
+    rc = GRIFFIN_ENOMEM;
+    goto done;
+  }
+  m.anc = d_anc;
+  m.token = d_tok;
+  m.parent = d_par;
+  m.depth = d_dep;
+  m.n_nodes = d_nodes;
+  m.pos = d_dep;
+  m.prefix_len = d_nodes;
+  if ((e = hipMemcpyAsync(d_anc, anc.data(), n_anc, hipMemcpyHostToDevice, s)) != hipSuccess ||
+      (e = hipMemcpyAsync(d_tok, tok.data(), n_int, hipMemcpyHostToDevice, s)) != hipSuccess ||
+      (e = hipMemcpyAsync(d_par, par.data(), n_int, hipMemcpyHostToDevice, s)) != hipSuccess ||
+      (e = hipMemcpyAsync(d_dep, dep.data(), n_int, hipMemcpyHostToDevice, s)) != hipSuccess ||
+      (e = hipMemcpyAsync(d_pred, pred, n_int, hipMemcpyHostToDevice, s)) != hipSuccess ||
+      (e = hipMemsetAsync(d_nan, 0, n_int, s)) != hipSuccess ||
+      (e = hipMemcpyAsync(d_nodes, nodes.data(), sizeof(int32_t) * batch, hipMemcpyHostToDevice, s)) != hipSuccess ||
+      (e = launch_accept(m, d_pred, d_nan, batch, max_tree, max_depth, d_res, s)) != hipSuccess ||
+      (e = hipMemcpyAsync(res.data(), d_res, sizeof(int32_t) * batch * st, hipMemcpyDeviceToHost, s)) !=
+          hipSuccess ||
+      (e = hipStreamSynchronize(s)) != hipSuccess) {
+    rc = GRIFFIN_EHIP;
+    goto done;
+  }
+  for (int b = 0; b < batch; ++b) {
+    const int32_t* r = res.data() + (size_t)b * st;
+    if (accept_len) accept_len[b] = r[0];
+    if (tokens_out) memcpy(tokens_out + (size_t)b * (max_depth + 1), r + 2, sizeof(int32_t) * (max_depth + 1));
+    if (path_nodes && max_depth > 0)
+      memcpy(path_nodes + (size_t)b * max_depth, r + 3 + max_depth, sizeof(int32_t) * max_depth);
+  }
+done:
+  hipStreamSynchronize(s);
+  hipFree(dev);
+  return rc;
+}
+
+}  // extern "C"

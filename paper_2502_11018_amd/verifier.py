@@ -1,0 +1,213 @@
+"""Python binding of the tree-verification library (argument marshalling only).
+
+Every step of the verify pass runs in the HIP library; PyTorch only owns device
+memory (weights, KV cache, optional logits) and provides the stream.
+"""
+
+from __future__ import annotations
+
+import ctypes
+from ctypes import POINTER, byref, c_int32, c_uint64, c_void_p
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import _native as N
+
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+def _p32(a: np.ndarray):
+    return a.ctypes.data_as(POINTER(c_int32))
+
+
+def _check(rc: int, what: str, ctx=None):
+    if rc != N.GRIFFIN_OK:
+        detail = ""
+        if ctx is not None and ctx.value:
+            detail = N.lib.griffin_last_error(ctx).decode()
+        raise N.GriffinError(rc, what + (f" ({detail})" if detail else ""))
+
+
+@dataclass
+class AcceptResult:
+    length: np.ndarray     # [B] accepted draft tokens L
+    tokens: np.ndarray     # [B, max_depth + 1] L tokens then the target's next token, -1 padded
+    path: np.ndarray       # [B, max_depth] accepted node ids, -1 padded
+    status: int = 0        # GRIFFIN_OK or GRIFFIN_ENUMERIC
+
+    def sequence(self, b: int):
+        L = int(self.length[b])
+        return L, [int(t) for t in self.tokens[b, : L + 1]], [int(n) for n in self.path[b, :L]]
+
+
+def pack_trees(trees: Sequence, max_tree: int):
+    """Lay out trees (objects with .tokens / .parents) as [B][max_tree] arrays."""
+    B = len(trees)
+    tok = np.zeros((B, max_tree), dtype=np.int32)
+    par = np.full((B, max_tree), -1, dtype=np.int32)
+    n = np.zeros(B, dtype=np.int32)
+    for b, t in enumerate(trees):
+        k = len(t.tokens)
+        tok[b, :k] = t.tokens
+        par[b, :k] = t.parents
+        n[b] = k
+    return n, tok, par
+
+
+def tree_prepare(tokens, parents, prefix_len: int, max_tree: int, max_depth: int, vocab: int, kv_capacity: int):
+    """Host-only validation + metadata (depth, position, ancestor masks) of one tree."""
+    tok, par = _i32(tokens), _i32(parents)
+    n = len(tok)
+    depth = np.zeros(max(n, 1), dtype=np.int32)
+    pos = np.zeros(max(n, 1), dtype=np.int32)
+    anc = np.zeros(max(n, 1), dtype=np.uint64)
+    rc = N.lib.griffin_tree_prepare(n, _p32(tok), _p32(par), prefix_len, max_tree, max_depth, vocab, kv_capacity,
+                                    _p32(depth), _p32(pos), anc.ctypes.data_as(POINTER(c_uint64)))
+    return rc, depth[:n], pos[:n], anc[:n]
+
+
+def accept_walk(trees: Sequence, pred: np.ndarray, max_tree: int, max_depth: int, vocab: int,
+                stream: Optional[torch.cuda.Stream] = None) -> AcceptResult:
+    """Device acceptance walk on given per-node predictions pred [B][max_tree]."""
+    n, tok, par = pack_trees(trees, max_tree)
+    B = len(trees)
+    pred = _i32(pred)
+    L = np.zeros(B, dtype=np.int32)
+    out = np.zeros((B, max_depth + 1), dtype=np.int32)
+    path = np.zeros((B, max(max_depth, 1)), dtype=np.int32)
+    s = (stream or torch.cuda.current_stream()).cuda_stream
+    rc = N.lib.griffin_accept_walk(c_void_p(s), B, max_tree, max_depth, vocab, _p32(n), _p32(tok), _p32(par),
+                                   _p32(pred), _p32(L), _p32(out), _p32(path))
+    _check(rc, "griffin_accept_walk")
+    return AcceptResult(L, out, path[:, :max_depth])
+
+
+class TreeVerifier:
+    """One verify context: borrowed weights, a KV cache, and the library's workspace.
+
+    shape: object with n_layers, d_model, n_q_heads, n_kv_heads, head_dim, d_ff,
+           vocab, n_experts, top_k, rms_eps, rope_base.
+    weights: object with embed, lm_head, final_norm (bf16 CUDA tensors) and
+           layers[l] = dict(attn_norm, w_qkv, w_o, mlp_norm, w_gate_up, w_down, w_router).
+    """
+
+    def __init__(self, shape, weights, *, max_batch: int, max_tree: int, max_depth: int, kv_capacity: int,
+                 k_cache: Optional[torch.Tensor] = None, v_cache: Optional[torch.Tensor] = None,
+                 stream: Optional[torch.cuda.Stream] = None):
+        self.shape = shape
+        self.max_batch, self.max_tree, self.max_depth, self.kv_capacity = max_batch, max_tree, max_depth, kv_capacity
+        self.desc = N.ModelDesc(shape.n_layers, shape.d_model, shape.n_q_heads, shape.n_kv_heads, shape.head_dim,
+                                shape.d_ff, shape.vocab, shape.n_experts, shape.top_k, shape.rms_eps,
+                                shape.rope_base, max_batch, max_tree, max_depth, kv_capacity)
+        dev = weights.embed.device
+        if dev.type != "cuda":
+            raise ValueError("weights must be device tensors")
+        L, Hkv, dh = shape.n_layers, shape.n_kv_heads, shape.head_dim
+        if k_cache is None:
+            k_cache = torch.zeros((L, max_batch, Hkv, kv_capacity, dh), dtype=torch.bfloat16, device=dev)
+        if v_cache is None:
+            v_cache = torch.zeros((L, max_batch, Hkv, dh, kv_capacity), dtype=torch.bfloat16, device=dev)
+        need = N.lib.griffin_kv_cache_bytes(byref(self.desc))
+        for t in (k_cache, v_cache):
+            if t.dtype != torch.bfloat16 or not t.is_contiguous() or t.numel() * 2 != need:
+                raise ValueError("KV cache tensors must be contiguous bf16 of griffin_kv_cache_bytes bytes")
+        self.k_cache, self.v_cache = k_cache, v_cache
+        self.stream = stream or torch.cuda.current_stream(dev)
+        self._weights = weights  # keep alive
+
+        def arr(key):
+            ptrs = [(lay[key].data_ptr() if lay.get(key) is not None else None) for lay in weights.layers]
+            return (c_void_p * L)(*ptrs)
+
+        self._arrays = {k: arr(k) for k in ("attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")}
+        self._arrays["w_router"] = arr("w_router") if shape.n_experts > 1 else None
+        cast = lambda a: ctypes.cast(a, POINTER(c_void_p)) if a is not None else None  # noqa: E731
+        self.w = N.Weights(weights.embed.data_ptr(), weights.lm_head.data_ptr(), weights.final_norm.data_ptr(),
+                           cast(self._arrays["attn_norm"]), cast(self._arrays["w_qkv"]), cast(self._arrays["w_o"]),
+                           cast(self._arrays["mlp_norm"]), cast(self._arrays["w_gate_up"]),
+                           cast(self._arrays["w_down"]), cast(self._arrays["w_router"]))
+        self.ctx = c_void_p()
+        rc = N.lib.griffin_verify_init(byref(self.desc), byref(self.w), k_cache.data_ptr(), v_cache.data_ptr(),
+                                       c_void_p(self.stream.cuda_stream), byref(self.ctx))
+        _check(rc, "griffin_verify_init")
+        self._batch = 0
+
+    # ------------------------------------------------------------ KV cache ----
+    def write_prefix(self, layer: int, seq: int, k: torch.Tensor, v: torch.Tensor):
+        """Place a cached prefix: k, v bf16 [Hkv, P, dh] (k post-rotary)."""
+        P = k.shape[1]
+        with torch.cuda.stream(self.stream):
+            self.k_cache[layer, seq, :, :P, :].copy_(k)
+            self.v_cache[layer, seq, :, :, :P].copy_(v.transpose(-1, -2))
+
+    # ---------------------------------------------------------------- step ----
+    def step(self, prefix_len, trees: Sequence, logits_out: Optional[torch.Tensor] = None):
+        n, tok, par = pack_trees(trees, self.max_tree)
+        return self.step_arrays(prefix_len, n, tok, par, logits_out)
+
+    def step_arrays(self, prefix_len, n_nodes, tokens, parents, logits_out: Optional[torch.Tensor] = None):
+        B = len(n_nodes)
+        pl, nn, tk, pa = _i32(prefix_len), _i32(n_nodes), _i32(tokens), _i32(parents)
+        lp = None
+        if logits_out is not None:
+            if logits_out.dtype != torch.float32 or not logits_out.is_contiguous() or \
+                    logits_out.numel() < B * self.max_tree * self.shape.vocab:
+                raise ValueError("logits_out must be contiguous fp32 [B*max_tree, vocab]")
+            lp = c_void_p(logits_out.data_ptr())
+        rc = N.lib.griffin_verify_step(self.ctx, B, _p32(pl), _p32(nn), _p32(tk), _p32(pa), lp)
+        _check(rc, "griffin_verify_step", self.ctx)
+        self._batch = B
+
+    def accept(self, check: bool = True) -> AcceptResult:
+        B, D = self._batch, self.max_depth
+        L = np.zeros(max(B, 1), dtype=np.int32)
+        out = np.zeros((max(B, 1), D + 1), dtype=np.int32)
+        path = np.zeros((max(B, 1), max(D, 1)), dtype=np.int32)
+        rc = N.lib.griffin_accept(self.ctx, _p32(L), _p32(out), _p32(path))
+        if rc != N.CODES["GRIFFIN_ENUMERIC"] or check:
+            _check(rc, "griffin_accept", self.ctx)
+        return AcceptResult(L[:B], out[:B], path[:B, :D], rc)
+
+    def predictions(self) -> np.ndarray:
+        pred = np.zeros((max(self._batch, 1), self.max_tree), dtype=np.int32)
+        rc = N.lib.griffin_read_predictions(self.ctx, _p32(pred))
+        _check(rc, "griffin_read_predictions", self.ctx)
+        return pred[: self._batch]
+
+    def close(self):
+        if getattr(self, "ctx", None) is not None and self.ctx.value:
+            N.lib.griffin_verify_free(self.ctx)
+            self.ctx = c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+
+def _profile_enable(self, mask: int = (1 << 9) - 1):
+    _check(N.lib.griffin_profile_enable(self.ctx, mask), "griffin_profile_enable", self.ctx)
+
+
+def _profile_read(self) -> dict:
+    """Per kernel class: (summed ms, launches) since the last read."""
+    ms = (ctypes.c_double * 9)()
+    n = (ctypes.c_int64 * 9)()
+    _check(N.lib.griffin_profile_read(self.ctx, ms, n), "griffin_profile_read", self.ctx)
+    return {name: (float(ms[k]), int(n[k])) for k, name in enumerate(N.KERNEL_CLASSES)}
+
+
+TreeVerifier.profile_enable = _profile_enable
+TreeVerifier.profile_read = _profile_read

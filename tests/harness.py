@@ -92,3 +92,79 @@ def build_sequence(ow: oracle.OracleWeights, w: Workload, tree_index: int, seq: 
         greedy, margins, _ = oracle.greedy_chain(ow, kv.decode_cache(m), int(tree.tokens[0]), len(path))
         tree = gen.apply_plant(tree, path, greedy)
     return SeqCase(toks, kv, tree, path, greedy, margins)
+
+
+# ------------------------------------------------------------ GPU parity ----
+
+LOGIT_REL_TOL = 2e-2      # max |gpu - oracle| per row, relative to the oracle row's range
+MARGIN_GATE = 1e-2        # argmax / acceptance compared bit-exactly where the top-2 margin exceeds this
+# MoE: a node is left out of the gates when its own or an ancestor's router has
+# its last kept and first dropped expert logits closer than this (in any
+# layer): the GPU router sees bf16-path activations whose relative error
+# (~3e-3) moves router logits of std ~0.45 by ~1e-3, so a closer pair can
+# route differently.
+ROUTER_GAP = 5e-3
+
+
+@dataclass
+class OracleSeq:
+    case: SeqCase
+    logits: np.ndarray
+    pred: np.ndarray
+    margin: np.ndarray
+    accept: "oracle.accept.AcceptResult"
+    router_logits: Optional[np.ndarray]
+
+
+def oracle_sequence(ow: oracle.OracleWeights, case: SeqCase) -> OracleSeq:
+    res = oracle.verify_tree(ow, case.kv.fn(), case.tree, case.kv.length)
+    pred = oracle.argmax_first(res.logits)
+    return OracleSeq(case, res.logits, pred, oracle.top2_margin(res.logits),
+                     oracle.accept_dfs(case.tree, pred), res.router_logits)
+
+
+def visited_nodes(tree, pred) -> List[int]:
+    """Nodes whose whole root path is accepted under predictions pred."""
+    out = [0]
+    for i in range(1, tree.n):
+        path = tree.root_path(i)
+        if all(int(tree.tokens[n]) == int(pred[int(tree.parents[n])]) for n in path):
+            out.append(i)
+    return out
+
+
+def router_near_tie_nodes(os_: OracleSeq, top_k: int, gap: float) -> set:
+    """Nodes whose own or ancestors' routing has a kept/dropped expert logit gap below `gap`."""
+    if os_.router_logits is None:
+        return set()
+    rl = os_.router_logits                     # [L, T, E]
+    srt = -np.sort(-rl, axis=-1)
+    close = np.any(srt[..., top_k - 1] - srt[..., top_k] < gap, axis=0)   # [T]
+    tree = os_.case.tree
+    bad = set()
+    for i in range(tree.n):
+        if any(close[n] for n in [0] + tree.root_path(i)):
+            bad.add(i)
+    return bad
+
+
+def check_parity(os_: OracleSeq, gpu_logits: np.ndarray, gpu_pred: np.ndarray, gpu_accept, exclude=frozenset()):
+    """Assert the spec gates for one sequence; returns stats."""
+    T = os_.case.tree.n
+    keep = [i for i in range(T) if i not in exclude]
+    ol = os_.logits[keep]
+    gl = gpu_logits[keep].astype(np.float64)
+    rng = ol.max(axis=1) - ol.min(axis=1)
+    rel = np.abs(gl - ol).max(axis=1) / rng
+    assert rel.max() <= LOGIT_REL_TOL, f"logit error {rel.max():.3e} (relative to range) above {LOGIT_REL_TOL}"
+    gated = [i for i in keep if os_.margin[i] > MARGIN_GATE]
+    mism = [i for i in gated if int(gpu_pred[i]) != int(os_.pred[i])]
+    assert not mism, f"argmax differs at nodes {mism} (margins {[os_.margin[i] for i in mism]})"
+    vis = visited_nodes(os_.case.tree, os_.pred)
+    accept_gated = all(os_.margin[i] > MARGIN_GATE and i not in exclude for i in vis)
+    if accept_gated:
+        L, toks, _path = gpu_accept
+        assert L == os_.accept.length, f"accept length {L} != oracle {os_.accept.length}"
+        assert toks == os_.accept.tokens, f"accepted tokens {toks} != oracle {os_.accept.tokens}"
+    return dict(max_rel=float(rel.max()), gated=len(gated), total=T, accept_checked=accept_gated,
+                L=os_.accept.length)
