@@ -105,8 +105,9 @@ size_t griffin_kv_cache_bytes(const griffin_model_desc *desc);
 /* Create a context.
  * k_cache: device bf16 [n_layers][max_batch][n_kv_heads][kv_capacity][head_dim],
  *          keys after rotation.
- * v_cache: device bf16 [n_layers][max_batch][n_kv_heads][head_dim][kv_capacity]
- *          (values stored transposed: one row per head dimension).
+ * v_cache: device bf16 [n_layers][max_batch][n_kv_heads][kv_capacity/32][head_dim][32]
+ *          (values in 32-slot tiles, each stored transposed: slot s of a
+ *          head, dimension j lives at tile s/32, row j, column s%32).
  * hip_stream: the hipStream_t every launch is enqueued on (NULL = default).
  * The context allocates its own workspace (activations, partial sums,
  * metadata, pinned staging) and frees it in griffin_verify_free.

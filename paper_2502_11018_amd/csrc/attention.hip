@@ -12,8 +12,9 @@
 //  * Keys are fed to the MFMA in a permuted row order so that accumulator
 //    register q of lane half h holds key 16 h + q of the block; the P operand
 //    of the second product is then the lane's own registers 8 t .. 8 t + 7.
-//  * V is cached transposed ([dim][slot]), so the V^T operand is one 16-byte
-//    load of 8 consecutive slots per lane.
+//  * V is cached in 32-slot tiles stored transposed ([tile][dim][32]), so a
+//    block's V^T is one contiguous 8 KB tile and each operand piece is one
+//    16-byte load of 8 consecutive slots.
 //  * Q and K use the same head-dim permutation as the projection GEMMs: a lane
 //    reads 32 consecutive head dims and feeds 8 of them to each of 4 MFMAs.
 // Scores are kept in the log2 domain (scaled by log2(e)/sqrt(dh)) and exp2 is
@@ -30,10 +31,22 @@ __global__ __launch_bounds__(64) void tree_attention_kernel(AttnArgs a) {
   constexpr int DB = DH / 32;   // 32-dim blocks of the output
   const int lane = threadIdx.x;
   const int col = lane & 31, hh = lane >> 5;
-  const int split = blockIdx.x;
-  const int hq = blockIdx.y;
-  const int b = blockIdx.z / a.qblocks, qb = blockIdx.z % a.qblocks;
-  const int hk = hq / (a.Hq / a.Hkv);
+  // XCD-aware decode: workgroups are dispatched round-robin over the 8 XCDs
+  // (id % 8), so every workgroup of one (sequence, KV head) stream gets the
+  // same id % 8 and its K/V blocks are shared through that XCD's L2.
+  const int G = a.Hq / a.Hkv;
+  const int per_stream = G * a.qblocks * a.splits;
+  const int id = blockIdx.x;
+  const int rest = id >> 3;
+  const int stream = (rest / per_stream) * 8 + (id & 7);
+  if (stream >= a.batch * a.Hkv) return;
+  int within = rest % per_stream;
+  const int split = within % a.splits;
+  within /= a.splits;
+  const int qb = within % a.qblocks;
+  const int hq = (stream % a.Hkv) * G + within / a.qblocks;
+  const int b = stream / a.Hkv;
+  const int hk = hq / G;
   const int n_nodes = a.meta.n_nodes[b];
   const int P = a.meta.prefix_len[b];
   const int Lb = P + n_nodes;
@@ -71,33 +84,40 @@ __global__ __launch_bounds__(64) void tree_attention_kernel(AttnArgs a) {
   // MFMA row -> key offset inside a 32-key block: row 8q + 4h + e holds key 16h + 4q + e
   const int krow = 16 * ((col >> 2) & 1) + 4 * (col >> 3) + (col & 3);
 
-  float m_run = -INFINITY, l_run = 0.f;
+  float m_ref = -INFINITY, l_run = 0.f;
   f32x16 oacc[DB];
 #pragma unroll
   for (int d = 0; d < DB; ++d)
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[d][r] = 0.f;
 
-  for (int kb = kb0; kb < kb1; ++kb) {
+  // K and V operands of one 32-key block; two register sets, the next block's
+  // loads are issued before the current block is computed
+  u32x4 kf[2][CH][4];
+  u32x4 vf[2][DB][2];
+  auto load_kv = [&](int buf, int kb) {
     const int key0 = kb * 32;
-    // ---- S^T = K Q^T (rows: keys, cols: queries)
-    u32x4 kf[CH][4];
-    {
-      const uint16_t* kp = kbase + (long long)(key0 + krow) * DH + 32 * hh;
+    const uint16_t* kp = kbase + (long long)(key0 + krow) * DH + 32 * hh;
 #pragma unroll
-      for (int c = 0; c < CH; ++c)
+    for (int c = 0; c < CH; ++c)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) kf[c][j] = ld_u4(kp + 64 * c + 8 * j);
-    }
+      for (int j = 0; j < 4; ++j) kf[buf][c][j] = ld_u4(kp + 64 * c + 8 * j);
     // V^T operand (A): lane (dim row col of block d, k-group hh); step t covers
     // keys 16 hh + 8 t + [0, 8)
-    u32x4 vf[DB][2];
 #pragma unroll
     for (int d = 0; d < DB; ++d)
 #pragma unroll
       for (int t = 0; t < 2; ++t)
-        vf[d][t] = ld_u4(vbase + (long long)(32 * d + col) * a.kv_cap + key0 + 16 * hh + 8 * t);
+        vf[buf][d][t] = ld_u4(vbase + (long long)kb * DH * 32 + (32 * d + col) * 32 + 16 * hh + 8 * t);
+  };
 
+  // Online softmax with a lazily moved reference max: p = 2^(s - m_ref) may
+  // reach 2^8 before the reference is raised, so the accumulator rescale only
+  // runs when some lane's block maximum exceeds its reference by more than 8
+  // (a wave-uniform branch with no loads inside).
+  auto compute = [&](int buf, int kb, bool live_blk) {
+    const int key0 = kb * 32;
+    // ---- S^T = K Q^T (rows: keys, cols: queries)
     f32x16 s;
 #pragma unroll
     for (int r = 0; r < 16; ++r) s[r] = 0.f;
@@ -105,26 +125,38 @@ __global__ __launch_bounds__(64) void tree_attention_kernel(AttnArgs a) {
     for (int c = 0; c < CH; ++c)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[c][j]), as_bf16x8(qf[c][j]), s, 0, 0, 0);
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[buf][c][j]), as_bf16x8(qf[c][j]), s, 0, 0, 0);
 
-    // ---- mask + online softmax (this lane: query qi, keys key0 + 16 hh + r)
+    // ---- scale + mask (this lane: query qi, keys key0 + 16 hh + r)
     float mx = -INFINITY;
+    if (live_blk && key0 + 32 <= P) {  // whole block inside the cached prefix: all visible
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int key = key0 + 16 * hh + r;
-      bool vis;
-      if (key < P) vis = true;
-      else {
-        const int j = key - P;
-        vis = (j < n_nodes) && ((anc >> j) & 1ull);
+      for (int r = 0; r < 16; ++r) {
+        s[r] *= a.scale_log2;
+        mx = fmaxf(mx, s[r]);
       }
-      s[r] = vis ? s[r] * a.scale_log2 : -INFINITY;
-      mx = fmaxf(mx, s[r]);
+    } else {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = key0 + 16 * hh + r;
+        const int j = key - P;
+        const bool vis = live_blk && (key < P || (j < n_nodes && ((anc >> (j & 63)) & 1ull)));
+        s[r] = vis ? s[r] * a.scale_log2 : -INFINITY;
+        mx = fmaxf(mx, s[r]);
+      }
     }
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(m_run, mx);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = exp2f(m_run - m_use);
+    if (__any(mx > m_ref + 8.f)) {
+      const float m_new = fmaxf(m_ref, mx);
+      const float alpha = m_ref == -INFINITY ? 0.f : exp2f(m_ref - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int d = 0; d < DB; ++d)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[d][r] *= alpha;
+      m_ref = m_new;
+    }
+    const float m_use = m_ref == -INFINITY ? 0.f : m_ref;
     float psum = 0.f;
     float p[16];
 #pragma unroll
@@ -132,13 +164,7 @@ __global__ __launch_bounds__(64) void tree_attention_kernel(AttnArgs a) {
       p[r] = exp2f(s[r] - m_use);
       psum += p[r];
     }
-    psum += __shfl_xor(psum, 32, 64);
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int d = 0; d < DB; ++d)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[d][r] *= alpha;
+    l_run += psum + __shfl_xor(psum, 32, 64);
 
     // keys at or beyond the end of the sequence may hold stale or never
     // written cache bytes; zero their V so that 0 * garbage cannot appear
@@ -150,10 +176,9 @@ __global__ __launch_bounds__(64) void tree_attention_kernel(AttnArgs a) {
           const int kfirst = key0 + 16 * hh + 8 * t;
 #pragma unroll
           for (int w = 0; w < 4; ++w) {  // bf16 element 2w is the low half of dword w
-            uint32_t v = vf[d][t][w];
-            if (kfirst + 2 * w >= Lb) v &= 0xffff0000u;
-            if (kfirst + 2 * w + 1 >= Lb) v &= 0x0000ffffu;
-            vf[d][t][w] = v;
+            const uint32_t keep =
+                (kfirst + 2 * w < Lb ? 0x0000ffffu : 0u) | (kfirst + 2 * w + 1 < Lb ? 0xffff0000u : 0u);
+            vf[buf][d][t][w] &= keep;
           }
         }
     }
@@ -168,7 +193,20 @@ __global__ __launch_bounds__(64) void tree_attention_kernel(AttnArgs a) {
       pf[3] = pack_bf16x2(p[8 * t + 6], p[8 * t + 7]);
 #pragma unroll
       for (int d = 0; d < DB; ++d)
-        oacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf[d][t]), as_bf16x8(pf), oacc[d], 0, 0, 0);
+        oacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf[buf][d][t]), as_bf16x8(pf), oacc[d], 0, 0, 0);
+    }
+  };
+
+  // Branch-free pipeline: loads past the split's end re-read its last block
+  // (in bounds) and a block past the end is computed fully masked, which
+  // leaves m, l and the output exactly unchanged.
+  if (kb0 < kb1) {
+    load_kv(0, kb0);
+    for (int kb = kb0; kb < kb1; kb += 2) {
+      load_kv(1, min(kb + 1, kb1 - 1));
+      compute(0, kb, true);
+      load_kv(0, min(kb + 2, kb1 - 1));
+      compute(1, kb + 1, kb + 1 < kb1);
     }
   }
 
@@ -181,13 +219,16 @@ __global__ __launch_bounds__(64) void tree_attention_kernel(AttnArgs a) {
       *reinterpret_cast<float4*>(orow + 32 * d + 8 * rg + 4 * hh) =
           make_float4(oacc[d][4 * rg], oacc[d][4 * rg + 1], oacc[d][4 * rg + 2], oacc[d][4 * rg + 3]);
   if (hh == 0) {
-    pml[2 * col] = m_run;
+    pml[2 * col] = m_ref;
     pml[2 * col + 1] = l_run;
   }
 }
 
 hipError_t launch_attention(const AttnArgs& a, int batch, hipStream_t s) {
-  dim3 grid(a.splits, a.Hq, batch * a.qblocks);
+  if (a.batch != batch) return hipErrorInvalidValue;
+  const int streams = batch * a.Hkv;
+  const int per_stream = (a.Hq / a.Hkv) * a.qblocks * a.splits;
+  dim3 grid(((streams + 7) / 8) * 8 * per_stream);
   if (a.dh == 128) hipLaunchKernelGGL(tree_attention_kernel<128>, grid, dim3(64), 0, s, a);
   else if (a.dh == 64) hipLaunchKernelGGL(tree_attention_kernel<64>, grid, dim3(64), 0, s, a);
   else return hipErrorInvalidValue;
@@ -196,40 +237,70 @@ hipError_t launch_attention(const AttnArgs& a, int batch, hipStream_t s) {
 
 // Merge the splits of every (row, head): o = sum_s 2^(m_s - M) o_s / sum_s 2^(m_s - M) l_s.
 // Absent rows get zeros.  One workgroup per row, one thread per (head, dim).
+// The merged rows are written fragment-packed (o_ks K steps per tile) as the
+// activation operand of the output projection.  One thread per (head, 4 dims).
+template <int MAXS>
 __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ part_o,
                                                            const float* __restrict__ part_ml, StepMeta meta,
-                                                           int Hq, int dh, int splits, int qrows, int max_tree,
-                                                           uint16_t* __restrict__ o_out) {
+                                                           int Hq, int dh, int splits_unused, int qrows,
+                                                           int max_tree, uint16_t* __restrict__ o_out, int o_ks) {
+  (void)splits_unused;
   const int r = blockIdx.x;
   const int b = r / max_tree, i = r % max_tree;
-  const bool live = i < meta.n_nodes[b];
-  for (int t = threadIdx.x; t < Hq * dh; t += blockDim.x) {
-    const int h = t / dh, d = t % dh;
-    float out = 0.f;
-    if (live) {
-      const long long base = ((long long)b * Hq + h) * splits;
-      float M = -INFINITY;
-      for (int s = 0; s < splits; ++s) M = fmaxf(M, part_ml[((base + s) * qrows + i) * 2]);
-      float num = 0.f, den = 0.f;
-      if (M != -INFINITY) {
-        for (int s = 0; s < splits; ++s) {
-          const float ms = part_ml[((base + s) * qrows + i) * 2];
-          if (ms == -INFINITY) continue;
-          const float w = exp2f(ms - M);
-          num += w * part_o[((base + s) * qrows + i) * dh + d];
-          den += w * part_ml[((base + s) * qrows + i) * 2 + 1];
-        }
-        out = num / den;
-      }
+  const int quads = dh / 4;
+  const int t = blockIdx.y * blockDim.x + threadIdx.x;
+  if (t >= Hq * quads) return;
+  const int h = t / quads, d = (t % quads) * 4;
+  float4 out = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (i < meta.n_nodes[b]) {
+    const long long base = ((long long)b * Hq + h) * MAXS;
+    float ms[MAXS], ls[MAXS];
+    float4 os[MAXS];
+#pragma unroll
+    for (int s = 0; s < MAXS; ++s) {
+      const long long row = (base + s) * qrows + i;
+      ms[s] = part_ml[row * 2];
+      ls[s] = part_ml[row * 2 + 1];
+      os[s] = *reinterpret_cast<const float4*>(part_o + row * dh + d);
     }
-    o_out[(long long)r * Hq * dh + t] = f32_to_bf16(out);
+    float M = -INFINITY;
+#pragma unroll
+    for (int s = 0; s < MAXS; ++s) M = fmaxf(M, ms[s]);
+    if (M != -INFINITY) {
+      float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
+      float den = 0.f;
+#pragma unroll
+      for (int s = 0; s < MAXS; ++s)
+        if (ms[s] != -INFINITY) {
+          const float w = exp2f(ms[s] - M);
+          num.x += w * os[s].x; num.y += w * os[s].y; num.z += w * os[s].z; num.w += w * os[s].w;
+          den += w * ls[s];
+        }
+      const float inv = 1.f / den;
+      out = make_float4(num.x * inv, num.y * inv, num.z * inv, num.w * inv);
+    }
   }
+  *reinterpret_cast<uint2*>(o_out + xpack_off(r, h * dh + d, o_ks)) =
+      make_uint2(pack_bf16x2(out.x, out.y), pack_bf16x2(out.z, out.w));
 }
 
 hipError_t launch_attn_combine(const float* part_o, const float* part_ml, StepMeta meta, int Hq, int dh, int splits,
-                               int qrows, int max_tree, int batch, uint16_t* o_out, hipStream_t s) {
-  hipLaunchKernelGGL(attn_combine_kernel, dim3(batch * max_tree), dim3(256), 0, s, part_o, part_ml, meta, Hq, dh,
-                     splits, qrows, max_tree, o_out);
+                               int qrows, int max_tree, int batch, uint16_t* o_out, int o_ks, hipStream_t s) {
+  const int items = Hq * dh / 4;
+  const dim3 grid(batch * max_tree, (items + 255) / 256);
+  switch (splits) {
+#define GRIFFIN_COMB_CASE(n)                                                                                   \
+  case n:                                                                                                     \
+    hipLaunchKernelGGL(attn_combine_kernel<n>, grid, dim3(256), 0, s, part_o, part_ml, meta, Hq, dh, splits, qrows, \
+                       max_tree, o_out, o_ks);                                                                \
+    break;
+    GRIFFIN_COMB_CASE(1) GRIFFIN_COMB_CASE(2) GRIFFIN_COMB_CASE(3) GRIFFIN_COMB_CASE(4) GRIFFIN_COMB_CASE(5)
+    GRIFFIN_COMB_CASE(6) GRIFFIN_COMB_CASE(7) GRIFFIN_COMB_CASE(8) GRIFFIN_COMB_CASE(9) GRIFFIN_COMB_CASE(10)
+    GRIFFIN_COMB_CASE(11) GRIFFIN_COMB_CASE(12) GRIFFIN_COMB_CASE(13) GRIFFIN_COMB_CASE(14) GRIFFIN_COMB_CASE(15)
+    GRIFFIN_COMB_CASE(16)
+#undef GRIFFIN_COMB_CASE
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 

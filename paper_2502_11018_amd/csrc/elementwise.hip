@@ -31,68 +31,143 @@ hipError_t launch_embed(const uint16_t* embed, const int32_t* token, int rows, i
 // ------------------------------------------------ residual update + RMSNorm ----
 // x[r] += (split partial sums | weighted MoE expert outputs); then
 // xn[r] = bf16(x[r] * rsqrt(mean(x[r]^2) + eps) * gain).
-// 256 threads, each owning up to RN_MAX float4 groups of the row in registers.
-constexpr int RN_THREADS = 256;
-constexpr int RN_MAX = 8;  // d <= 8192
+// 1024 threads per row, each owning GPT float4 groups of the row.  The number
+// of dense partials NP is a template parameter so that every load of the row
+// is issued before the first one is waited on (no branches between loads);
+// NP < 0 selects the MoE form (per-row expert slots).
+constexpr int RN_THREADS = 1024;
+constexpr int RN_SPLITS = 16;  // K-split partials per residual update
 
+__device__ __forceinline__ void add4(float4& a, const float4& p) {
+  a.x += p.x; a.y += p.y; a.z += p.z; a.w += p.w;
+}
+
+template <int NP, int GPT>
 __global__ __launch_bounds__(RN_THREADS) void residual_rmsnorm_kernel(float* __restrict__ x, ResidualAdd add,
                                                                       const uint16_t* __restrict__ gain,
                                                                       float eps, int d,
-                                                                      uint16_t* __restrict__ xn) {
+                                                                      uint16_t* __restrict__ xn, int xn_ks) {
   __shared__ float red[16];
   const int r = blockIdx.x;
-  float* xr = x + (long long)r * d;
+  float* __restrict__ xr = x + (long long)r * d;
+  const float* __restrict__ parts = add.parts;
   const int groups = d >> 2;
-  float4 v[RN_MAX];
-  float ss = 0.f;
-  const bool upd = add.parts != nullptr;
+  int gi[GPT];
+  bool ok[GPT];
+  float4 v[GPT];
 #pragma unroll
-  for (int u = 0; u < RN_MAX; ++u) {
-    const int gi = threadIdx.x + u * RN_THREADS;
-    if (gi < groups) {
-      float4 a = reinterpret_cast<const float4*>(xr)[gi];
-      if (upd) {
-        if (add.slot == nullptr) {
-          for (int s = 0; s < add.n_parts; ++s) {
-            const float4 p = reinterpret_cast<const float4*>(add.parts + s * add.part_stride + (long long)r * d)[gi];
-            a.x += p.x; a.y += p.y; a.z += p.z; a.w += p.w;
-          }
-        } else {
-          for (int k = 0; k < add.top_k; ++k) {
-            const int sl = add.slot[r * add.top_k + k];
-            if (sl < 0) continue;
-            const float w = add.slot_w[r * add.top_k + k];
-            const float4 p = reinterpret_cast<const float4*>(add.parts + (long long)sl * d)[gi];
-            a.x += w * p.x; a.y += w * p.y; a.z += w * p.z; a.w += w * p.w;
-          }
-        }
-        reinterpret_cast<float4*>(xr)[gi] = a;
+  for (int u = 0; u < GPT; ++u) {
+    const int g = threadIdx.x + u * RN_THREADS;
+    ok[u] = g < groups;
+    gi[u] = ok[u] ? g : groups - 1;  // clamped: loads stay unconditional
+    v[u] = reinterpret_cast<const float4*>(xr)[gi[u]];
+  }
+  if constexpr (NP > 0) {
+    // dense: K-split partial sums, all loaded first, added in split order
+    float4 p[NP][GPT];
+#pragma unroll
+    for (int s = 0; s < NP; ++s)
+#pragma unroll
+      for (int u = 0; u < GPT; ++u)
+        p[s][u] = reinterpret_cast<const float4*>(parts + s * add.part_stride + (long long)r * d)[gi[u]];
+#pragma unroll
+    for (int s = 0; s < NP; ++s)
+#pragma unroll
+      for (int u = 0; u < GPT; ++u) add4(v[u], p[s][u]);
+  } else if constexpr (NP < 0) {
+    // MoE: kept experts in rank order, each the sum of its K-split partials
+    for (int k = 0; k < add.top_k; ++k) {
+      const int sl = add.slot[r * add.top_k + k];
+      if (sl < 0) continue;
+      const float w = add.slot_w[r * add.top_k + k];
+      float4 y[GPT];
+#pragma unroll
+      for (int u = 0; u < GPT; ++u) y[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+      for (int s = 0; s < add.n_parts; ++s) {
+        const float4* ps = reinterpret_cast<const float4*>(parts + s * add.part_stride + (long long)sl * d);
+#pragma unroll
+        for (int u = 0; u < GPT; ++u) add4(y[u], ps[gi[u]]);
       }
-      v[u] = a;
-      ss += a.x * a.x + a.y * a.y + a.z * a.z + a.w * a.w;
+#pragma unroll
+      for (int u = 0; u < GPT; ++u) {
+        v[u].x += w * y[u].x; v[u].y += w * y[u].y; v[u].z += w * y[u].z; v[u].w += w * y[u].w;
+      }
     }
   }
+  if constexpr (NP != 0) {
+#pragma unroll
+    for (int u = 0; u < GPT; ++u)
+      if (ok[u]) reinterpret_cast<float4*>(xr)[gi[u]] = v[u];
+  }
+  float ss = 0.f;
+#pragma unroll
+  for (int u = 0; u < GPT; ++u)
+    ss += ok[u] ? v[u].x * v[u].x + v[u].y * v[u].y + v[u].z * v[u].z + v[u].w * v[u].w : 0.f;
   const float tot = block_sum(ss, red);
   const float rs = rsqrtf(tot / (float)d + eps);
-  uint16_t* xo = xn + (long long)r * d;
 #pragma unroll
-  for (int u = 0; u < RN_MAX; ++u) {
-    const int gi = threadIdx.x + u * RN_THREADS;
-    if (gi < groups) {
-      const uint2 gg = *reinterpret_cast<const uint2*>(gain + 4 * gi);
+  for (int u = 0; u < GPT; ++u) {
+    if (ok[u]) {
+      const uint2 gg = *reinterpret_cast<const uint2*>(gain + 4 * gi[u]);
       const float4 a = v[u];
       uint2 o;
       o.x = pack_bf16x2(a.x * rs * bf16_to_f32(gg.x & 0xffff), a.y * rs * bf16_to_f32(gg.x >> 16));
       o.y = pack_bf16x2(a.z * rs * bf16_to_f32(gg.y & 0xffff), a.w * rs * bf16_to_f32(gg.y >> 16));
-      *reinterpret_cast<uint2*>(xo + 4 * gi) = o;
+      *reinterpret_cast<uint2*>(xn + xpack_off(r, 4 * gi[u], xn_ks)) = o;  // fragment-packed GEMM operand
     }
   }
 }
 
+template <int NP>
+static hipError_t launch_rn(float* x, const ResidualAdd& add, const uint16_t* gain, float eps, int rows, int d,
+                            uint16_t* xn, int xn_ks, hipStream_t s) {
+  const int groups = d / 4;
+  if (groups <= RN_THREADS)
+    hipLaunchKernelGGL((residual_rmsnorm_kernel<NP, 1>), dim3(rows), dim3(RN_THREADS), 0, s, x, add, gain, eps, d,
+                       xn, xn_ks);
+  else
+    hipLaunchKernelGGL((residual_rmsnorm_kernel<NP, 2>), dim3(rows), dim3(RN_THREADS), 0, s, x, add, gain, eps, d,
+                       xn, xn_ks);
+  return hipGetLastError();
+}
+
 hipError_t launch_residual_rmsnorm(float* x, const ResidualAdd& add, const uint16_t* gain, float eps, int rows,
-                                   int d, uint16_t* xn, hipStream_t s) {
-  if (d % 4 != 0 || d > 4 * RN_THREADS * RN_MAX) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(residual_rmsnorm_kernel, dim3(rows), dim3(RN_THREADS), 0, s, x, add, gain, eps, d, xn);
+                                   int d, uint16_t* xn, int xn_ks, hipStream_t s) {
+  if (d % 4 != 0 || d > 8 * RN_THREADS || add.n_parts > RN_SPLITS) return hipErrorInvalidValue;
+  if (add.parts == nullptr) return launch_rn<0>(x, add, gain, eps, rows, d, xn, xn_ks, s);
+  if (add.slot != nullptr) return launch_rn<-1>(x, add, gain, eps, rows, d, xn, xn_ks, s);
+  switch (add.n_parts) {
+#define GRIFFIN_RN_CASE(n) \
+  case n: return launch_rn<n>(x, add, gain, eps, rows, d, xn, xn_ks, s);
+    GRIFFIN_RN_CASE(1) GRIFFIN_RN_CASE(2) GRIFFIN_RN_CASE(3) GRIFFIN_RN_CASE(4) GRIFFIN_RN_CASE(5)
+    GRIFFIN_RN_CASE(6) GRIFFIN_RN_CASE(7) GRIFFIN_RN_CASE(8) GRIFFIN_RN_CASE(9) GRIFFIN_RN_CASE(10)
+    GRIFFIN_RN_CASE(11) GRIFFIN_RN_CASE(12) GRIFFIN_RN_CASE(13) GRIFFIN_RN_CASE(14) GRIFFIN_RN_CASE(15)
+    GRIFFIN_RN_CASE(16)
+#undef GRIFFIN_RN_CASE
+    default: return hipErrorInvalidValue;
+  }
+}
+
+// ----------------------------------------------------- MoE input gather ----
+// Copy the rows routed to each expert into that expert's activation tiles
+// (both fragment-packed with ks steps): expert e, row c <- xn row gather[e][c].
+__global__ __launch_bounds__(256) void moe_gather_kernel(const uint16_t* __restrict__ xn, int ks,
+                                                         const int32_t* __restrict__ gather,
+                                                         const int32_t* __restrict__ count, int cap, int d,
+                                                         uint16_t* __restrict__ xe, int xe_tiles) {
+  const int e = blockIdx.y, c = blockIdx.x;
+  if (c >= count[e]) return;
+  const int src = gather[e * cap + c];
+  const long long dst_row = (long long)e * xe_tiles * 64 + c;
+  for (int k = threadIdx.x * 8; k < d; k += blockDim.x * 8)
+    *reinterpret_cast<u32x4*>(xe + xpack_off(dst_row, k, ks)) =
+        *reinterpret_cast<const u32x4*>(xn + xpack_off(src, k, ks));
+}
+
+hipError_t launch_moe_gather(const uint16_t* xn, int xn_ks, const int32_t* gather, const int32_t* count,
+                             int n_experts, int cap, int d, uint16_t* xe, int xe_tiles, hipStream_t s) {
+  hipLaunchKernelGGL(moe_gather_kernel, dim3(cap, n_experts), dim3(256), 0, s, xn, xn_ks, gather, count, cap, d,
+                     xe, xe_tiles);
   return hipGetLastError();
 }
 
@@ -101,7 +176,8 @@ hipError_t launch_residual_rmsnorm(float* x, const ResidualAdd& add, const uint1
 // QKV projection, rotate q and k (rotate-half pairing j <-> j + dh/2) at the
 // node's position, write q (bf16) for attention, and k / v into cache slot
 // prefix_len[b] + i (k row-major per slot, v transposed: one row per dim).
-__global__ __launch_bounds__(256) void qkv_rope_kernel(const float* __restrict__ parts, int n_parts,
+template <int NP>
+__global__ __launch_bounds__(256) void qkv_rope_kernel(const float* __restrict__ parts, int n_parts_unused,
                                                        long long part_stride, StepMeta meta,
                                                        const float* __restrict__ rcos,
                                                        const float* __restrict__ rsin, int Hq, int Hkv,
@@ -116,14 +192,23 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* __restrict__
   const int width = heads * dh;
   const int pos = meta.pos[r];
   const int slot = meta.prefix_len[b] + i;
-  const float* row = parts + (long long)r * width;
-  for (int t = threadIdx.x; t < heads * half; t += blockDim.x) {
+  const float* __restrict__ row = parts + (long long)r * width;
+  const int t = blockIdx.y * blockDim.x + threadIdx.x;  // one (head, rotation pair) per thread
+  if (t < heads * half) {
     const int h = t / half, j = t % half;
     const int c1 = h * dh + j, c2 = c1 + half;
+    (void)n_parts_unused;
+    float a1[NP], a2[NP];  // all K-split partials loaded before any is summed
+#pragma unroll
+    for (int s = 0; s < NP; ++s) {
+      a1[s] = row[s * part_stride + c1];
+      a2[s] = row[s * part_stride + c2];
+    }
     float x1 = 0.f, x2 = 0.f;
-    for (int s = 0; s < n_parts; ++s) {
-      x1 += row[s * part_stride + c1];
-      x2 += row[s * part_stride + c2];
+#pragma unroll
+    for (int s = 0; s < NP; ++s) {
+      x1 += a1[s];
+      x2 += a2[s];
     }
     if (h < Hq + Hkv) {
       const float c = rcos[(long long)pos * half + j], sn = rsin[(long long)pos * half + j];
@@ -139,9 +224,11 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* __restrict__
         k[j + half] = f32_to_bf16(y2);
       }
     } else {
-      uint16_t* v = vc + ((long long)b * Hkv + (h - Hq - Hkv)) * dh * kv_cap;
-      v[(long long)j * kv_cap + slot] = f32_to_bf16(x1);
-      v[(long long)(j + half) * kv_cap + slot] = f32_to_bf16(x2);
+      // 32-slot tiles, transposed within the tile: [tile][dim][32]
+      uint16_t* v = vc + ((long long)b * Hkv + (h - Hq - Hkv)) * dh * kv_cap + (long long)(slot >> 5) * dh * 32 +
+                    (slot & 31);
+      v[j * 32] = f32_to_bf16(x1);
+      v[(j + half) * 32] = f32_to_bf16(x2);
     }
   }
 }
@@ -150,8 +237,21 @@ hipError_t launch_qkv_rope(const float* qkv_parts, int n_parts, long long part_s
                            const float* rope_cos, const float* rope_sin, int Hq, int Hkv, int dh, int max_tree,
                            int batch, int kv_cap, uint16_t* q_out, uint16_t* k_cache_l, uint16_t* v_cache_l,
                            hipStream_t s) {
-  hipLaunchKernelGGL(qkv_rope_kernel, dim3(batch * max_tree), dim3(256), 0, s, qkv_parts, n_parts, part_stride,
-                     meta, rope_cos, rope_sin, Hq, Hkv, dh, max_tree, kv_cap, q_out, k_cache_l, v_cache_l);
+  const int items = (Hq + 2 * Hkv) * (dh / 2);
+  const dim3 grid(batch * max_tree, (items + 255) / 256);
+  switch (n_parts) {
+#define GRIFFIN_ROPE_CASE(n)                                                                                   \
+  case n:                                                                                                     \
+    hipLaunchKernelGGL(qkv_rope_kernel<n>, grid, dim3(256), 0, s, qkv_parts, n_parts, part_stride, meta, rope_cos, \
+                       rope_sin, Hq, Hkv, dh, max_tree, kv_cap, q_out, k_cache_l, v_cache_l);                 \
+    break;
+    GRIFFIN_ROPE_CASE(1) GRIFFIN_ROPE_CASE(2) GRIFFIN_ROPE_CASE(3) GRIFFIN_ROPE_CASE(4) GRIFFIN_ROPE_CASE(5)
+    GRIFFIN_ROPE_CASE(6) GRIFFIN_ROPE_CASE(7) GRIFFIN_ROPE_CASE(8) GRIFFIN_ROPE_CASE(9) GRIFFIN_ROPE_CASE(10)
+    GRIFFIN_ROPE_CASE(11) GRIFFIN_ROPE_CASE(12) GRIFFIN_ROPE_CASE(13) GRIFFIN_ROPE_CASE(14) GRIFFIN_ROPE_CASE(15)
+    GRIFFIN_ROPE_CASE(16)
+#undef GRIFFIN_ROPE_CASE
+    default: return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
@@ -338,13 +438,10 @@ __global__ __launch_bounds__(64) void moe_lists_kernel(const int32_t* __restrict
   count[e] = c;
 }
 
-hipError_t launch_moe_lists(const int32_t* route_ids, int rows, const int32_t* n_nodes, int max_tree,
-                            int n_experts, int top_k, int cap, int32_t* gather, int32_t* count, int32_t* slot,
-                            hipStream_t s) {
-  (void)n_nodes;
-  (void)max_tree;
-  hipLaunchKernelGGL(moe_lists_kernel, dim3(1), dim3(64), 0, s, route_ids, rows, cap, n_experts, top_k, cap,
-                     gather, count, slot);
+hipError_t launch_moe_lists(const int32_t* route_ids, int rows, int padded_rows, int n_experts, int top_k,
+                            int cap, int32_t* gather, int32_t* count, int32_t* slot, hipStream_t s) {
+  hipLaunchKernelGGL(moe_lists_kernel, dim3(1), dim3(64), 0, s, route_ids, rows, padded_rows, n_experts, top_k,
+                     cap, gather, count, slot);
   return hipGetLastError();
 }
 

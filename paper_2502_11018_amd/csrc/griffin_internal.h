@@ -19,36 +19,56 @@ struct StepMeta {
   const uint64_t* anc;        // [R] ancestor-or-self bitmask over node ids
 };
 
-// GEMM with a bf16 activation operand X [rows][K] and a bf16 weight W [N][K]
-// (out = X W^T), fp32 accumulation.  See gemm.hip for the tiling.
 enum GemmEpilogue : int {
-  EPI_STORE = 0,    // fp32 out[s][row][n] (s = K-split index)
-  EPI_SWIGLU = 1,   // bf16 out[row][n] = silu(gate) * up; W rows: gate [0,N), up [N,2N)
-  EPI_ARGMAX = 2,   // per (row, 32-column tile) max/argmax/NaN count; optional fp32 logits
+  EPI_STORE = 0,    // fp32 out[split][row][n]
+  EPI_SWIGLU = 1,   // packed bf16 act[row][n] = silu(gate) * up (one gate + one up block per wave)
+  EPI_ARGMAX = 2,   // per (row, wave column group) max/argmax/NaN count; optional fp32 logits
 };
 
+// Shape of a packed weight matrix: the launch it is packed for.  A stream is
+// one wave's slice: (split, wg, wave) -> NB blocks of 32 rows for `len`
+// 64-wide K steps starting at split * len.
+struct PackShape {
+  int nb, wn, splits, len, n_wgs;
+  int swiglu;   // 1: rows [0, n_out) are gate rows, [n_out, 2 n_out) up rows; nb == 2
+  int n_out;    // SwiGLU output columns (d_ff)
+};
+
+__host__ __device__ inline long long packed_elems(const PackShape& p) {
+  return (long long)p.len * p.n_wgs * p.splits * p.wn * p.nb * 2048;
+}
+
+// Element offset of activation (row m, column k) in the fragment-packed layout
+// whose 64-row tiles hold ks 64-wide K steps: tile, step, 32-row half mb, then
+// piece j = (k % 32) / 8 and lane r + 32 g (r = m % 32, g = (k % 64) / 32).
+__host__ __device__ inline long long xpack_off(long long m, int k, int ks) {
+  const long long tile = m >> 6;
+  const int mb = (int)((m >> 5) & 1), r = (int)(m & 31);
+  const int s = k >> 6, kk = k & 63, g = kk >> 5, j = (kk >> 3) & 3, e = kk & 7;
+  return ((tile * ks + s) * 2 + mb) * 2048 + j * 512 + (r + 32 * g) * 8 + e;
+}
+
 struct GemmArgs {
-  const uint16_t* X;         // activations, bf16
-  int ldx;                   // row stride of X (elements)
-  const int32_t* gather;     // optional [E][cap] X row of each (expert, tile row); NULL = identity
-  const int32_t* count;      // optional [E] valid rows per expert; NULL = m_tiles*64
-  int cap;                   // rows per expert in gather space
-  int x_erows;               // without gather: X row = e * x_erows + tile row
+  int epi, nb, wn, pf;       // kernel variant
+  int n_wgs, splits, len;    // launch shape (matches the weight packing)
+  int N;                     // output columns (SwiGLU: d_ff)
+  int m_tiles;               // 64-row activation tiles
+  const uint16_t* X;         // packed activations
+  int x_ks;                  // K steps per activation tile
+  int x_etiles;              // MoE: activation tiles per expert (0 for dense)
+  const int32_t* count;      // MoE: [E] valid rows per expert; NULL = m_tiles * 64
+  const uint16_t* W;         // packed weights (+ e * w_estride)
+  long long w_estride;
   int o_erows;               // output row = e * o_erows + tile row
-  const uint16_t* W;         // weights, bf16 [N or 2N][K] (+ e * w_estride)
-  long long w_estride;       // elements between experts' weights
-  int N, K;
-  int m_tiles;               // 64-row tiles
-  int splits;                // K split across workgroups (EPI_STORE only)
   // EPI_STORE
-  float* out;                // [splits][out_rows][ldo]
+  float* out;
   long long out_split_stride;
   int ldo;
   // EPI_SWIGLU
-  uint16_t* act;             // bf16 [rows][lda]
-  int lda;
+  uint16_t* act;             // packed activations of the next GEMM
+  int act_ks;
   // EPI_ARGMAX
-  float* pmax;               // [rows][ld_part]
+  float* pmax;
   int32_t* pidx;
   int32_t* pnan;
   int ld_part;
@@ -76,22 +96,24 @@ struct AttnArgs {
   float* part_o;             // [B][Hq][S][qrows][dh]
   float* part_ml;            // [B][Hq][S][qrows][2]
   StepMeta meta;
-  int Hq, Hkv, dh, kv_cap, max_tree, qblocks, splits;
+  int Hq, Hkv, dh, kv_cap, max_tree, qblocks, splits, batch;
   float scale_log2;          // log2(e) / sqrt(dh)
 };
 
 // launchers (return hipGetLastError())
-hipError_t launch_gemm(int epi, int nb, int kw, const GemmArgs& a, int experts, hipStream_t s);
+hipError_t launch_gemm(const GemmArgs& a, int experts, hipStream_t s);
+hipError_t launch_pack_weight(const uint16_t* src, int rows, int K, const PackShape& p, uint16_t* dst,
+                              hipStream_t s);
 hipError_t launch_embed(const uint16_t* embed, const int32_t* token, int rows, int d, float* x, hipStream_t s);
 hipError_t launch_residual_rmsnorm(float* x, const ResidualAdd& add, const uint16_t* gain, float eps,
-                                   int rows, int d, uint16_t* xn, hipStream_t s);
+                                   int rows, int d, uint16_t* xn, int xn_ks, hipStream_t s);
 hipError_t launch_qkv_rope(const float* qkv_parts, int n_parts, long long part_stride, StepMeta meta,
                            const float* rope_cos, const float* rope_sin, int Hq, int Hkv, int dh,
                            int max_tree, int batch, int kv_cap, uint16_t* q_out, uint16_t* k_cache_l,
                            uint16_t* v_cache_l, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, int batch, hipStream_t s);
 hipError_t launch_attn_combine(const float* part_o, const float* part_ml, StepMeta meta, int Hq, int dh,
-                               int splits, int qrows, int max_tree, int batch, uint16_t* o_out,
+                               int splits, int qrows, int max_tree, int batch, uint16_t* o_out, int o_ks,
                                hipStream_t s);
 hipError_t launch_argmax_reduce(const float* pmax, const int32_t* pidx, const int32_t* pnan, int n_tiles,
                                 int ld_part, int rows, int32_t* pred, int32_t* nan_row, hipStream_t s);
@@ -100,9 +122,10 @@ hipError_t launch_accept(StepMeta meta, const int32_t* pred, const int32_t* nan_
 hipError_t launch_moe_route(const float* x, const uint16_t* gain, float eps, const uint16_t* w_router,
                             int rows, int d, int n_experts, int top_k, const int32_t* n_nodes,
                             int max_tree, int32_t* route_ids, float* route_w, hipStream_t s);
-hipError_t launch_moe_lists(const int32_t* route_ids, int rows, const int32_t* n_nodes, int max_tree,
-                            int n_experts, int top_k, int cap, int32_t* gather, int32_t* count,
-                            int32_t* slot, hipStream_t s);
+hipError_t launch_moe_lists(const int32_t* route_ids, int rows, int padded_rows, int n_experts, int top_k,
+                            int cap, int32_t* gather, int32_t* count, int32_t* slot, hipStream_t s);
+hipError_t launch_moe_gather(const uint16_t* xn, int xn_ks, const int32_t* gather, const int32_t* count,
+                             int n_experts, int cap, int d, uint16_t* xe, int xe_tiles, hipStream_t s);
 
 // Result block written by the acceptance kernel, per sequence b:
 // [0] accept_len, [1] nan flag, [2 .. 2+max_depth] tokens_out (max_depth+1),

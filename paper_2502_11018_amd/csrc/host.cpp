@@ -1,6 +1,6 @@
 // Host side of the C ABI declared in include/griffin_verify.h: argument and
-// tree validation, per-step metadata, workspace ownership and the launch
-// sequence of one verification pass.
+// tree validation, per-step metadata, weight packing, workspace ownership and
+// the launch sequence of one verification pass.
 
 #include <hip/hip_runtime.h>
 
@@ -19,6 +19,7 @@ using namespace griffin;
 namespace {
 
 constexpr int kMaxTree = 64;
+constexpr int kTargetWaves = 896;  // ~3.5 streaming waves per CU on 256 CUs
 
 int round_up(int x, int m) { return (x + m - 1) / m * m; }
 int cdiv(int x, int m) { return (x + m - 1) / m; }
@@ -83,23 +84,81 @@ int validate_desc(const griffin_model_desc* d, std::string* why) {
   return GRIFFIN_OK;
 }
 
+// Launch shape of one weight matrix (fixed at init; the packing follows it).
+struct GemmPlan {
+  int epi = 0, nb = 1, wn = 4, pf = 4;
+  int n_out = 0;   // output columns
+  int rows = 0;    // weight rows (SwiGLU: 2 * n_out)
+  int K = 0, ks = 0, ks_pad = 0;
+  PackShape shape{};
+  long long elems = 0;  // packed elements of one matrix (one expert)
+};
+
+GemmPlan plan_gemm(int epi, int n_out, int K, int experts = 1) {
+  GemmPlan p;
+  p.epi = epi;
+  p.n_out = n_out;
+  p.K = K;
+  p.ks = cdiv(K, 64);
+  int splits = 1;
+  if (epi == EPI_SWIGLU) {
+    p.nb = 2;
+    p.wn = 2;
+    p.rows = 2 * n_out;
+  } else {
+    p.nb = 1;
+    p.wn = 4;
+    p.rows = n_out;
+  }
+  const int n_blocks = cdiv(n_out, 32 * (epi == EPI_SWIGLU ? 1 : p.nb));
+  const int n_wgs = cdiv(n_blocks, p.wn);
+  if (epi == EPI_STORE) {
+    // split K so that the launch has ~kTargetWaves waves, preferring splits
+    // that divide the K steps (little or no zero padding)
+    const double want = (double)kTargetWaves / ((double)n_wgs * p.wn * experts);
+    double best_cost = 1e30;
+    for (int s = 1; s <= std::max(1, p.ks / 2) && s <= 16; ++s) {
+      const int len = cdiv(p.ks, s);
+      const double pad = (double)(len * s - p.ks) / p.ks;
+      const double cost = std::fabs(std::log((double)s / std::max(want, 1.0))) + 8.0 * pad;
+      if (cost < best_cost) {
+        best_cost = cost;
+        splits = s;
+      }
+    }
+  }
+  const int len = cdiv(p.ks, splits);
+  p.ks_pad = len * splits;
+  p.pf = len >= 8 ? 4 : 2;
+  p.shape = PackShape{p.nb, p.wn, splits, len, n_wgs, epi == EPI_SWIGLU ? 1 : 0, n_out};
+  p.elems = packed_elems(p.shape);
+  return p;
+}
+
 }  // namespace
 
 struct griffin_ctx {
   griffin_model_desc d{};
-  const uint16_t *embed = nullptr, *lm_head = nullptr, *final_norm = nullptr;
-  std::vector<const uint16_t*> attn_norm, w_qkv, w_o, mlp_norm, w_gu, w_down, w_router;
+  const uint16_t *embed = nullptr, *final_norm = nullptr;
+  std::vector<const uint16_t*> attn_norm, mlp_norm, w_router;
   uint16_t *k_cache = nullptr, *v_cache = nullptr;
   hipStream_t stream = nullptr;
 
-  int R = 0, Mpad = 0, qkv_n = 0, attn_w = 0, lm_tiles = 0, attn_splits = 1, qblocks = 1;
+  int R = 0, Mpad = 0, qkv_n = 0, attn_w = 0, attn_splits = 1, qblocks = 1;
   int E = 1, topk = 1;
   long long parts_elems = 0;
+
+  // launch plans and packed weights (owned)
+  GemmPlan p_qkv, p_o, p_gu, p_down, p_lm;
+  int xd_ks = 0;  // K steps per tile of activations with K = d_model
+  uint16_t* wpack = nullptr;
+  std::vector<const uint16_t*> pk_qkv, pk_o, pk_gu, pk_down;
+  const uint16_t* pk_lm = nullptr;
 
   std::vector<void*> allocs;
   float *x = nullptr, *parts = nullptr, *attn_po = nullptr, *attn_pml = nullptr;
   float *rope_cos = nullptr, *rope_sin = nullptr, *pmax = nullptr, *route_w = nullptr, *yslots = nullptr;
-  uint16_t *xn = nullptr, *q = nullptr, *o = nullptr, *act = nullptr;
+  uint16_t *xn = nullptr, *q = nullptr, *o = nullptr, *act = nullptr, *xe = nullptr;
   int32_t *pidx = nullptr, *pnan = nullptr, *pred = nullptr, *nan_row = nullptr, *result = nullptr;
   int32_t *route_ids = nullptr, *gather = nullptr, *count = nullptr, *slot = nullptr;
 
@@ -141,6 +200,12 @@ int hip_err(griffin_ctx* c, const char* what, hipError_t e) {
     if (e_ != hipSuccess) return hip_err((ctx), #call, e_);         \
   } while (0)
 
+#define TRY(expr)                      \
+  do {                                 \
+    int rc_ = (expr);                  \
+    if (rc_ != GRIFFIN_OK) return rc_; \
+  } while (0)
+
 template <typename T>
 int dev_alloc(griffin_ctx* c, T** p, size_t count) {
   void* raw = nullptr;
@@ -154,41 +219,20 @@ int dev_alloc(griffin_ctx* c, T** p, size_t count) {
   return GRIFFIN_OK;
 }
 
-#define TRY(expr)                   \
-  do {                              \
-    int rc_ = (expr);               \
-    if (rc_ != GRIFFIN_OK) return rc_; \
-  } while (0)
-
-// K-split count for a streaming GEMM: aim at ~512 workgroups, keep >= 4
-// 64-wide K steps per wave.
-int choose_splits(int tiles, int K, int kw) {
-  const int steps = cdiv(K, 64);
-  const int max_split = std::max(1, steps / (kw * 4));
-  return std::max(1, std::min(cdiv(512, tiles), max_split));
-}
-
-struct Plan {
-  int qkv_splits, o_splits, down_splits;
-};
-
-Plan make_plan(const griffin_ctx* c, int m_tiles) {
-  Plan p{};
-  p.qkv_splits = choose_splits(cdiv(c->qkv_n, 32) * m_tiles, c->d.d_model, 4);
-  p.o_splits = choose_splits(cdiv(c->d.d_model, 32) * m_tiles, c->attn_w, 4);
-  p.down_splits = choose_splits(cdiv(c->d.d_model, 32) * m_tiles, c->d.d_ff, 4);
-  return p;
-}
-
-GemmArgs gemm_base(const uint16_t* X, int ldx, const uint16_t* W, int N, int K, int m_tiles) {
+GemmArgs gemm_args(const GemmPlan& p, const uint16_t* X, int x_ks, const uint16_t* W, int m_tiles) {
   GemmArgs a{};
-  a.X = X;
-  a.ldx = ldx;
-  a.W = W;
-  a.N = N;
-  a.K = K;
+  a.epi = p.epi;
+  a.nb = p.nb;
+  a.wn = p.wn;
+  a.pf = p.pf;
+  a.n_wgs = p.shape.n_wgs;
+  a.splits = p.shape.splits;
+  a.len = p.shape.len;
+  a.N = p.n_out;
   a.m_tiles = m_tiles;
-  a.splits = 1;
+  a.X = X;
+  a.x_ks = x_ks;
+  a.W = W;
   return a;
 }
 
@@ -227,7 +271,6 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
   const int rows = B * d.max_tree;
   const int Mpad = round_up(rows, 64);
   const int m_tiles = Mpad / 64;
-  const Plan plan = make_plan(c, m_tiles);
   const long long ps = (long long)Mpad;  // rows per split slice of `parts`
   hipStream_t s = c->stream;
   const size_t layer_kv = (size_t)d.max_batch * d.n_kv_heads * d.kv_capacity * d.head_dim;
@@ -237,21 +280,20 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
   ResidualAdd add_down{};
   for (int l = 0; l < d.n_layers; ++l) {
     // ---- attention block
-    LAUNCH(GRIFFIN_KC_NORM, launch_residual_rmsnorm(c->x, l == 0 ? none : add_down, c->attn_norm[l], d.rms_eps, Mpad,
-                                       d.d_model, c->xn, s));
+    LAUNCH(GRIFFIN_KC_NORM, launch_residual_rmsnorm(c->x, l == 0 ? none : add_down, c->attn_norm[l], d.rms_eps,
+                                                    Mpad, d.d_model, c->xn, c->xd_ks, s));
     {
-      GemmArgs a = gemm_base(c->xn, d.d_model, c->w_qkv[l], c->qkv_n, d.d_model, m_tiles);
-      a.splits = plan.qkv_splits;
+      GemmArgs a = gemm_args(c->p_qkv, c->xn, c->xd_ks, c->pk_qkv[l], m_tiles);
       a.out = c->parts;
       a.ldo = c->qkv_n;
       a.out_split_stride = ps * c->qkv_n;
-      LAUNCH(GRIFFIN_KC_QKV, launch_gemm(EPI_STORE, 1, 4, a, 1, s));
+      LAUNCH(GRIFFIN_KC_QKV, launch_gemm(a, 1, s));
     }
     uint16_t* kc = c->k_cache + (size_t)l * layer_kv;
     uint16_t* vc = c->v_cache + (size_t)l * layer_kv;
-    LAUNCH(GRIFFIN_KC_ROPE, launch_qkv_rope(c->parts, plan.qkv_splits, ps * c->qkv_n, c->meta, c->rope_cos, c->rope_sin,
-                               d.n_q_heads, d.n_kv_heads, d.head_dim, d.max_tree, B, d.kv_capacity, c->q, kc, vc,
-                               s));
+    LAUNCH(GRIFFIN_KC_ROPE, launch_qkv_rope(c->parts, c->p_qkv.shape.splits, ps * c->qkv_n, c->meta, c->rope_cos,
+                                            c->rope_sin, d.n_q_heads, d.n_kv_heads, d.head_dim, d.max_tree, B,
+                                            d.kv_capacity, c->q, kc, vc, s));
     {
       AttnArgs a{};
       a.q = c->q;
@@ -267,86 +309,94 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
       a.max_tree = d.max_tree;
       a.qblocks = c->qblocks;
       a.splits = c->attn_splits;
+      a.batch = B;
       a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.head_dim));
       LAUNCH(GRIFFIN_KC_ATTN, launch_attention(a, B, s));
     }
-    LAUNCH(GRIFFIN_KC_ATTN, launch_attn_combine(c->attn_po, c->attn_pml, c->meta, d.n_q_heads, d.head_dim, c->attn_splits,
-                                   c->qblocks * 32, d.max_tree, B, c->o, s));
+    LAUNCH(GRIFFIN_KC_ATTN, launch_attn_combine(c->attn_po, c->attn_pml, c->meta, d.n_q_heads, d.head_dim,
+                                                c->attn_splits, c->qblocks * 32, d.max_tree, B, c->o,
+                                                c->p_o.ks_pad, s));
     {
-      GemmArgs a = gemm_base(c->o, c->attn_w, c->w_o[l], d.d_model, c->attn_w, m_tiles);
-      a.splits = plan.o_splits;
+      GemmArgs a = gemm_args(c->p_o, c->o, c->p_o.ks_pad, c->pk_o[l], m_tiles);
       a.out = c->parts;
       a.ldo = d.d_model;
       a.out_split_stride = ps * d.d_model;
-      LAUNCH(GRIFFIN_KC_O, launch_gemm(EPI_STORE, 1, 4, a, 1, s));
+      LAUNCH(GRIFFIN_KC_O, launch_gemm(a, 1, s));
     }
     ResidualAdd add_o{};
     add_o.parts = c->parts;
-    add_o.n_parts = plan.o_splits;
+    add_o.n_parts = c->p_o.shape.splits;
     add_o.part_stride = ps * d.d_model;
-    LAUNCH(GRIFFIN_KC_NORM, launch_residual_rmsnorm(c->x, add_o, c->mlp_norm[l], d.rms_eps, Mpad, d.d_model, c->xn, s));
+    LAUNCH(GRIFFIN_KC_NORM, launch_residual_rmsnorm(c->x, add_o, c->mlp_norm[l], d.rms_eps, Mpad, d.d_model, c->xn,
+                                                    c->xd_ks, s));
 
     // ---- MLP block
     if (c->E == 1) {
-      GemmArgs g = gemm_base(c->xn, d.d_model, c->w_gu[l], d.d_ff, d.d_model, m_tiles);
+      GemmArgs g = gemm_args(c->p_gu, c->xn, c->xd_ks, c->pk_gu[l], m_tiles);
       g.act = c->act;
-      g.lda = d.d_ff;
-      LAUNCH(GRIFFIN_KC_GATE_UP, launch_gemm(EPI_SWIGLU, 2, 4, g, 1, s));
-      GemmArgs dn = gemm_base(c->act, d.d_ff, c->w_down[l], d.d_model, d.d_ff, m_tiles);
-      dn.splits = plan.down_splits;
+      g.act_ks = c->p_down.ks_pad;
+      LAUNCH(GRIFFIN_KC_GATE_UP, launch_gemm(g, 1, s));
+      GemmArgs dn = gemm_args(c->p_down, c->act, c->p_down.ks_pad, c->pk_down[l], m_tiles);
       dn.out = c->parts;
       dn.ldo = d.d_model;
       dn.out_split_stride = ps * d.d_model;
-      LAUNCH(GRIFFIN_KC_DOWN, launch_gemm(EPI_STORE, 1, 4, dn, 1, s));
+      LAUNCH(GRIFFIN_KC_DOWN, launch_gemm(dn, 1, s));
       add_down = ResidualAdd{};
       add_down.parts = c->parts;
-      add_down.n_parts = plan.down_splits;
+      add_down.n_parts = c->p_down.shape.splits;
       add_down.part_stride = ps * d.d_model;
     } else {
-      LAUNCH(GRIFFIN_KC_OTHER, launch_moe_route(c->x, c->mlp_norm[l], d.rms_eps, c->w_router[l], rows, d.d_model, c->E, c->topk,
-                                  c->meta.n_nodes, d.max_tree, c->route_ids, c->route_w, s));
-      LAUNCH(GRIFFIN_KC_OTHER, launch_moe_lists(c->route_ids, rows, c->meta.n_nodes, d.max_tree, c->E, c->topk, Mpad, c->gather,
-                                  c->count, c->slot, s));
-      GemmArgs g = gemm_base(c->xn, d.d_model, c->w_gu[l], d.d_ff, d.d_model, m_tiles);
-      g.gather = c->gather;
+      const int xe_tiles = Mpad / 64;
+      LAUNCH(GRIFFIN_KC_OTHER, launch_moe_route(c->x, c->mlp_norm[l], d.rms_eps, c->w_router[l], rows, d.d_model,
+                                                c->E, c->topk, c->meta.n_nodes, d.max_tree, c->route_ids,
+                                                c->route_w, s));
+      LAUNCH(GRIFFIN_KC_OTHER, launch_moe_lists(c->route_ids, rows, Mpad, c->E, c->topk, Mpad, c->gather, c->count,
+                                                c->slot, s));
+      LAUNCH(GRIFFIN_KC_OTHER, launch_moe_gather(c->xn, c->xd_ks, c->gather, c->count, c->E, Mpad, d.d_model,
+                                                 c->xe, xe_tiles, s));
+      GemmArgs g = gemm_args(c->p_gu, c->xe, c->xd_ks, c->pk_gu[l], m_tiles);
+      g.x_etiles = xe_tiles;
       g.count = c->count;
-      g.cap = Mpad;
       g.o_erows = Mpad;
-      g.w_estride = 2LL * d.d_ff * d.d_model;
+      g.w_estride = c->p_gu.elems;
       g.act = c->act;
-      g.lda = d.d_ff;
-      LAUNCH(GRIFFIN_KC_GATE_UP, launch_gemm(EPI_SWIGLU, 2, 4, g, c->E, s));
-      GemmArgs dn = gemm_base(c->act, d.d_ff, c->w_down[l], d.d_model, d.d_ff, m_tiles);
+      g.act_ks = c->p_down.ks_pad;
+      LAUNCH(GRIFFIN_KC_GATE_UP, launch_gemm(g, c->E, s));
+      GemmArgs dn = gemm_args(c->p_down, c->act, c->p_down.ks_pad, c->pk_down[l], m_tiles);
+      dn.x_etiles = xe_tiles;
       dn.count = c->count;
-      dn.cap = Mpad;
-      dn.x_erows = Mpad;
       dn.o_erows = Mpad;
-      dn.w_estride = (long long)d.d_model * d.d_ff;
+      dn.w_estride = c->p_down.elems;
       dn.out = c->yslots;
       dn.ldo = d.d_model;
-      LAUNCH(GRIFFIN_KC_DOWN, launch_gemm(EPI_STORE, 1, 4, dn, c->E, s));
+      dn.out_split_stride = (long long)c->E * Mpad * d.d_model;
+      LAUNCH(GRIFFIN_KC_DOWN, launch_gemm(dn, c->E, s));
       add_down = ResidualAdd{};
       add_down.parts = c->yslots;
       add_down.slot = c->slot;
       add_down.slot_w = c->route_w;
       add_down.top_k = c->topk;
-      add_down.n_parts = 1;
+      add_down.n_parts = c->p_down.shape.splits;
+      add_down.part_stride = (long long)c->E * Mpad * d.d_model;
     }
   }
-  // ---- final norm, LM head with fused per-tile argmax, reduction, acceptance
-  LAUNCH(GRIFFIN_KC_NORM, launch_residual_rmsnorm(c->x, add_down, c->final_norm, d.rms_eps, Mpad, d.d_model, c->xn, s));
+  // ---- final norm, LM head with fused per-wave argmax, reduction, acceptance
+  LAUNCH(GRIFFIN_KC_NORM, launch_residual_rmsnorm(c->x, add_down, c->final_norm, d.rms_eps, Mpad, d.d_model, c->xn,
+                                                  c->xd_ks, s));
+  const int lm_parts = c->p_lm.shape.n_wgs * c->p_lm.wn;
   {
-    GemmArgs a = gemm_base(c->xn, d.d_model, c->lm_head, d.vocab, d.d_model, m_tiles);
+    GemmArgs a = gemm_args(c->p_lm, c->xn, c->xd_ks, c->pk_lm, m_tiles);
     a.pmax = c->pmax;
     a.pidx = c->pidx;
     a.pnan = c->pnan;
-    a.ld_part = c->lm_tiles;
+    a.ld_part = lm_parts;
     a.logits = logits_out;
     a.ld_logits = d.vocab;
     a.logit_rows = rows;
-    LAUNCH(GRIFFIN_KC_LM_HEAD, launch_gemm(EPI_ARGMAX, 1, 4, a, 1, s));
+    LAUNCH(GRIFFIN_KC_LM_HEAD, launch_gemm(a, 1, s));
   }
-  LAUNCH(GRIFFIN_KC_OTHER, launch_argmax_reduce(c->pmax, c->pidx, c->pnan, c->lm_tiles, c->lm_tiles, rows, c->pred, c->nan_row, s));
+  LAUNCH(GRIFFIN_KC_OTHER, launch_argmax_reduce(c->pmax, c->pidx, c->pnan, lm_parts, lm_parts, rows, c->pred,
+                                                c->nan_row, s));
   LAUNCH(GRIFFIN_KC_OTHER, launch_accept(c->meta, c->pred, c->nan_row, B, d.max_tree, d.max_depth, c->result, s));
   return GRIFFIN_OK;
 }
@@ -413,7 +463,8 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
   if (!w->embed || !w->lm_head || !w->final_norm || !w->attn_norm || !w->w_qkv || !w->w_o || !w->mlp_norm ||
       !w->w_gate_up || !w->w_down || (moe && !w->w_router))
     return GRIFFIN_EINVAL;
-  if (!aligned16(w->embed) || !aligned16(w->lm_head) || !aligned16(k_cache) || !aligned16(v_cache))
+  if (!aligned16(w->embed) || !aligned16(w->lm_head) || !aligned16(w->final_norm) || !aligned16(k_cache) ||
+      !aligned16(v_cache))
     return GRIFFIN_EINVAL;
   for (int l = 0; l < d.n_layers; ++l) {
     const void* ps[] = {w->attn_norm[l], w->w_qkv[l], w->w_o[l], w->mlp_norm[l], w->w_gate_up[l], w->w_down[l],
@@ -426,15 +477,10 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
   if (!c) return GRIFFIN_ENOMEM;
   c->d = d;
   c->embed = static_cast<const uint16_t*>(w->embed);
-  c->lm_head = static_cast<const uint16_t*>(w->lm_head);
   c->final_norm = static_cast<const uint16_t*>(w->final_norm);
   for (int l = 0; l < d.n_layers; ++l) {
     c->attn_norm.push_back(static_cast<const uint16_t*>(w->attn_norm[l]));
-    c->w_qkv.push_back(static_cast<const uint16_t*>(w->w_qkv[l]));
-    c->w_o.push_back(static_cast<const uint16_t*>(w->w_o[l]));
     c->mlp_norm.push_back(static_cast<const uint16_t*>(w->mlp_norm[l]));
-    c->w_gu.push_back(static_cast<const uint16_t*>(w->w_gate_up[l]));
-    c->w_down.push_back(static_cast<const uint16_t*>(w->w_down[l]));
     c->w_router.push_back(moe ? static_cast<const uint16_t*>(w->w_router[l]) : nullptr);
   }
   c->k_cache = static_cast<uint16_t*>(k_cache);
@@ -447,44 +493,49 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
   c->Mpad = round_up(c->R, 64);
   c->qkv_n = (d.n_q_heads + 2 * d.n_kv_heads) * d.head_dim;
   c->attn_w = d.n_q_heads * d.head_dim;
-  c->lm_tiles = cdiv(d.vocab, 32);
   c->qblocks = cdiv(d.max_tree, 32);
   {
     const int by_len = cdiv(d.kv_capacity, 256);
     const int by_par = std::max(1, cdiv(2048, d.max_batch * d.n_q_heads * c->qblocks));
-    c->attn_splits = std::max(1, std::min(std::min(by_len, by_par), 64));
+    c->attn_splits = std::max(1, std::min(std::min(by_len, by_par), 16));
   }
+  c->p_qkv = plan_gemm(EPI_STORE, c->qkv_n, d.d_model);
+  c->p_o = plan_gemm(EPI_STORE, d.d_model, c->attn_w);
+  c->p_gu = plan_gemm(EPI_SWIGLU, d.d_ff, d.d_model, c->E);
+  c->p_down = plan_gemm(EPI_STORE, d.d_model, d.d_ff, c->E);
+  c->p_lm = plan_gemm(EPI_ARGMAX, d.vocab, d.d_model);
+  c->xd_ks = std::max({c->p_qkv.ks_pad, c->p_gu.ks_pad, c->p_lm.ks_pad});
   const long long Mp = c->Mpad;
-  // the split plan depends on the batch of each step: size for the largest
-  for (int mt = 1; mt <= c->Mpad / 64; ++mt) {
-    const Plan plan = make_plan(c, mt);
-    c->parts_elems = std::max(c->parts_elems,
-                              64LL * mt * std::max({(long long)plan.qkv_splits * c->qkv_n,
-                                                    (long long)plan.o_splits * d.d_model,
-                                                    (long long)plan.down_splits * d.d_model}));
-  }
+  const long long tiles = Mp / 64;
+  c->parts_elems = Mp * std::max({(long long)c->p_qkv.shape.splits * c->qkv_n,
+                                  (long long)c->p_o.shape.splits * d.d_model,
+                                  (long long)c->p_down.shape.splits * d.d_model});
   const int qrows = c->qblocks * 32;
 
-#define ALLOC(ptr, n)                          \
-  do {                                         \
-    int rc_ = dev_alloc(c, &(ptr), (size_t)(n)); \
-    if (rc_ != GRIFFIN_OK) {                   \
-      griffin_verify_free(c);                  \
-      return rc_;                              \
-    }                                          \
+#define ALLOC(ptr, n)                              \
+  do {                                             \
+    int rc_ = dev_alloc(c, &(ptr), (size_t)(n));   \
+    if (rc_ != GRIFFIN_OK) {                       \
+      griffin_verify_free(c);                      \
+      return rc_;                                  \
+    }                                              \
   } while (0)
 
+  // packed weights, one buffer: per layer qkv, o, gate/up (E experts), down (E experts); then the LM head
+  const long long per_layer = c->p_qkv.elems + c->p_o.elems + (long long)c->E * (c->p_gu.elems + c->p_down.elems);
+  ALLOC(c->wpack, per_layer * d.n_layers + c->p_lm.elems);
   ALLOC(c->x, Mp * d.d_model);
-  ALLOC(c->xn, Mp * d.d_model);
+  ALLOC(c->xn, tiles * c->xd_ks * 4096);
   ALLOC(c->parts, c->parts_elems);
   ALLOC(c->q, Mp * c->attn_w);
-  ALLOC(c->o, Mp * c->attn_w);
+  ALLOC(c->o, tiles * c->p_o.ks_pad * 4096);
   ALLOC(c->attn_po, (long long)d.max_batch * d.n_q_heads * c->attn_splits * qrows * d.head_dim);
   ALLOC(c->attn_pml, (long long)d.max_batch * d.n_q_heads * c->attn_splits * qrows * 2);
-  ALLOC(c->act, (long long)c->E * Mp * d.d_ff);
-  ALLOC(c->pmax, Mp * c->lm_tiles);
-  ALLOC(c->pidx, Mp * c->lm_tiles);
-  ALLOC(c->pnan, Mp * c->lm_tiles);
+  ALLOC(c->act, (long long)c->E * tiles * c->p_down.ks_pad * 4096);
+  const long long lm_parts = (long long)c->p_lm.shape.n_wgs * c->p_lm.wn;
+  ALLOC(c->pmax, Mp * lm_parts);
+  ALLOC(c->pidx, Mp * lm_parts);
+  ALLOC(c->pnan, Mp * lm_parts);
   ALLOC(c->pred, Mp);
   ALLOC(c->nan_row, Mp);
   ALLOC(c->result, (long long)d.max_batch * result_stride(d.max_depth));
@@ -496,9 +547,48 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
     ALLOC(c->gather, (long long)c->E * Mp);
     ALLOC(c->count, c->E);
     ALLOC(c->slot, Mp * c->topk);
-    ALLOC(c->yslots, (long long)c->E * Mp * d.d_model);
+    ALLOC(c->yslots, (long long)c->p_down.shape.splits * c->E * Mp * d.d_model);
+    ALLOC(c->xe, (long long)c->E * tiles * c->xd_ks * 4096);
   }
 #undef ALLOC
+
+  // pack the weight matrices (the caller's copies are not read after this)
+  {
+    uint16_t* dst = c->wpack;
+    hipError_t e = hipSuccess;
+    for (int l = 0; l < d.n_layers && e == hipSuccess; ++l) {
+      c->pk_qkv.push_back(dst);
+      e = launch_pack_weight(static_cast<const uint16_t*>(w->w_qkv[l]), c->qkv_n, d.d_model, c->p_qkv.shape, dst,
+                             c->stream);
+      dst += c->p_qkv.elems;
+      c->pk_o.push_back(dst);
+      if (e == hipSuccess)
+        e = launch_pack_weight(static_cast<const uint16_t*>(w->w_o[l]), d.d_model, c->attn_w, c->p_o.shape, dst,
+                               c->stream);
+      dst += c->p_o.elems;
+      c->pk_gu.push_back(dst);
+      for (int x = 0; x < c->E && e == hipSuccess; ++x) {
+        e = launch_pack_weight(static_cast<const uint16_t*>(w->w_gate_up[l]) + (size_t)x * 2 * d.d_ff * d.d_model,
+                               2 * d.d_ff, d.d_model, c->p_gu.shape, dst, c->stream);
+        dst += c->p_gu.elems;
+      }
+      c->pk_down.push_back(dst);
+      for (int x = 0; x < c->E && e == hipSuccess; ++x) {
+        e = launch_pack_weight(static_cast<const uint16_t*>(w->w_down[l]) + (size_t)x * d.d_model * d.d_ff,
+                               d.d_model, d.d_ff, c->p_down.shape, dst, c->stream);
+        dst += c->p_down.elems;
+      }
+    }
+    c->pk_lm = dst;
+    if (e == hipSuccess)
+      e = launch_pack_weight(static_cast<const uint16_t*>(w->lm_head), d.vocab, d.d_model, c->p_lm.shape, dst,
+                             c->stream);
+    if (e == hipSuccess) e = hipStreamSynchronize(c->stream);
+    if (e != hipSuccess) {
+      griffin_verify_free(c);
+      return GRIFFIN_EHIP;
+    }
+  }
 
   // rotary tables: angle pos * base^(-2j/dh) evaluated in double, stored fp32
   {
@@ -520,7 +610,7 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
     }
   }
 
-  // metadata layout (8-byte aligned sections)
+  // metadata layout (256-byte aligned sections)
   {
     size_t off = 0;
     auto take = [&](size_t bytes) {

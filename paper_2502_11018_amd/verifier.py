@@ -111,7 +111,7 @@ class TreeVerifier:
         if k_cache is None:
             k_cache = torch.zeros((L, max_batch, Hkv, kv_capacity, dh), dtype=torch.bfloat16, device=dev)
         if v_cache is None:
-            v_cache = torch.zeros((L, max_batch, Hkv, dh, kv_capacity), dtype=torch.bfloat16, device=dev)
+            v_cache = torch.zeros((L, max_batch, Hkv, kv_capacity // 32, dh, 32), dtype=torch.bfloat16, device=dev)
         need = N.lib.griffin_kv_cache_bytes(byref(self.desc))
         for t in (k_cache, v_cache):
             if t.dtype != torch.bfloat16 or not t.is_contiguous() or t.numel() * 2 != need:
@@ -138,12 +138,28 @@ class TreeVerifier:
         self._batch = 0
 
     # ------------------------------------------------------------ KV cache ----
+    def _v_tiles(self, layer: int, seq: int) -> torch.Tensor:
+        Hkv, dh = self.shape.n_kv_heads, self.shape.head_dim
+        return self.v_cache.view(self.shape.n_layers, self.max_batch, Hkv, self.kv_capacity // 32, dh, 32)[layer, seq]
+
     def write_prefix(self, layer: int, seq: int, k: torch.Tensor, v: torch.Tensor):
         """Place a cached prefix: k, v bf16 [Hkv, P, dh] (k post-rotary)."""
         P = k.shape[1]
+        full, rem = divmod(P, 32)
+        tiles = self._v_tiles(layer, seq)                      # [Hkv, cap/32, dh, 32]
         with torch.cuda.stream(self.stream):
-            self.k_cache[layer, seq, :, :P, :].copy_(k)
-            self.v_cache[layer, seq, :, :, :P].copy_(v.transpose(-1, -2))
+            self.k_cache.view(self.shape.n_layers, self.max_batch, self.shape.n_kv_heads, self.kv_capacity,
+                              self.shape.head_dim)[layer, seq, :, :P, :].copy_(k)
+            if full:
+                tiles[:, :full].copy_(v[:, : full * 32].reshape(v.shape[0], full, 32, v.shape[2]).transpose(-1, -2))
+            if rem:
+                tiles[:, full, :, :rem].copy_(v[:, full * 32:].transpose(-1, -2))
+
+    def read_v(self, layer: int, seq: int, n: int) -> torch.Tensor:
+        """Cached values of slots [0, n) as [Hkv, n, dh]."""
+        tiles = self._v_tiles(layer, seq)
+        Hkv, nt, dh, _ = tiles.shape
+        return tiles.transpose(-1, -2).reshape(Hkv, nt * 32, dh)[:, :n]
 
     # ---------------------------------------------------------------- step ----
     def step(self, prefix_len, trees: Sequence, logits_out: Optional[torch.Tensor] = None):

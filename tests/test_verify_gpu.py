@@ -278,7 +278,7 @@ def test_gpu_prefill_by_chain_steps_matches_oracle_prefill():
         torch.cuda.synchronize()
         for l in range(m.n_layers):
             kg = v.k_cache[l, 0, :, : len(toks), :].float().cpu().numpy()
-            vg = v.v_cache[l, 0, :, :, : len(toks)].transpose(-1, -2).float().cpu().numpy()
+            vg = v.read_v(l, 0, len(toks)).float().cpu().numpy()
             for ref, got in ((kv.K[l], kg), (kv.V[l], vg)):
                 rel = np.abs(got - ref).max() / np.abs(ref).max()
                 assert rel < 3e-2, (l, rel)
