@@ -17,6 +17,8 @@
 //    16-byte load of 8 consecutive slots.
 //  * Q and K use the same head-dim permutation as the projection GEMMs: a lane
 //    reads 32 consecutive head dims and feeds 8 of them to each of 4 MFMAs.
+//  * Q and P enter the matrix cores as split bf16 (hi + lo, two MFMAs each),
+//    so only the cached K/V carry bf16 rounding.
 // Scores are kept in the log2 domain (scaled by log2(e)/sqrt(dh)) and exp2 is
 // used throughout; masked keys contribute exactly zero.
 
@@ -68,14 +70,18 @@ __global__ __launch_bounds__(64) void tree_attention_kernel(AttnArgs a) {
   const int qr = b * a.max_tree + (qlive ? qi : 0);
   const uint64_t anc = qlive ? a.meta.anc[qr] : 0ull;
 
-  // Q^T operand (B): lane (col = query row, hh = k-group), 32 dims per chunk
-  u32x4 qf[CH][4];
+  // Q^T operand (B): lane (col = query row, hh = k-group), 32 dims per chunk;
+  // split bf16, so S = K (q_hi + q_lo)
+  u32x4 qf[2][CH][4];
   {
-    const uint16_t* qp = a.q + ((long long)qr * a.Hq + hq) * DH + 32 * hh;
+    const long long qo = ((long long)qr * a.Hq + hq) * DH + 32 * hh;
 #pragma unroll
     for (int c = 0; c < CH; ++c)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) qf[c][j] = ld_u4(qp + 64 * c + 8 * j);
+      for (int j = 0; j < 4; ++j) {
+        qf[0][c][j] = ld_u4(a.q + qo + 64 * c + 8 * j);
+        qf[1][c][j] = ld_u4(a.q_lo + qo + 64 * c + 8 * j);
+      }
   }
 
   const long long head = ((long long)b * a.Hkv + hk) * a.kv_cap * DH;
@@ -125,7 +131,9 @@ __global__ __launch_bounds__(64) void tree_attention_kernel(AttnArgs a) {
     for (int c = 0; c < CH; ++c)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[buf][c][j]), as_bf16x8(qf[c][j]), s, 0, 0, 0);
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+          s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[buf][c][j]), as_bf16x8(qf[h][c][j]), s, 0, 0, 0);
 
     // ---- scale + mask (this lane: query qi, keys key0 + 16 hh + r)
     float mx = -INFINITY;
@@ -183,17 +191,22 @@ __global__ __launch_bounds__(64) void tree_attention_kernel(AttnArgs a) {
         }
     }
 
-    // ---- O^T += V^T P^T
+    // ---- O^T += V^T P^T, P as split bf16 (p_hi + p_lo)
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
-      u32x4 pf;
-      pf[0] = pack_bf16x2(p[8 * t + 0], p[8 * t + 1]);
-      pf[1] = pack_bf16x2(p[8 * t + 2], p[8 * t + 3]);
-      pf[2] = pack_bf16x2(p[8 * t + 4], p[8 * t + 5]);
-      pf[3] = pack_bf16x2(p[8 * t + 6], p[8 * t + 7]);
+      u32x4 pf[2];
 #pragma unroll
-      for (int d = 0; d < DB; ++d)
-        oacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf[buf][d][t]), as_bf16x8(pf), oacc[d], 0, 0, 0);
+      for (int w = 0; w < 4; ++w) {
+        const Hilo2 hl = pack_hilo2(p[8 * t + 2 * w], p[8 * t + 2 * w + 1]);
+        pf[0][w] = hl.hi;
+        pf[1][w] = hl.lo;
+      }
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int d = 0; d < DB; ++d)
+          oacc[d] =
+              __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf[buf][d][t]), as_bf16x8(pf[h]), oacc[d], 0, 0, 0);
     }
   };
 
@@ -237,7 +250,7 @@ hipError_t launch_attention(const AttnArgs& a, int batch, hipStream_t s) {
 
 // Merge the splits of every (row, head): o = sum_s 2^(m_s - M) o_s / sum_s 2^(m_s - M) l_s.
 // Absent rows get zeros.  One workgroup per row, one thread per (head, dim).
-// The merged rows are written fragment-packed (o_ks K steps per tile) as the
+// The merged rows are written fragment-packed split bf16 (o_ks K steps per tile) as the
 // activation operand of the output projection.  One thread per (head, 4 dims).
 template <int MAXS>
 __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ part_o,
@@ -280,8 +293,10 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
       out = make_float4(num.x * inv, num.y * inv, num.z * inv, num.w * inv);
     }
   }
-  *reinterpret_cast<uint2*>(o_out + xpack_off(r, h * dh + d, o_ks)) =
-      make_uint2(pack_bf16x2(out.x, out.y), pack_bf16x2(out.z, out.w));
+  uint16_t* dst = o_out + xpack_off(r, h * dh + d, o_ks);
+  const Hilo2 p0 = pack_hilo2(out.x, out.y), p1 = pack_hilo2(out.z, out.w);
+  *reinterpret_cast<uint2*>(dst) = make_uint2(p0.hi, p1.hi);
+  *reinterpret_cast<uint2*>(dst + XPACK_LO) = make_uint2(p0.lo, p1.lo);
 }
 
 hipError_t launch_attn_combine(const float* part_o, const float* part_ml, StepMeta meta, int Hq, int dh, int splits,

@@ -26,6 +26,17 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return uint32_t(f32_to_bf16(lo)) | (uint32_t(f32_to_bf16(hi)) << 16);
 }
 
+// Split-bf16 operand: x ~ hi + lo with hi = bf16(x) and lo = bf16(x - hi),
+// which carries about 16 significant bits through the bf16 matrix cores.
+struct Hilo2 {
+  uint32_t hi, lo;
+};
+__device__ __forceinline__ Hilo2 pack_hilo2(float a, float b) {
+  const uint16_t ha = f32_to_bf16(a), hb = f32_to_bf16(b);
+  return {uint32_t(ha) | (uint32_t(hb) << 16),
+          pack_bf16x2(a - bf16_to_f32(ha), b - bf16_to_f32(hb))};
+}
+
 __device__ __forceinline__ bf16x8 as_bf16x8(const u32x4& v) { return __builtin_bit_cast(bf16x8, v); }
 
 __device__ __forceinline__ u32x4 zero_u4() { return u32x4{0u, 0u, 0u, 0u}; }
@@ -36,6 +47,17 @@ __device__ __forceinline__ u32x4 ld_u4(const uint16_t* p) { return *reinterpret_
 // non-temporal: data read once (streamed weights)
 __device__ __forceinline__ u32x4 ld_u4_nt(const uint16_t* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Wait until at most N vector-memory instructions of this wave are
+// outstanding and all of its LDS reads have returned (gfx9 s_waitcnt encoding:
+// vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_lds() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0x0 << 8) | ((N >> 4) << 14));
 }
 
 __device__ __forceinline__ float wave_sum(float v) {

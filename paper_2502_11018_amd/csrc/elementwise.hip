@@ -110,10 +110,11 @@ __global__ __launch_bounds__(RN_THREADS) void residual_rmsnorm_kernel(float* __r
     if (ok[u]) {
       const uint2 gg = *reinterpret_cast<const uint2*>(gain + 4 * gi[u]);
       const float4 a = v[u];
-      uint2 o;
-      o.x = pack_bf16x2(a.x * rs * bf16_to_f32(gg.x & 0xffff), a.y * rs * bf16_to_f32(gg.x >> 16));
-      o.y = pack_bf16x2(a.z * rs * bf16_to_f32(gg.y & 0xffff), a.w * rs * bf16_to_f32(gg.y >> 16));
-      *reinterpret_cast<uint2*>(xn + xpack_off(r, 4 * gi[u], xn_ks)) = o;  // fragment-packed GEMM operand
+      const Hilo2 p0 = pack_hilo2(a.x * rs * bf16_to_f32(gg.x & 0xffff), a.y * rs * bf16_to_f32(gg.x >> 16));
+      const Hilo2 p1 = pack_hilo2(a.z * rs * bf16_to_f32(gg.y & 0xffff), a.w * rs * bf16_to_f32(gg.y >> 16));
+      uint16_t* dst = xn + xpack_off(r, 4 * gi[u], xn_ks);  // fragment-packed split-bf16 GEMM operand
+      *reinterpret_cast<uint2*>(dst) = make_uint2(p0.hi, p1.hi);
+      *reinterpret_cast<uint2*>(dst + XPACK_LO) = make_uint2(p0.lo, p1.lo);
     }
   }
 }
@@ -159,9 +160,11 @@ __global__ __launch_bounds__(256) void moe_gather_kernel(const uint16_t* __restr
   if (c >= count[e]) return;
   const int src = gather[e * cap + c];
   const long long dst_row = (long long)e * xe_tiles * 64 + c;
-  for (int k = threadIdx.x * 8; k < d; k += blockDim.x * 8)
-    *reinterpret_cast<u32x4*>(xe + xpack_off(dst_row, k, ks)) =
-        *reinterpret_cast<const u32x4*>(xn + xpack_off(src, k, ks));
+  for (int k = threadIdx.x * 8; k < d; k += blockDim.x * 8) {
+    const long long o = xpack_off(dst_row, k, ks), i = xpack_off(src, k, ks);
+    *reinterpret_cast<u32x4*>(xe + o) = *reinterpret_cast<const u32x4*>(xn + i);
+    *reinterpret_cast<u32x4*>(xe + o + XPACK_LO) = *reinterpret_cast<const u32x4*>(xn + i + XPACK_LO);
+  }
 }
 
 hipError_t launch_moe_gather(const uint16_t* xn, int xn_ks, const int32_t* gather, const int32_t* count,
@@ -176,13 +179,14 @@ hipError_t launch_moe_gather(const uint16_t* xn, int xn_ks, const int32_t* gathe
 // QKV projection, rotate q and k (rotate-half pairing j <-> j + dh/2) at the
 // node's position, write q (bf16) for attention, and k / v into cache slot
 // prefix_len[b] + i (k row-major per slot, v transposed: one row per dim).
+// q is kept as split bf16: q_out holds bf16(q), q_lo the bf16 residual.
 template <int NP>
 __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* __restrict__ parts, int n_parts_unused,
                                                        long long part_stride, StepMeta meta,
                                                        const float* __restrict__ rcos,
                                                        const float* __restrict__ rsin, int Hq, int Hkv,
                                                        int dh, int max_tree, int kv_cap,
-                                                       uint16_t* __restrict__ q_out,
+                                                       uint16_t* __restrict__ q_out, uint16_t* __restrict__ q_lo,
                                                        uint16_t* __restrict__ kc, uint16_t* __restrict__ vc) {
   const int r = blockIdx.x;
   const int b = r / max_tree, i = r % max_tree;
@@ -215,9 +219,12 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* __restrict__
       const float y1 = x1 * c - x2 * sn;
       const float y2 = x2 * c + x1 * sn;
       if (h < Hq) {
-        uint16_t* q = q_out + ((long long)r * Hq + h) * dh;
-        q[j] = f32_to_bf16(y1);
-        q[j + half] = f32_to_bf16(y2);
+        const long long o = ((long long)r * Hq + h) * dh;
+        const uint16_t h1 = f32_to_bf16(y1), h2 = f32_to_bf16(y2);
+        q_out[o + j] = h1;
+        q_out[o + j + half] = h2;
+        q_lo[o + j] = f32_to_bf16(y1 - bf16_to_f32(h1));
+        q_lo[o + j + half] = f32_to_bf16(y2 - bf16_to_f32(h2));
       } else {
         uint16_t* k = kc + (((long long)b * Hkv + (h - Hq)) * kv_cap + slot) * dh;
         k[j] = f32_to_bf16(y1);
@@ -235,15 +242,15 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* __restrict__
 
 hipError_t launch_qkv_rope(const float* qkv_parts, int n_parts, long long part_stride, StepMeta meta,
                            const float* rope_cos, const float* rope_sin, int Hq, int Hkv, int dh, int max_tree,
-                           int batch, int kv_cap, uint16_t* q_out, uint16_t* k_cache_l, uint16_t* v_cache_l,
-                           hipStream_t s) {
+                           int batch, int kv_cap, uint16_t* q_out, uint16_t* q_lo, uint16_t* k_cache_l,
+                           uint16_t* v_cache_l, hipStream_t s) {
   const int items = (Hq + 2 * Hkv) * (dh / 2);
   const dim3 grid(batch * max_tree, (items + 255) / 256);
   switch (n_parts) {
 #define GRIFFIN_ROPE_CASE(n)                                                                                   \
   case n:                                                                                                     \
     hipLaunchKernelGGL(qkv_rope_kernel<n>, grid, dim3(256), 0, s, qkv_parts, n_parts, part_stride, meta, rope_cos, \
-                       rope_sin, Hq, Hkv, dh, max_tree, kv_cap, q_out, k_cache_l, v_cache_l);                 \
+                       rope_sin, Hq, Hkv, dh, max_tree, kv_cap, q_out, q_lo, k_cache_l, v_cache_l);                 \
     break;
     GRIFFIN_ROPE_CASE(1) GRIFFIN_ROPE_CASE(2) GRIFFIN_ROPE_CASE(3) GRIFFIN_ROPE_CASE(4) GRIFFIN_ROPE_CASE(5)
     GRIFFIN_ROPE_CASE(6) GRIFFIN_ROPE_CASE(7) GRIFFIN_ROPE_CASE(8) GRIFFIN_ROPE_CASE(9) GRIFFIN_ROPE_CASE(10)

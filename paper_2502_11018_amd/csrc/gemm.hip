@@ -36,8 +36,12 @@ namespace griffin {
 
 template <int EPI, int NB, int WN, int PF>
 __global__ __launch_bounds__(64 * WN) void gemm_kernel(GemmArgs a) {
-  constexpr int XP = 8 / WN;   // activation pieces (1 KB) each wave stages per step
-  __shared__ u32x4 xs[PF][8][64];
+  constexpr int XPIECES = 16;          // per step: {hi, lo} x {rows 0-31, 32-63} x 4 pieces of 1 KB
+  constexpr int XP = XPIECES / WN;     // activation pieces each wave stages per step
+  constexpr int LOADS = NB * 4 + XP;   // vector-memory instructions per stage per wave
+  static_assert(LOADS * (PF - 2) < 64, "wait count out of range");
+  static_assert(PF >= 2 && XPIECES % WN == 0, "pipeline shape");
+  __shared__ u32x4 xs[PF][XPIECES][64];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lr = lane & 31, g = lane >> 5;
@@ -52,7 +56,7 @@ __global__ __launch_bounds__(64 * WN) void gemm_kernel(GemmArgs a) {
   const long long q = ((long long)split * a.n_wgs + wg) * WN + wave;
   const uint16_t* W = a.W + (long long)e * a.w_estride + q * NB * 2048 + lane * 8;
   const long long wstep = Q * NB * 2048;  // elements between consecutive steps of a stream
-  const uint16_t* X = a.X + ((long long)(e * a.x_etiles + m_tile) * a.x_ks + (long long)split * a.len) * 4096 +
+  const uint16_t* X = a.X + ((long long)(e * a.x_etiles + m_tile) * a.x_ks + (long long)split * a.len) * XPACK_STEP +
                       lane * 8;
 
   f32x16 acc[NB][2];
@@ -63,52 +67,69 @@ __global__ __launch_bounds__(64 * WN) void gemm_kernel(GemmArgs a) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) acc[b][mb][i] = 0.f;
 
+  // Stage t: this wave's weight blocks into registers, its share of the
+  // activation stage straight into LDS slot t % PF (lane l's 16 bytes land at
+  // the piece base + 16 l, which is the fragment order).
   u32x4 wb[PF][NB][4];
-  u32x4 xr[PF][XP];
-  auto load = [&](int slot_unused, u32x4 (&wv)[NB][4], u32x4 (&xv)[XP], int t) {
-    (void)slot_unused;
+  auto issue = [&](u32x4 (&wv)[NB][4], int slot, int t) {
     const uint16_t* wp = W + t * wstep;
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
       for (int b = 0; b < NB; ++b) wv[b][j] = ld_u4(wp + b * 2048 + j * 512);
 #pragma unroll
-    for (int p = 0; p < XP; ++p) xv[p] = ld_u4(X + (long long)t * 4096 + (wave * XP + p) * 512);
+    for (int p = 0; p < XP; ++p)
+      __builtin_amdgcn_global_load_lds((const void*)(X + (long long)t * XPACK_STEP + (wave * XP + p) * 512),
+                                       (lds_void*)&xs[slot][wave * XP + p][0], 16, 0, 0);
   };
-  auto step = [&](int u) {
+  // Consume stage t from slot u: the weights times the activation's bf16 high
+  // part plus its bf16 low part (two MFMAs into the same accumulator).
+  auto compute = [&](int u) {
+    u32x4 xv[2][2][4];
 #pragma unroll
-    for (int p = 0; p < XP; ++p) xs[u][wave * XP + p][lane] = xr[u][p];
-    __syncthreads();
-    u32x4 xv[2][4];
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+      for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) xv[mb][j] = xs[u][mb * 4 + j][lane];
+        for (int j = 0; j < 4; ++j) xv[h][mb][j] = xs[u][h * 8 + mb * 4 + j][lane];
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int b = 0; b < NB; ++b)
+      for (int h = 0; h < 2; ++h)
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
-          acc[b][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(wb[u][b][j]), as_bf16x8(xv[mb][j]),
-                                                               acc[b][mb], 0, 0, 0);
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+          for (int mb = 0; mb < 2; ++mb)
+            acc[b][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(wb[u][b][j]), as_bf16x8(xv[h][mb][j]),
+                                                                 acc[b][mb], 0, 0, 0);
   };
 
+  // Pipeline: stages t+1 .. t+PF-2 stay in flight while stage t is consumed.
+  // At the top of iteration t the wave waits for its own stage-t loads
+  // (vector-memory counters retire in issue order) and for its LDS reads of
+  // slot (t-1) % PF; the barrier then makes every wave's share of stage t
+  // visible and guarantees that no wave still reads slot (t-1) % PF, which
+  // stage t+PF-1 overwrites.  A plain s_barrier: the explicit waits are the
+  // only ones needed (a fence would drain all loads in flight).
   const int len = a.len;
 #pragma unroll
-  for (int p = 0; p < PF - 1; ++p) load(p, wb[p], xr[p], min(p, len - 1));
+  for (int p = 0; p < PF - 1; ++p) issue(wb[p], p, min(p, len - 1));
   int base = 0;
   for (; base + PF <= len; base += PF) {
 #pragma unroll
     for (int u = 0; u < PF; ++u) {
-      load(0, wb[(u + PF - 1) % PF], xr[(u + PF - 1) % PF], min(base + u + PF - 1, len - 1));
-      step(u);
+      wait_vmcnt_lds<(PF - 2) * LOADS>();
+      __builtin_amdgcn_s_barrier();
+      issue(wb[(u + PF - 1) % PF], (u + PF - 1) % PF, min(base + u + PF - 1, len - 1));
+      compute(u);
     }
   }
-  const int rem = len - base;  // < PF steps, already loaded in slots 0 .. rem-1 (uniform)
+  const int rem = len - base;  // < PF steps, already issued into slots 0 .. rem-1 (uniform)
+  wait_vmcnt_lds<0>();
+  __builtin_amdgcn_s_barrier();
 #pragma unroll
   for (int u = 0; u < PF - 1; ++u)
-    if (u < rem) step(u);
+    if (u < rem) compute(u);
 
   // ---- epilogues, every wave for its own NB blocks
 #pragma unroll
@@ -138,8 +159,10 @@ __global__ __launch_bounds__(64 * WN) void gemm_kernel(GemmArgs a) {
           float h[4];
 #pragma unroll
           for (int i = 0; i < 4; ++i) h[i] = silu_f32(acc[0][mb][4 * rg + i]) * acc[NB - 1][mb][4 * rg + i];
-          *reinterpret_cast<uint2*>(a.act + xpack_off(orow, n, a.act_ks)) =
-              make_uint2(pack_bf16x2(h[0], h[1]), pack_bf16x2(h[2], h[3]));
+          uint16_t* dst = a.act + xpack_off(orow, n, a.act_ks);
+          const Hilo2 p0 = pack_hilo2(h[0], h[1]), p1 = pack_hilo2(h[2], h[3]);
+          *reinterpret_cast<uint2*>(dst) = make_uint2(p0.hi, p1.hi);
+          *reinterpret_cast<uint2*>(dst + XPACK_LO) = make_uint2(p0.lo, p1.lo);
         }
       }
     } else {  // EPI_ARGMAX: partial (max, argmax, NaN count) over this wave's columns

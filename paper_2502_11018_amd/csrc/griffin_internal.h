@@ -38,14 +38,19 @@ __host__ __device__ inline long long packed_elems(const PackShape& p) {
   return (long long)p.len * p.n_wgs * p.splits * p.wn * p.nb * 2048;
 }
 
-// Element offset of activation (row m, column k) in the fragment-packed layout
-// whose 64-row tiles hold ks 64-wide K steps: tile, step, 32-row half mb, then
-// piece j = (k % 32) / 8 and lane r + 32 g (r = m % 32, g = (k % 64) / 32).
+// Activations feeding a GEMM are stored as split bf16 (hi + lo planes) in
+// fragment order.  Per 64-row tile and 64-wide K step there is one block of
+// XPACK_STEP elements: plane (hi, lo), 32-row half mb, piece j = (k % 32) / 8,
+// lane r + 32 g (r = m % 32, g = (k % 64) / 32), 8 values.  xpack_off gives
+// the offset of the hi value of (row m, column k) in a layout whose tiles hold
+// ks steps; the lo value sits XPACK_LO elements further.
+constexpr int XPACK_STEP = 8192;
+constexpr int XPACK_LO = 4096;
 __host__ __device__ inline long long xpack_off(long long m, int k, int ks) {
   const long long tile = m >> 6;
   const int mb = (int)((m >> 5) & 1), r = (int)(m & 31);
   const int s = k >> 6, kk = k & 63, g = kk >> 5, j = (kk >> 3) & 3, e = kk & 7;
-  return ((tile * ks + s) * 2 + mb) * 2048 + j * 512 + (r + 32 * g) * 8 + e;
+  return (tile * ks + s) * XPACK_STEP + mb * 2048 + j * 512 + (r + 32 * g) * 8 + e;
 }
 
 struct GemmArgs {
@@ -91,8 +96,9 @@ struct ResidualAdd {
 
 struct AttnArgs {
   const uint16_t* q;         // bf16 [R][Hq][dh]
+  const uint16_t* q_lo;      // bf16 residual q - bf16(q), same layout
   const uint16_t* k_cache;   // this layer: [max_batch][Hkv][cap][dh]
-  const uint16_t* v_cache;   // this layer: [max_batch][Hkv][dh][cap]
+  const uint16_t* v_cache;   // this layer: [max_batch][Hkv][cap / 32][dh][32]
   float* part_o;             // [B][Hq][S][qrows][dh]
   float* part_ml;            // [B][Hq][S][qrows][2]
   StepMeta meta;
@@ -109,8 +115,8 @@ hipError_t launch_residual_rmsnorm(float* x, const ResidualAdd& add, const uint1
                                    int rows, int d, uint16_t* xn, int xn_ks, hipStream_t s);
 hipError_t launch_qkv_rope(const float* qkv_parts, int n_parts, long long part_stride, StepMeta meta,
                            const float* rope_cos, const float* rope_sin, int Hq, int Hkv, int dh,
-                           int max_tree, int batch, int kv_cap, uint16_t* q_out, uint16_t* k_cache_l,
-                           uint16_t* v_cache_l, hipStream_t s);
+                           int max_tree, int batch, int kv_cap, uint16_t* q_out, uint16_t* q_lo,
+                           uint16_t* k_cache_l, uint16_t* v_cache_l, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, int batch, hipStream_t s);
 hipError_t launch_attn_combine(const float* part_o, const float* part_ml, StepMeta meta, int Hq, int dh,
                                int splits, int qrows, int max_tree, int batch, uint16_t* o_out, int o_ks,

@@ -158,7 +158,7 @@ struct griffin_ctx {
   std::vector<void*> allocs;
   float *x = nullptr, *parts = nullptr, *attn_po = nullptr, *attn_pml = nullptr;
   float *rope_cos = nullptr, *rope_sin = nullptr, *pmax = nullptr, *route_w = nullptr, *yslots = nullptr;
-  uint16_t *xn = nullptr, *q = nullptr, *o = nullptr, *act = nullptr, *xe = nullptr;
+  uint16_t *xn = nullptr, *q = nullptr, *q_lo = nullptr, *o = nullptr, *act = nullptr, *xe = nullptr;
   int32_t *pidx = nullptr, *pnan = nullptr, *pred = nullptr, *nan_row = nullptr, *result = nullptr;
   int32_t *route_ids = nullptr, *gather = nullptr, *count = nullptr, *slot = nullptr;
 
@@ -293,10 +293,11 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
     uint16_t* vc = c->v_cache + (size_t)l * layer_kv;
     LAUNCH(GRIFFIN_KC_ROPE, launch_qkv_rope(c->parts, c->p_qkv.shape.splits, ps * c->qkv_n, c->meta, c->rope_cos,
                                             c->rope_sin, d.n_q_heads, d.n_kv_heads, d.head_dim, d.max_tree, B,
-                                            d.kv_capacity, c->q, kc, vc, s));
+                                            d.kv_capacity, c->q, c->q_lo, kc, vc, s));
     {
       AttnArgs a{};
       a.q = c->q;
+      a.q_lo = c->q_lo;
       a.k_cache = kc;
       a.v_cache = vc;
       a.part_o = c->attn_po;
@@ -525,13 +526,14 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
   const long long per_layer = c->p_qkv.elems + c->p_o.elems + (long long)c->E * (c->p_gu.elems + c->p_down.elems);
   ALLOC(c->wpack, per_layer * d.n_layers + c->p_lm.elems);
   ALLOC(c->x, Mp * d.d_model);
-  ALLOC(c->xn, tiles * c->xd_ks * 4096);
+  ALLOC(c->xn, tiles * c->xd_ks * XPACK_STEP);
   ALLOC(c->parts, c->parts_elems);
   ALLOC(c->q, Mp * c->attn_w);
-  ALLOC(c->o, tiles * c->p_o.ks_pad * 4096);
+  ALLOC(c->q_lo, Mp * c->attn_w);
+  ALLOC(c->o, tiles * c->p_o.ks_pad * XPACK_STEP);
   ALLOC(c->attn_po, (long long)d.max_batch * d.n_q_heads * c->attn_splits * qrows * d.head_dim);
   ALLOC(c->attn_pml, (long long)d.max_batch * d.n_q_heads * c->attn_splits * qrows * 2);
-  ALLOC(c->act, (long long)c->E * tiles * c->p_down.ks_pad * 4096);
+  ALLOC(c->act, (long long)c->E * tiles * c->p_down.ks_pad * XPACK_STEP);
   const long long lm_parts = (long long)c->p_lm.shape.n_wgs * c->p_lm.wn;
   ALLOC(c->pmax, Mp * lm_parts);
   ALLOC(c->pidx, Mp * lm_parts);
@@ -548,7 +550,7 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
     ALLOC(c->count, c->E);
     ALLOC(c->slot, Mp * c->topk);
     ALLOC(c->yslots, (long long)c->p_down.shape.splits * c->E * Mp * d.d_model);
-    ALLOC(c->xe, (long long)c->E * tiles * c->xd_ks * 4096);
+    ALLOC(c->xe, (long long)c->E * tiles * c->xd_ks * XPACK_STEP);
   }
 #undef ALLOC
 
