@@ -1,20 +1,26 @@
 // Tree-masked attention of the verify pass.
 //
 // A tree node r of sequence b sees the cached prefix slots [0, P_b) and the
-// tree slots P_b + j for every node j on its root path (bit j of anc[r]).  One
-// wavefront handles one query head and a block of 32 tree rows over one split
-// of the key range; splits are merged by attn_combine with the usual
+// tree slots P_b + j for every node j on its root path (bit j of anc[r]).
+// A workgroup handles one (sequence, KV head, block of 32 tree rows, key
+// split, chunk of NW query heads of that KV head's group): its NW waves share
+// every 32-key block of K and V, which the workgroup stages once into an LDS
+// ring with global_load_lds_dwordx4 (each wave issues an equal share of the
+// block's 1 KB pieces), so the cache is read once per head group rather than
+// once per head.  Splits are merged by attn_combine with the usual
 // (max, sum, weighted output) rescaling in a fixed order.
 //
-// Per 32-key block the wave computes S^T = K Q^T and O^T += V^T P^T with
+// Per 32-key block each wave computes S^T = K Q^T and O^T += V^T P^T with
 // v_mfma_f32_32x32x16_bf16, so that each lane owns one query row (column of
 // the MFMA output) and the softmax bookkeeping is lane-local:
 //  * Keys are fed to the MFMA in a permuted row order so that accumulator
 //    register q of lane half h holds key 16 h + q of the block; the P operand
 //    of the second product is then the lane's own registers 8 t .. 8 t + 7.
 //  * V is cached in 32-slot tiles stored transposed ([tile][dim][32]), so a
-//    block's V^T is one contiguous 8 KB tile and each operand piece is one
-//    16-byte load of 8 consecutive slots.
+//    block's V^T is one contiguous 8 KB tile.
+//  * The ring holds each block in MFMA fragment order (piece, lane, 8 values):
+//    the DMA gathers every lane's 16 bytes from the cache, and the compute
+//    side reads each operand with one conflict-free ds_read_b128.
 //  * Q and K use the same head-dim permutation as the projection GEMMs: a lane
 //    reads 32 consecutive head dims and feeds 8 of them to each of 4 MFMAs.
 //  * Q and P enter the matrix cores as split bf16 (hi + lo, two MFMAs each),
@@ -22,47 +28,58 @@
 // Scores are kept in the log2 domain (scaled by log2(e)/sqrt(dh)) and exp2 is
 // used throughout; masked keys contribute exactly zero.
 
+#include <type_traits>
+
 #include "device_common.h"
 #include "griffin_internal.h"
 
 namespace griffin {
 
-template <int DH>
-__global__ __launch_bounds__(64) void tree_attention_kernel(AttnArgs a) {
-  constexpr int CH = DH / 64;   // 64-dim chunks of Q/K per lane pair
-  constexpr int DB = DH / 32;   // 32-dim blocks of the output
-  const int lane = threadIdx.x;
+template <int DH, int NW>
+__global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
+  constexpr int CH = DH / 64;          // 64-dim chunks of Q/K per lane pair
+  constexpr int DB = DH / 32;          // 32-dim blocks of the output
+  constexpr int KP = CH * 4;           // 1 KB pieces of a K block
+  constexpr int PIECES = KP + DB * 2;  // K and V pieces of one 32-key block
+  constexpr int PPW = PIECES / NW;     // pieces each wave stages per block
+  constexpr int D = ATTN_RING;         // ring slots
+  static_assert(PIECES % NW == 0 && PPW * (D - 2) < 64, "ring shape");
+  __shared__ u32x4 ring[D][PIECES][64];
+
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int col = lane & 31, hh = lane >> 5;
   // XCD-aware decode: workgroups are dispatched round-robin over the 8 XCDs
   // (id % 8), so every workgroup of one (sequence, KV head) stream gets the
-  // same id % 8 and its K/V blocks are shared through that XCD's L2.
+  // same id % 8 and the K/V blocks it re-reads are shared through that XCD's L2.
   const int G = a.Hq / a.Hkv;
-  const int per_stream = G * a.qblocks * a.splits;
+  const int chunks = (G + NW - 1) / NW;
+  const int per_stream = chunks * a.qblocks * a.splits;
   const int id = blockIdx.x;
   const int rest = id >> 3;
   const int stream = (rest / per_stream) * 8 + (id & 7);
-  if (stream >= a.batch * a.Hkv) return;
+  if (stream >= a.batch * a.Hkv) return;  // uniform over the workgroup
   int within = rest % per_stream;
   const int split = within % a.splits;
   within /= a.splits;
   const int qb = within % a.qblocks;
-  const int hq = (stream % a.Hkv) * G + within / a.qblocks;
+  const int chunk = within / a.qblocks;
   const int b = stream / a.Hkv;
-  const int hk = hq / G;
+  const int hk = stream % a.Hkv;
+  const int gh = chunk * NW + w;           // head within the group
+  const bool head_live = gh < G;           // wave-uniform
+  const int hq = hk * G + (head_live ? gh : 0);
   const int n_nodes = a.meta.n_nodes[b];
   const int P = a.meta.prefix_len[b];
   const int Lb = P + n_nodes;
   const int qrows = a.qblocks * 32;
 
-  float* po = a.part_o + ((((long long)b * a.Hq + hq) * a.splits + split) * qrows + qb * 32) * DH;
-  float* pml = a.part_ml + ((((long long)b * a.Hq + hq) * a.splits + split) * qrows + qb * 32) * 2;
-
-  if (qb * 32 >= n_nodes) return;  // no live query rows in this block
+  if (qb * 32 >= n_nodes) return;  // no live query rows in this block (uniform)
 
   // key range of this split, in whole 32-key blocks
   const int nblk = (Lb + 31) >> 5;
   const int kb0 = (int)((long long)nblk * split / a.splits);
   const int kb1 = (int)((long long)nblk * (split + 1) / a.splits);
+  const int nb = kb1 - kb0;
 
   // query row of this lane
   const int qi = qb * 32 + col;
@@ -89,6 +106,27 @@ __global__ __launch_bounds__(64) void tree_attention_kernel(AttnArgs a) {
   const uint16_t* vbase = a.v_cache + head;
   // MFMA row -> key offset inside a 32-key block: row 8q + 4h + e holds key 16h + 4q + e
   const int krow = 16 * ((col >> 2) & 1) + 4 * (col >> 3) + (col & 3);
+  // this lane's element offset inside a block, for each piece this wave stages
+  int goff[PPW];
+#pragma unroll
+  for (int p = 0; p < PPW; ++p) {
+    const int pc = w * PPW + p;
+    if (pc < KP) {
+      const int c = pc >> 2, j = pc & 3;
+      goff[p] = krow * DH + 64 * c + 32 * hh + 8 * j;
+    } else {
+      const int v = pc - KP, d = v >> 1, t = v & 1;
+      goff[p] = (32 * d + col) * 32 + 16 * hh + 8 * t;
+    }
+  }
+  auto issue = [&](int slot, int kb) {
+#pragma unroll
+    for (int p = 0; p < PPW; ++p) {
+      const int pc = w * PPW + p;
+      const uint16_t* src = (pc < KP ? kbase : vbase) + (long long)kb * 32 * DH + goff[p];
+      __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)&ring[slot][pc][0], 16, 0, 0);
+    }
+  };
 
   float m_ref = -INFINITY, l_run = 0.f;
   f32x16 oacc[DB];
@@ -97,66 +135,50 @@ __global__ __launch_bounds__(64) void tree_attention_kernel(AttnArgs a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[d][r] = 0.f;
 
-  // K and V operands of one 32-key block; two register sets, the next block's
-  // loads are issued before the current block is computed
-  u32x4 kf[2][CH][4];
-  u32x4 vf[2][DB][2];
-  auto load_kv = [&](int buf, int kb) {
-    const int key0 = kb * 32;
-    const uint16_t* kp = kbase + (long long)(key0 + krow) * DH + 32 * hh;
-#pragma unroll
-    for (int c = 0; c < CH; ++c)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) kf[buf][c][j] = ld_u4(kp + 64 * c + 8 * j);
-    // V^T operand (A): lane (dim row col of block d, k-group hh); step t covers
-    // keys 16 hh + 8 t + [0, 8)
-#pragma unroll
-    for (int d = 0; d < DB; ++d)
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-        vf[buf][d][t] = ld_u4(vbase + (long long)kb * DH * 32 + (32 * d + col) * 32 + 16 * hh + 8 * t);
-  };
-
   // Online softmax with a lazily moved reference max: p = 2^(s - m_ref) may
   // reach 2^8 before the reference is raised, so the accumulator rescale only
   // runs when some lane's block maximum exceeds its reference by more than 8
-  // (a wave-uniform branch with no loads inside).
-  auto compute = [&](int buf, int kb, bool live_blk) {
+  // (a wave-uniform branch with no loads inside).  MASKED is false for blocks
+  // wholly inside the cached prefix (every key visible); the block holding
+  // the tree slots and the end of the sequence takes the masked variant, whose
+  // masks are branch-free selects.
+  auto compute = [&](auto masked, int slot, int kb) {
+    constexpr bool MASKED = decltype(masked)::value;
     const int key0 = kb * 32;
-    // ---- S^T = K Q^T (rows: keys, cols: queries)
-    f32x16 s;
+    // ---- S^T = K Q^T (rows: keys, cols: queries), q = q_hi + q_lo
+    f32x16 sacc;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) s[r] = 0.f;
+    for (int r = 0; r < 16; ++r) sacc[r] = 0.f;
 #pragma unroll
     for (int c = 0; c < CH; ++c)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < 4; ++j) {
+        const u32x4 kf = ring[slot][c * 4 + j][lane];
 #pragma unroll
         for (int h = 0; h < 2; ++h)
-          s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[buf][c][j]), as_bf16x8(qf[h][c][j]), s, 0, 0, 0);
-
-    // ---- scale + mask (this lane: query qi, keys key0 + 16 hh + r)
-    float mx = -INFINITY;
-    if (live_blk && key0 + 32 <= P) {  // whole block inside the cached prefix: all visible
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        s[r] *= a.scale_log2;
-        mx = fmaxf(mx, s[r]);
+          sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf), as_bf16x8(qf[h][c][j]), sacc, 0, 0, 0);
       }
-    } else {
+
+    // ---- mask (this lane: query qi, keys key0 + 16 hh + r); the log2-domain
+    // scale is applied inside the exponent (scale > 0 commutes with max)
+    float s[16];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
+    for (int r = 0; r < 16; ++r) {
+      s[r] = sacc[r];
+      if constexpr (MASKED) {
         const int key = key0 + 16 * hh + r;
         const int j = key - P;
-        const bool vis = live_blk && (key < P || (j < n_nodes && ((anc >> (j & 63)) & 1ull)));
-        s[r] = vis ? s[r] * a.scale_log2 : -INFINITY;
-        mx = fmaxf(mx, s[r]);
+        const bool tree_vis = ((unsigned)j < (unsigned)n_nodes) & (((anc >> (j & 63)) & 1ull) != 0ull);
+        s[r] = ((key < P) | tree_vis) ? s[r] : -INFINITY;
       }
     }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    float mx = fmaxf(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])), fmaxf(fmaxf(s[4], s[5]), fmaxf(s[6], s[7])));
+    mx = fmaxf(mx, fmaxf(fmaxf(fmaxf(s[8], s[9]), fmaxf(s[10], s[11])),
+                         fmaxf(fmaxf(s[12], s[13]), fmaxf(s[14], s[15]))));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * a.scale_log2;
     if (__any(mx > m_ref + 8.f)) {
       const float m_new = fmaxf(m_ref, mx);
-      const float alpha = m_ref == -INFINITY ? 0.f : exp2f(m_ref - m_new);
+      const float alpha = m_ref == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_ref - m_new);
       l_run *= alpha;
 #pragma unroll
       for (int d = 0; d < DB; ++d)
@@ -165,65 +187,72 @@ __global__ __launch_bounds__(64) void tree_attention_kernel(AttnArgs a) {
       m_ref = m_new;
     }
     const float m_use = m_ref == -INFINITY ? 0.f : m_ref;
-    float psum = 0.f;
     float p[16];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      p[r] = exp2f(s[r] - m_use);
-      psum += p[r];
-    }
+    for (int r = 0; r < 16; ++r) p[r] = __builtin_amdgcn_exp2f(fmaf(s[r], a.scale_log2, -m_use));
+    const float psum = ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7])) +
+                       (((p[8] + p[9]) + (p[10] + p[11])) + ((p[12] + p[13]) + (p[14] + p[15])));
     l_run += psum + __shfl_xor(psum, 32, 64);
-
-    // keys at or beyond the end of the sequence may hold stale or never
-    // written cache bytes; zero their V so that 0 * garbage cannot appear
-    if (key0 + 32 > Lb) {
-#pragma unroll
-      for (int d = 0; d < DB; ++d)
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          const int kfirst = key0 + 16 * hh + 8 * t;
-#pragma unroll
-          for (int w = 0; w < 4; ++w) {  // bf16 element 2w is the low half of dword w
-            const uint32_t keep =
-                (kfirst + 2 * w < Lb ? 0x0000ffffu : 0u) | (kfirst + 2 * w + 1 < Lb ? 0xffff0000u : 0u);
-            vf[buf][d][t][w] &= keep;
-          }
-        }
-    }
 
     // ---- O^T += V^T P^T, P as split bf16 (p_hi + p_lo)
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       u32x4 pf[2];
 #pragma unroll
-      for (int w = 0; w < 4; ++w) {
-        const Hilo2 hl = pack_hilo2(p[8 * t + 2 * w], p[8 * t + 2 * w + 1]);
-        pf[0][w] = hl.hi;
-        pf[1][w] = hl.lo;
+      for (int q = 0; q < 4; ++q) {
+        const Hilo2 hl = pack_hilo2(p[8 * t + 2 * q], p[8 * t + 2 * q + 1]);
+        pf[0][q] = hl.hi;
+        pf[1][q] = hl.lo;
+      }
+      // keys at or beyond the end of the sequence may hold stale or never
+      // written cache bytes; zero their V so that 0 * garbage cannot appear
+      uint32_t keep[4];
+      if constexpr (MASKED) {
+        const int kfirst = key0 + 16 * hh + 8 * t;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)  // bf16 element 2q is the low half of dword q
+          keep[q] = (kfirst + 2 * q < Lb ? 0x0000ffffu : 0u) | (kfirst + 2 * q + 1 < Lb ? 0xffff0000u : 0u);
       }
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
+      for (int d = 0; d < DB; ++d) {
+        u32x4 vf = ring[slot][KP + d * 2 + t][lane];
+        if constexpr (MASKED) {
 #pragma unroll
-        for (int d = 0; d < DB; ++d)
-          oacc[d] =
-              __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf[buf][d][t]), as_bf16x8(pf[h]), oacc[d], 0, 0, 0);
+          for (int q = 0; q < 4; ++q) vf[q] &= keep[q];
+        }
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+          oacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf), as_bf16x8(pf[h]), oacc[d], 0, 0, 0);
+      }
     }
   };
 
-  // Branch-free pipeline: loads past the split's end re-read its last block
-  // (in bounds) and a block past the end is computed fully masked, which
-  // leaves m, l and the output exactly unchanged.
-  if (kb0 < kb1) {
-    load_kv(0, kb0);
-    for (int kb = kb0; kb < kb1; kb += 2) {
-      load_kv(1, min(kb + 1, kb1 - 1));
-      compute(0, kb, true);
-      load_kv(0, min(kb + 2, kb1 - 1));
-      compute(1, kb + 1, kb + 1 < kb1);
+  // Ring pipeline over the split's blocks (same structure as the GEMM's): at
+  // the top of iteration i every wave waits for its own DMA pieces of block i
+  // (vector-memory counters retire in issue order) and for its LDS reads of
+  // the previous slot; the barrier then publishes block i and frees slot
+  // (i - 1) % D, which block i + D - 1 overwrites.  Issues past the last block
+  // re-read it into slots that are never consumed; every DMA has landed
+  // before the waves leave.
+  if (nb > 0) {
+#pragma unroll
+    for (int i = 0; i < D - 1; ++i) issue(i, kb0 + min(i, nb - 1));
+    for (int i = 0; i < nb; ++i) {
+      wait_vmcnt_lds<(D - 2) * PPW>();
+      __builtin_amdgcn_s_barrier();
+      issue((i + D - 1) % D, kb0 + min(i + D - 1, nb - 1));
+      // waves past the end of the head group compute a duplicate of the
+      // group's first head and write nothing
+      if ((kb0 + i + 1) * 32 <= P) compute(std::false_type{}, i % D, kb0 + i);
+      else compute(std::true_type{}, i % D, kb0 + i);
     }
+    wait_vmcnt_lds<0>();
   }
+  if (!head_live) return;
 
   // ---- partials: O^T layout, lane owns query col, dims 32 d + 8 (r/4) + 4 hh + r%4
+  float* po = a.part_o + ((((long long)b * a.Hq + hq) * a.splits + split) * qrows + qb * 32) * DH;
+  float* pml = a.part_ml + ((((long long)b * a.Hq + hq) * a.splits + split) * qrows + qb * 32) * 2;
   float* orow = po + (long long)col * DH;
 #pragma unroll
   for (int d = 0; d < DB; ++d)
@@ -237,13 +266,29 @@ __global__ __launch_bounds__(64) void tree_attention_kernel(AttnArgs a) {
   }
 }
 
+int attn_waves(int group) { return group >= 4 ? 4 : group >= 2 ? 2 : 1; }
+
+template <int DH, int NW>
+static void launch_attn_nw(const AttnArgs& a, dim3 grid, hipStream_t s) {
+  hipLaunchKernelGGL((tree_attention_kernel<DH, NW>), grid, dim3(64 * NW), 0, s, a);
+}
+
+template <int DH>
+static void launch_attn_dh(const AttnArgs& a, int nw, dim3 grid, hipStream_t s) {
+  if (nw == 4) launch_attn_nw<DH, 4>(a, grid, s);
+  else if (nw == 2) launch_attn_nw<DH, 2>(a, grid, s);
+  else launch_attn_nw<DH, 1>(a, grid, s);
+}
+
 hipError_t launch_attention(const AttnArgs& a, int batch, hipStream_t s) {
   if (a.batch != batch) return hipErrorInvalidValue;
+  const int G = a.Hq / a.Hkv;
+  const int nw = attn_waves(G);
   const int streams = batch * a.Hkv;
-  const int per_stream = (a.Hq / a.Hkv) * a.qblocks * a.splits;
+  const int per_stream = ((G + nw - 1) / nw) * a.qblocks * a.splits;
   dim3 grid(((streams + 7) / 8) * 8 * per_stream);
-  if (a.dh == 128) hipLaunchKernelGGL(tree_attention_kernel<128>, grid, dim3(64), 0, s, a);
-  else if (a.dh == 64) hipLaunchKernelGGL(tree_attention_kernel<64>, grid, dim3(64), 0, s, a);
+  if (a.dh == 128) launch_attn_dh<128>(a, nw, grid, s);
+  else if (a.dh == 64) launch_attn_dh<64>(a, nw, grid, s);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

@@ -14,17 +14,16 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(uint32_t(h) << 16); }
 
-// fp32 -> bf16, round to nearest even; NaN stays a quiet NaN.
-__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return uint16_t((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return uint16_t(u >> 16);
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// fp32 -> bf16 with the hardware conversion (v_cvt_pk_bf16_f32: round to
+// nearest even, NaN stays NaN).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{lo, hi}, bf16x2));
 }
 
-__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
-  return uint32_t(f32_to_bf16(lo)) | (uint32_t(f32_to_bf16(hi)) << 16);
-}
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) { return uint16_t(pack_bf16x2(f, 0.f)); }
 
 // Split-bf16 operand: x ~ hi + lo with hi = bf16(x) and lo = bf16(x - hi),
 // which carries about 16 significant bits through the bf16 matrix cores.
@@ -32,9 +31,8 @@ struct Hilo2 {
   uint32_t hi, lo;
 };
 __device__ __forceinline__ Hilo2 pack_hilo2(float a, float b) {
-  const uint16_t ha = f32_to_bf16(a), hb = f32_to_bf16(b);
-  return {uint32_t(ha) | (uint32_t(hb) << 16),
-          pack_bf16x2(a - bf16_to_f32(ha), b - bf16_to_f32(hb))};
+  const uint32_t hi = pack_bf16x2(a, b);
+  return {hi, pack_bf16x2(a - __uint_as_float(hi << 16), b - __uint_as_float(hi & 0xffff0000u))};
 }
 
 __device__ __forceinline__ bf16x8 as_bf16x8(const u32x4& v) { return __builtin_bit_cast(bf16x8, v); }

@@ -34,30 +34,34 @@
 
 namespace griffin {
 
-template <int EPI, int NB, int WN, int PF>
-__global__ __launch_bounds__(64 * WN) void gemm_kernel(GemmArgs a) {
+template <int EPI, int NB, int WN, int PF, int KS>
+__global__ __launch_bounds__(64 * WN * KS) void gemm_kernel(GemmArgs a) {
   constexpr int XPIECES = 16;          // per step: {hi, lo} x {rows 0-31, 32-63} x 4 pieces of 1 KB
   constexpr int XP = XPIECES / WN;     // activation pieces each wave stages per step
   constexpr int LOADS = NB * 4 + XP;   // vector-memory instructions per stage per wave
   static_assert(LOADS * (PF - 2) < 64, "wait count out of range");
   static_assert(PF >= 2 && XPIECES % WN == 0, "pipeline shape");
-  __shared__ u32x4 xs[PF][XPIECES][64];
+  static_assert(WN * NB * 8 <= PF * KS * 16 || KS == 1, "K-split merge buffer");
+  __shared__ u32x4 xs[PF][KS][XPIECES][64];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wc = wave % WN;            // column group of this wave
+  const int kh = wave / WN;            // K slice of this wave inside the workgroup
   const int lr = lane & 31, g = lane >> 5;
   const int e = blockIdx.y;
   const int m_tile = blockIdx.x % a.m_tiles;
   const int wg = blockIdx.x / a.m_tiles;
-  const int split = blockIdx.z;
+  const int zsplit = blockIdx.z;       // output split (its KS slices are merged in the workgroup)
+  const int split = zsplit * KS + kh;  // K slice of this wave's weight stream
   const int rows_e = a.count ? a.count[e] : a.m_tiles * 64;
   if (m_tile * 64 >= rows_e) return;  // uniform over the workgroup
 
   const long long Q = (long long)a.n_wgs * a.splits * WN;
-  const long long q = ((long long)split * a.n_wgs + wg) * WN + wave;
+  const long long q = ((long long)split * a.n_wgs + wg) * WN + wc;
   const uint16_t* W = a.W + (long long)e * a.w_estride + q * NB * 2048 + lane * 8;
   const long long wstep = Q * NB * 2048;  // elements between consecutive steps of a stream
-  const uint16_t* X = a.X + ((long long)(e * a.x_etiles + m_tile) * a.x_ks + (long long)split * a.len) * XPACK_STEP +
-                      lane * 8;
+  const uint16_t* X = a.X + ((long long)(e * a.x_etiles + m_tile) * a.x_ks + (long long)zsplit * KS * a.len) *
+                                XPACK_STEP + lane * 8;
 
   f32x16 acc[NB][2];
 #pragma unroll
@@ -78,9 +82,12 @@ __global__ __launch_bounds__(64 * WN) void gemm_kernel(GemmArgs a) {
 #pragma unroll
       for (int b = 0; b < NB; ++b) wv[b][j] = ld_u4(wp + b * 2048 + j * 512);
 #pragma unroll
-    for (int p = 0; p < XP; ++p)
-      __builtin_amdgcn_global_load_lds((const void*)(X + (long long)t * XPACK_STEP + (wave * XP + p) * 512),
-                                       (lds_void*)&xs[slot][wave * XP + p][0], 16, 0, 0);
+    for (int p = 0; p < XP; ++p) {
+      const int pp = wave * XP + p, sk = pp / XPIECES, pc = pp % XPIECES;  // slice, piece
+      __builtin_amdgcn_global_load_lds(
+          (const void*)(X + ((long long)sk * a.len + t) * XPACK_STEP + pc * 512),
+          (lds_void*)&xs[slot][sk][pc][0], 16, 0, 0);
+    }
   };
   // Consume stage t from slot u: the weights times the activation's bf16 high
   // part plus its bf16 low part (two MFMAs into the same accumulator).
@@ -91,7 +98,7 @@ __global__ __launch_bounds__(64 * WN) void gemm_kernel(GemmArgs a) {
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) xv[h][mb][j] = xs[u][h * 8 + mb * 4 + j][lane];
+        for (int j = 0; j < 4; ++j) xv[h][mb][j] = xs[u][kh][h * 8 + mb * 4 + j][lane];
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
@@ -131,6 +138,37 @@ __global__ __launch_bounds__(64 * WN) void gemm_kernel(GemmArgs a) {
   for (int u = 0; u < PF - 1; ++u)
     if (u < rem) compute(u);
 
+  if constexpr (KS > 1) {
+    // merge the K slices in slice order through LDS (the ring is free once
+    // every wave's reads have returned)
+    float* red = reinterpret_cast<float*>(&xs[0][0][0][0]);
+    wait_vmcnt_lds<0>();
+    __builtin_amdgcn_s_barrier();
+    for (int k = 1; k < KS; ++k) {
+      if (kh == k) {
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+          for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) red[(((wc * NB + b) * 2 + mb) * 16 + i) * 64 + lane] = acc[b][mb][i];
+      }
+      wait_vmcnt_lds<0>();
+      __builtin_amdgcn_s_barrier();
+      if (kh == 0) {
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+          for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) acc[b][mb][i] += red[(((wc * NB + b) * 2 + mb) * 16 + i) * 64 + lane];
+      }
+      wait_vmcnt_lds<0>();
+      __builtin_amdgcn_s_barrier();
+    }
+    if (kh != 0) return;
+  }
+
   // ---- epilogues, every wave for its own NB blocks
 #pragma unroll
   for (int mb = 0; mb < 2; ++mb) {
@@ -139,12 +177,12 @@ __global__ __launch_bounds__(64 * WN) void gemm_kernel(GemmArgs a) {
     const long long orow = (long long)e * a.o_erows + ml;
     if constexpr (EPI == EPI_STORE) {
       if (!row_ok) continue;
-      float* out = a.out + (long long)split * a.out_split_stride + orow * a.ldo;
+      float* out = a.out + (long long)zsplit * a.out_split_stride + orow * a.ldo;
 #pragma unroll
       for (int b = 0; b < NB; ++b)
 #pragma unroll
         for (int rg = 0; rg < 4; ++rg) {
-          const int n = ((wg * WN + wave) * NB + b) * 32 + 8 * rg + 4 * g;
+          const int n = ((wg * WN + wc) * NB + b) * 32 + 8 * rg + 4 * g;
           if (n < a.N)
             *reinterpret_cast<float4*>(out + n) = make_float4(acc[b][mb][4 * rg], acc[b][mb][4 * rg + 1],
                                                               acc[b][mb][4 * rg + 2], acc[b][mb][4 * rg + 3]);
@@ -154,7 +192,7 @@ __global__ __launch_bounds__(64 * WN) void gemm_kernel(GemmArgs a) {
       if (!row_ok) continue;
 #pragma unroll
       for (int rg = 0; rg < 4; ++rg) {
-        const int n = (wg * WN + wave) * 32 + 8 * rg + 4 * g;
+        const int n = (wg * WN + wc) * 32 + 8 * rg + 4 * g;
         if (n < a.N) {
           float h[4];
 #pragma unroll
@@ -175,7 +213,7 @@ __global__ __launch_bounds__(64 * WN) void gemm_kernel(GemmArgs a) {
         for (int rg = 0; rg < 4; ++rg)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const int n = ((wg * WN + wave) * NB + b) * 32 + 8 * rg + 4 * g + i;
+            const int n = ((wg * WN + wc) * NB + b) * 32 + 8 * rg + 4 * g + i;
             const float v = acc[b][mb][4 * rg + i];
             if (n < a.N) {
               if (v != v) ++nan_cnt;
@@ -186,7 +224,7 @@ __global__ __launch_bounds__(64 * WN) void gemm_kernel(GemmArgs a) {
       const int oi = __shfl_xor(bidx, 32, 64);
       nan_cnt += __shfl_xor(nan_cnt, 32, 64);
       if (ob > best || (ob == best && oi < bidx)) { best = ob; bidx = oi; }
-      const int part = wg * WN + wave;
+      const int part = wg * WN + wc;
       if (g == 0) {
         a.pmax[orow * a.ld_part + part] = best;
         a.pidx[orow * a.ld_part + part] = bidx;
@@ -198,7 +236,7 @@ __global__ __launch_bounds__(64 * WN) void gemm_kernel(GemmArgs a) {
         for (int b = 0; b < NB; ++b)
 #pragma unroll
           for (int rg = 0; rg < 4; ++rg) {
-            const int n = ((wg * WN + wave) * NB + b) * 32 + 8 * rg + 4 * g;
+            const int n = ((wg * WN + wc) * NB + b) * 32 + 8 * rg + 4 * g;
             if (n < a.N)
               *reinterpret_cast<float4*>(out + n) = make_float4(acc[b][mb][4 * rg], acc[b][mb][4 * rg + 1],
                                                                 acc[b][mb][4 * rg + 2], acc[b][mb][4 * rg + 3]);
@@ -208,26 +246,27 @@ __global__ __launch_bounds__(64 * WN) void gemm_kernel(GemmArgs a) {
   }
 }
 
-template <int EPI, int NB, int WN, int PF>
+template <int EPI, int NB, int WN, int PF, int KS>
 static hipError_t launch_one(const GemmArgs& a, int experts, hipStream_t s) {
-  dim3 grid(a.n_wgs * a.m_tiles, experts, a.splits);
-  hipLaunchKernelGGL((gemm_kernel<EPI, NB, WN, PF>), grid, dim3(64 * WN), 0, s, a);
+  dim3 grid(a.n_wgs * a.m_tiles, experts, a.splits / KS);
+  hipLaunchKernelGGL((gemm_kernel<EPI, NB, WN, PF, KS>), grid, dim3(64 * WN * KS), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_gemm(const GemmArgs& a, int experts, hipStream_t s) {
-  const int epi = a.epi, nb = a.nb, wn = a.wn, pf = a.pf;
-#define GRIFFIN_GEMM_CASE(E, B, N_, P)                                              \
-  if (epi == (E) && nb == (B) && wn == (N_) && pf == (P)) return launch_one<E, B, N_, P>(a, experts, s);
-  GRIFFIN_GEMM_CASE(EPI_STORE, 1, 4, 4)
-  GRIFFIN_GEMM_CASE(EPI_STORE, 1, 4, 2)
-  GRIFFIN_GEMM_CASE(EPI_STORE, 1, 1, 2)
-  GRIFFIN_GEMM_CASE(EPI_SWIGLU, 2, 2, 4)
-  GRIFFIN_GEMM_CASE(EPI_SWIGLU, 2, 2, 2)
-  GRIFFIN_GEMM_CASE(EPI_SWIGLU, 2, 1, 2)
-  GRIFFIN_GEMM_CASE(EPI_ARGMAX, 1, 4, 4)
-  GRIFFIN_GEMM_CASE(EPI_ARGMAX, 1, 4, 2)
-  GRIFFIN_GEMM_CASE(EPI_ARGMAX, 1, 1, 2)
+  const int epi = a.epi, nb = a.nb, wn = a.wn, pf = a.pf, ks = a.kslices;
+  if (ks < 1 || a.splits % ks != 0) return hipErrorInvalidValue;
+#define GRIFFIN_GEMM_CASE(E, B, N_, P, K_)                                                        \
+  if (epi == (E) && nb == (B) && wn == (N_) && pf == (P) && ks == (K_)) return launch_one<E, B, N_, P, K_>(a, experts, s);
+  GRIFFIN_GEMM_CASE(EPI_STORE, 1, 4, 4, 1)
+  GRIFFIN_GEMM_CASE(EPI_STORE, 1, 4, 2, 1)
+  GRIFFIN_GEMM_CASE(EPI_STORE, 1, 1, 2, 1)
+  GRIFFIN_GEMM_CASE(EPI_SWIGLU, 2, 2, 3, 2)
+  GRIFFIN_GEMM_CASE(EPI_SWIGLU, 2, 2, 2, 2)
+  GRIFFIN_GEMM_CASE(EPI_SWIGLU, 2, 2, 2, 1)
+  GRIFFIN_GEMM_CASE(EPI_ARGMAX, 1, 4, 4, 1)
+  GRIFFIN_GEMM_CASE(EPI_ARGMAX, 1, 4, 2, 1)
+  GRIFFIN_GEMM_CASE(EPI_ARGMAX, 1, 1, 2, 1)
 #undef GRIFFIN_GEMM_CASE
   return hipErrorInvalidValue;
 }

@@ -55,7 +55,8 @@ __host__ __device__ inline long long xpack_off(long long m, int k, int ks) {
 
 struct GemmArgs {
   int epi, nb, wn, pf;       // kernel variant
-  int n_wgs, splits, len;    // launch shape (matches the weight packing)
+  int n_wgs, splits, len;    // launch shape (matches the weight packing): splits = K slices
+  int kslices;               // K slices merged inside one workgroup (output splits = splits / kslices)
   int N;                     // output columns (SwiGLU: d_ff)
   int m_tiles;               // 64-row activation tiles
   const uint16_t* X;         // packed activations
@@ -118,6 +119,8 @@ hipError_t launch_qkv_rope(const float* qkv_parts, int n_parts, long long part_s
                            int max_tree, int batch, int kv_cap, uint16_t* q_out, uint16_t* q_lo,
                            uint16_t* k_cache_l, uint16_t* v_cache_l, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, int batch, hipStream_t s);
+constexpr int ATTN_RING = 4;  // 32-key K/V blocks in flight per attention workgroup
+int attn_waves(int group);    // waves (query heads) per attention workgroup
 hipError_t launch_attn_combine(const float* part_o, const float* part_ml, StepMeta meta, int Hq, int dh,
                                int splits, int qrows, int max_tree, int batch, uint16_t* o_out, int o_ks,
                                hipStream_t s);

@@ -87,6 +87,8 @@ int validate_desc(const griffin_model_desc* d, std::string* why) {
 // Launch shape of one weight matrix (fixed at init; the packing follows it).
 struct GemmPlan {
   int epi = 0, nb = 1, wn = 4, pf = 4;
+  int kslices = 1;  // K slices merged inside a workgroup (shape.splits / kslices output splits)
+  int out_splits() const { return shape.splits / kslices; }
   int n_out = 0;   // output columns
   int rows = 0;    // weight rows (SwiGLU: 2 * n_out)
   int K = 0, ks = 0, ks_pad = 0;
@@ -127,9 +129,16 @@ GemmPlan plan_gemm(int epi, int n_out, int K, int experts = 1) {
       }
     }
   }
+  if (epi == EPI_SWIGLU && p.ks >= 4) {
+    // one column block per wave gives too few waves to keep the matrix cores
+    // of every SIMD busy with split-bf16 operands: two waves per column block
+    // take the two K halves and merge in LDS
+    p.kslices = 2;
+    splits = 2;
+  }
   const int len = cdiv(p.ks, splits);
   p.ks_pad = len * splits;
-  p.pf = len >= 8 ? 4 : 2;
+  p.pf = len >= 8 ? (p.kslices > 1 ? 3 : 4) : 2;
   p.shape = PackShape{p.nb, p.wn, splits, len, n_wgs, epi == EPI_SWIGLU ? 1 : 0, n_out};
   p.elems = packed_elems(p.shape);
   return p;
@@ -227,6 +236,7 @@ GemmArgs gemm_args(const GemmPlan& p, const uint16_t* X, int x_ks, const uint16_
   a.pf = p.pf;
   a.n_wgs = p.shape.n_wgs;
   a.splits = p.shape.splits;
+  a.kslices = p.kslices;
   a.len = p.shape.len;
   a.N = p.n_out;
   a.m_tiles = m_tiles;
@@ -291,7 +301,7 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
     }
     uint16_t* kc = c->k_cache + (size_t)l * layer_kv;
     uint16_t* vc = c->v_cache + (size_t)l * layer_kv;
-    LAUNCH(GRIFFIN_KC_ROPE, launch_qkv_rope(c->parts, c->p_qkv.shape.splits, ps * c->qkv_n, c->meta, c->rope_cos,
+    LAUNCH(GRIFFIN_KC_ROPE, launch_qkv_rope(c->parts, c->p_qkv.out_splits(), ps * c->qkv_n, c->meta, c->rope_cos,
                                             c->rope_sin, d.n_q_heads, d.n_kv_heads, d.head_dim, d.max_tree, B,
                                             d.kv_capacity, c->q, c->q_lo, kc, vc, s));
     {
@@ -326,7 +336,7 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
     }
     ResidualAdd add_o{};
     add_o.parts = c->parts;
-    add_o.n_parts = c->p_o.shape.splits;
+    add_o.n_parts = c->p_o.out_splits();
     add_o.part_stride = ps * d.d_model;
     LAUNCH(GRIFFIN_KC_NORM, launch_residual_rmsnorm(c->x, add_o, c->mlp_norm[l], d.rms_eps, Mpad, d.d_model, c->xn,
                                                     c->xd_ks, s));
@@ -344,7 +354,7 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
       LAUNCH(GRIFFIN_KC_DOWN, launch_gemm(dn, 1, s));
       add_down = ResidualAdd{};
       add_down.parts = c->parts;
-      add_down.n_parts = c->p_down.shape.splits;
+      add_down.n_parts = c->p_down.out_splits();
       add_down.part_stride = ps * d.d_model;
     } else {
       const int xe_tiles = Mpad / 64;
@@ -377,7 +387,7 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
       add_down.slot = c->slot;
       add_down.slot_w = c->route_w;
       add_down.top_k = c->topk;
-      add_down.n_parts = c->p_down.shape.splits;
+      add_down.n_parts = c->p_down.out_splits();
       add_down.part_stride = (long long)c->E * Mpad * d.d_model;
     }
   }
@@ -496,8 +506,12 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
   c->attn_w = d.n_q_heads * d.head_dim;
   c->qblocks = cdiv(d.max_tree, 32);
   {
-    const int by_len = cdiv(d.kv_capacity, 256);
-    const int by_par = std::max(1, cdiv(2048, d.max_batch * d.n_q_heads * c->qblocks));
+    // key splits: about 256 attention workgroups (one per CU), at least two
+    // 32-key blocks per split
+    const int G = d.n_q_heads / d.n_kv_heads, nw = attn_waves(G);
+    const int units = d.max_batch * d.n_kv_heads * cdiv(G, nw) * c->qblocks;
+    const int by_par = cdiv(256, units);
+    const int by_len = std::max(1, d.kv_capacity / 64);
     c->attn_splits = std::max(1, std::min(std::min(by_len, by_par), 16));
   }
   c->p_qkv = plan_gemm(EPI_STORE, c->qkv_n, d.d_model);
@@ -508,9 +522,9 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
   c->xd_ks = std::max({c->p_qkv.ks_pad, c->p_gu.ks_pad, c->p_lm.ks_pad});
   const long long Mp = c->Mpad;
   const long long tiles = Mp / 64;
-  c->parts_elems = Mp * std::max({(long long)c->p_qkv.shape.splits * c->qkv_n,
-                                  (long long)c->p_o.shape.splits * d.d_model,
-                                  (long long)c->p_down.shape.splits * d.d_model});
+  c->parts_elems = Mp * std::max({(long long)c->p_qkv.out_splits() * c->qkv_n,
+                                  (long long)c->p_o.out_splits() * d.d_model,
+                                  (long long)c->p_down.out_splits() * d.d_model});
   const int qrows = c->qblocks * 32;
 
 #define ALLOC(ptr, n)                              \
@@ -549,7 +563,7 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
     ALLOC(c->gather, (long long)c->E * Mp);
     ALLOC(c->count, c->E);
     ALLOC(c->slot, Mp * c->topk);
-    ALLOC(c->yslots, (long long)c->p_down.shape.splits * c->E * Mp * d.d_model);
+    ALLOC(c->yslots, (long long)c->p_down.out_splits() * c->E * Mp * d.d_model);
     ALLOC(c->xe, (long long)c->E * tiles * c->xd_ks * XPACK_STEP);
   }
 #undef ALLOC
