@@ -189,7 +189,8 @@ def main():
     total_bytes, parts = algorithmic_bytes(w)
     log(f"{ms_per_step:.3f} ms/step (events {ev_ms:.3f}), {steps_per_s:.1f} steps/s")
 
-    # per kernel class timing (separate pass: event records between launches)
+    # per kernel class timing (separate pass: HIP events recorded on the
+    # library's stream around every launch of the class)
     kernels, roofline = {}, None
     if not args.no_profile:
         v.profile_enable()
@@ -210,8 +211,12 @@ def main():
             kernels[name] = ent
         dom = max((k for k in kernels if k in per_launch), key=lambda k: kernels[k]["ms_per_step"])
         ach = kernels[dom]["achieved_GBs"]
+        from paper_2502_11018_amd.profiling import read_traffic_record
+        traffic = read_traffic_record(os.path.join(ROOT, "profiles"), dom, w.name, ROOT)
         roofline = {"bound": "hbm", "kernel": dom, "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                    "frac": round(ach / PEAK_HBM_GBS, 4), "traffic": None,
+                    "frac": round(ach / PEAK_HBM_GBS, 4),
+                    "traffic": None if traffic is None else int(round(traffic)),
+                    "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-scaled)",
                     "bytes_per_launch": kernels[dom]["bytes_per_launch"],
                     "avg_launch_us": kernels[dom]["avg_launch_us"]}
 
@@ -233,7 +238,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (random-init weights, seeded prefix KV and draft trees)",
-        "config": {"workload": w.name, "model_shape": m.name, "batch": w.batch, "prefix_len": w.prefix_len,
+        "config": {"workload": w.name, "batch": w.batch, "prefix_len": w.prefix_len,
                    "tree_nodes": w.tree_nodes, "draft_tokens": w.n_draft, "depth": w.depth},
         "draft_tree_tokens_per_s": round(steps_per_s * w.batch * w.n_draft, 1),
         "algorithmic_bytes_per_step": total_bytes,

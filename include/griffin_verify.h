@@ -76,8 +76,12 @@ typedef struct griffin_model_desc {
   int32_t kv_capacity; /* cache slots per (layer, sequence, KV head) */
 } griffin_model_desc;
 
-/* Device weights, bf16, row-major, borrowed.  Per-layer fields point to host
- * arrays of n_layers device pointers (the host arrays are copied at init).
+/* Device weights, bf16, row-major.  Per-layer fields point to host arrays of
+ * n_layers device pointers (the host arrays are copied at init).
+ * The projection matrices (w_qkv, w_o, w_gate_up, w_down) and lm_head are read
+ * only by griffin_verify_init, which repacks them into a buffer the context
+ * owns (same size as the originals); the caller may free them after init.
+ * embed, the norm gains and w_router are borrowed for the context's lifetime.
  *   embed       [vocab][d_model]
  *   lm_head     [vocab][d_model]          (untied)
  *   final_norm  [d_model]
@@ -109,8 +113,9 @@ size_t griffin_kv_cache_bytes(const griffin_model_desc *desc);
  *          (values in 32-slot tiles, each stored transposed: slot s of a
  *          head, dimension j lives at tile s/32, row j, column s%32).
  * hip_stream: the hipStream_t every launch is enqueued on (NULL = default).
- * The context allocates its own workspace (activations, partial sums,
- * metadata, pinned staging) and frees it in griffin_verify_free.
+ * The context allocates its own workspace (the repacked weights, activations,
+ * partial sums, metadata, pinned staging) and frees it in griffin_verify_free;
+ * init synchronises the stream once the repacking is done.
  * Errors: EINVAL (null pointer, misaligned pointer), ESHAPE, ENOMEM, EHIP. */
 int griffin_verify_init(const griffin_model_desc *desc, const griffin_weights *weights,
                         void *k_cache, void *v_cache, void *hip_stream, griffin_ctx **out);
