@@ -23,8 +23,9 @@
 //    side reads each operand with one conflict-free ds_read_b128.
 //  * Q and K use the same head-dim permutation as the projection GEMMs: a lane
 //    reads 32 consecutive head dims and feeds 8 of them to each of 4 MFMAs.
-//  * Q and P enter the matrix cores as split bf16 (hi + lo, two MFMAs each),
-//    so only the cached K/V carry bf16 rounding.
+//  * Q and P enter the matrix cores as split bf16 (hi + lo, two MFMAs each);
+//    the tree's own K/V add their bf16 residuals (one more MFMA each, against
+//    the hi part of q or p), so only the prefix K/V carry bf16 rounding.
 // Scores are kept in the log2 domain (scaled by log2(e)/sqrt(dh)) and exp2 is
 // used throughout; masked keys contribute exactly zero.
 
@@ -102,6 +103,7 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
   }
 
   const long long head = ((long long)b * a.Hkv + hk) * a.kv_cap * DH;
+  const long long lo_head = ((long long)b * a.Hkv + hk) * a.tree_lo.tiles * 32 * DH;
   const uint16_t* kbase = a.k_cache + head;
   const uint16_t* vbase = a.v_cache + head;
   // MFMA row -> key offset inside a 32-key block: row 8q + 4h + e holds key 16h + 4q + e
@@ -146,6 +148,37 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
     constexpr bool MASKED = decltype(masked)::value;
     const int key0 = kb * 32;
     // ---- S^T = K Q^T (rows: keys, cols: queries), q = q_hi + q_lo
+    // Tree blocks also carry the bf16 residuals of the tree K/V (zero outside
+    // the tree slots); they are loaded first so that their latency overlaps
+    // the MFMAs of the cached part.
+    u32x4 klo[CH][4], vlo[DB][2];
+    if constexpr (MASKED) {
+      const int tile = kb - (P >> 5);
+      const uint16_t* kl = a.tree_lo.k + lo_head + ((long long)tile * 32 + krow) * DH + 32 * hh;
+      const uint16_t* vl = a.tree_lo.v + lo_head + (long long)tile * DH * 32 + col * 32 + 16 * hh;
+      const int kkey = key0 + krow;
+      const bool kin = kkey >= P && kkey < Lb;
+#pragma unroll
+      for (int c = 0; c < CH; ++c)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          klo[c][j] = ld_u4(kl + 64 * c + 8 * j);
+          if (!kin) klo[c][j] = zero_u4();
+        }
+#pragma unroll
+      for (int d = 0; d < DB; ++d)
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+          vlo[d][t] = ld_u4(vl + d * 32 * 32 + 8 * t);
+          const int kfirst = key0 + 16 * hh + 8 * t;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {  // bf16 element 2q is the low half of dword q
+            const int k0 = kfirst + 2 * q, k1 = k0 + 1;
+            const uint32_t keep = (k0 >= P && k0 < Lb ? 0x0000ffffu : 0u) | (k1 >= P && k1 < Lb ? 0xffff0000u : 0u);
+            vlo[d][t][q] &= keep;
+          }
+        }
+    }
     f32x16 sacc;
 #pragma unroll
     for (int r = 0; r < 16; ++r) sacc[r] = 0.f;
@@ -158,6 +191,13 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
         for (int h = 0; h < 2; ++h)
           sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf), as_bf16x8(qf[h][c][j]), sacc, 0, 0, 0);
       }
+    if constexpr (MASKED) {
+#pragma unroll
+      for (int c = 0; c < CH; ++c)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(klo[c][j]), as_bf16x8(qf[0][c][j]), sacc, 0, 0, 0);
+    }
 
     // ---- mask (this lane: query qi, keys key0 + 16 hh + r); the log2-domain
     // scale is applied inside the exponent (scale > 0 commutes with max)
@@ -223,6 +263,8 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
 #pragma unroll
         for (int h = 0; h < 2; ++h)
           oacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf), as_bf16x8(pf[h]), oacc[d], 0, 0, 0);
+        if constexpr (MASKED)
+          oacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vlo[d][t]), as_bf16x8(pf[0]), oacc[d], 0, 0, 0);
       }
     }
   };

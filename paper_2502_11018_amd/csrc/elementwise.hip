@@ -178,7 +178,8 @@ hipError_t launch_moe_gather(const uint16_t* xn, int xn_ks, const int32_t* gathe
 // For a valid tree row r = b*max_tree + i: sum the K-split partials of its
 // QKV projection, rotate q and k (rotate-half pairing j <-> j + dh/2) at the
 // node's position, write q (bf16) for attention, and k / v into cache slot
-// prefix_len[b] + i (k row-major per slot, v transposed: one row per dim).
+// prefix_len[b] + i (k row-major per slot, v transposed: one row per dim),
+// and their bf16 residuals into the tree tiles.
 // q is kept as split bf16: q_out holds bf16(q), q_lo the bf16 residual.
 template <int NP>
 __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* __restrict__ parts, int n_parts_unused,
@@ -187,7 +188,8 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* __restrict__
                                                        const float* __restrict__ rsin, int Hq, int Hkv,
                                                        int dh, int max_tree, int kv_cap,
                                                        uint16_t* __restrict__ q_out, uint16_t* __restrict__ q_lo,
-                                                       uint16_t* __restrict__ kc, uint16_t* __restrict__ vc) {
+                                                       uint16_t* __restrict__ kc, uint16_t* __restrict__ vc,
+                                                       TreeKVLo lo) {
   const int r = blockIdx.x;
   const int b = r / max_tree, i = r % max_tree;
   if (i >= meta.n_nodes[b]) return;
@@ -195,7 +197,10 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* __restrict__
   const int heads = Hq + 2 * Hkv;
   const int width = heads * dh;
   const int pos = meta.pos[r];
-  const int slot = meta.prefix_len[b] + i;
+  const int P = meta.prefix_len[b];
+  const int slot = P + i;
+  const int rel = slot - (P & ~31);  // slot inside the residual tiles
+  const long long lo_head = (long long)lo.tiles * 32 * dh;
   const float* __restrict__ row = parts + (long long)r * width;
   const int t = blockIdx.y * blockDim.x + threadIdx.x;  // one (head, rotation pair) per thread
   if (t < heads * half) {
@@ -227,15 +232,24 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* __restrict__
         q_lo[o + j + half] = f32_to_bf16(y2 - bf16_to_f32(h2));
       } else {
         uint16_t* k = kc + (((long long)b * Hkv + (h - Hq)) * kv_cap + slot) * dh;
-        k[j] = f32_to_bf16(y1);
-        k[j + half] = f32_to_bf16(y2);
+        const uint16_t h1 = f32_to_bf16(y1), h2 = f32_to_bf16(y2);
+        k[j] = h1;
+        k[j + half] = h2;
+        uint16_t* kl = lo.k + ((long long)b * Hkv + (h - Hq)) * lo_head + (long long)rel * dh;
+        kl[j] = f32_to_bf16(y1 - bf16_to_f32(h1));
+        kl[j + half] = f32_to_bf16(y2 - bf16_to_f32(h2));
       }
     } else {
       // 32-slot tiles, transposed within the tile: [tile][dim][32]
       uint16_t* v = vc + ((long long)b * Hkv + (h - Hq - Hkv)) * dh * kv_cap + (long long)(slot >> 5) * dh * 32 +
                     (slot & 31);
-      v[j * 32] = f32_to_bf16(x1);
-      v[(j + half) * 32] = f32_to_bf16(x2);
+      const uint16_t h1 = f32_to_bf16(x1), h2 = f32_to_bf16(x2);
+      v[j * 32] = h1;
+      v[(j + half) * 32] = h2;
+      uint16_t* vl = lo.v + ((long long)b * Hkv + (h - Hq - Hkv)) * lo_head + (long long)(rel >> 5) * dh * 32 +
+                     (rel & 31);
+      vl[j * 32] = f32_to_bf16(x1 - bf16_to_f32(h1));
+      vl[(j + half) * 32] = f32_to_bf16(x2 - bf16_to_f32(h2));
     }
   }
 }
@@ -243,14 +257,16 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* __restrict__
 hipError_t launch_qkv_rope(const float* qkv_parts, int n_parts, long long part_stride, StepMeta meta,
                            const float* rope_cos, const float* rope_sin, int Hq, int Hkv, int dh, int max_tree,
                            int batch, int kv_cap, uint16_t* q_out, uint16_t* q_lo, uint16_t* k_cache_l,
-                           uint16_t* v_cache_l, hipStream_t s) {
+                           uint16_t* v_cache_l, TreeKVLo tree_lo, hipStream_t s) {
+  if (tree_lo.tiles * 32 < max_tree + 31) return hipErrorInvalidValue;  // slot offsets reach 31 + max_tree - 1
   const int items = (Hq + 2 * Hkv) * (dh / 2);
   const dim3 grid(batch * max_tree, (items + 255) / 256);
   switch (n_parts) {
 #define GRIFFIN_ROPE_CASE(n)                                                                                   \
   case n:                                                                                                     \
     hipLaunchKernelGGL(qkv_rope_kernel<n>, grid, dim3(256), 0, s, qkv_parts, n_parts, part_stride, meta, rope_cos, \
-                       rope_sin, Hq, Hkv, dh, max_tree, kv_cap, q_out, q_lo, k_cache_l, v_cache_l);                 \
+                       rope_sin, Hq, Hkv, dh, max_tree, kv_cap, q_out, q_lo, k_cache_l, v_cache_l, \
+                       tree_lo);                 \
     break;
     GRIFFIN_ROPE_CASE(1) GRIFFIN_ROPE_CASE(2) GRIFFIN_ROPE_CASE(3) GRIFFIN_ROPE_CASE(4) GRIFFIN_ROPE_CASE(5)
     GRIFFIN_ROPE_CASE(6) GRIFFIN_ROPE_CASE(7) GRIFFIN_ROPE_CASE(8) GRIFFIN_ROPE_CASE(9) GRIFFIN_ROPE_CASE(10)
@@ -263,31 +279,66 @@ hipError_t launch_qkv_rope(const float* qkv_parts, int n_parts, long long part_s
 }
 
 // ------------------------------------------------------ argmax reduction ----
-// pred[r] = argmax over the LM-head tiles' partial maxima (ascending tile
-// order, strict comparison, so ties keep the lowest token id).
-__global__ __launch_bounds__(64) void argmax_reduce_kernel(const float* __restrict__ pmax,
-                                                           const int32_t* __restrict__ pidx,
-                                                           const int32_t* __restrict__ pnan, int n_tiles,
-                                                           int ld_part, int32_t* pred, int32_t* nan_row) {
+// pred[r] = argmax over the LM-head column groups' partial maxima; ties keep
+// the lowest token id.
+__device__ __forceinline__ void argmax_merge(float& best, int& bidx, float v, int id) {
+  if (v > best || (v == best && id < bidx)) { best = v; bidx = id; }
+}
+
+// One 256-thread workgroup per row; each thread issues all loads of its
+// entries of a 4096-entry chunk before comparing any.  (max, lowest index) is
+// a total order, so the result does not depend on the reduction order.
+constexpr int AR_THREADS = 256, AR_PER = 16;
+__global__ __launch_bounds__(AR_THREADS) void argmax_reduce_kernel(const float* __restrict__ pmax,
+                                                                   const int32_t* __restrict__ pidx,
+                                                                   const int32_t* __restrict__ pnan, int n_tiles,
+                                                                   int ld_part, int32_t* pred, int32_t* nan_row) {
+  __shared__ float sb[AR_THREADS / 64];
+  __shared__ int si[AR_THREADS / 64], sn[AR_THREADS / 64];
   const int r = blockIdx.x;
-  const int lane = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const float* pm = pmax + (long long)r * ld_part;
+  const int32_t* pi = pidx + (long long)r * ld_part;
+  const int32_t* pn = pnan + (long long)r * ld_part;
   float best = -INFINITY;
   int bidx = 0x7fffffff;
   int nan_cnt = 0;
-  for (int t = lane; t < n_tiles; t += 64) {
-    const float v = pmax[(long long)r * ld_part + t];
-    const int id = pidx[(long long)r * ld_part + t];
-    nan_cnt += pnan[(long long)r * ld_part + t];
-    if (v > best || (v == best && id < bidx)) { best = v; bidx = id; }
+  for (int base = 0; base < n_tiles; base += AR_THREADS * AR_PER) {
+    float v[AR_PER];
+    int id[AR_PER], nn[AR_PER];
+#pragma unroll
+    for (int k = 0; k < AR_PER; ++k) {
+      const int t = min(base + k * AR_THREADS + tid, n_tiles - 1);  // clamped: loads stay unconditional
+      v[k] = pm[t];
+      id[k] = pi[t];
+      nn[k] = pn[t];
+    }
+#pragma unroll
+    for (int k = 0; k < AR_PER; ++k) {
+      if (base + k * AR_THREADS + tid < n_tiles) {
+        argmax_merge(best, bidx, v[k], id[k]);
+        nan_cnt += nn[k];
+      }
+    }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {
     const float ob = __shfl_xor(best, o, 64);
     const int oi = __shfl_xor(bidx, o, 64);
     nan_cnt += __shfl_xor(nan_cnt, o, 64);
-    if (ob > best || (ob == best && oi < bidx)) { best = ob; bidx = oi; }
+    argmax_merge(best, bidx, ob, oi);
   }
   if (lane == 0) {
+    sb[w] = best;
+    si[w] = bidx;
+    sn[w] = nan_cnt;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    for (int k = 1; k < AR_THREADS / 64; ++k) {
+      argmax_merge(best, bidx, sb[k], si[k]);
+      nan_cnt += sn[k];
+    }
     pred[r] = bidx;
     nan_row[r] = nan_cnt;
   }
@@ -295,8 +346,9 @@ __global__ __launch_bounds__(64) void argmax_reduce_kernel(const float* __restri
 
 hipError_t launch_argmax_reduce(const float* pmax, const int32_t* pidx, const int32_t* pnan, int n_tiles,
                                 int ld_part, int rows, int32_t* pred, int32_t* nan_row, hipStream_t s) {
-  hipLaunchKernelGGL(argmax_reduce_kernel, dim3(rows), dim3(64), 0, s, pmax, pidx, pnan, n_tiles, ld_part, pred,
-                     nan_row);
+  if (n_tiles < 1) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(argmax_reduce_kernel, dim3(rows), dim3(AR_THREADS), 0, s, pmax, pidx, pnan, n_tiles, ld_part,
+                     pred, nan_row);
   return hipGetLastError();
 }
 

@@ -95,11 +95,24 @@ struct ResidualAdd {
   int top_k;
 };
 
+// bf16 residuals x - bf16(x) of the tree nodes' K and V (the cache holds
+// bf16(x)), for the layer being computed, in 32-slot tiles counted from the
+// tile that holds slot prefix_len of each sequence (P0 = prefix_len & ~31):
+//   k: [B][Hkv][tiles][32][dh]      v: [B][Hkv][tiles][dh][32]
+// Entries outside [prefix_len, prefix_len + n_nodes) are never written and
+// are masked by the reader.
+struct TreeKVLo {
+  uint16_t* k;
+  uint16_t* v;
+  int tiles;  // ceil((max_tree + 31) / 32)
+};
+
 struct AttnArgs {
   const uint16_t* q;         // bf16 [R][Hq][dh]
   const uint16_t* q_lo;      // bf16 residual q - bf16(q), same layout
   const uint16_t* k_cache;   // this layer: [max_batch][Hkv][cap][dh]
   const uint16_t* v_cache;   // this layer: [max_batch][Hkv][cap / 32][dh][32]
+  TreeKVLo tree_lo;          // residuals of the tree K/V (written by qkv_rope)
   float* part_o;             // [B][Hq][S][qrows][dh]
   float* part_ml;            // [B][Hq][S][qrows][2]
   StepMeta meta;
@@ -117,7 +130,7 @@ hipError_t launch_residual_rmsnorm(float* x, const ResidualAdd& add, const uint1
 hipError_t launch_qkv_rope(const float* qkv_parts, int n_parts, long long part_stride, StepMeta meta,
                            const float* rope_cos, const float* rope_sin, int Hq, int Hkv, int dh,
                            int max_tree, int batch, int kv_cap, uint16_t* q_out, uint16_t* q_lo,
-                           uint16_t* k_cache_l, uint16_t* v_cache_l, hipStream_t s);
+                           uint16_t* k_cache_l, uint16_t* v_cache_l, TreeKVLo tree_lo, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, int batch, hipStream_t s);
 constexpr int ATTN_RING = 4;  // 32-key K/V blocks in flight per attention workgroup
 int attn_waves(int group);    // waves (query heads) per attention workgroup

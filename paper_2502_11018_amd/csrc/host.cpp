@@ -168,6 +168,7 @@ struct griffin_ctx {
   float *x = nullptr, *parts = nullptr, *attn_po = nullptr, *attn_pml = nullptr;
   float *rope_cos = nullptr, *rope_sin = nullptr, *pmax = nullptr, *route_w = nullptr, *yslots = nullptr;
   uint16_t *xn = nullptr, *q = nullptr, *q_lo = nullptr, *o = nullptr, *act = nullptr, *xe = nullptr;
+  TreeKVLo tree_lo{};  // tree K/V residual tiles, reused by every layer
   int32_t *pidx = nullptr, *pnan = nullptr, *pred = nullptr, *nan_row = nullptr, *result = nullptr;
   int32_t *route_ids = nullptr, *gather = nullptr, *count = nullptr, *slot = nullptr;
 
@@ -303,13 +304,14 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
     uint16_t* vc = c->v_cache + (size_t)l * layer_kv;
     LAUNCH(GRIFFIN_KC_ROPE, launch_qkv_rope(c->parts, c->p_qkv.out_splits(), ps * c->qkv_n, c->meta, c->rope_cos,
                                             c->rope_sin, d.n_q_heads, d.n_kv_heads, d.head_dim, d.max_tree, B,
-                                            d.kv_capacity, c->q, c->q_lo, kc, vc, s));
+                                            d.kv_capacity, c->q, c->q_lo, kc, vc, c->tree_lo, s));
     {
       AttnArgs a{};
       a.q = c->q;
       a.q_lo = c->q_lo;
       a.k_cache = kc;
       a.v_cache = vc;
+      a.tree_lo = c->tree_lo;
       a.part_o = c->attn_po;
       a.part_ml = c->attn_pml;
       a.meta = c->meta;
@@ -544,6 +546,9 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
   ALLOC(c->parts, c->parts_elems);
   ALLOC(c->q, Mp * c->attn_w);
   ALLOC(c->q_lo, Mp * c->attn_w);
+  c->tree_lo.tiles = cdiv(d.max_tree + 31, 32);
+  ALLOC(c->tree_lo.k, (long long)d.max_batch * d.n_kv_heads * c->tree_lo.tiles * 32 * d.head_dim);
+  ALLOC(c->tree_lo.v, (long long)d.max_batch * d.n_kv_heads * c->tree_lo.tiles * 32 * d.head_dim);
   ALLOC(c->o, tiles * c->p_o.ks_pad * XPACK_STEP);
   ALLOC(c->attn_po, (long long)d.max_batch * d.n_q_heads * c->attn_splits * qrows * d.head_dim);
   ALLOC(c->attn_pml, (long long)d.max_batch * d.n_q_heads * c->attn_splits * qrows * 2);
