@@ -134,12 +134,18 @@ def moe_route(h: np.ndarray, w_router: np.ndarray, top_k: int):
 
 
 def moe(h: np.ndarray, L: Dict[str, np.ndarray], top_k: int):
+    """Each row gets the weighted sum of its kept experts' SwiGLU outputs,
+    added in rank order (highest probability first).  Every expert's SwiGLU is
+    evaluated once over all rows that keep it (rows are independent)."""
     ids, wts, logits = moe_route(h, L["w_router"], top_k)
+    y = {}
+    for e in sorted(set(int(x) for x in ids.ravel())):
+        rows = np.nonzero((ids == e).any(axis=1))[0]
+        y[e] = dict(zip(rows.tolist(), swiglu(h[rows], L["w_gate_up"][e], L["w_down"][e])))
     out = np.zeros_like(h)
     for r in range(h.shape[0]):
         for j in range(top_k):
-            e = int(ids[r, j])
-            out[r] += wts[r, j] * swiglu(h[r:r + 1], L["w_gate_up"][e], L["w_down"][e])[0]
+            out[r] += wts[r, j] * y[int(ids[r, j])][r]
     return out, logits
 
 

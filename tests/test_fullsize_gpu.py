@@ -36,6 +36,20 @@ def test_generator_is_device_independent():
         assert torch.equal(a.view(torch.int16), b.view(torch.int16))
 
 
+class LoudKV(H.PrefixKV):
+    """PrefixKV that reports the oracle's progress (it reads layer l's cache
+    when it reaches layer l), so that a long host computation is never silent."""
+
+    def fn(self):
+        t0 = time.time()
+
+        def get(l):
+            if l % 8 == 0:
+                say(f"  oracle at layer {l} ({time.time() - t0:.0f}s)")
+            return self.K[l], self.V[l]
+        return get
+
+
 def _planted(w, ow, kv, max_index=64):
     """First tree of the pool that the workload plants, with its oracle greedy path."""
     for i in range(max_index):
@@ -82,4 +96,83 @@ def test_full_size_verify_matches_oracle(name):
             f"gated {st['gated']}/{st['total']}, accept checked {st['accept_checked']}, L={st['L']}")
         if label.startswith("planted") and st["accept_checked"]:
             assert int(acc.length[0]) >= len(path)
+    v.close()
+
+
+def test_full_size_moe_verify_matches_oracle():
+    """Mixtral-8x7B shape (about 94 GB of bf16 weights, 8 experts, top-2): one
+    unplanted tree through all 32 layers; nodes whose routing has an oracle
+    near-tie on their ancestry are left out of the gates and counted."""
+    import paper_2502_11018_amd as P
+    w = get_workload("mixtral-8x7b")
+    m = w.model
+    t0 = time.time()
+    say("mixtral-8x7b: generate weights on the GPU")
+    mw_gpu = gen.make_weights(m, w.weight_seed, device="cuda")
+    v = P.TreeVerifier(m, mw_gpu, max_batch=1, max_tree=64, max_depth=w.depth, kv_capacity=w.kv_capacity())
+    Ks, Vs = [], []
+    for l in range(m.n_layers):
+        k, vv = gen.synthetic_kv(m, l, 0, w.prefix_len, w.weight_seed, "cuda")
+        v.write_prefix(l, 0, k, vv)
+        Ks.append(k.to(torch.float64).cpu().numpy())
+        Vs.append(vv.to(torch.float64).cpu().numpy())
+    kv = LoudKV(Ks, Vs)
+    tree = next(gen.workload_tree(w, i)[0] for i in range(64) if not gen.workload_tree(w, i)[1])
+    say("mixtral-8x7b: GPU verify")
+    logits = torch.empty((64, m.vocab), device="cuda")
+    v.step([w.prefix_len], [tree], logits)
+    acc = v.accept()
+    pred = v.predictions()[0]
+    lg = logits[: tree.n].cpu().numpy()
+    v.close()
+    say(f"mixtral-8x7b: host copy of the weights ({time.time() - t0:.0f}s)")
+    ow = oracle.OracleWeights(mw_gpu.to("cpu"), cache=False)
+    del mw_gpu
+    say(f"mixtral-8x7b: oracle verify ({time.time() - t0:.0f}s)")
+    os_ = H.oracle_sequence(ow, H.SeqCase(None, kv, tree, [], [], []))
+    ex = H.router_near_tie_nodes(os_, m.top_k, H.ROUTER_GAP)
+    st = H.check_parity(os_, lg, pred[: tree.n], acc.sequence(0), exclude=ex)
+    say(f"mixtral-8x7b: max rel err {st['max_rel']:.2e}, gated {st['gated']}/{st['total']}, "
+        f"router near-tie nodes {len(ex)}, accept checked {st['accept_checked']} ({time.time() - t0:.0f}s)")
+    assert len(ex) < tree.n
+
+
+def test_full_size_long_context_batch_matches_oracle():
+    """Llama-3-8B shape, batch 8 x 16384-token prefixes (about 17 GB of KV),
+    eight different trees packed into one verify call; sequences 0, 3 and 7
+    are checked against the oracle."""
+    import paper_2502_11018_amd as P
+    w = get_workload("llama3-8b-longctx")
+    m = w.model
+    B = w.batch
+    t0 = time.time()
+    say("llama3-8b-longctx: generate weights on the GPU")
+    mw_gpu = gen.make_weights(m, w.weight_seed, device="cuda")
+    v = P.TreeVerifier(m, mw_gpu, max_batch=B, max_tree=64, max_depth=w.depth, kv_capacity=w.kv_capacity())
+    checked = (0, 3, 7)
+    host_kv = {b: ([], []) for b in checked}
+    for l in range(m.n_layers):
+        for b in range(B):
+            k, vv = gen.synthetic_kv(m, l, b, w.prefix_len, w.weight_seed, "cuda")
+            v.write_prefix(l, b, k, vv)
+            if b in checked:
+                host_kv[b][0].append(k.to(torch.float64).cpu().numpy())
+                host_kv[b][1].append(vv.to(torch.float64).cpu().numpy())
+    trees = [gen.workload_tree(w, 0, b)[0] for b in range(B)]
+    say(f"llama3-8b-longctx: GPU verify of {B} trees ({time.time() - t0:.0f}s)")
+    logits = torch.empty((B * 64, m.vocab), device="cuda")
+    v.step([w.prefix_len] * B, trees, logits)
+    acc = v.accept()
+    pred = v.predictions()
+    lg_all = logits.view(B, 64, m.vocab)
+    say(f"llama3-8b-longctx: host copy of the weights ({time.time() - t0:.0f}s)")
+    ow = oracle.OracleWeights(mw_gpu.to("cpu"), cache=True)
+    for b in checked:
+        say(f"llama3-8b-longctx: oracle verify of sequence {b} ({time.time() - t0:.0f}s)")
+        kv = LoudKV(*host_kv[b])
+        os_ = H.oracle_sequence(ow, H.SeqCase(None, kv, trees[b], [], [], []))
+        lg = lg_all[b, : trees[b].n].cpu().numpy()
+        st = H.check_parity(os_, lg, pred[b, : trees[b].n], acc.sequence(b))
+        say(f"llama3-8b-longctx seq {b}: max rel err {st['max_rel']:.2e}, gated {st['gated']}/{st['total']}, "
+            f"accept checked {st['accept_checked']}, L={st['L']}")
     v.close()
