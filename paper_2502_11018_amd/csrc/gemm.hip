@@ -49,8 +49,17 @@ __global__ __launch_bounds__(64 * WN * KS) void gemm_kernel(GemmArgs a) {
   const int kh = wave / WN;            // K slice of this wave inside the workgroup
   const int lr = lane & 31, g = lane >> 5;
   const int e = blockIdx.y;
-  const int m_tile = blockIdx.x % a.m_tiles;
-  const int wg = blockIdx.x / a.m_tiles;
+  // XCD-aware decode: workgroups are dispatched round-robin over the 8 XCDs
+  // (linear id % 8, and the grid's x extent is a multiple of 8), so the
+  // m_tiles workgroups that stream the same weights get the same id % 8 and
+  // the re-reads of those weights hit that XCD's L2.
+  int m_tile = 0, wg = blockIdx.x;
+  if (a.m_tiles > 1) {
+    const int grp = blockIdx.x / (8 * a.m_tiles), r = blockIdx.x % (8 * a.m_tiles);
+    m_tile = r >> 3;
+    wg = grp * 8 + (r & 7);
+    if (wg >= a.n_wgs) return;  // padding of the grid to a multiple of 8 (uniform)
+  }
   const int zsplit = blockIdx.z;       // output split (its KS slices are merged in the workgroup)
   const int split = zsplit * KS + kh;  // K slice of this wave's weight stream
   const int rows_e = a.count ? a.count[e] : a.m_tiles * 64;
@@ -248,7 +257,8 @@ __global__ __launch_bounds__(64 * WN * KS) void gemm_kernel(GemmArgs a) {
 
 template <int EPI, int NB, int WN, int PF, int KS>
 static hipError_t launch_one(const GemmArgs& a, int experts, hipStream_t s) {
-  dim3 grid(a.n_wgs * a.m_tiles, experts, a.splits / KS);
+  const int gx = a.m_tiles > 1 ? (a.n_wgs + 7) / 8 * 8 * a.m_tiles : a.n_wgs;
+  dim3 grid(gx, experts, a.splits / KS);
   hipLaunchKernelGGL((gemm_kernel<EPI, NB, WN, PF, KS>), grid, dim3(64 * WN * KS), 0, s, a);
   return hipGetLastError();
 }
