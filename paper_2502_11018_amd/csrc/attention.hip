@@ -46,6 +46,8 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
   constexpr int D = ATTN_RING;         // ring slots
   static_assert(PIECES % NW == 0 && PPW * (D - 2) < 64, "ring shape");
   __shared__ u32x4 ring[D][PIECES][64];
+  constexpr int LOT = 3;                // residual tiles of the tree region (max_tree <= 64)
+  __shared__ u32x4 lo_lds[LOT][PIECES][64];
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int col = lane & 31, hh = lane >> 5;
@@ -148,28 +150,25 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
     constexpr bool MASKED = decltype(masked)::value;
     const int key0 = kb * 32;
     // ---- S^T = K Q^T (rows: keys, cols: queries), q = q_hi + q_lo
-    // Tree blocks also carry the bf16 residuals of the tree K/V (zero outside
-    // the tree slots); they are loaded first so that their latency overlaps
-    // the MFMAs of the cached part.
+    // Tree blocks also carry the bf16 residuals of the tree K/V (staged in LDS
+    // at the start; zero outside the tree slots).
     u32x4 klo[CH][4], vlo[DB][2];
     if constexpr (MASKED) {
       const int tile = kb - (P >> 5);
-      const uint16_t* kl = a.tree_lo.k + lo_head + ((long long)tile * 32 + krow) * DH + 32 * hh;
-      const uint16_t* vl = a.tree_lo.v + lo_head + (long long)tile * DH * 32 + col * 32 + 16 * hh;
       const int kkey = key0 + krow;
       const bool kin = kkey >= P && kkey < Lb;
 #pragma unroll
       for (int c = 0; c < CH; ++c)
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          klo[c][j] = ld_u4(kl + 64 * c + 8 * j);
+          klo[c][j] = lo_lds[tile][c * 4 + j][lane];
           if (!kin) klo[c][j] = zero_u4();
         }
 #pragma unroll
       for (int d = 0; d < DB; ++d)
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
-          vlo[d][t] = ld_u4(vl + d * 32 * 32 + 8 * t);
+          vlo[d][t] = lo_lds[tile][KP + d * 2 + t][lane];
           const int kfirst = key0 + 16 * hh + 8 * t;
 #pragma unroll
           for (int q = 0; q < 4; ++q) {  // bf16 element 2q is the low half of dword q
@@ -277,6 +276,19 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
   // re-read it into slots that are never consumed; every DMA has landed
   // before the waves leave.
   if (nb > 0) {
+    if (kb1 * 32 > P) {
+      // this split reaches the tree slots: stage the residual tiles of the
+      // tree region ahead of the ring (older loads, so the ring's first wait
+      // and barrier also cover them)
+      for (int tl = 0; tl < a.tree_lo.tiles; ++tl) {
+#pragma unroll
+        for (int p = 0; p < PPW; ++p) {
+          const int pc = w * PPW + p;
+          const uint16_t* src = (pc < KP ? a.tree_lo.k : a.tree_lo.v) + lo_head + (long long)tl * 32 * DH + goff[p];
+          __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)&lo_lds[tl][pc][0], 16, 0, 0);
+        }
+      }
+    }
 #pragma unroll
     for (int i = 0; i < D - 1; ++i) issue(i, kb0 + min(i, nb - 1));
     for (int i = 0; i < nb; ++i) {
@@ -323,7 +335,7 @@ static void launch_attn_dh(const AttnArgs& a, int nw, dim3 grid, hipStream_t s) 
 }
 
 hipError_t launch_attention(const AttnArgs& a, int batch, hipStream_t s) {
-  if (a.batch != batch) return hipErrorInvalidValue;
+  if (a.batch != batch || a.tree_lo.tiles > 3) return hipErrorInvalidValue;
   const int G = a.Hq / a.Hkv;
   const int nw = attn_waves(G);
   const int streams = batch * a.Hkv;

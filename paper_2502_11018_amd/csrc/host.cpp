@@ -546,7 +546,7 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
   ALLOC(c->parts, c->parts_elems);
   ALLOC(c->q, Mp * c->attn_w);
   ALLOC(c->q_lo, Mp * c->attn_w);
-  c->tree_lo.tiles = cdiv(d.max_tree + 31, 32);
+  c->tree_lo.tiles = cdiv(d.max_tree + 31, 32);  // <= 3: the attention kernel stages at most 3 tiles
   ALLOC(c->tree_lo.k, (long long)d.max_batch * d.n_kv_heads * c->tree_lo.tiles * 32 * d.head_dim);
   ALLOC(c->tree_lo.v, (long long)d.max_batch * d.n_kv_heads * c->tree_lo.tiles * 32 * d.head_dim);
   ALLOC(c->o, tiles * c->p_o.ks_pad * XPACK_STEP);
