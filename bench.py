@@ -104,6 +104,7 @@ def main():
     ap.add_argument("--pool", type=int, default=16)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true")
+    ap.add_argument("--no-graphs", action="store_true", help="plain launches instead of graph replay")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on exactly one GPU; --gpus {args.gpus} is not supported", file=sys.stderr)
@@ -127,6 +128,7 @@ def main():
     max_tree = 64
     v = P.TreeVerifier(m, weights, max_batch=w.batch, max_tree=max_tree, max_depth=w.depth,
                        kv_capacity=w.kv_capacity())
+    v.set_graphs(not args.no_graphs)
     for l in range(m.n_layers):
         for b in range(w.batch):
             k, vv = gen.synthetic_kv(m, l, b, w.prefix_len, w.weight_seed, dev)

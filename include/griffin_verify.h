@@ -152,6 +152,16 @@ int griffin_accept(griffin_ctx *ctx, int32_t *accept_len, int32_t *tokens_out, i
  * Errors: EORDER, EHIP. */
 int griffin_read_predictions(griffin_ctx *ctx, int32_t *pred);
 
+/* Replay the launch sequence of a step from a captured HIP graph (default:
+ * enabled).  One graph is captured per (batch, logits_out) pair on its first
+ * step and replayed afterwards (at most 8 are kept, the oldest is dropped);
+ * every per-step input travels through device buffers whose addresses are
+ * fixed for the context, so replays compute exactly what plain launches do.
+ * Steps use plain launches while per-class timing is enabled or when the
+ * context was created on the legacy null stream.  enable: 0 = plain launches.
+ * Errors: EINVAL (null context). */
+int griffin_set_graphs(griffin_ctx *ctx, int32_t enable);
+
 /* Release the context (waits for its stream first).  NULL is a no-op. */
 void griffin_verify_free(griffin_ctx *ctx);
 

@@ -69,6 +69,7 @@ def _load() -> ctypes.CDLL:
                                           I32P, I32P, I32P]),
         "griffin_profile_enable": (c_int32, [c_void_p, c_uint32]),
         "griffin_profile_read": (c_int32, [c_void_p, POINTER(c_double), POINTER(c_int64)]),
+        "griffin_set_graphs": (c_int32, [c_void_p, c_int32]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -80,6 +81,7 @@ def _load() -> ctypes.CDLL:
 lib = _load()
 EXPORTED = ("griffin_kv_cache_bytes", "griffin_verify_init", "griffin_verify_step", "griffin_accept",
             "griffin_read_predictions", "griffin_verify_free", "griffin_status_str", "griffin_last_error",
-            "griffin_tree_prepare", "griffin_accept_walk", "griffin_profile_enable", "griffin_profile_read")
+            "griffin_tree_prepare", "griffin_accept_walk", "griffin_profile_enable", "griffin_profile_read",
+            "griffin_set_graphs")
 KERNEL_CLASSES = ("qkv_gemm", "rope_kv_write", "tree_attention", "o_gemm", "residual_rmsnorm", "gate_up_gemm",
                   "down_gemm", "lm_head_gemm", "argmax_accept_route")

@@ -185,6 +185,15 @@ struct griffin_ctx {
   int32_t* pred_host = nullptr;
   // per-class launch timing (griffin_profile_*)
   uint32_t prof_mask = 0;
+
+  // captured launch sequences of a pass, keyed by (batch, logits_out)
+  struct GraphEntry {
+    int batch;
+    float* logits;
+    hipGraphExec_t exec;
+  };
+  std::vector<GraphEntry> graphs;
+  bool use_graphs = true;
   std::vector<hipEvent_t> prof_ev;     // pairs: start, stop
   std::vector<int> prof_cls;           // class of each pair
   size_t prof_used = 0;                // pairs recorded since the last read
@@ -414,6 +423,43 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
   return GRIFFIN_OK;
 }
 
+// Enqueue one pass: replay a captured HIP graph of the launch sequence when
+// possible (one per batch size and logits_out pointer, at most kMaxGraphs
+// kept, captured on first use), otherwise launch kernel by kernel.  Every
+// per-step input lives in device buffers whose addresses are fixed for the
+// context, so a graph stays valid for its key.  Per-class timing and the
+// legacy null stream use the plain launches.
+constexpr size_t kMaxGraphs = 8;
+
+int run_pass(griffin_ctx* c, float* logits_out) {
+  if (!c->use_graphs || c->prof_mask != 0 || c->stream == nullptr) return enqueue_pass(c, logits_out);
+  for (auto& g : c->graphs)
+    if (g.batch == c->batch && g.logits == logits_out) {
+      HIP_TRY(c, hipGraphLaunch(g.exec, c->stream));
+      return GRIFFIN_OK;
+    }
+  HIP_TRY(c, hipStreamBeginCapture(c->stream, hipStreamCaptureModeThreadLocal));
+  const int rc = enqueue_pass(c, logits_out);
+  hipGraph_t graph = nullptr;
+  const hipError_t e = hipStreamEndCapture(c->stream, &graph);
+  if (rc != GRIFFIN_OK) {
+    if (graph) hipGraphDestroy(graph);
+    return rc;
+  }
+  HIP_TRY(c, e);
+  hipGraphExec_t exec = nullptr;
+  const hipError_t ei = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+  hipGraphDestroy(graph);
+  HIP_TRY(c, ei);
+  if (c->graphs.size() == kMaxGraphs) {
+    hipGraphExecDestroy(c->graphs.front().exec);
+    c->graphs.erase(c->graphs.begin());
+  }
+  c->graphs.push_back({c->batch, logits_out, exec});
+  HIP_TRY(c, hipGraphLaunch(exec, c->stream));
+  return GRIFFIN_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -458,6 +504,7 @@ void griffin_verify_free(griffin_ctx* c) {
     if (c->meta_ev[k]) hipEventDestroy(c->meta_ev[k]);
   }
   for (hipEvent_t e : c->prof_ev) hipEventDestroy(e);
+  for (auto& g : c->graphs) hipGraphExecDestroy(g.exec);
   if (c->result_host) hipHostFree(c->result_host);
   if (c->pred_host) hipHostFree(c->pred_host);
   delete c;
@@ -729,9 +776,15 @@ int griffin_verify_step(griffin_ctx* c, int32_t batch, const int32_t* prefix_len
   c->meta_cur = k;
   c->batch = batch;
   c->stepped = false;
-  const int rc = enqueue_pass(c, logits_out);
+  const int rc = run_pass(c, logits_out);
   if (rc != GRIFFIN_OK) return rc;
   c->stepped = true;
+  return GRIFFIN_OK;
+}
+
+int griffin_set_graphs(griffin_ctx* c, int32_t enable) {
+  if (!c) return GRIFFIN_EINVAL;
+  c->use_graphs = enable != 0;
   return GRIFFIN_OK;
 }
 

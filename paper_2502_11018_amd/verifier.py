@@ -225,5 +225,12 @@ def _profile_read(self) -> dict:
     return {name: (float(ms[k]), int(n[k])) for k, name in enumerate(N.KERNEL_CLASSES)}
 
 
+def _set_graphs(self, enable: bool = True):
+    """Replay each step's launch sequence from a captured HIP graph (default)
+    or launch kernel by kernel."""
+    _check(N.lib.griffin_set_graphs(self.ctx, 1 if enable else 0), "griffin_set_graphs", self.ctx)
+
+
 TreeVerifier.profile_enable = _profile_enable
 TreeVerifier.profile_read = _profile_read
+TreeVerifier.set_graphs = _set_graphs

@@ -282,3 +282,43 @@ def test_gpu_prefill_by_chain_steps_matches_oracle_prefill():
             for ref, got in ((kv.K[l], kg), (kv.V[l], vg)):
                 rel = np.abs(got - ref).max() / np.abs(ref).max()
                 assert rel < 3e-2, (l, rel)
+
+
+def test_graph_replay_matches_plain_launches():
+    """Steps replayed from captured HIP graphs give the same bits as plain
+    launches, on every replay, with plain steps and synchronisations between
+    the replays and two graph keys (batch sizes) in use."""
+    name = "small-gqa"
+    s = Setup(name, n_trees=3)
+    try:
+        m = s.w.model
+        B = s.w.batch
+        trees = [[c.tree for c in s.cases[i]] for i in range(3)]
+        out = torch.empty((B * s.max_tree, m.vocab), device=s.dev)
+
+        def step(ts):
+            out.fill_(float("nan"))
+            s.v.step([s.w.prefix_len] * len(ts), ts, out)
+            acc = s.v.accept(check=False)
+            return out[: len(ts) * s.max_tree].cpu().numpy().copy(), s.v.predictions(), \
+                [acc.sequence(b) for b in range(len(ts))]
+
+        say(f"{name}: plain launches")
+        s.v.set_graphs(False)
+        ref = [step(t) for t in trees]
+        ref1 = step(trees[0][:1])
+        s.v.set_graphs(True)
+        for rep in range(3):
+            for i, t in enumerate(trees):
+                say(f"{name}: graph replay {rep} tree set {i}")
+                lg, pred, acc = step(t)
+                assert np.array_equal(lg.view(np.uint32), ref[i][0].view(np.uint32))
+                assert np.array_equal(pred, ref[i][1]) and acc == ref[i][2]
+            lg1, pred1, acc1 = step(trees[0][:1])  # batch 1: a second graph
+            assert np.array_equal(lg1.view(np.uint32), ref1[0].view(np.uint32)) and acc1 == ref1[2]
+            s.v.set_graphs(False)            # plain step between replays
+            step(trees[(rep + 1) % 3])
+            torch.cuda.synchronize()
+            s.v.set_graphs(True)
+    finally:
+        s.v.close()
