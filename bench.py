@@ -55,6 +55,29 @@ def class_bytes_per_launch(w):
     }
 
 
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+
+
+def class_mfma_flops_per_launch(w):
+    """Executed MFMA flops of one launch of each matrix-core class: 64-row
+    activation tiles, split-bf16 operands (two MFMAs per product).  For the
+    batch-1 MoE shape every expert is assumed to receive rows (61 rows x top-2
+    over 8 experts leave one idle with probability ~2e-7)."""
+    m = w.model
+    rows = -(-w.batch * 64 // 64) * 64
+    d, f, e = m.d_model, m.d_ff, m.n_experts
+    keys = -(-(w.prefix_len + w.tree_nodes) // 32) * 32
+    return {
+        "qkv_gemm": 2 * 2 * rows * m.qkv_rows * d,
+        "o_gemm": 2 * 2 * rows * d * m.n_q_heads * m.head_dim,
+        # MoE: every expert that receives rows runs one 64-row tile per 64 routed rows
+        "gate_up_gemm": 2 * 2 * (e * 64 if e > 1 else rows) * 2 * f * d,
+        "down_gemm": 2 * 2 * (e * 64 if e > 1 else rows) * d * f,
+        "lm_head_gemm": 2 * 2 * rows * m.vocab * d,
+        "tree_attention": 2 * 2 * 2 * w.batch * m.n_q_heads * 64 * keys * m.head_dim,
+    }
+
+
 def cpu_baseline(w, weights_gpu, n_trees=2):
     """Time the fp64 oracle on a bounded sample of the same workload: the full
     verify pass (all layers, LM head, argmax, acceptance) of the first
@@ -193,6 +216,7 @@ def main():
         prof = v.profile_read()
         v.profile_enable(0)
         per_launch = class_bytes_per_launch(w)
+        flops = class_mfma_flops_per_launch(w)
         for name, (ms, n) in prof.items():
             if n == 0:
                 continue
@@ -201,6 +225,10 @@ def main():
             if name in per_launch:
                 ent["bytes_per_launch"] = per_launch[name]
                 ent["achieved_GBs"] = round(per_launch[name] / (ms / n * 1e-3) / 1e9, 1)
+            if name in flops:
+                tf = flops[name] / (ms / n * 1e-3) / 1e12
+                ent["mfma_TFLOPs"] = round(tf, 1)
+                ent["mfma_frac"] = round(tf / PEAK_BF16_TFLOPS, 4)
             kernels[name] = ent
         dom = max((k for k in kernels if k in per_launch), key=lambda k: kernels[k]["ms_per_step"])
         ach = kernels[dom]["achieved_GBs"]
