@@ -147,6 +147,18 @@ int griffin_verify_step(griffin_ctx *ctx, int32_t batch, const int32_t *prefix_l
  * the outputs are still written). */
 int griffin_accept(griffin_ctx *ctx, int32_t *accept_len, int32_t *tokens_out, int32_t *path_nodes);
 
+/* Commit the last step's accepted path into the KV cache (asynchronous, on
+ * the context's stream; needs no host round trip).  For every sequence b of
+ * that step, with L accepted draft nodes n_1..n_L at depths 1..L: their K/V,
+ * already rotated at positions prefix_len + k, move from scratch slots
+ * prefix_len + n_k to slots prefix_len + k, so that slots [0, prefix_len + L]
+ * hold the plain causal cache of prefix + root + accepted tokens.  The caller
+ * continues with prefix_len + L + 1 and the target's extra token (tokens_out
+ * entry L of griffin_accept) as the next root.  The paper's losslessness: a
+ * loop of step / accept / commit emits exactly the target's greedy tokens.
+ * Errors: EINVAL, EORDER (no step yet), EHIP. */
+int griffin_commit(griffin_ctx *ctx);
+
 /* Wait for the last step and copy the target's greedy prediction (argmax of
  * the logits) of every node: pred [batch][max_tree] host, -1 for absent nodes.
  * Errors: EORDER, EHIP. */

@@ -70,6 +70,7 @@ def _load() -> ctypes.CDLL:
         "griffin_profile_enable": (c_int32, [c_void_p, c_uint32]),
         "griffin_profile_read": (c_int32, [c_void_p, POINTER(c_double), POINTER(c_int64)]),
         "griffin_set_graphs": (c_int32, [c_void_p, c_int32]),
+        "griffin_commit": (c_int32, [c_void_p]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -82,6 +83,6 @@ lib = _load()
 EXPORTED = ("griffin_kv_cache_bytes", "griffin_verify_init", "griffin_verify_step", "griffin_accept",
             "griffin_read_predictions", "griffin_verify_free", "griffin_status_str", "griffin_last_error",
             "griffin_tree_prepare", "griffin_accept_walk", "griffin_profile_enable", "griffin_profile_read",
-            "griffin_set_graphs")
+            "griffin_set_graphs", "griffin_commit")
 KERNEL_CLASSES = ("qkv_gemm", "rope_kv_write", "tree_attention", "o_gemm", "residual_rmsnorm", "gate_up_gemm",
                   "down_gemm", "lm_head_gemm", "argmax_accept_route")

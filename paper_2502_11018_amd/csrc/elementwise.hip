@@ -405,6 +405,51 @@ hipError_t launch_accept(StepMeta meta, const int32_t* pred, const int32_t* nan_
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------ KV commit ----
+// After the acceptance walk: the accepted path's nodes n_1..n_L (depths
+// 1..L) hold K/V already rotated at positions prefix_len + k, in scratch slots
+// prefix_len + n_k.  Move them to slots prefix_len + k so that the cache is the
+// plain causal cache of prefix + root + accepted tokens.  One workgroup per
+// (KV head, sequence, layer); every source is read into LDS before any
+// destination is written (a destination slot can be a later source).
+constexpr int COMMIT_MAX_DEPTH = 63;
+__global__ __launch_bounds__(256) void commit_kernel(const int32_t* __restrict__ result, int max_depth,
+                                                     StepMeta meta, int Hkv, int dh, int kv_cap, long long layer_kv,
+                                                     uint16_t* __restrict__ kc, uint16_t* __restrict__ vc) {
+  __shared__ uint16_t ks[COMMIT_MAX_DEPTH * 128], vs[COMMIT_MAX_DEPTH * 128];
+  const int hk = blockIdx.x, b = blockIdx.y, l = blockIdx.z;
+  const int32_t* res = result + (long long)b * result_stride(max_depth);
+  const int L = res[0];
+  const int32_t* path = res + 3 + max_depth;
+  const int P = meta.prefix_len[b];
+  const long long head = (long long)l * layer_kv + ((long long)b * Hkv + hk) * kv_cap * dh;
+  uint16_t* K = kc + head;
+  uint16_t* V = vc + head;
+  const int n = L * dh;
+  for (int e = threadIdx.x; e < n; e += blockDim.x) {
+    const int k = e / dh, j = e % dh;
+    const int src = P + path[k];
+    ks[e] = K[(long long)src * dh + j];
+    vs[e] = V[(long long)(src >> 5) * dh * 32 + j * 32 + (src & 31)];
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < n; e += blockDim.x) {
+    const int k = e / dh, j = e % dh;
+    const int dst = P + 1 + k;
+    K[(long long)dst * dh + j] = ks[e];
+    V[(long long)(dst >> 5) * dh * 32 + j * 32 + (dst & 31)] = vs[e];
+  }
+}
+
+hipError_t launch_commit(const int32_t* result, int max_depth, StepMeta meta, int batch, int n_layers, int Hkv,
+                         int dh, int kv_cap, long long layer_kv, uint16_t* k_cache, uint16_t* v_cache,
+                         hipStream_t s) {
+  if (max_depth > COMMIT_MAX_DEPTH || dh > 128) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(commit_kernel, dim3(Hkv, batch, n_layers), dim3(256), 0, s, result, max_depth, meta, Hkv, dh,
+                     kv_cap, layer_kv, k_cache, v_cache);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------ MoE router ----
 // For a valid row: h = RMSNorm(x) (fp32, from the fp32 residual), router
 // logits h . w_e in fp32, softmax, keep the top_k experts (ties to the lower

@@ -139,6 +139,9 @@ hipError_t launch_attn_combine(const float* part_o, const float* part_ml, StepMe
                                hipStream_t s);
 hipError_t launch_argmax_reduce(const float* pmax, const int32_t* pidx, const int32_t* pnan, int n_tiles,
                                 int ld_part, int rows, int32_t* pred, int32_t* nan_row, hipStream_t s);
+hipError_t launch_commit(const int32_t* result, int max_depth, StepMeta meta, int batch, int n_layers, int Hkv,
+                         int dh, int kv_cap, long long layer_kv, uint16_t* k_cache, uint16_t* v_cache,
+                         hipStream_t s);
 hipError_t launch_accept(StepMeta meta, const int32_t* pred, const int32_t* nan_row, int batch,
                          int max_tree, int max_depth, int32_t* result, hipStream_t s);
 hipError_t launch_moe_route(const float* x, const uint16_t* gain, float eps, const uint16_t* w_router,

@@ -782,6 +782,16 @@ int griffin_verify_step(griffin_ctx* c, int32_t batch, const int32_t* prefix_len
   return GRIFFIN_OK;
 }
 
+int griffin_commit(griffin_ctx* c) {
+  if (!c) return GRIFFIN_EINVAL;
+  if (!c->stepped) return set_err(c, GRIFFIN_EORDER, "no verification step has been enqueued");
+  const griffin_model_desc& d = c->d;
+  const long long layer_kv = (long long)d.max_batch * d.n_kv_heads * d.kv_capacity * d.head_dim;
+  HIP_TRY(c, launch_commit(c->result, d.max_depth, c->meta, c->batch, d.n_layers, d.n_kv_heads, d.head_dim,
+                           d.kv_capacity, layer_kv, c->k_cache, c->v_cache, c->stream));
+  return GRIFFIN_OK;
+}
+
 int griffin_set_graphs(griffin_ctx* c, int32_t enable) {
   if (!c) return GRIFFIN_EINVAL;
   c->use_graphs = enable != 0;

@@ -233,4 +233,11 @@ def _set_graphs(self, enable: bool = True):
 
 TreeVerifier.profile_enable = _profile_enable
 TreeVerifier.profile_read = _profile_read
+def _commit(self):
+    """Move the last step's accepted path into the KV cache (slots
+    prefix_len + 1 .. prefix_len + L); continue with prefix_len + L + 1."""
+    _check(N.lib.griffin_commit(self.ctx), "griffin_commit", self.ctx)
+
+
 TreeVerifier.set_graphs = _set_graphs
+TreeVerifier.commit = _commit

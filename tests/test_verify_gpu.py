@@ -322,3 +322,53 @@ def test_graph_replay_matches_plain_launches():
             s.v.set_graphs(True)
     finally:
         s.v.close()
+
+
+@pytest.mark.parametrize("name", ["tiny", "small-gqa"])
+def test_speculative_loop_is_lossless(name):
+    """The paper's decoding is lossless (Sec. 5): cycles of step / accept /
+    commit on random draft trees, part of each tree planted with the target's
+    true continuation, emit exactly the oracle's greedy tokens; every
+    sequence of a batch runs its own loop at its own prefix length."""
+    N = 40
+    s = Setup(name, n_trees=1, kv_extra=N + 8)
+    try:
+        m = s.w.model
+        B = s.w.batch
+        rng = np.random.default_rng(5)
+        greedy, roots = [], []
+        for b in range(B):
+            root = int(s.cases[0][b].tree.tokens[0])
+            g, margins, _ = oracle.greedy_chain(s.ow, s.kvs[b].decode_cache(m), root, N + 8)
+            assert min(margins) > 1e-3, "pick another seed: a near tie in the greedy chain"
+            greedy.append([int(t) for t in g])
+            roots.append(root)
+        P = [s.w.prefix_len] * B
+        out = [[] for _ in range(B)]
+        cycle, accepted = 0, 0
+        while min(len(o) for o in out) < N:
+            trees = []
+            for b in range(B):
+                tree, _ = gen.random_tree(s.w.widths, m.vocab, 9000 + 97 * cycle + b)
+                tree.tokens[0] = roots[b]
+                depth = tree.depths()
+                deepest = [i for i in range(1, tree.n) if depth[i] == depth.max()]
+                path = tree.root_path(deepest[int(rng.integers(len(deepest)))])
+                l = int(rng.integers(0, len(path) + 1))
+                trees.append(gen.apply_plant(tree, path[:l], greedy[b][len(out[b]): len(out[b]) + l]))
+            say(f"{name}: cycle {cycle} prefix {P}")
+            s.v.step(P, trees)
+            acc = s.v.accept()
+            s.v.commit()
+            for b in range(B):
+                L, toks, _ = acc.sequence(b)
+                out[b] += toks
+                P[b] += L + 1
+                roots[b] = toks[-1]
+                accepted += L
+            cycle += 1
+        for b in range(B):
+            assert out[b][:N] == greedy[b][:N], f"sequence {b} diverged from greedy decoding"
+        assert accepted > cycle  # the planted parts were accepted (more than one token per cycle on average)
+    finally:
+        s.v.close()
