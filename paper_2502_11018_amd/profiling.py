@@ -14,13 +14,13 @@
     python -m paper_2502_11018_amd.profiling traffic \\
             --kernel-regex REGEX --fetch BENCH_fetch.csv --write BENCH_write.csv \\
             --copy-fetch COPY_fetch.csv --copy-write COPY_write.csv --copy-bytes N \\
-            --label gate_up_gemm --workload llama3-8b --source FILE \\
+            --label gate_up_gemm --workload llama3-8b --source FILE [FILE ...] \\
             --out profiles/NAME.md --command "CMD ..."
         HBM traffic per dispatch of the kernels whose name matches REGEX, from
         two `rocprofv3 --pmc` passes (FETCH_SIZE, then WRITE_SIZE, KiB per
         dispatch), scaled by the same counters read on the copy kernel.  The
         summary ends with one machine-readable `traffic-record:` line that
-        bench.py reads; it carries the sha256 of the kernel's source file so
+        bench.py reads; it carries the sha256 of the kernel's source files so
         that a later change of the kernel voids the record.
 """
 
@@ -37,9 +37,15 @@ import sys
 PKG = os.path.dirname(os.path.abspath(__file__))
 
 
-def source_sha256(path: str) -> str:
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+def source_sha256(paths) -> str:
+    """sha256 over the concatenated contents of one or more source files."""
+    if isinstance(paths, str):
+        paths = [paths]
+    h = hashlib.sha256()
+    for p in paths:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def _rows(path):
@@ -144,7 +150,7 @@ def cmd_traffic(args):
     fetch = fk * 1024.0 * sf
     write = wk * 1024.0 * sw
     sha = source_sha256(args.source)
-    rel = os.path.relpath(args.source, os.path.dirname(PKG))
+    rel = ",".join(os.path.relpath(x, os.path.dirname(PKG)) for x in args.source)
     out = [f"# HBM traffic per dispatch: {args.label} ({args.workload})", "",
            "Commands (each a separate rocprofv3 pass):", "", "```", args.command, "```", "",
            f"* kernels matching `{args.kernel_regex}`: {nf} dispatches with FETCH_SIZE, {nw} with WRITE_SIZE",
@@ -153,7 +159,7 @@ def cmd_traffic(args):
            f"WRITE_SIZE {cw:.1f} KiB -> scale {sf:.4f} (fetch), {sw:.4f} (write)",
            f"* scaled: fetch {fetch / 1e6:.2f} MB, write {write / 1e6:.2f} MB, total {(fetch + write) / 1e6:.2f} MB "
            f"per dispatch",
-           f"* kernel source `{rel}` sha256 {sha}", "",
+           f"* kernel sources `{rel}` sha256 {sha}", "",
            f"traffic-record: label={args.label} workload={args.workload} fetch_bytes={fetch:.0f} "
            f"write_bytes={write:.0f} source={rel} sha256={sha}"]
     with open(args.out, "w") as f:
@@ -176,8 +182,8 @@ def read_traffic_record(profiles_dir: str, label: str, workload: str, repo_root:
                 kv = dict(t.split("=", 1) for t in line.split()[1:])
                 if kv.get("label") != label or kv.get("workload") != workload:
                     continue
-                src = os.path.join(repo_root, kv["source"])
-                if not os.path.exists(src) or source_sha256(src) != kv["sha256"]:
+                srcs = [os.path.join(repo_root, x) for x in kv["source"].split(",")]
+                if not all(os.path.exists(x) for x in srcs) or source_sha256(srcs) != kv["sha256"]:
                     return None
                 return float(kv["fetch_bytes"]) + float(kv["write_bytes"])
     return None
@@ -208,7 +214,7 @@ def main(argv=None):
     t.add_argument("--copy-bytes", type=int, required=True)
     t.add_argument("--label", required=True)
     t.add_argument("--workload", required=True)
-    t.add_argument("--source", required=True)
+    t.add_argument("--source", required=True, nargs="+", help="kernel source files (hashed together)")
     t.add_argument("--out", required=True)
     t.add_argument("--command", required=True)
     args = ap.parse_args(argv)
