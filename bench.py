@@ -66,7 +66,7 @@ def class_mfma_flops_per_launch(w):
     m = w.model
     rows = -(-w.batch * 64 // 64) * 64
     d, f, e = m.d_model, m.d_ff, m.n_experts
-    keys = -(-(w.prefix_len + w.tree_nodes) // 32) * 32
+    keys = -(-w.prefix_len // 32) * 32   # prefix keys; tree keys are scored on the vector ALU in the merge
     return {
         "qkv_gemm": 2 * 2 * rows * m.qkv_rows * d,
         "o_gemm": 2 * 2 * rows * d * m.n_q_heads * m.head_dim,

@@ -207,14 +207,15 @@ int griffin_accept_walk(void *hip_stream, int32_t batch, int32_t max_tree, int32
 /* Kernel classes of one verification pass, for griffin_profile_*. */
 #define GRIFFIN_KC_QKV 0     /* QKV projection GEMM */
 #define GRIFFIN_KC_ROPE 1    /* rotary embedding + tree K/V write */
-#define GRIFFIN_KC_ATTN 2    /* tree-masked attention and split merge */
+#define GRIFFIN_KC_ATTN 2    /* prefix attention: split-KV partials */
 #define GRIFFIN_KC_O 3       /* output projection GEMM */
 #define GRIFFIN_KC_NORM 4    /* residual update + RMSNorm (and embedding) */
 #define GRIFFIN_KC_GATE_UP 5 /* gate/up GEMM with SwiGLU (MoE: routed experts) */
 #define GRIFFIN_KC_DOWN 6    /* down GEMM (MoE: routed experts) */
 #define GRIFFIN_KC_LM_HEAD 7 /* LM head GEMM with per-tile argmax */
 #define GRIFFIN_KC_OTHER 8   /* argmax reduction, acceptance walk, MoE routing */
-#define GRIFFIN_KC_COUNT 9
+#define GRIFFIN_KC_MERGE 9   /* split merge + ancestor (tree-key) attention */
+#define GRIFFIN_KC_COUNT 10
 
 /* Per-class timing with HIP events recorded on the context's stream around
  * every launch of the classes in `class_mask` (bit k = class k); 0 disables.

@@ -85,4 +85,4 @@ EXPORTED = ("griffin_kv_cache_bytes", "griffin_verify_init", "griffin_verify_ste
             "griffin_tree_prepare", "griffin_accept_walk", "griffin_profile_enable", "griffin_profile_read",
             "griffin_set_graphs", "griffin_commit")
 KERNEL_CLASSES = ("qkv_gemm", "rope_kv_write", "tree_attention", "o_gemm", "residual_rmsnorm", "gate_up_gemm",
-                  "down_gemm", "lm_head_gemm", "argmax_accept_route")
+                  "down_gemm", "lm_head_gemm", "argmax_accept_route", "attn_merge")

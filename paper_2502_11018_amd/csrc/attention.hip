@@ -2,13 +2,16 @@
 //
 // A tree node r of sequence b sees the cached prefix slots [0, P_b) and the
 // tree slots P_b + j for every node j on its root path (bit j of anc[r]).
-// A workgroup handles one (sequence, KV head, block of 32 tree rows, key
-// split, chunk of NW query heads of that KV head's group): its NW waves share
-// every 32-key block of K and V, which the workgroup stages once into an LDS
-// ring with global_load_lds_dwordx4 (each wave issues an equal share of the
-// block's 1 KB pieces), so the cache is read once per head group rather than
-// once per head.  Splits are merged by attn_combine with the usual
-// (max, sum, weighted output) rescaling in a fixed order.
+// The prefix part is the bulk of the work and is computed here; the few tree
+// keys of each node (its ancestors) are added by attn_combine in fp32, from
+// fp32 copies of the tree K/V, while it merges the prefix splits.
+//
+// tree_attention_kernel: a workgroup handles one (sequence, KV head, block of
+// 32 tree rows, prefix split, chunk of NW query heads of that KV head's
+// group).  Its NW waves share every 32-key block of K and V, which the
+// workgroup stages once into an LDS ring with global_load_lds_dwordx4 (each
+// wave issues an equal share of the block's 1 KB pieces), so the cache is read
+// once per head group rather than once per head.
 //
 // Per 32-key block each wave computes S^T = K Q^T and O^T += V^T P^T with
 // v_mfma_f32_32x32x16_bf16, so that each lane owns one query row (column of
@@ -23,9 +26,8 @@
 //    side reads each operand with one conflict-free ds_read_b128.
 //  * Q and K use the same head-dim permutation as the projection GEMMs: a lane
 //    reads 32 consecutive head dims and feeds 8 of them to each of 4 MFMAs.
-//  * Q and P enter the matrix cores as split bf16 (hi + lo, two MFMAs each);
-//    the tree's own K/V add their bf16 residuals (one more MFMA each, against
-//    the hi part of q or p), so only the prefix K/V carry bf16 rounding.
+//  * Q and P enter the matrix cores as split bf16 (hi + lo, two MFMAs each),
+//    so only the cached K/V carry bf16 rounding.
 // Scores are kept in the log2 domain (scaled by log2(e)/sqrt(dh)) and exp2 is
 // used throughout; masked keys contribute exactly zero.
 
@@ -46,8 +48,6 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
   constexpr int D = ATTN_RING;         // ring slots
   static_assert(PIECES % NW == 0 && PPW * (D - 2) < 64, "ring shape");
   __shared__ u32x4 ring[D][PIECES][64];
-  constexpr int LOT = 3;                // residual tiles of the tree region (max_tree <= 64)
-  __shared__ u32x4 lo_lds[LOT][PIECES][64];
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int col = lane & 31, hh = lane >> 5;
@@ -73,13 +73,12 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
   const int hq = hk * G + (head_live ? gh : 0);
   const int n_nodes = a.meta.n_nodes[b];
   const int P = a.meta.prefix_len[b];
-  const int Lb = P + n_nodes;
   const int qrows = a.qblocks * 32;
 
   if (qb * 32 >= n_nodes) return;  // no live query rows in this block (uniform)
 
-  // key range of this split, in whole 32-key blocks
-  const int nblk = (Lb + 31) >> 5;
+  // prefix key range of this split, in whole 32-key blocks
+  const int nblk = (P + 31) >> 5;
   const int kb0 = (int)((long long)nblk * split / a.splits);
   const int kb1 = (int)((long long)nblk * (split + 1) / a.splits);
   const int nb = kb1 - kb0;
@@ -88,7 +87,6 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
   const int qi = qb * 32 + col;
   const bool qlive = qi < n_nodes;
   const int qr = b * a.max_tree + (qlive ? qi : 0);
-  const uint64_t anc = qlive ? a.meta.anc[qr] : 0ull;
 
   // Q^T operand (B): lane (col = query row, hh = k-group), 32 dims per chunk;
   // split bf16, so S = K (q_hi + q_lo)
@@ -105,7 +103,6 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
   }
 
   const long long head = ((long long)b * a.Hkv + hk) * a.kv_cap * DH;
-  const long long lo_head = ((long long)b * a.Hkv + hk) * a.tree_lo.tiles * 32 * DH;
   const uint16_t* kbase = a.k_cache + head;
   const uint16_t* vbase = a.v_cache + head;
   // MFMA row -> key offset inside a 32-key block: row 8q + 4h + e holds key 16h + 4q + e
@@ -142,42 +139,14 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
   // Online softmax with a lazily moved reference max: p = 2^(s - m_ref) may
   // reach 2^8 before the reference is raised, so the accumulator rescale only
   // runs when some lane's block maximum exceeds its reference by more than 8
-  // (a wave-uniform branch with no loads inside).  MASKED is false for blocks
-  // wholly inside the cached prefix (every key visible); the block holding
-  // the tree slots and the end of the sequence takes the masked variant, whose
-  // masks are branch-free selects.
-  auto compute = [&](auto masked, int slot, int kb) {
-    constexpr bool MASKED = decltype(masked)::value;
+  // (a wave-uniform branch with no loads inside).  TAIL is true only for the
+  // last prefix block when P is not a multiple of 32: its keys at or beyond P
+  // get probability 0 and their V is zeroed (those slots hold tree or stale
+  // values), with branch-free selects.
+  auto compute = [&](auto tail, int slot, int kb) {
+    constexpr bool TAIL = decltype(tail)::value;
     const int key0 = kb * 32;
     // ---- S^T = K Q^T (rows: keys, cols: queries), q = q_hi + q_lo
-    // Tree blocks also carry the bf16 residuals of the tree K/V (staged in LDS
-    // at the start; zero outside the tree slots).
-    u32x4 klo[CH][4], vlo[DB][2];
-    if constexpr (MASKED) {
-      const int tile = kb - (P >> 5);
-      const int kkey = key0 + krow;
-      const bool kin = kkey >= P && kkey < Lb;
-#pragma unroll
-      for (int c = 0; c < CH; ++c)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          klo[c][j] = lo_lds[tile][c * 4 + j][lane];
-          if (!kin) klo[c][j] = zero_u4();
-        }
-#pragma unroll
-      for (int d = 0; d < DB; ++d)
-#pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          vlo[d][t] = lo_lds[tile][KP + d * 2 + t][lane];
-          const int kfirst = key0 + 16 * hh + 8 * t;
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {  // bf16 element 2q is the low half of dword q
-            const int k0 = kfirst + 2 * q, k1 = k0 + 1;
-            const uint32_t keep = (k0 >= P && k0 < Lb ? 0x0000ffffu : 0u) | (k1 >= P && k1 < Lb ? 0xffff0000u : 0u);
-            vlo[d][t][q] &= keep;
-          }
-        }
-    }
     f32x16 sacc;
 #pragma unroll
     for (int r = 0; r < 16; ++r) sacc[r] = 0.f;
@@ -190,26 +159,14 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
         for (int h = 0; h < 2; ++h)
           sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf), as_bf16x8(qf[h][c][j]), sacc, 0, 0, 0);
       }
-    if constexpr (MASKED) {
-#pragma unroll
-      for (int c = 0; c < CH; ++c)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(klo[c][j]), as_bf16x8(qf[0][c][j]), sacc, 0, 0, 0);
-    }
 
-    // ---- mask (this lane: query qi, keys key0 + 16 hh + r); the log2-domain
-    // scale is applied inside the exponent (scale > 0 commutes with max)
+    // ---- mask (this lane: keys key0 + 16 hh + r); the log2-domain scale is
+    // applied inside the exponent (scale > 0 commutes with max)
     float s[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       s[r] = sacc[r];
-      if constexpr (MASKED) {
-        const int key = key0 + 16 * hh + r;
-        const int j = key - P;
-        const bool tree_vis = ((unsigned)j < (unsigned)n_nodes) & (((anc >> (j & 63)) & 1ull) != 0ull);
-        s[r] = ((key < P) | tree_vis) ? s[r] : -INFINITY;
-      }
+      if constexpr (TAIL) s[r] = (key0 + 16 * hh + r < P) ? s[r] : -INFINITY;
     }
     float mx = fmaxf(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])), fmaxf(fmaxf(s[4], s[5]), fmaxf(s[6], s[7])));
     mx = fmaxf(mx, fmaxf(fmaxf(fmaxf(s[8], s[9]), fmaxf(s[10], s[11])),
@@ -243,27 +200,23 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
         pf[0][q] = hl.hi;
         pf[1][q] = hl.lo;
       }
-      // keys at or beyond the end of the sequence may hold stale or never
-      // written cache bytes; zero their V so that 0 * garbage cannot appear
       uint32_t keep[4];
-      if constexpr (MASKED) {
+      if constexpr (TAIL) {
         const int kfirst = key0 + 16 * hh + 8 * t;
 #pragma unroll
         for (int q = 0; q < 4; ++q)  // bf16 element 2q is the low half of dword q
-          keep[q] = (kfirst + 2 * q < Lb ? 0x0000ffffu : 0u) | (kfirst + 2 * q + 1 < Lb ? 0xffff0000u : 0u);
+          keep[q] = (kfirst + 2 * q < P ? 0x0000ffffu : 0u) | (kfirst + 2 * q + 1 < P ? 0xffff0000u : 0u);
       }
 #pragma unroll
       for (int d = 0; d < DB; ++d) {
         u32x4 vf = ring[slot][KP + d * 2 + t][lane];
-        if constexpr (MASKED) {
+        if constexpr (TAIL) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) vf[q] &= keep[q];
         }
 #pragma unroll
         for (int h = 0; h < 2; ++h)
           oacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vf), as_bf16x8(pf[h]), oacc[d], 0, 0, 0);
-        if constexpr (MASKED)
-          oacc[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(vlo[d][t]), as_bf16x8(pf[0]), oacc[d], 0, 0, 0);
       }
     }
   };
@@ -276,19 +229,6 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
   // re-read it into slots that are never consumed; every DMA has landed
   // before the waves leave.
   if (nb > 0) {
-    if (kb1 * 32 > P) {
-      // this split reaches the tree slots: stage the residual tiles of the
-      // tree region ahead of the ring (older loads, so the ring's first wait
-      // and barrier also cover them)
-      for (int tl = 0; tl < a.tree_lo.tiles; ++tl) {
-#pragma unroll
-        for (int p = 0; p < PPW; ++p) {
-          const int pc = w * PPW + p;
-          const uint16_t* src = (pc < KP ? a.tree_lo.k : a.tree_lo.v) + lo_head + (long long)tl * 32 * DH + goff[p];
-          __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)&lo_lds[tl][pc][0], 16, 0, 0);
-        }
-      }
-    }
 #pragma unroll
     for (int i = 0; i < D - 1; ++i) issue(i, kb0 + min(i, nb - 1));
     for (int i = 0; i < nb; ++i) {
@@ -298,7 +238,7 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
       // waves past the end of the head group compute a duplicate of the
       // group's first head and write nothing
       if ((kb0 + i + 1) * 32 <= P) compute(std::false_type{}, i % D, kb0 + i);
-      else compute(std::true_type{}, i % D, kb0 + i);
+      else compute(std::true_type{}, i % D, kb0 + i);  // the partial last prefix block
     }
     wait_vmcnt_lds<0>();
   }
@@ -335,7 +275,7 @@ static void launch_attn_dh(const AttnArgs& a, int nw, dim3 grid, hipStream_t s) 
 }
 
 hipError_t launch_attention(const AttnArgs& a, int batch, hipStream_t s) {
-  if (a.batch != batch || a.tree_lo.tiles > 3) return hipErrorInvalidValue;
+  if (a.batch != batch) return hipErrorInvalidValue;
   const int G = a.Hq / a.Hkv;
   const int nw = attn_waves(G);
   const int streams = batch * a.Hkv;
@@ -347,24 +287,31 @@ hipError_t launch_attention(const AttnArgs& a, int batch, hipStream_t s) {
   return hipGetLastError();
 }
 
-// Merge the splits of every (row, head): o = sum_s 2^(m_s - M) o_s / sum_s 2^(m_s - M) l_s.
-// Absent rows get zeros.  One workgroup per row, one thread per (head, dim).
-// The merged rows are written fragment-packed split bf16 (o_ks K steps per tile) as the
-// activation operand of the output projection.  One thread per (head, 4 dims).
+// Finish attention for every (row, head): merge the prefix splits and add the
+// node's tree keys.  Prefix split s contributes (m_s, l_s, o_s) in the log2
+// domain; the tree keys are the node's ancestors and itself (bits of anc),
+// scored in fp32 from q = q_hi + q_lo and the fp32 tree K/V, with a running
+// (m_t, l_t, o_t).  Then o = (sum_s 2^(m_s - M) o_s + 2^(m_t - M) o_t) /
+// (sum_s 2^(m_s - M) l_s + 2^(m_t - M) l_t).  Absent rows get zeros.  One
+// workgroup per row, one thread per (head, 4 dims); the dot products of a
+// tree key reduce over the head's dh/4 threads with xor shuffles (a fixed
+// order).  The merged rows are written fragment-packed split bf16 (o_ks K
+// steps per tile) as the activation operand of the output projection.
 template <int MAXS>
 __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ part_o,
                                                            const float* __restrict__ part_ml, StepMeta meta,
-                                                           int Hq, int dh, int splits_unused, int qrows,
-                                                           int max_tree, uint16_t* __restrict__ o_out, int o_ks) {
-  (void)splits_unused;
+                                                           int Hq, int Hkv, int dh, int qrows, int max_tree,
+                                                           const uint16_t* __restrict__ q,
+                                                           const uint16_t* __restrict__ q_lo, TreeKV32 tree,
+                                                           float scale_log2, uint16_t* __restrict__ o_out, int o_ks) {
   const int r = blockIdx.x;
   const int b = r / max_tree, i = r % max_tree;
   const int quads = dh / 4;
   const int t = blockIdx.y * blockDim.x + threadIdx.x;
-  if (t >= Hq * quads) return;
+  if (t >= Hq * quads) return;  // whole heads at a time (quads divides the block size)
   const int h = t / quads, d = (t % quads) * 4;
   float4 out = make_float4(0.f, 0.f, 0.f, 0.f);
-  if (i < meta.n_nodes[b]) {
+  if (i < meta.n_nodes[b]) {  // uniform over the workgroup
     const long long base = ((long long)b * Hq + h) * MAXS;
     float ms[MAXS], ls[MAXS];
     float4 os[MAXS];
@@ -375,22 +322,64 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
       ls[s] = part_ml[row * 2 + 1];
       os[s] = *reinterpret_cast<const float4*>(part_o + row * dh + d);
     }
-    float M = -INFINITY;
+    // tree keys
+    const int hk = h / (Hq / Hkv);
+    const long long qo = ((long long)r * Hq + h) * dh + d;
+    const uint2 qh = *reinterpret_cast<const uint2*>(q + qo), ql = *reinterpret_cast<const uint2*>(q_lo + qo);
+    const float q0 = bf16_to_f32(qh.x & 0xffff) + bf16_to_f32(ql.x & 0xffff);
+    const float q1 = bf16_to_f32(qh.x >> 16) + bf16_to_f32(ql.x >> 16);
+    const float q2 = bf16_to_f32(qh.y & 0xffff) + bf16_to_f32(ql.y & 0xffff);
+    const float q3 = bf16_to_f32(qh.y >> 16) + bf16_to_f32(ql.y >> 16);
+    const float* tk = tree.k + ((long long)b * Hkv + hk) * max_tree * dh + d;
+    const float* tv = tree.v + ((long long)b * Hkv + hk) * max_tree * dh + d;
+    uint64_t anc = meta.anc[r];
+    float mt = -INFINITY, lt = 0.f;
+    float4 ot = make_float4(0.f, 0.f, 0.f, 0.f);
+    constexpr int TB = 8;  // ancestors per batch: all their loads are issued before any is used
+    while (anc) {          // uniform over the workgroup (one row)
+      int js[TB];
+      bool ok[TB];
+#pragma unroll
+      for (int u = 0; u < TB; ++u) {
+        ok[u] = anc != 0;
+        js[u] = ok[u] ? __builtin_ctzll(anc) : 0;
+        anc &= anc - 1;
+      }
+      float4 k4[TB], v4[TB];
+#pragma unroll
+      for (int u = 0; u < TB; ++u) {
+        k4[u] = *reinterpret_cast<const float4*>(tk + (long long)js[u] * dh);
+        v4[u] = *reinterpret_cast<const float4*>(tv + (long long)js[u] * dh);
+      }
+#pragma unroll
+      for (int u = 0; u < TB; ++u) {
+        if (!ok[u]) break;
+        float dot = q0 * k4[u].x + q1 * k4[u].y + q2 * k4[u].z + q3 * k4[u].w;
+        for (int o = quads >> 1; o > 0; o >>= 1) dot += __shfl_xor(dot, o, 64);
+        const float sj = dot * scale_log2;
+        const float mn = fmaxf(mt, sj);
+        const float al = exp2f(mt - mn), e = exp2f(sj - mn);
+        lt = lt * al + e;
+        ot = make_float4(ot.x * al + e * v4[u].x, ot.y * al + e * v4[u].y, ot.z * al + e * v4[u].z,
+                         ot.w * al + e * v4[u].w);
+        mt = mn;
+      }
+    }
+    float M = mt;
 #pragma unroll
     for (int s = 0; s < MAXS; ++s) M = fmaxf(M, ms[s]);
-    if (M != -INFINITY) {
-      float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
-      float den = 0.f;
+    const float wt = exp2f(mt - M);
+    float4 num = make_float4(wt * ot.x, wt * ot.y, wt * ot.z, wt * ot.w);
+    float den = wt * lt;
 #pragma unroll
-      for (int s = 0; s < MAXS; ++s)
-        if (ms[s] != -INFINITY) {
-          const float w = exp2f(ms[s] - M);
-          num.x += w * os[s].x; num.y += w * os[s].y; num.z += w * os[s].z; num.w += w * os[s].w;
-          den += w * ls[s];
-        }
-      const float inv = 1.f / den;
-      out = make_float4(num.x * inv, num.y * inv, num.z * inv, num.w * inv);
-    }
+    for (int s = 0; s < MAXS; ++s)
+      if (ms[s] != -INFINITY) {
+        const float w = exp2f(ms[s] - M);
+        num.x += w * os[s].x; num.y += w * os[s].y; num.z += w * os[s].z; num.w += w * os[s].w;
+        den += w * ls[s];
+      }
+    const float inv = 1.f / den;
+    out = make_float4(num.x * inv, num.y * inv, num.z * inv, num.w * inv);
   }
   uint16_t* dst = o_out + xpack_off(r, h * dh + d, o_ks);
   const Hilo2 p0 = pack_hilo2(out.x, out.y), p1 = pack_hilo2(out.z, out.w);
@@ -398,15 +387,19 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
   *reinterpret_cast<uint2*>(dst + XPACK_LO) = make_uint2(p0.lo, p1.lo);
 }
 
-hipError_t launch_attn_combine(const float* part_o, const float* part_ml, StepMeta meta, int Hq, int dh, int splits,
-                               int qrows, int max_tree, int batch, uint16_t* o_out, int o_ks, hipStream_t s) {
-  const int items = Hq * dh / 4;
+hipError_t launch_attn_combine(const float* part_o, const float* part_ml, StepMeta meta, int Hq, int Hkv, int dh,
+                               int splits, int qrows, int max_tree, int batch, const uint16_t* q,
+                               const uint16_t* q_lo, TreeKV32 tree, float scale_log2, uint16_t* o_out, int o_ks,
+                               hipStream_t s) {
+  const int quads = dh / 4;
+  if (256 % quads != 0) return hipErrorInvalidValue;
+  const int items = Hq * quads;
   const dim3 grid(batch * max_tree, (items + 255) / 256);
   switch (splits) {
 #define GRIFFIN_COMB_CASE(n)                                                                                   \
   case n:                                                                                                     \
-    hipLaunchKernelGGL(attn_combine_kernel<n>, grid, dim3(256), 0, s, part_o, part_ml, meta, Hq, dh, splits, qrows, \
-                       max_tree, o_out, o_ks);                                                                \
+    hipLaunchKernelGGL(attn_combine_kernel<n>, grid, dim3(256), 0, s, part_o, part_ml, meta, Hq, Hkv, dh, qrows,  \
+                       max_tree, q, q_lo, tree, scale_log2, o_out, o_ks);                                     \
     break;
     GRIFFIN_COMB_CASE(1) GRIFFIN_COMB_CASE(2) GRIFFIN_COMB_CASE(3) GRIFFIN_COMB_CASE(4) GRIFFIN_COMB_CASE(5)
     GRIFFIN_COMB_CASE(6) GRIFFIN_COMB_CASE(7) GRIFFIN_COMB_CASE(8) GRIFFIN_COMB_CASE(9) GRIFFIN_COMB_CASE(10)

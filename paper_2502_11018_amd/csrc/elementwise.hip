@@ -179,7 +179,7 @@ hipError_t launch_moe_gather(const uint16_t* xn, int xn_ks, const int32_t* gathe
 // QKV projection, rotate q and k (rotate-half pairing j <-> j + dh/2) at the
 // node's position, write q (bf16) for attention, and k / v into cache slot
 // prefix_len[b] + i (k row-major per slot, v transposed: one row per dim),
-// and their bf16 residuals into the tree tiles.
+// and fp32 copies of the tree K/V for the attention merge.
 // q is kept as split bf16: q_out holds bf16(q), q_lo the bf16 residual.
 template <int NP>
 __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* __restrict__ parts, int n_parts_unused,
@@ -189,7 +189,7 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* __restrict__
                                                        int dh, int max_tree, int kv_cap,
                                                        uint16_t* __restrict__ q_out, uint16_t* __restrict__ q_lo,
                                                        uint16_t* __restrict__ kc, uint16_t* __restrict__ vc,
-                                                       TreeKVLo lo) {
+                                                       TreeKV32 tree) {
   const int r = blockIdx.x;
   const int b = r / max_tree, i = r % max_tree;
   if (i >= meta.n_nodes[b]) return;
@@ -199,8 +199,6 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* __restrict__
   const int pos = meta.pos[r];
   const int P = meta.prefix_len[b];
   const int slot = P + i;
-  const int rel = slot - (P & ~31);  // slot inside the residual tiles
-  const long long lo_head = (long long)lo.tiles * 32 * dh;
   const float* __restrict__ row = parts + (long long)r * width;
   const int t = blockIdx.y * blockDim.x + threadIdx.x;  // one (head, rotation pair) per thread
   if (t < heads * half) {
@@ -232,24 +230,21 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* __restrict__
         q_lo[o + j + half] = f32_to_bf16(y2 - bf16_to_f32(h2));
       } else {
         uint16_t* k = kc + (((long long)b * Hkv + (h - Hq)) * kv_cap + slot) * dh;
-        const uint16_t h1 = f32_to_bf16(y1), h2 = f32_to_bf16(y2);
-        k[j] = h1;
-        k[j + half] = h2;
-        uint16_t* kl = lo.k + ((long long)b * Hkv + (h - Hq)) * lo_head + (long long)rel * dh;
-        kl[j] = f32_to_bf16(y1 - bf16_to_f32(h1));
-        kl[j + half] = f32_to_bf16(y2 - bf16_to_f32(h2));
+        k[j] = f32_to_bf16(y1);
+        k[j + half] = f32_to_bf16(y2);
+        float* k32 = tree.k + (((long long)b * Hkv + (h - Hq)) * max_tree + i) * dh;
+        k32[j] = y1;
+        k32[j + half] = y2;
       }
     } else {
       // 32-slot tiles, transposed within the tile: [tile][dim][32]
       uint16_t* v = vc + ((long long)b * Hkv + (h - Hq - Hkv)) * dh * kv_cap + (long long)(slot >> 5) * dh * 32 +
                     (slot & 31);
-      const uint16_t h1 = f32_to_bf16(x1), h2 = f32_to_bf16(x2);
-      v[j * 32] = h1;
-      v[(j + half) * 32] = h2;
-      uint16_t* vl = lo.v + ((long long)b * Hkv + (h - Hq - Hkv)) * lo_head + (long long)(rel >> 5) * dh * 32 +
-                     (rel & 31);
-      vl[j * 32] = f32_to_bf16(x1 - bf16_to_f32(h1));
-      vl[(j + half) * 32] = f32_to_bf16(x2 - bf16_to_f32(h2));
+      v[j * 32] = f32_to_bf16(x1);
+      v[(j + half) * 32] = f32_to_bf16(x2);
+      float* v32 = tree.v + (((long long)b * Hkv + (h - Hq - Hkv)) * max_tree + i) * dh;
+      v32[j] = x1;
+      v32[j + half] = x2;
     }
   }
 }
@@ -257,8 +252,7 @@ __global__ __launch_bounds__(256) void qkv_rope_kernel(const float* __restrict__
 hipError_t launch_qkv_rope(const float* qkv_parts, int n_parts, long long part_stride, StepMeta meta,
                            const float* rope_cos, const float* rope_sin, int Hq, int Hkv, int dh, int max_tree,
                            int batch, int kv_cap, uint16_t* q_out, uint16_t* q_lo, uint16_t* k_cache_l,
-                           uint16_t* v_cache_l, TreeKVLo tree_lo, hipStream_t s) {
-  if (tree_lo.tiles * 32 < max_tree + 31) return hipErrorInvalidValue;  // slot offsets reach 31 + max_tree - 1
+                           uint16_t* v_cache_l, TreeKV32 tree, hipStream_t s) {
   const int items = (Hq + 2 * Hkv) * (dh / 2);
   const dim3 grid(batch * max_tree, (items + 255) / 256);
   switch (n_parts) {
@@ -266,7 +260,7 @@ hipError_t launch_qkv_rope(const float* qkv_parts, int n_parts, long long part_s
   case n:                                                                                                     \
     hipLaunchKernelGGL(qkv_rope_kernel<n>, grid, dim3(256), 0, s, qkv_parts, n_parts, part_stride, meta, rope_cos, \
                        rope_sin, Hq, Hkv, dh, max_tree, kv_cap, q_out, q_lo, k_cache_l, v_cache_l, \
-                       tree_lo);                 \
+                       tree);                    \
     break;
     GRIFFIN_ROPE_CASE(1) GRIFFIN_ROPE_CASE(2) GRIFFIN_ROPE_CASE(3) GRIFFIN_ROPE_CASE(4) GRIFFIN_ROPE_CASE(5)
     GRIFFIN_ROPE_CASE(6) GRIFFIN_ROPE_CASE(7) GRIFFIN_ROPE_CASE(8) GRIFFIN_ROPE_CASE(9) GRIFFIN_ROPE_CASE(10)

@@ -95,16 +95,13 @@ struct ResidualAdd {
   int top_k;
 };
 
-// bf16 residuals x - bf16(x) of the tree nodes' K and V (the cache holds
-// bf16(x)), for the layer being computed, in 32-slot tiles counted from the
-// tile that holds slot prefix_len of each sequence (P0 = prefix_len & ~31):
-//   k: [B][Hkv][tiles][32][dh]      v: [B][Hkv][tiles][dh][32]
-// Entries outside [prefix_len, prefix_len + n_nodes) are never written and
-// are masked by the reader.
-struct TreeKVLo {
-  uint16_t* k;
-  uint16_t* v;
-  int tiles;  // ceil((max_tree + 31) / 32)
+// fp32 copies of the tree nodes' K (after rotation) and V for the layer being
+// computed, written by qkv_rope next to the bf16 cache entries and read by the
+// attention merge, which adds each node's own ancestors in fp32:
+//   k, v: [B][Hkv][max_tree][dh]
+struct TreeKV32 {
+  float* k;
+  float* v;
 };
 
 struct AttnArgs {
@@ -112,7 +109,6 @@ struct AttnArgs {
   const uint16_t* q_lo;      // bf16 residual q - bf16(q), same layout
   const uint16_t* k_cache;   // this layer: [max_batch][Hkv][cap][dh]
   const uint16_t* v_cache;   // this layer: [max_batch][Hkv][cap / 32][dh][32]
-  TreeKVLo tree_lo;          // residuals of the tree K/V (written by qkv_rope)
   float* part_o;             // [B][Hq][S][qrows][dh]
   float* part_ml;            // [B][Hq][S][qrows][2]
   StepMeta meta;
@@ -130,12 +126,13 @@ hipError_t launch_residual_rmsnorm(float* x, const ResidualAdd& add, const uint1
 hipError_t launch_qkv_rope(const float* qkv_parts, int n_parts, long long part_stride, StepMeta meta,
                            const float* rope_cos, const float* rope_sin, int Hq, int Hkv, int dh,
                            int max_tree, int batch, int kv_cap, uint16_t* q_out, uint16_t* q_lo,
-                           uint16_t* k_cache_l, uint16_t* v_cache_l, TreeKVLo tree_lo, hipStream_t s);
+                           uint16_t* k_cache_l, uint16_t* v_cache_l, TreeKV32 tree, hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, int batch, hipStream_t s);
 constexpr int ATTN_RING = 4;  // 32-key K/V blocks in flight per attention workgroup
 int attn_waves(int group);    // waves (query heads) per attention workgroup
-hipError_t launch_attn_combine(const float* part_o, const float* part_ml, StepMeta meta, int Hq, int dh,
-                               int splits, int qrows, int max_tree, int batch, uint16_t* o_out, int o_ks,
+hipError_t launch_attn_combine(const float* part_o, const float* part_ml, StepMeta meta, int Hq, int Hkv, int dh,
+                               int splits, int qrows, int max_tree, int batch, const uint16_t* q,
+                               const uint16_t* q_lo, TreeKV32 tree, float scale_log2, uint16_t* o_out, int o_ks,
                                hipStream_t s);
 hipError_t launch_argmax_reduce(const float* pmax, const int32_t* pidx, const int32_t* pnan, int n_tiles,
                                 int ld_part, int rows, int32_t* pred, int32_t* nan_row, hipStream_t s);

@@ -168,7 +168,7 @@ struct griffin_ctx {
   float *x = nullptr, *parts = nullptr, *attn_po = nullptr, *attn_pml = nullptr;
   float *rope_cos = nullptr, *rope_sin = nullptr, *pmax = nullptr, *route_w = nullptr, *yslots = nullptr;
   uint16_t *xn = nullptr, *q = nullptr, *q_lo = nullptr, *o = nullptr, *act = nullptr, *xe = nullptr;
-  TreeKVLo tree_lo{};  // tree K/V residual tiles, reused by every layer
+  TreeKV32 tree{};  // fp32 tree K/V of the layer being computed (reused by every layer)
   int32_t *pidx = nullptr, *pnan = nullptr, *pred = nullptr, *nan_row = nullptr, *result = nullptr;
   int32_t *route_ids = nullptr, *gather = nullptr, *count = nullptr, *slot = nullptr;
 
@@ -294,6 +294,7 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
   const long long ps = (long long)Mpad;  // rows per split slice of `parts`
   hipStream_t s = c->stream;
   const size_t layer_kv = (size_t)d.max_batch * d.n_kv_heads * d.kv_capacity * d.head_dim;
+  const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.head_dim));  // log2(e) / sqrt(dh)
 
   LAUNCH(GRIFFIN_KC_NORM, launch_embed(c->embed, c->meta.token, Mpad, d.d_model, c->x, s));
   ResidualAdd none{};
@@ -313,14 +314,13 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
     uint16_t* vc = c->v_cache + (size_t)l * layer_kv;
     LAUNCH(GRIFFIN_KC_ROPE, launch_qkv_rope(c->parts, c->p_qkv.out_splits(), ps * c->qkv_n, c->meta, c->rope_cos,
                                             c->rope_sin, d.n_q_heads, d.n_kv_heads, d.head_dim, d.max_tree, B,
-                                            d.kv_capacity, c->q, c->q_lo, kc, vc, c->tree_lo, s));
+                                            d.kv_capacity, c->q, c->q_lo, kc, vc, c->tree, s));
     {
       AttnArgs a{};
       a.q = c->q;
       a.q_lo = c->q_lo;
       a.k_cache = kc;
       a.v_cache = vc;
-      a.tree_lo = c->tree_lo;
       a.part_o = c->attn_po;
       a.part_ml = c->attn_pml;
       a.meta = c->meta;
@@ -332,12 +332,12 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
       a.qblocks = c->qblocks;
       a.splits = c->attn_splits;
       a.batch = B;
-      a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.head_dim));
+      a.scale_log2 = scale_log2;
       LAUNCH(GRIFFIN_KC_ATTN, launch_attention(a, B, s));
     }
-    LAUNCH(GRIFFIN_KC_ATTN, launch_attn_combine(c->attn_po, c->attn_pml, c->meta, d.n_q_heads, d.head_dim,
-                                                c->attn_splits, c->qblocks * 32, d.max_tree, B, c->o,
-                                                c->p_o.ks_pad, s));
+    LAUNCH(GRIFFIN_KC_MERGE, launch_attn_combine(c->attn_po, c->attn_pml, c->meta, d.n_q_heads, d.n_kv_heads,
+                                                d.head_dim, c->attn_splits, c->qblocks * 32, d.max_tree, B, c->q,
+                                                c->q_lo, c->tree, scale_log2, c->o, c->p_o.ks_pad, s));
     {
       GemmArgs a = gemm_args(c->p_o, c->o, c->p_o.ks_pad, c->pk_o[l], m_tiles);
       a.out = c->parts;
@@ -593,9 +593,8 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
   ALLOC(c->parts, c->parts_elems);
   ALLOC(c->q, Mp * c->attn_w);
   ALLOC(c->q_lo, Mp * c->attn_w);
-  c->tree_lo.tiles = cdiv(d.max_tree + 31, 32);  // <= 3: the attention kernel stages at most 3 tiles
-  ALLOC(c->tree_lo.k, (long long)d.max_batch * d.n_kv_heads * c->tree_lo.tiles * 32 * d.head_dim);
-  ALLOC(c->tree_lo.v, (long long)d.max_batch * d.n_kv_heads * c->tree_lo.tiles * 32 * d.head_dim);
+  ALLOC(c->tree.k, (long long)d.max_batch * d.n_kv_heads * d.max_tree * d.head_dim);
+  ALLOC(c->tree.v, (long long)d.max_batch * d.n_kv_heads * d.max_tree * d.head_dim);
   ALLOC(c->o, tiles * c->p_o.ks_pad * XPACK_STEP);
   ALLOC(c->attn_po, (long long)d.max_batch * d.n_q_heads * c->attn_splits * qrows * d.head_dim);
   ALLOC(c->attn_pml, (long long)d.max_batch * d.n_q_heads * c->attn_splits * qrows * 2);

@@ -213,14 +213,14 @@ class TreeVerifier:
         self.close()
 
 
-def _profile_enable(self, mask: int = (1 << 9) - 1):
+def _profile_enable(self, mask: int = (1 << len(N.KERNEL_CLASSES)) - 1):
     _check(N.lib.griffin_profile_enable(self.ctx, mask), "griffin_profile_enable", self.ctx)
 
 
 def _profile_read(self) -> dict:
     """Per kernel class: (summed ms, launches) since the last read."""
-    ms = (ctypes.c_double * 9)()
-    n = (ctypes.c_int64 * 9)()
+    ms = (ctypes.c_double * len(N.KERNEL_CLASSES))()
+    n = (ctypes.c_int64 * len(N.KERNEL_CLASSES))()
     _check(N.lib.griffin_profile_read(self.ctx, ms, n), "griffin_profile_read", self.ctx)
     return {name: (float(ms[k]), int(n[k])) for k, name in enumerate(N.KERNEL_CLASSES)}
 

@@ -37,6 +37,20 @@ def test_library_exports_every_declared_function():
     assert sorted(N.EXPORTED) == declared
 
 
+def test_kernel_classes_match_header():
+    """The binding's class names line up with the header's GRIFFIN_KC_* indices."""
+    N = _native()
+    text = open(HEADER).read()
+    idx = {m[0]: int(m[1]) for m in re.findall(r"#define GRIFFIN_KC_([A-Z_]+) (\d+)", text)}
+    assert idx.pop("COUNT") == len(N.KERNEL_CLASSES)
+    assert sorted(idx.values()) == list(range(len(N.KERNEL_CLASSES)))
+    expect = {"QKV": "qkv_gemm", "ROPE": "rope_kv_write", "ATTN": "tree_attention", "O": "o_gemm",
+              "NORM": "residual_rmsnorm", "GATE_UP": "gate_up_gemm", "DOWN": "down_gemm",
+              "LM_HEAD": "lm_head_gemm", "OTHER": "argmax_accept_route", "MERGE": "attn_merge"}
+    for k, i in idx.items():
+        assert N.KERNEL_CLASSES[i] == expect[k]
+
+
 def test_status_strings():
     N = _native()
     for code in N.STATUS:

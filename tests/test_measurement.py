@@ -31,7 +31,7 @@ def test_class_bytes_and_flops_per_launch():
     f = bench.class_mfma_flops_per_launch(w)
     # 64 rows, split-bf16 (2 MFMAs per product), 2 flops per multiply-add
     assert f["gate_up_gemm"] == 2 * 2 * 64 * 2 * 14336 * 4096
-    assert f["tree_attention"] == 2 * 2 * 2 * 32 * 64 * 2112 * 128
+    assert f["tree_attention"] == 2 * 2 * 2 * 32 * 64 * 2048 * 128
 
 
 def _write_csv(path, header, rows):
