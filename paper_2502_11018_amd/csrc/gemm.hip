@@ -270,13 +270,11 @@ hipError_t launch_gemm(const GemmArgs& a, int experts, hipStream_t s) {
   if (epi == (E) && nb == (B) && wn == (N_) && pf == (P) && ks == (K_)) return launch_one<E, B, N_, P, K_>(a, experts, s);
   GRIFFIN_GEMM_CASE(EPI_STORE, 1, 4, 4, 1)
   GRIFFIN_GEMM_CASE(EPI_STORE, 1, 4, 2, 1)
-  GRIFFIN_GEMM_CASE(EPI_STORE, 1, 1, 2, 1)
   GRIFFIN_GEMM_CASE(EPI_SWIGLU, 2, 2, 3, 2)
   GRIFFIN_GEMM_CASE(EPI_SWIGLU, 2, 2, 2, 2)
   GRIFFIN_GEMM_CASE(EPI_SWIGLU, 2, 2, 2, 1)
-  GRIFFIN_GEMM_CASE(EPI_ARGMAX, 1, 4, 4, 1)
-  GRIFFIN_GEMM_CASE(EPI_ARGMAX, 1, 4, 2, 1)
-  GRIFFIN_GEMM_CASE(EPI_ARGMAX, 1, 1, 2, 1)
+  GRIFFIN_GEMM_CASE(EPI_ARGMAX, 2, 4, 4, 1)
+  GRIFFIN_GEMM_CASE(EPI_ARGMAX, 2, 4, 2, 1)
 #undef GRIFFIN_GEMM_CASE
   return hipErrorInvalidValue;
 }

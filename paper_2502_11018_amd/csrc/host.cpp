@@ -19,7 +19,7 @@ using namespace griffin;
 namespace {
 
 constexpr int kMaxTree = 64;
-constexpr int kTargetWaves = 896;  // ~3.5 streaming waves per CU on 256 CUs
+constexpr int kTargetWaves = 1024;  // one streaming wave per SIMD on 256 CUs
 
 int round_up(int x, int m) { return (x + m - 1) / m * m; }
 int cdiv(int x, int m) { return (x + m - 1) / m; }
@@ -108,7 +108,10 @@ GemmPlan plan_gemm(int epi, int n_out, int K, int experts = 1) {
     p.wn = 2;
     p.rows = 2 * n_out;
   } else {
-    p.nb = 1;
+    // the LM head streams two adjacent 32-row blocks per wave: half the
+    // activation staging per weight byte, and its ~500 workgroups run in
+    // one round at two per CU
+    p.nb = epi == EPI_ARGMAX ? 2 : 1;
     p.wn = 4;
     p.rows = n_out;
   }
