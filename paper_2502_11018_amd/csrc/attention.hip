@@ -71,25 +71,14 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
   const int gh = chunk * NW + w;           // head within the group
   const bool head_live = gh < G;           // wave-uniform
   const int hq = hk * G + (head_live ? gh : 0);
-  const int n_nodes = a.meta.n_nodes[b];
-  const int P = a.meta.prefix_len[b];
   const int qrows = a.qblocks * 32;
 
-  if (qb * 32 >= n_nodes) return;  // no live query rows in this block (uniform)
-
-  // prefix key range of this split, in whole 32-key blocks
-  const int nblk = (P + 31) >> 5;
-  const int kb0 = (int)((long long)nblk * split / a.splits);
-  const int kb1 = (int)((long long)nblk * (split + 1) / a.splits);
-  const int nb = kb1 - kb0;
-
-  // query row of this lane
-  const int qi = qb * 32 + col;
-  const bool qlive = qi < n_nodes;
-  const int qr = b * a.max_tree + (qlive ? qi : 0);
-
   // Q^T operand (B): lane (col = query row, hh = k-group), 32 dims per chunk;
-  // split bf16, so S = K (q_hi + q_lo)
+  // split bf16, so S = K (q_hi + q_lo).  Loaded before the per-sequence
+  // metadata is known (rows past the tree hold stale values and are never
+  // written out; the row index stays inside the sequence's max_tree rows).
+  const int qi = qb * 32 + col;
+  const int qr = b * a.max_tree + min(qi, a.max_tree - 1);
   u32x4 qf[2][CH][4];
   {
     const long long qo = ((long long)qr * a.Hq + hq) * DH + 32 * hh;
@@ -102,65 +91,98 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
       }
   }
 
+  const int n_nodes = a.meta.n_nodes[b];
+  const int P = a.meta.prefix_len[b];
+
+  // prefix key range of this split, in whole 32-key blocks
+  const int nblk = (P + 31) >> 5;
+  const int kb0 = (int)((long long)nblk * split / a.splits);
+  const int kb1 = (int)((long long)nblk * (split + 1) / a.splits);
+  const int nb = kb1 - kb0;
+
   const long long head = ((long long)b * a.Hkv + hk) * a.kv_cap * DH;
   const uint16_t* kbase = a.k_cache + head;
   const uint16_t* vbase = a.v_cache + head;
   // MFMA row -> key offset inside a 32-key block: row 8q + 4h + e holds key 16h + 4q + e
   const int krow = 16 * ((col >> 2) & 1) + 4 * (col >> 3) + (col & 3);
-  // this lane's element offset inside a block, for each piece this wave stages
-  int goff[PPW];
+  // this lane's byte offset inside a block, for each piece this wave stages
+  // (each DMA takes a wave-uniform block base plus this offset)
+  const int wu = __builtin_amdgcn_readfirstlane(w);
+  uint32_t goff[PPW];
 #pragma unroll
   for (int p = 0; p < PPW; ++p) {
-    const int pc = w * PPW + p;
+    const int pc = wu * PPW + p;
     if (pc < KP) {
       const int c = pc >> 2, j = pc & 3;
-      goff[p] = krow * DH + 64 * c + 32 * hh + 8 * j;
+      goff[p] = 2u * (krow * DH + 64 * c + 32 * hh + 8 * j);
     } else {
       const int v = pc - KP, d = v >> 1, t = v & 1;
-      goff[p] = (32 * d + col) * 32 + 16 * hh + 8 * t;
+      goff[p] = 2u * ((32 * d + col) * 32 + 16 * hh + 8 * t);
     }
   }
   auto issue = [&](int slot, int kb) {
 #pragma unroll
     for (int p = 0; p < PPW; ++p) {
-      const int pc = w * PPW + p;
-      const uint16_t* src = (pc < KP ? kbase : vbase) + (long long)kb * 32 * DH + goff[p];
-      __builtin_amdgcn_global_load_lds((const void*)src, (lds_void*)&ring[slot][pc][0], 16, 0, 0);
+      const int pc = wu * PPW + p;
+      const char* blk = reinterpret_cast<const char*>((pc < KP ? kbase : vbase) + (long long)kb * 32 * DH);
+      __builtin_amdgcn_global_load_lds((const void*)(blk + goff[p]), (lds_void*)&ring[slot][pc][0], 16, 0, 0);
     }
   };
+  // The first D - 1 blocks go out as soon as the prefix length is known (the
+  // longest latency of the prologue), before the check for live rows: a
+  // workgroup without live rows lets them land and leaves.
+  if (nb > 0) {
+#pragma unroll
+    for (int i = 0; i < D - 1; ++i) issue(i, kb0 + min(i, nb - 1));
+  }
+  if (qb * 32 >= n_nodes) {  // no live query rows in this block (uniform)
+    wait_vmcnt_lds<0>();
+    return;
+  }
 
-  float m_ref = -INFINITY, l_run = 0.f;
+  // Softmax reference: each lane's row uses a fixed reference m_ref (log2
+  // domain), the maximum of its scores in the split's first block, so the
+  // output accumulators are never rescaled inside the block loop (a rescale
+  // there would make the compiler shuttle them between register files every
+  // block).  Later scores may exceed m_ref; p = 2^(s - m_ref) is capped at
+  // 2^kExpCap to stay finite, and m_true tracks the real maximum.  A row that
+  // went past the cap (scores spread over more than 2^64 within one split)
+  // is flagged, and the merge recomputes its split exactly.
+  constexpr float kExpCap = 64.f;
+  float m_ref = -INFINITY, m_true = -INFINITY, l_run = 0.f;
   f32x16 oacc[DB];
-#pragma unroll
-  for (int d = 0; d < DB; ++d)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) oacc[d][r] = 0.f;
 
-  // Online softmax with a lazily moved reference max: p = 2^(s - m_ref) may
-  // reach 2^8 before the reference is raised, so the accumulator rescale only
-  // runs when some lane's block maximum exceeds its reference by more than 8
-  // (a wave-uniform branch with no loads inside).  TAIL is true only for the
-  // last prefix block when P is not a multiple of 32: its keys at or beyond P
-  // get probability 0 and their V is zeroed (those slots hold tree or stale
-  // values), with branch-free selects.
-  auto compute = [&](auto tail, int slot, int kb) {
-    constexpr bool TAIL = decltype(tail)::value;
-    const int key0 = kb * 32;
-    // ---- S^T = K Q^T (rows: keys, cols: queries), q = q_hi + q_lo
+  // QK: S^T = K Q^T for the block in `slot` (rows: keys, cols: queries),
+  // q = q_hi + q_lo.
+  auto qk = [&](int slot) {
+    // all K fragments are read before the first MFMA, so the LDS latency is
+    // paid once per block
+    u32x4 kf[CH * 4];
+#pragma unroll
+    for (int x = 0; x < CH * 4; ++x) kf[x] = ring[slot][x][lane];
     f32x16 sacc;
 #pragma unroll
     for (int r = 0; r < 16; ++r) sacc[r] = 0.f;
 #pragma unroll
     for (int c = 0; c < CH; ++c)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const u32x4 kf = ring[slot][c * 4 + j][lane];
+      for (int j = 0; j < 4; ++j)
 #pragma unroll
         for (int h = 0; h < 2; ++h)
-          sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf), as_bf16x8(qf[h][c][j]), sacc, 0, 0, 0);
-      }
+          sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[c * 4 + j]), as_bf16x8(qf[h][c][j]), sacc, 0,
+                                                         0, 0);
+    return sacc;
+  };
 
-    // ---- mask (this lane: keys key0 + 16 hh + r); the log2-domain scale is
+  // SV: softmax of one block's scores and O^T += V^T P^T.  TAIL is true only
+  // for the last prefix block when P is not a multiple of 32: its keys at or
+  // beyond P get probability 0 and their V is zeroed (those slots hold tree
+  // or stale values), with branch-free selects.  `first` marks the block
+  // that sets m_ref.
+  auto sv = [&](auto tail, const f32x16& sacc, int slot, int kb, bool first) {
+    constexpr bool TAIL = decltype(tail)::value;
+    const int key0 = kb * 32;
+    // mask (this lane: keys key0 + 16 hh + r); the log2-domain scale is
     // applied inside the exponent (scale > 0 commutes with max)
     float s[16];
 #pragma unroll
@@ -172,25 +194,22 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
     mx = fmaxf(mx, fmaxf(fmaxf(fmaxf(s[8], s[9]), fmaxf(s[10], s[11])),
                          fmaxf(fmaxf(s[12], s[13]), fmaxf(s[14], s[15]))));
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * a.scale_log2;
-    if (__any(mx > m_ref + 8.f)) {
-      const float m_new = fmaxf(m_ref, mx);
-      const float alpha = m_ref == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_ref - m_new);
-      l_run *= alpha;
-#pragma unroll
-      for (int d = 0; d < DB; ++d)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[d][r] *= alpha;
-      m_ref = m_new;
-    }
-    const float m_use = m_ref == -INFINITY ? 0.f : m_ref;
+    m_ref = first ? mx : m_ref;
+    m_true = fmaxf(m_true, mx);
     float p[16];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) p[r] = __builtin_amdgcn_exp2f(fmaf(s[r], a.scale_log2, -m_use));
+    for (int r = 0; r < 16; ++r) p[r] = __builtin_amdgcn_exp2f(fminf(fmaf(s[r], a.scale_log2, -m_ref), kExpCap));
     const float psum = ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7])) +
                        (((p[8] + p[9]) + (p[10] + p[11])) + ((p[12] + p[13]) + (p[14] + p[15])));
     l_run += psum + __shfl_xor(psum, 32, 64);
 
-    // ---- O^T += V^T P^T, P as split bf16 (p_hi + p_lo)
+    // O^T += V^T P^T, P as split bf16 (p_hi + p_lo); all V fragments are
+    // read before the first MFMA
+    u32x4 vfr[2][DB];
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int d = 0; d < DB; ++d) vfr[t][d] = ring[slot][KP + d * 2 + t][lane];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       u32x4 pf[2];
@@ -209,7 +228,7 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
       }
 #pragma unroll
       for (int d = 0; d < DB; ++d) {
-        u32x4 vf = ring[slot][KP + d * 2 + t][lane];
+        u32x4 vf = vfr[t][d];
         if constexpr (TAIL) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) vf[q] &= keep[q];
@@ -221,39 +240,91 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
     }
   };
 
-  // Ring pipeline over the split's blocks (same structure as the GEMM's): at
-  // the top of iteration i every wave waits for its own DMA pieces of block i
-  // (vector-memory counters retire in issue order) and for its LDS reads of
-  // the previous slot; the barrier then publishes block i and frees slot
-  // (i - 1) % D, which block i + D - 1 overwrites.  Issues past the last block
-  // re-read it into slots that are never consumed; every DMA has landed
-  // before the waves leave.
-  if (nb > 0) {
-#pragma unroll
-    for (int i = 0; i < D - 1; ++i) issue(i, kb0 + min(i, nb - 1));
-    for (int i = 0; i < nb; ++i) {
-      wait_vmcnt_lds<(D - 2) * PPW>();
-      __builtin_amdgcn_s_barrier();
-      issue((i + D - 1) % D, kb0 + min(i + D - 1, nb - 1));
-      // waves past the end of the head group compute a duplicate of the
-      // group's first head and write nothing
-      if ((kb0 + i + 1) * 32 <= P) compute(std::false_type{}, i % D, kb0 + i);
-      else compute(std::true_type{}, i % D, kb0 + i);  // the partial last prefix block
-    }
-    wait_vmcnt_lds<0>();
-  }
-  if (!head_live) return;
-
-  // ---- partials: O^T layout, lane owns query col, dims 32 d + 8 (r/4) + 4 hh + r%4
-  float* po = a.part_o + ((((long long)b * a.Hq + hq) * a.splits + split) * qrows + qb * 32) * DH;
-  float* pml = a.part_ml + ((((long long)b * a.Hq + hq) * a.splits + split) * qrows + qb * 32) * 2;
-  float* orow = po + (long long)col * DH;
+  // Ring pipeline over the split's blocks (same structure as the GEMM's),
+  // software-pipelined by one block: step i computes the scores of block
+  // i + 1 (matrix cores) before the softmax and P V of block i (vector ALU,
+  // then matrix cores), so the two overlap.  At the top of step i every wave
+  // waits for its own DMA pieces of block i + 1 (vector-memory counters
+  // retire in issue order) and for its LDS reads of earlier slots; the
+  // barrier then publishes block i + 1 and frees the slot of block i - 1,
+  // which block i + D - 1 overwrites.  Issues past the last block re-read it
+  // into slots that are never consumed; every DMA has landed before the waves
+  // leave.  The loop is unrolled by the ring depth (slot indices are
+  // compile-time constants) and the split's last block, the only one that
+  // can be partial (the TAIL form), is handled after it: with one path
+  // through the loop body the accumulators stay in place and the only
+  // vector-memory waits are the ones written here.
+  static_assert(D >= 3, "one block of scores runs ahead of the ring");
+  const int nfull = (kb0 + nb) * 32 <= P ? nb : nb - 1;
 #pragma unroll
   for (int d = 0; d < DB; ++d)
 #pragma unroll
-    for (int rg = 0; rg < 4; ++rg)
-      *reinterpret_cast<float4*>(orow + 32 * d + 8 * rg + 4 * hh) =
+    for (int r = 0; r < 16; ++r) oacc[d][r] = 0.f;
+  if (nb > 0) {
+    // Q (loaded before the first DMAs) and block 0
+    wait_vmcnt_lds<(D - 2) * PPW>();
+    __builtin_amdgcn_s_barrier();
+    f32x16 sc = qk(0);
+    // block i (slot u = i % D) when block i + 1 exists
+    auto step = [&](auto tail, int u, int i) {
+      wait_vmcnt_lds<(D - 3) * PPW>();
+      __builtin_amdgcn_s_barrier();
+      issue((u + D - 1) % D, kb0 + min(i + D - 1, nb - 1));
+      const f32x16 sn = qk((u + 1) % D);
+      // waves past the end of the head group compute a duplicate of the
+      // group's first head and write nothing
+      sv(tail, sc, u, kb0 + i, i == 0);
+      sc = sn;
+    };
+    int base = 0;
+    for (; base + D < nb && base + D <= nfull; base += D) {
+#pragma unroll
+      for (int u = 0; u < D; ++u) step(std::false_type{}, u, base + u);
+    }
+    // the remaining blocks (at most D): full ones with a successor, then the
+    // last block (full or partial)
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      const int i = base + u;
+      if (i + 1 < nb) step(std::false_type{}, u, i);  // uniform; i + 1 < nb implies a full block
+      else if (i + 1 == nb) {
+        if (i < nfull) sv(std::false_type{}, sc, u, kb0 + i, i == 0);
+        else sv(std::true_type{}, sc, u, kb0 + i, i == 0);
+      }
+    }
+    wait_vmcnt_lds<0>();
+  }
+  // a row whose scores went past the cap marks its partial invalid (l < 0);
+  // the merge recomputes that split exactly
+  if (m_true > m_ref + kExpCap) l_run = -1.f;
+
+  // ---- partials, row-major [32 rows][DH].  The accumulators hold O^T (lane:
+  // query col, dims 32 d + 8 (r/4) + 4 hh + r%4), so each wave transposes its
+  // tile through its own part of the ring, which every wave has left after
+  // this barrier: 16-byte chunk c of row `col` sits at chunk c ^ (col & 7)
+  // (conflict-free writes and reads), and the global stores are contiguous.
+  constexpr int CHUNKS = DH / 4;  // 16-byte chunks per row
+  constexpr int RPI = 64 / CHUNKS;  // rows per wave-wide store
+  static_assert(NW * 32 * DH * 4 <= (int)sizeof(ring), "transpose tiles fit in the ring");
+  __builtin_amdgcn_s_barrier();
+  if (!head_live) return;
+  float* po = a.part_o + ((((long long)b * a.Hq + hq) * a.splits + split) * qrows + qb * 32) * DH;
+  float* pml = a.part_ml + ((((long long)b * a.Hq + hq) * a.splits + split) * qrows + qb * 32) * 2;
+  float* tile = reinterpret_cast<float*>(&ring[0][0][0]) + w * 32 * DH;
+#pragma unroll
+  for (int d = 0; d < DB; ++d)
+#pragma unroll
+    for (int rg = 0; rg < 4; ++rg) {
+      const int c = 8 * d + 2 * rg + hh;
+      *reinterpret_cast<float4*>(tile + col * DH + 4 * (c ^ (col & 7))) =
           make_float4(oacc[d][4 * rg], oacc[d][4 * rg + 1], oacc[d][4 * rg + 2], oacc[d][4 * rg + 3]);
+    }
+#pragma unroll
+  for (int n = 0; n < 32 / RPI; ++n) {
+    const int r = n * RPI + lane / CHUNKS, c = lane % CHUNKS;
+    *reinterpret_cast<float4*>(po + r * DH + 4 * c) =
+        *reinterpret_cast<const float4*>(tile + r * DH + 4 * (c ^ (r & 7)));
+  }
   if (hh == 0) {
     pml[2 * col] = m_ref;
     pml[2 * col + 1] = l_run;
@@ -303,7 +374,8 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
                                                            int Hq, int Hkv, int dh, int qrows, int max_tree,
                                                            const uint16_t* __restrict__ q,
                                                            const uint16_t* __restrict__ q_lo, TreeKV32 tree,
-                                                           float scale_log2, uint16_t* __restrict__ o_out, int o_ks) {
+                                                           PrefixKV prefix, float scale_log2,
+                                                           uint16_t* __restrict__ o_out, int o_ks) {
   const int r = blockIdx.x;
   const int b = r / max_tree, i = r % max_tree;
   const int quads = dh / 4;
@@ -322,7 +394,6 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
       ls[s] = part_ml[row * 2 + 1];
       os[s] = *reinterpret_cast<const float4*>(part_o + row * dh + d);
     }
-    // tree keys
     const int hk = h / (Hq / Hkv);
     const long long qo = ((long long)r * Hq + h) * dh + d;
     const uint2 qh = *reinterpret_cast<const uint2*>(q + qo), ql = *reinterpret_cast<const uint2*>(q_lo + qo);
@@ -330,6 +401,42 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
     const float q1 = bf16_to_f32(qh.x >> 16) + bf16_to_f32(ql.x >> 16);
     const float q2 = bf16_to_f32(qh.y & 0xffff) + bf16_to_f32(ql.y & 0xffff);
     const float q3 = bf16_to_f32(qh.y >> 16) + bf16_to_f32(ql.y >> 16);
+    // splits flagged by the attention kernel (scores past its cap): recompute
+    // (m, l, o) over the split's prefix keys in fp32 from the bf16 cache, with
+    // an exact running maximum
+    {
+      const int P = meta.prefix_len[b];
+      const int nblk = (P + 31) >> 5;
+      const uint16_t* kh = prefix.k + ((long long)b * Hkv + hk) * prefix.kv_cap * dh + d;
+      const uint16_t* vh = prefix.v + ((long long)b * Hkv + hk) * prefix.kv_cap * dh;
+#pragma unroll
+      for (int s = 0; s < MAXS; ++s) {
+        if (!(ls[s] < 0.f)) continue;  // uniform over the head's lanes
+        const int k0 = 32 * (int)((long long)nblk * s / MAXS);
+        const int k1 = min(P, 32 * (int)((long long)nblk * (s + 1) / MAXS));
+        float m = -INFINITY, l = 0.f;
+        float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int key = k0; key < k1; ++key) {
+          const uint2 kk = *reinterpret_cast<const uint2*>(kh + (long long)key * dh);
+          float dot = q0 * bf16_to_f32(kk.x & 0xffff) + q1 * bf16_to_f32(kk.x >> 16) +
+                      q2 * bf16_to_f32(kk.y & 0xffff) + q3 * bf16_to_f32(kk.y >> 16);
+          for (int o2 = quads >> 1; o2 > 0; o2 >>= 1) dot += __shfl_xor(dot, o2, 64);
+          const float sj = dot * scale_log2;
+          const float mn = fmaxf(m, sj);
+          const float al = exp2f(m - mn), e = exp2f(sj - mn);
+          // V tiles: element (key, dim) at ((key / 32) * dh + dim) * 32 + key % 32
+          const uint16_t* vk = vh + ((long long)(key >> 5) * dh + d) * 32 + (key & 31);
+          l = l * al + e;
+          o = make_float4(o.x * al + e * bf16_to_f32(vk[0]), o.y * al + e * bf16_to_f32(vk[32]),
+                          o.z * al + e * bf16_to_f32(vk[64]), o.w * al + e * bf16_to_f32(vk[96]));
+          m = mn;
+        }
+        ms[s] = m;
+        ls[s] = l;
+        os[s] = o;
+      }
+    }
+    // tree keys
     const float* tk = tree.k + ((long long)b * Hkv + hk) * max_tree * dh + d;
     const float* tv = tree.v + ((long long)b * Hkv + hk) * max_tree * dh + d;
     uint64_t anc = meta.anc[r];
@@ -389,8 +496,8 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
 
 hipError_t launch_attn_combine(const float* part_o, const float* part_ml, StepMeta meta, int Hq, int Hkv, int dh,
                                int splits, int qrows, int max_tree, int batch, const uint16_t* q,
-                               const uint16_t* q_lo, TreeKV32 tree, float scale_log2, uint16_t* o_out, int o_ks,
-                               hipStream_t s) {
+                               const uint16_t* q_lo, TreeKV32 tree, PrefixKV prefix, float scale_log2,
+                               uint16_t* o_out, int o_ks, hipStream_t s) {
   const int quads = dh / 4;
   if (256 % quads != 0) return hipErrorInvalidValue;
   const int items = Hq * quads;
@@ -399,7 +506,7 @@ hipError_t launch_attn_combine(const float* part_o, const float* part_ml, StepMe
 #define GRIFFIN_COMB_CASE(n)                                                                                   \
   case n:                                                                                                     \
     hipLaunchKernelGGL(attn_combine_kernel<n>, grid, dim3(256), 0, s, part_o, part_ml, meta, Hq, Hkv, dh, qrows,  \
-                       max_tree, q, q_lo, tree, scale_log2, o_out, o_ks);                                     \
+                       max_tree, q, q_lo, tree, prefix, scale_log2, o_out, o_ks);                             \
     break;
     GRIFFIN_COMB_CASE(1) GRIFFIN_COMB_CASE(2) GRIFFIN_COMB_CASE(3) GRIFFIN_COMB_CASE(4) GRIFFIN_COMB_CASE(5)
     GRIFFIN_COMB_CASE(6) GRIFFIN_COMB_CASE(7) GRIFFIN_COMB_CASE(8) GRIFFIN_COMB_CASE(9) GRIFFIN_COMB_CASE(10)

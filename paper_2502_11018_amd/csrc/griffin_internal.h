@@ -104,6 +104,14 @@ struct TreeKV32 {
   float* v;
 };
 
+// One layer's prefix cache (bf16): K [max_batch][Hkv][kv_cap][dh], V in
+// 32-slot transposed tiles [max_batch][Hkv][kv_cap / 32][dh][32].
+struct PrefixKV {
+  const uint16_t* k;
+  const uint16_t* v;
+  int kv_cap;
+};
+
 struct AttnArgs {
   const uint16_t* q;         // bf16 [R][Hq][dh]
   const uint16_t* q_lo;      // bf16 residual q - bf16(q), same layout
@@ -132,8 +140,8 @@ constexpr int ATTN_RING = 4;  // 32-key K/V blocks in flight per attention workg
 int attn_waves(int group);    // waves (query heads) per attention workgroup
 hipError_t launch_attn_combine(const float* part_o, const float* part_ml, StepMeta meta, int Hq, int Hkv, int dh,
                                int splits, int qrows, int max_tree, int batch, const uint16_t* q,
-                               const uint16_t* q_lo, TreeKV32 tree, float scale_log2, uint16_t* o_out, int o_ks,
-                               hipStream_t s);
+                               const uint16_t* q_lo, TreeKV32 tree, PrefixKV prefix, float scale_log2,
+                               uint16_t* o_out, int o_ks, hipStream_t s);
 hipError_t launch_argmax_reduce(const float* pmax, const int32_t* pidx, const int32_t* pnan, int n_tiles,
                                 int ld_part, int rows, int32_t* pred, int32_t* nan_row, hipStream_t s);
 hipError_t launch_commit(const int32_t* result, int max_depth, StepMeta meta, int batch, int n_layers, int Hkv,

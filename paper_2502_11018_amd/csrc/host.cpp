@@ -340,7 +340,8 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
     }
     LAUNCH(GRIFFIN_KC_MERGE, launch_attn_combine(c->attn_po, c->attn_pml, c->meta, d.n_q_heads, d.n_kv_heads,
                                                 d.head_dim, c->attn_splits, c->qblocks * 32, d.max_tree, B, c->q,
-                                                c->q_lo, c->tree, scale_log2, c->o, c->p_o.ks_pad, s));
+                                                c->q_lo, c->tree, PrefixKV{kc, vc, d.kv_capacity}, scale_log2, c->o,
+                                                c->p_o.ks_pad, s));
     {
       GemmArgs a = gemm_args(c->p_o, c->o, c->p_o.ks_pad, c->pk_o[l], m_tiles);
       a.out = c->parts;

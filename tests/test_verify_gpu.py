@@ -198,6 +198,41 @@ def test_empty_prefix_matches_oracle():
         H.check_parity(os_, out[: tree.n].cpu().numpy(), v.predictions()[0], acc.sequence(0))
 
 
+def test_scores_past_the_attention_cap_match_oracle():
+    """Prefix keys after the first 32 are scaled by 2^14, so inside the first
+    key split (two 32-key blocks: 1024 keys over 16 splits) the second block's
+    scores exceed the first block's maximum by thousands of log2 units, far
+    past the attention kernel's 2^64 cap on unnormalised probabilities.  That
+    split is flagged and the merge recomputes it exactly; the rest of the
+    pass is unchanged.  The softmax then concentrates on a few keys, on both
+    sides."""
+    P = _lib()
+    w = get_workload("small-gqa")
+    m = w.model
+    mw = gen.make_weights(m, 0)
+    ow = oracle.OracleWeights(mw)
+    plen = 1024
+    K, V = [], []
+    for l in range(m.n_layers):
+        k, v = gen.synthetic_kv(m, l, 0, plen, 7, "cpu")
+        k = k.to(torch.float32)
+        k[:, 32:, :] *= 16384.0  # a power of two: still exactly bf16
+        K.append(k.to(torch.float64).numpy())
+        V.append(v.to(torch.float64).numpy())
+    tree, _ = gen.random_tree((3, 4, 4), m.vocab, 5)
+    os_ = H.oracle_sequence(ow, H.SeqCase(None, H.PrefixKV(K, V), tree, [], [], []))
+    say("scores past the attention cap")
+    with P.TreeVerifier(m, mw.to("cuda"), max_batch=1, max_tree=16, max_depth=15, kv_capacity=plen + 64) as v:
+        for l in range(m.n_layers):
+            v.write_prefix(l, 0, torch.from_numpy(K[l]).to(torch.bfloat16).cuda(),
+                           torch.from_numpy(V[l]).to(torch.bfloat16).cuda())
+        out = torch.empty((16, m.vocab), device="cuda")
+        v.step([plen], [tree], out)
+        acc = v.accept()
+        st = H.check_parity(os_, out[: tree.n].cpu().numpy(), v.predictions()[0], acc.sequence(0))
+    say(f"scores past the attention cap: max rel err {st['max_rel']:.2e}")
+
+
 def test_errors_leave_cache_untouched(tiny):
     P = _lib()
     v = tiny.v
