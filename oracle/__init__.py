@@ -22,6 +22,7 @@ Modules
   decode.py   plain causal decoding, fp64 prefill, greedy continuation,
               brute-force acceptance over root-to-leaf paths
   latency.py  the paper's speedup model (appendix on decoding latency)
+  sampling.py stochastic tree acceptance at temperature T > 0 (Sec. 5)
 
 Each function states which pins in ``tests/test_oracle_*.py`` hold it to the
 paper or to mathematics it does not share with itself.  Absolute logits of a
@@ -34,3 +35,4 @@ from .verify import verify_tree, VerifyResult  # noqa: F401
 from .accept import argmax_first, top2_margin, accept_dfs, accept_trie  # noqa: F401
 from .decode import DecodeCache, decode_step, prefill, greedy_chain, brute_force_accept  # noqa: F401
 from .latency import speedup_ratio  # noqa: F401
+from .sampling import softmax_t, draw, accept_sampled  # noqa: F401

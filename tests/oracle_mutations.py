@@ -8,9 +8,10 @@ import numpy as np
 import oracle.accept as oa
 import oracle.decode as od
 import oracle.model as om
+import oracle.sampling as osm
 import oracle.verify as ov
 
-_MODULES = (om, ov, od, oa)
+_MODULES = (om, ov, od, oa, osm)
 
 
 def _patch(name, fn):
@@ -189,11 +190,70 @@ def latency_missing_depth():
     oracle.speedup_ratio = ol.speedup_ratio
 
 
+def _sampled_with(kept_in_q=False, unnormalised=False, inverted=False):
+    """accept_sampled with one mistake in the rejection step."""
+    def accept_sampled(tree, logits, q_draft, u_accept, u_final, temperature):
+        tokens, parents = np.asarray(tree.tokens), np.asarray(tree.parents)
+        node, path = 0, []
+        while True:
+            p = osm.softmax_t(logits[node], temperature)
+            q = np.asarray(q_draft[node], dtype=np.float64) / np.sum(q_draft[node])
+            nxt = None
+            for c in [c for c in range(1, len(tokens)) if int(parents[c]) == node]:
+                t = int(tokens[c])
+                a = min(1.0, q[t] / p[t]) if inverted else min(1.0, p[t] / q[t])
+                if float(u_accept[c]) < a:
+                    nxt = c
+                    break
+                r = np.maximum(p - q, 0.0)
+                p = r if unnormalised else r / np.sum(r)
+                if not kept_in_q:
+                    q = q.copy()
+                    q[t] = 0.0
+                    q = q / np.sum(q)
+            if nxt is None:
+                emitted = osm.draw(p, u_final[node])
+                break
+            path.append(nxt)
+            node = nxt
+        return oa.AcceptResult(len(path), [int(tokens[c]) for c in path] + [emitted], path)
+    return accept_sampled
+
+
+def _patch_sampled(fn):
+    _patch("accept_sampled", fn)
+    import oracle
+    oracle.accept_sampled = fn
+
+
+def sampling_rejected_token_kept_in_q():
+    _patch_sampled(_sampled_with(kept_in_q=True))
+
+
+def sampling_residual_unnormalised():
+    _patch_sampled(_sampled_with(unnormalised=True))
+
+
+def sampling_ratio_inverted():
+    _patch_sampled(_sampled_with(inverted=True))
+
+
+def sampling_temperature_ignored():
+    def softmax_t(logits, temperature):
+        z = np.asarray(logits, dtype=np.float64)
+        e = np.exp(z - np.max(z))
+        return e / np.sum(e)
+    _patch("softmax_t", softmax_t)
+    import oracle
+    oracle.softmax_t = softmax_t
+
+
 MUTATIONS = {f.__name__: f for f in [
     rope_sign, rope_interleaved, rope_freq_exponent, rmsnorm_eps_outside, attention_unscaled,
     gqa_modulo, no_ancestor_mask, position_by_node_id, drop_attention_residual, swiglu_swapped,
     moe_unnormalised, qkv_kv_swapped, accept_no_bonus, accept_first_child_only,
-    argmax_last_on_ties, latency_missing_depth,
+    argmax_last_on_ties, latency_missing_depth, sampling_rejected_token_kept_in_q,
+    sampling_residual_unnormalised, sampling_ratio_inverted, sampling_temperature_ignored,
 ]}
 
 
