@@ -147,6 +147,35 @@ int griffin_verify_step(griffin_ctx *ctx, int32_t batch, const int32_t *prefix_l
  * the outputs are still written). */
 int griffin_accept(griffin_ctx *ctx, int32_t *accept_len, int32_t *tokens_out, int32_t *path_nodes);
 
+/* Stochastic acceptance of the last step's trees at temperature T > 0 (the
+ * paper evaluates T = 1 beside greedy decoding, Sec. 5, and relies on the
+ * method being lossless).  Recursive rejection sampling over each node's
+ * children, in node-id order; the children of node u must have been drawn
+ * from u's draft distribution q_u without replacement:
+ *   p = softmax(logits_u / T), q = q_u;
+ *   child with token t: accepted when u_accept[child] < min(1, p(t) / q(t));
+ *   otherwise p <- max(p - q, 0) renormalised and t leaves q (renormalised);
+ *   a child accepted: continue there; none accepted, or no children: emit one
+ *   token drawn from p with u_final[u] (the first token whose cumulative sum
+ *   exceeds u_final * sum, in token order).
+ * Degenerate inputs: q(t) = 0 accepts when p(t) > 0; a residual summing to
+ * zero leaves p unchanged.
+ *   logits    device fp32 [batch*max_tree][vocab]: the buffer the last
+ *             griffin_verify_step filled (logits_out must have been given)
+ *   q_draft   device fp32 [batch*max_tree][vocab]: row b*max_tree+u = the
+ *             draft distribution u's children were drawn from (finite, >= 0,
+ *             any positive scale; rows of leaves are not read)
+ *   u_accept  host [batch][max_tree], u_final host [batch][max_tree]:
+ *             uniform draws in [0, 1) (entries of absent nodes are checked
+ *             but not used)
+ * Outputs as for griffin_accept: L accepted draft tokens, then the emitted
+ * token.  Synchronises the context's stream.  Errors: EINVAL (NULL input,
+ * T <= 0 or not finite, a uniform outside [0, 1)), EORDER (no step yet),
+ * EHIP, ENUMERIC (a NaN logit at a node the walk visited). */
+int griffin_accept_sampled(griffin_ctx *ctx, const float *logits, const float *q_draft,
+                           const float *u_accept, const float *u_final, float temperature,
+                           int32_t *accept_len, int32_t *tokens_out, int32_t *path_nodes);
+
 /* Commit the last step's accepted path into the KV cache (asynchronous, on
  * the context's stream; needs no host round trip).  For every sequence b of
  * that step, with L accepted draft nodes n_1..n_L at depths 1..L: their K/V,
@@ -203,6 +232,18 @@ int griffin_accept_walk(void *hip_stream, int32_t batch, int32_t max_tree, int32
                         int32_t vocab, const int32_t *n_nodes, const int32_t *tokens,
                         const int32_t *parents, const int32_t *pred, int32_t *accept_len,
                         int32_t *tokens_out, int32_t *path_nodes);
+
+/* The stochastic acceptance of griffin_accept_sampled for trees given
+ * directly: n_nodes, tokens, parents and the uniforms are host arrays laid
+ * out as for griffin_verify_step / griffin_accept_sampled; logits and q_draft
+ * are device fp32 [batch*max_tree][vocab].  Allocates and frees its own
+ * device buffers and synchronises hip_stream.  Errors: EINVAL, ETREE, ETOKEN,
+ * ENOMEM, EHIP, ENUMERIC (outputs still written). */
+int griffin_accept_sampled_walk(void *hip_stream, int32_t batch, int32_t max_tree, int32_t max_depth,
+                                int32_t vocab, const int32_t *n_nodes, const int32_t *tokens,
+                                const int32_t *parents, const float *logits, const float *q_draft,
+                                const float *u_accept, const float *u_final, float temperature,
+                                int32_t *accept_len, int32_t *tokens_out, int32_t *path_nodes);
 
 /* Kernel classes of one verification pass, for griffin_profile_*. */
 #define GRIFFIN_KC_QKV 0     /* QKV projection GEMM */

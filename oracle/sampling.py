@@ -34,7 +34,7 @@ rejection had probability zero) leaves p unchanged.
 
 from __future__ import annotations
 
-from typing import Sequence
+from typing import Optional, Sequence
 
 import numpy as np
 
@@ -51,11 +51,18 @@ def softmax_t(logits: np.ndarray, temperature: float) -> np.ndarray:
     return e / np.sum(e)
 
 
-def draw(p: np.ndarray, r: float) -> int:
-    """First token whose cumulative probability exceeds r * sum(p)."""
+def draw(p: np.ndarray, r: float, trace: Optional[list] = None) -> int:
+    """First token whose cumulative probability exceeds r * sum(p).  With a
+    trace list, appends ("draw", margin, r, cdf): margin = the distance of
+    r * sum(p) from the nearest cumulative boundary of the chosen token, and
+    cdf = the cumulative sums, both as fractions of sum(p)."""
     c = np.cumsum(np.asarray(p, dtype=np.float64))
-    idx = int(np.searchsorted(c, float(r) * c[-1], side="right"))
-    return min(idx, len(c) - 1)
+    thr = float(r) * c[-1]
+    idx = min(int(np.searchsorted(c, thr, side="right")), len(c) - 1)
+    if trace is not None:
+        lo = c[idx - 1] if idx > 0 else 0.0
+        trace.append(("draw", min(thr - lo, c[idx] - thr) / c[-1], float(r), c / c[-1]))
+    return idx
 
 
 def _children(parents: np.ndarray, n: int, u: int):
@@ -63,14 +70,16 @@ def _children(parents: np.ndarray, n: int, u: int):
 
 
 def accept_sampled(tree, logits: np.ndarray, q_draft: np.ndarray, u_accept: Sequence[float],
-                   u_final: Sequence[float], temperature: float) -> AcceptResult:
+                   u_final: Sequence[float], temperature: float, trace: Optional[list] = None) -> AcceptResult:
     """Recursive rejection sampling down the tree (one sequence).
 
     tree: tokens [T], parents [T] (node 0 = root).  logits: [T, V] target
     logits at every node.  q_draft: [T, V], row u = the draft distribution
     u's children were drawn from (rows of leaves are not read).  u_accept,
     u_final: [T] uniforms in [0, 1).  Returns the accepted path (L draft
-    tokens and their node ids) and the emitted token appended to the tokens."""
+    tokens and their node ids) and the emitted token appended to the tokens.
+    With a trace list, every decision appends its margin: ("accept", u - a)
+    for each test and the draw's entry (see `draw`)."""
     tokens = np.asarray(tree.tokens)
     parents = np.asarray(tree.parents)
     n = len(tokens)
@@ -86,6 +95,8 @@ def accept_sampled(tree, logits: np.ndarray, q_draft: np.ndarray, u_accept: Sequ
                 a = min(1.0, p[t] / q[t])
             else:
                 a = 1.0 if p[t] > 0 else 0.0
+            if trace is not None:
+                trace.append(("accept", float(u_accept[c]) - a))
             if float(u_accept[c]) < a:
                 nxt = c
                 break
@@ -96,7 +107,7 @@ def accept_sampled(tree, logits: np.ndarray, q_draft: np.ndarray, u_accept: Sequ
             if np.sum(q) > 0:
                 q = q / np.sum(q)
         if nxt is None:
-            emitted = draw(p, u_final[node])
+            emitted = draw(p, u_final[node], trace)
             break
         path.append(nxt)
         node = nxt

@@ -53,6 +53,7 @@ def _load() -> ctypes.CDLL:
             "(the verify path has no non-HIP fallback)")
     lib = ctypes.CDLL(LIB_PATH)
     I32P = POINTER(c_int32)
+    F32P = POINTER(c_float)
     sig = {
         "griffin_kv_cache_bytes": (c_size_t, [POINTER(ModelDesc)]),
         "griffin_verify_init": (c_int32, [POINTER(ModelDesc), POINTER(Weights), c_void_p, c_void_p, c_void_p,
@@ -71,6 +72,9 @@ def _load() -> ctypes.CDLL:
         "griffin_profile_read": (c_int32, [c_void_p, POINTER(c_double), POINTER(c_int64)]),
         "griffin_set_graphs": (c_int32, [c_void_p, c_int32]),
         "griffin_commit": (c_int32, [c_void_p]),
+        "griffin_accept_sampled": (c_int32, [c_void_p, c_void_p, c_void_p, F32P, F32P, c_float, I32P, I32P, I32P]),
+        "griffin_accept_sampled_walk": (c_int32, [c_void_p, c_int32, c_int32, c_int32, c_int32, I32P, I32P, I32P,
+                                                  c_void_p, c_void_p, F32P, F32P, c_float, I32P, I32P, I32P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -83,6 +87,6 @@ lib = _load()
 EXPORTED = ("griffin_kv_cache_bytes", "griffin_verify_init", "griffin_verify_step", "griffin_accept",
             "griffin_read_predictions", "griffin_verify_free", "griffin_status_str", "griffin_last_error",
             "griffin_tree_prepare", "griffin_accept_walk", "griffin_profile_enable", "griffin_profile_read",
-            "griffin_set_graphs", "griffin_commit")
+            "griffin_set_graphs", "griffin_commit", "griffin_accept_sampled", "griffin_accept_sampled_walk")
 KERNEL_CLASSES = ("qkv_gemm", "rope_kv_write", "tree_attention", "o_gemm", "residual_rmsnorm", "gate_up_gemm",
                   "down_gemm", "lm_head_gemm", "argmax_accept_route", "attn_merge")

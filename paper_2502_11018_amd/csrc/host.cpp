@@ -174,6 +174,10 @@ struct griffin_ctx {
   TreeKV32 tree{};  // fp32 tree K/V of the layer being computed (reused by every layer)
   int32_t *pidx = nullptr, *pnan = nullptr, *pred = nullptr, *nan_row = nullptr, *result = nullptr;
   int32_t *route_ids = nullptr, *gather = nullptr, *count = nullptr, *slot = nullptr;
+  // stochastic acceptance: residual rows [max_batch][2][vocab], uniforms
+  // [2][max_batch * max_tree] (accept, final), results
+  float *samp_res = nullptr, *samp_u = nullptr;
+  int32_t* samp_result = nullptr;
 
   // metadata: one device buffer, double-buffered pinned staging
   char* meta_dev = nullptr;
@@ -610,6 +614,9 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
   ALLOC(c->pred, Mp);
   ALLOC(c->nan_row, Mp);
   ALLOC(c->result, (long long)d.max_batch * result_stride(d.max_depth));
+  ALLOC(c->samp_res, (long long)d.max_batch * 2 * d.vocab);
+  ALLOC(c->samp_u, 2LL * d.max_batch * d.max_tree);
+  ALLOC(c->samp_result, (long long)d.max_batch * result_stride(d.max_depth));
   ALLOC(c->rope_cos, (long long)d.kv_capacity * (d.head_dim / 2));
   ALLOC(c->rope_sin, (long long)d.kv_capacity * (d.head_dim / 2));
   if (moe) {
@@ -822,6 +829,57 @@ int griffin_accept(griffin_ctx* c, int32_t* accept_len, int32_t* tokens_out, int
   return GRIFFIN_OK;
 }
 
+int griffin_accept_sampled(griffin_ctx* c, const float* logits, const float* q_draft, const float* u_accept,
+                           const float* u_final, float temperature, int32_t* accept_len, int32_t* tokens_out,
+                           int32_t* path_nodes) {
+  if (!c) return GRIFFIN_EINVAL;
+  if (!logits || !q_draft || !u_accept || !u_final)
+    return set_err(c, GRIFFIN_EINVAL, "logits, q_draft and both uniform arrays are required");
+  if (!(temperature > 0.f) || !std::isfinite(temperature))
+    return set_err(c, GRIFFIN_EINVAL, "temperature must be finite and > 0");
+  if (!c->stepped) return set_err(c, GRIFFIN_EORDER, "no verification step has been enqueued");
+  const griffin_model_desc& d = c->d;
+  const int rows = c->batch * d.max_tree;
+  for (int r = 0; r < rows; ++r)
+    if (!(u_accept[r] >= 0.f && u_accept[r] < 1.f) || !(u_final[r] >= 0.f && u_final[r] < 1.f))
+      return set_err(c, GRIFFIN_EINVAL, "uniforms must lie in [0, 1)");
+  const size_t ub = sizeof(float) * rows;
+  float* ua = c->samp_u;
+  float* uf = c->samp_u + (size_t)d.max_batch * d.max_tree;
+  HIP_TRY(c, hipMemcpyAsync(ua, u_accept, ub, hipMemcpyHostToDevice, c->stream));
+  HIP_TRY(c, hipMemcpyAsync(uf, u_final, ub, hipMemcpyHostToDevice, c->stream));
+  SampledArgs a{};
+  a.n_nodes = c->meta.n_nodes;
+  a.token = c->meta.token;
+  a.parent = c->meta.parent;
+  a.logits = logits;
+  a.q = q_draft;
+  a.u_accept = ua;
+  a.u_final = uf;
+  a.res = c->samp_res;
+  a.result = c->samp_result;
+  a.inv_t = 1.f / temperature;
+  a.max_tree = d.max_tree;
+  a.max_depth = d.max_depth;
+  a.vocab = d.vocab;
+  HIP_TRY(c, launch_sampled_accept(a, c->batch, c->stream));
+  const int st = result_stride(d.max_depth);
+  HIP_TRY(c, hipMemcpyAsync(c->result_host, c->samp_result, sizeof(int32_t) * c->batch * st, hipMemcpyDeviceToHost,
+                            c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  bool nan = false;
+  for (int b = 0; b < c->batch; ++b) {
+    const int32_t* r = c->result_host + (size_t)b * st;
+    if (accept_len) accept_len[b] = r[0];
+    nan |= r[1] != 0;
+    if (tokens_out) memcpy(tokens_out + (size_t)b * (d.max_depth + 1), r + 2, sizeof(int32_t) * (d.max_depth + 1));
+    if (path_nodes && d.max_depth > 0)
+      memcpy(path_nodes + (size_t)b * d.max_depth, r + 3 + d.max_depth, sizeof(int32_t) * d.max_depth);
+  }
+  if (nan) return set_err(c, GRIFFIN_ENUMERIC, "NaN in the logits of a visited tree node");
+  return GRIFFIN_OK;
+}
+
 int griffin_read_predictions(griffin_ctx* c, int32_t* pred) {
   if (!c || !pred) return GRIFFIN_EINVAL;
   if (!c->stepped) return set_err(c, GRIFFIN_EORDER, "no verification step has been enqueued");
@@ -934,6 +992,102 @@ int griffin_accept_walk(void* hip_stream, int32_t batch, int32_t max_tree, int32
   for (int b = 0; b < batch; ++b) {
     const int32_t* r = res.data() + (size_t)b * st;
     if (accept_len) accept_len[b] = r[0];
+    if (tokens_out) memcpy(tokens_out + (size_t)b * (max_depth + 1), r + 2, sizeof(int32_t) * (max_depth + 1));
+    if (path_nodes && max_depth > 0)
+      memcpy(path_nodes + (size_t)b * max_depth, r + 3 + max_depth, sizeof(int32_t) * max_depth);
+  }
+done:
+  hipStreamSynchronize(s);
+  hipFree(dev);
+  return rc;
+}
+
+int griffin_accept_sampled_walk(void* hip_stream, int32_t batch, int32_t max_tree, int32_t max_depth, int32_t vocab,
+                                const int32_t* n_nodes, const int32_t* tokens, const int32_t* parents,
+                                const float* logits, const float* q_draft, const float* u_accept,
+                                const float* u_final, float temperature, int32_t* accept_len, int32_t* tokens_out,
+                                int32_t* path_nodes) {
+  if (batch < 1 || max_tree < 1 || max_tree > kMaxTree || max_depth < 0 || max_depth >= max_tree || vocab < 1 ||
+      !n_nodes || !tokens || !parents || !logits || !q_draft || !u_accept || !u_final)
+    return GRIFFIN_EINVAL;
+  if (!(temperature > 0.f) || !std::isfinite(temperature)) return GRIFFIN_EINVAL;
+  const int rows = batch * max_tree;
+  std::vector<uint64_t> anc(rows, 0);
+  std::vector<int32_t> tok(rows, 0), par(rows, 0), dep(rows, 0), pos(rows, 0), nodes(batch);
+  std::vector<float> uu(2 * (size_t)rows, 0.f);
+  for (int b = 0; b < batch; ++b) {
+    const size_t r0 = (size_t)b * max_tree;
+    const int rc = prepare_tree(n_nodes[b], tokens + r0, parents + r0, 0, max_tree, max_depth, vocab,
+                                1 << 30, dep.data() + r0, pos.data() + r0, anc.data() + r0, nullptr);
+    if (rc != GRIFFIN_OK) return rc;
+    nodes[b] = n_nodes[b];
+    for (int i = 0; i < n_nodes[b]; ++i) {
+      tok[r0 + i] = tokens[r0 + i];
+      par[r0 + i] = i == 0 ? 0 : parents[r0 + i];
+    }
+  }
+  for (int r = 0; r < rows; ++r) {
+    if (!(u_accept[r] >= 0.f && u_accept[r] < 1.f) || !(u_final[r] >= 0.f && u_final[r] < 1.f))
+      return GRIFFIN_EINVAL;
+    uu[r] = u_accept[r];
+    uu[rows + r] = u_final[r];
+  }
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  const int st = result_stride(max_depth);
+  const size_t n_int = sizeof(int32_t) * rows;
+  const size_t n_res = sizeof(float) * 2 * (size_t)batch * vocab;
+  const size_t total = 2 * n_int + sizeof(int32_t) * batch + sizeof(float) * 2 * rows + n_res +
+                       sizeof(int32_t) * batch * st + 6 * 256;
+  char* dev = nullptr;
+  if (hipMalloc((void**)&dev, total) != hipSuccess) return GRIFFIN_ENOMEM;
+  char* p = dev;
+  auto carve = [&](size_t bytes) {
+    char* q = p;
+    p += (bytes + 255) / 256 * 256;
+    return q;
+  };
+  int32_t* d_tok = reinterpret_cast<int32_t*>(carve(n_int));
+  int32_t* d_par = reinterpret_cast<int32_t*>(carve(n_int));
+  int32_t* d_nodes = reinterpret_cast<int32_t*>(carve(sizeof(int32_t) * batch));
+  float* d_u = reinterpret_cast<float*>(carve(sizeof(float) * 2 * rows));
+  float* d_res = reinterpret_cast<float*>(carve(n_res));
+  int32_t* d_out = reinterpret_cast<int32_t*>(carve(sizeof(int32_t) * batch * st));
+  int rc = GRIFFIN_OK;
+  std::vector<int32_t> res((size_t)batch * st);
+  hipError_t e = hipSuccess;
+  SampledArgs a{};
+  a.n_nodes = d_nodes;
+  a.token = d_tok;
+  a.parent = d_par;
+  a.logits = logits;
+  a.q = q_draft;
+  a.u_accept = d_u;
+  a.u_final = d_u + rows;
+  a.res = d_res;
+  a.result = d_out;
+  a.inv_t = 1.f / temperature;
+  a.max_tree = max_tree;
+  a.max_depth = max_depth;
+  a.vocab = vocab;
+  if (p > dev + total) {
+    rc = GRIFFIN_ENOMEM;
+    goto done;
+  }
+  if ((e = hipMemcpyAsync(d_tok, tok.data(), n_int, hipMemcpyHostToDevice, s)) != hipSuccess ||
+      (e = hipMemcpyAsync(d_par, par.data(), n_int, hipMemcpyHostToDevice, s)) != hipSuccess ||
+      (e = hipMemcpyAsync(d_nodes, nodes.data(), sizeof(int32_t) * batch, hipMemcpyHostToDevice, s)) != hipSuccess ||
+      (e = hipMemcpyAsync(d_u, uu.data(), sizeof(float) * 2 * rows, hipMemcpyHostToDevice, s)) != hipSuccess ||
+      (e = launch_sampled_accept(a, batch, s)) != hipSuccess ||
+      (e = hipMemcpyAsync(res.data(), d_out, sizeof(int32_t) * batch * st, hipMemcpyDeviceToHost, s)) !=
+          hipSuccess ||
+      (e = hipStreamSynchronize(s)) != hipSuccess) {
+    rc = GRIFFIN_EHIP;
+    goto done;
+  }
+  for (int b = 0; b < batch; ++b) {
+    const int32_t* r = res.data() + (size_t)b * st;
+    if (accept_len) accept_len[b] = r[0];
+    if (r[1] != 0) rc = GRIFFIN_ENUMERIC;
     if (tokens_out) memcpy(tokens_out + (size_t)b * (max_depth + 1), r + 2, sizeof(int32_t) * (max_depth + 1));
     if (path_nodes && max_depth > 0)
       memcpy(path_nodes + (size_t)b * max_depth, r + 3 + max_depth, sizeof(int32_t) * max_depth);

@@ -7,7 +7,7 @@ memory (weights, KV cache, optional logits) and provides the stream.
 from __future__ import annotations
 
 import ctypes
-from ctypes import POINTER, byref, c_int32, c_uint64, c_void_p
+from ctypes import POINTER, byref, c_float, c_int32, c_uint64, c_void_p
 from dataclasses import dataclass
 from typing import Optional, Sequence
 
@@ -84,6 +84,41 @@ def accept_walk(trees: Sequence, pred: np.ndarray, max_tree: int, max_depth: int
     rc = N.lib.griffin_accept_walk(c_void_p(s), B, max_tree, max_depth, vocab, _p32(n), _p32(tok), _p32(par),
                                    _p32(pred), _p32(L), _p32(out), _p32(path))
     _check(rc, "griffin_accept_walk")
+    return AcceptResult(L, out, path[:, :max_depth])
+
+
+def _f32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.float32))
+
+
+def _pf32(a: np.ndarray):
+    return a.ctypes.data_as(POINTER(c_float))
+
+
+def _device_rows(t: torch.Tensor, rows: int, vocab: int, what: str):
+    if not (t.is_cuda and t.dtype == torch.float32 and t.is_contiguous() and t.numel() >= rows * vocab):
+        raise ValueError(f"{what} must be a contiguous fp32 CUDA tensor with [B*max_tree, vocab] elements")
+    return c_void_p(t.data_ptr())
+
+
+def accept_sampled_walk(trees: Sequence, logits: torch.Tensor, q_draft: torch.Tensor, u_accept, u_final,
+                        temperature: float, max_tree: int, max_depth: int, vocab: int,
+                        stream: Optional[torch.cuda.Stream] = None) -> AcceptResult:
+    """Device stochastic acceptance (temperature > 0) on given logits and
+    draft distributions, both fp32 [B*max_tree, vocab] CUDA tensors; the
+    uniforms are [B, max_tree] arrays in [0, 1)."""
+    n, tok, par = pack_trees(trees, max_tree)
+    B = len(trees)
+    ua, uf = _f32(u_accept).reshape(B, max_tree), _f32(u_final).reshape(B, max_tree)
+    L = np.zeros(B, dtype=np.int32)
+    out = np.zeros((B, max_depth + 1), dtype=np.int32)
+    path = np.zeros((B, max(max_depth, 1)), dtype=np.int32)
+    s = (stream or torch.cuda.current_stream()).cuda_stream
+    rc = N.lib.griffin_accept_sampled_walk(
+        c_void_p(s), B, max_tree, max_depth, vocab, _p32(n), _p32(tok), _p32(par),
+        _device_rows(logits, B * max_tree, vocab, "logits"), _device_rows(q_draft, B * max_tree, vocab, "q_draft"),
+        _pf32(ua), _pf32(uf), float(temperature), _p32(L), _p32(out), _p32(path))
+    _check(rc, "griffin_accept_sampled_walk")
     return AcceptResult(L, out, path[:, :max_depth])
 
 
@@ -187,6 +222,25 @@ class TreeVerifier:
         rc = N.lib.griffin_accept(self.ctx, _p32(L), _p32(out), _p32(path))
         if rc != N.CODES["GRIFFIN_ENUMERIC"] or check:
             _check(rc, "griffin_accept", self.ctx)
+        return AcceptResult(L[:B], out[:B], path[:B, :D], rc)
+
+    def accept_sampled(self, logits: torch.Tensor, q_draft: torch.Tensor, u_accept, u_final,
+                       temperature: float = 1.0, check: bool = True) -> AcceptResult:
+        """Stochastic acceptance (temperature > 0) of the last step: logits is
+        the logits_out tensor that step filled, q_draft the draft distributions
+        (fp32 [B*max_tree, vocab] CUDA tensor), u_accept / u_final uniforms
+        [B, max_tree] in [0, 1)."""
+        B, D, T = self._batch, self.max_depth, self.max_tree
+        V = self.shape.vocab
+        ua, uf = _f32(u_accept).reshape(B, T), _f32(u_final).reshape(B, T)
+        L = np.zeros(max(B, 1), dtype=np.int32)
+        out = np.zeros((max(B, 1), D + 1), dtype=np.int32)
+        path = np.zeros((max(B, 1), max(D, 1)), dtype=np.int32)
+        rc = N.lib.griffin_accept_sampled(self.ctx, _device_rows(logits, B * T, V, "logits"),
+                                          _device_rows(q_draft, B * T, V, "q_draft"), _pf32(ua), _pf32(uf),
+                                          float(temperature), _p32(L), _p32(out), _p32(path))
+        if rc != N.CODES["GRIFFIN_ENUMERIC"] or check:
+            _check(rc, "griffin_accept_sampled", self.ctx)
         return AcceptResult(L[:B], out[:B], path[:B, :D], rc)
 
     def predictions(self) -> np.ndarray:

@@ -1,0 +1,220 @@
+"""Stochastic (temperature > 0) acceptance on the GPU, through the C ABI.
+
+Parity with the fp64 oracle (oracle/sampling.py) on the same seeded inputs:
+a decision taken in fp32 on the device and in fp64 by the oracle can only
+differ when it lies within rounding of its boundary.  So the accepted path is
+compared exactly when every accept test on the oracle's path clears
+ACCEPT_MARGIN (else the sequence is counted, not compared), and the drawn
+token exactly when it clears DRAW_MARGIN, else it must be a valid draw within
+DRAW_TOL.  Also: losslessness of the
+device walk (chi-square against the exact enumeration of
+tests/test_oracle_sampling.py), the small-temperature limit equals the greedy
+walk, and the error paths.  Every case prints its name before touching the
+GPU.
+"""
+
+from collections import defaultdict
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from workloads import gen
+from tests import test_oracle_sampling as S
+
+pytestmark = pytest.mark.gpu
+
+# An accept test is compared exactly when |u - a| clears ACCEPT_MARGIN; the
+# drawn token when u * sum lies DRAW_MARGIN (fraction of the sum) inside its
+# interval, and otherwise it must be a token whose interval comes within
+# DRAW_TOL of u * sum (fp32 sums over up to 128K terms on the device).
+ACCEPT_MARGIN = 1e-5
+DRAW_MARGIN = 2e-5
+DRAW_TOL = 1e-4
+
+
+def say(msg):
+    print(f"[gpu-case] {msg}", flush=True)
+
+
+def _lib():
+    import paper_2502_11018_amd as P
+    return P
+
+
+def _pack(cases, max_tree, V):
+    B = len(cases)
+    lg = np.zeros((B * max_tree, V), np.float32)
+    q = np.zeros((B * max_tree, V), np.float32)
+    ua = np.zeros((B, max_tree), np.float32)
+    uf = np.zeros((B, max_tree), np.float32)
+    for b, c in enumerate(cases):
+        n = c.tree.n
+        lg[b * max_tree: b * max_tree + n] = c.logits
+        q[b * max_tree: b * max_tree + n] = c.q
+        ua[b, :n] = c.u_accept
+        uf[b, :n] = c.u_final
+    return torch.from_numpy(lg).cuda(), torch.from_numpy(q).cuda(), ua, uf
+
+
+def _compare(tree, logits, q, ua, uf, T, dev, b, accept_margin=ACCEPT_MARGIN, draw_margin=DRAW_MARGIN,
+             draw_tol=DRAW_TOL):
+    """Compare device row b with the oracle.  Returns (compared, oracle
+    result): False when an accept test on the oracle's path is within
+    accept_margin of its boundary (nothing asserted)."""
+    tr = []
+    r = oracle.accept_sampled(tree, np.asarray(logits, np.float64), np.asarray(q, np.float64), ua, uf, T, tr)
+    if any(abs(e[1]) <= accept_margin for e in tr if e[0] == "accept"):
+        return False, r
+    L = int(dev.length[b])
+    assert L == r.length and list(dev.path[b, :L]) == r.path, (b, r, dev.path[b])
+    assert list(dev.tokens[b, :L]) == r.tokens[:-1]
+    assert all(dev.tokens[b, L + 1:] == -1) and all(dev.path[b, L:] == -1)
+    _, margin, rr, cdf = [e for e in tr if e[0] == "draw"][0]
+    g = int(dev.tokens[b, L])
+    if margin > draw_margin:
+        assert g == r.tokens[-1], (b, g, r.tokens[-1], margin)
+    else:  # a boundary case: the device token must be a valid draw at u
+        lo = cdf[g - 1] if g > 0 else 0.0
+        assert lo - draw_tol <= rr <= cdf[g] + draw_tol, (b, g, r.tokens[-1], rr, lo, cdf[g])
+    return True, r
+
+
+@pytest.mark.parametrize("V,T,B", [(3000, 1.0, 8), (128256, 1.0, 3), (3000, 0.7, 8)])
+def test_sampled_walk_matches_oracle(V, T, B):
+    P = _lib()
+    max_tree, D = 64, 6
+    cases = [gen.sampled_case((10,) * 6, V, 500 + 17 * i, temperature=T) for i in range(B)]
+    lg, q, ua, uf = _pack(cases, max_tree, V)
+    say(f"sampled walk V={V} T={T} B={B}")
+    res = P.accept_sampled_walk([c.tree for c in cases], lg, q, ua, uf, T, max_tree, D, V)
+    compared, lengths = 0, []
+    for b, c in enumerate(cases):
+        ok, r = _compare(c.tree, c.logits, c.q, c.u_accept, c.u_final, T, res, b)
+        compared += ok
+        lengths.append(r.length)
+    say(f"sampled walk V={V} T={T}: compared {compared}/{B}, oracle lengths {lengths}")
+    assert compared >= B - 1
+
+
+def test_sampled_walk_is_lossless_on_gpu():
+    """Trees drawn from a draft table, accepted on the device: the emitted
+    sequences, extended by target sampling, follow the exact enumeration
+    (which equals target sampling)."""
+    P = _lib()
+    shape = S.SHAPES[1]
+    D = S._depth(shape)
+    Ptab, Qtab = S._tables(5, D)
+    exact = S._extend(Ptab, S._exact(Ptab, Qtab, (), shape), D + 1)
+    rng = np.random.default_rng(21)
+    n, max_tree = 20000, 8
+    trees, lg, q = [], np.zeros((n * max_tree, S.V), np.float32), np.full((n * max_tree, S.V), 1.0 / S.V, np.float32)
+    for i in range(n):
+        tokens, parents, prefixes = [int(rng.integers(S.V))], [-1], [()]
+        frontier = [(0, shape)]
+        while frontier:
+            nxt = []
+            for node, sh in frontier:
+                draws = rng.choice(S.V, size=len(sh), replace=False, p=Qtab[prefixes[node]])
+                for t, csh in zip(draws, sh):
+                    tokens.append(int(t))
+                    parents.append(node)
+                    prefixes.append(prefixes[node] + (int(t),))
+                    nxt.append((len(tokens) - 1, csh))
+            frontier = nxt
+        trees.append(gen.Tree(np.array(tokens, np.int32), np.array(parents, np.int32)))
+        for j, pre in enumerate(prefixes):
+            lg[i * max_tree + j] = np.log(Ptab[pre])
+            q[i * max_tree + j] = Qtab[pre]
+    ua = rng.random((n, max_tree)).astype(np.float32)
+    uf = rng.random((n, max_tree)).astype(np.float32)
+    say(f"sampled walk losslessness: {n} trees")
+    res = P.accept_sampled_walk(trees, torch.from_numpy(lg).cuda(), torch.from_numpy(q).cuda(), ua, uf, 1.0,
+                                max_tree, D, S.V)
+    counts = defaultdict(int)
+    for i in range(n):
+        L = int(res.length[i])
+        seq = tuple(int(t) for t in res.tokens[i, : L + 1])
+        while len(seq) < D + 1:
+            seq = seq + (int(rng.choice(S.V, p=Ptab[seq])),)
+        counts[seq] += 1
+    chi2 = sum((counts[s] - n * e) ** 2 / (n * e) for s, e in exact.items() if e > 0)
+    dof = sum(1 for e in exact.values() if e > 0) - 1
+    say(f"sampled walk losslessness: chi2 {chi2:.1f} with {dof} degrees of freedom")
+    assert chi2 < dof + 6 * np.sqrt(2 * dof)
+
+
+def test_small_temperature_equals_greedy_walk():
+    P = _lib()
+    V, max_tree, D, B = 2000, 64, 6, 6
+    cases = [gen.sampled_case((6,) * 6, V, 900 + i, temperature=1.0, logit_std=3.0) for i in range(B)]
+    lg, q, ua, uf = _pack(cases, max_tree, V)
+    say("sampled walk at T = 1e-3 vs greedy walk")
+    res = P.accept_sampled_walk([c.tree for c in cases], lg, q, ua, uf, 1e-3, max_tree, D, V)
+    pred = np.zeros((B, max_tree), np.int32)
+    for b, c in enumerate(cases):
+        pred[b, : c.tree.n] = np.argmax(c.logits, axis=1)
+    ref = P.accept_walk([c.tree for c in cases], pred, max_tree, D, V)
+    assert (res.length == ref.length).all()
+    assert (res.tokens == ref.tokens).all()
+
+
+def test_sampled_errors():
+    P = _lib()
+    V, max_tree, D = 100, 16, 4
+    c = gen.sampled_case((3, 3), V, 1)
+    lg, q, ua, uf = _pack([c], max_tree, V)
+    say("sampled walk error paths")
+    for T in (0.0, -1.0, float("inf")):
+        with pytest.raises(P.GriffinError):
+            P.accept_sampled_walk([c.tree], lg, q, ua, uf, T, max_tree, D, V)
+    bad = ua.copy()
+    bad[0, 1] = 1.0
+    with pytest.raises(P.GriffinError):
+        P.accept_sampled_walk([c.tree], lg, q, bad, uf, 1.0, max_tree, D, V)
+
+
+def test_accept_sampled_after_a_step_matches_oracle():
+    """The context path: a verify step writes the logits, accept_sampled reads
+    them.  The oracle uses its own fp64 logits, so decisions are compared
+    where they clear a wider margin (the logits differ by ~1e-5 of their
+    range)."""
+    P = _lib()
+    from tests.test_verify_gpu import Setup
+    s = Setup("tiny", n_trees=8)
+    try:
+        V, T = s.w.model.vocab, 1.0
+        rng = np.random.default_rng(33)
+        compared = 0
+        for i, cases in enumerate(s.cases):
+            c = cases[0]
+            say(f"accept_sampled after step, tree {i}")
+            out = torch.zeros((s.max_tree, V), device="cuda")
+            s.v.step([s.w.prefix_len], [c.tree], out)
+            q = rng.dirichlet(np.ones(V), size=s.max_tree).astype(np.float32)
+            ua = rng.random((1, s.max_tree)).astype(np.float32)
+            uf = rng.random((1, s.max_tree)).astype(np.float32)
+            res = s.v.accept_sampled(out, torch.from_numpy(q).cuda(), ua, uf, T)
+            from tests import harness as H
+            ol = H.oracle_sequence(s.ow, c).logits
+            ok, _ = _compare(c.tree, ol, q[: c.tree.n], ua[0, : c.tree.n], uf[0, : c.tree.n], T, res, 0,
+                             accept_margin=1e-3, draw_margin=1e-3, draw_tol=2e-3)
+            compared += ok
+        say(f"accept_sampled after step: compared {compared}/8")
+        assert compared >= 4
+    finally:
+        s.v.close()
+
+
+def test_accept_sampled_before_a_step_is_an_order_error():
+    P = _lib()
+    from workloads.configs import get_workload
+    w = get_workload("tiny")
+    mw = gen.make_weights(w.model, 0)
+    say("accept_sampled before any step")
+    with P.TreeVerifier(w.model, mw.to("cuda"), max_batch=1, max_tree=8, max_depth=7, kv_capacity=64) as v:
+        v._batch = 1
+        t = torch.zeros((8, w.model.vocab), device="cuda")
+        with pytest.raises(P.GriffinError):
+            v.accept_sampled(t, t, np.zeros((1, 8)), np.zeros((1, 8)), 1.0)

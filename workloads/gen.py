@@ -240,6 +240,43 @@ def random_tree(widths: Sequence[int], vocab: int, seed: int) -> tuple[Tree, np.
     return Tree(tokens, parents), rng
 
 
+@dataclass
+class SampledCase:
+    """Inputs of the stochastic (temperature > 0) acceptance for one tree."""
+    tree: Tree
+    logits: np.ndarray    # float32 [T, V] target logits at every node
+    q: np.ndarray         # float32 [T, V] draft distribution of each node's children
+    u_accept: np.ndarray  # float32 [T] uniform for the test at each child
+    u_final: np.ndarray   # float32 [T] uniform for the token drawn at each node
+
+
+def sampled_case(widths: Sequence[int], vocab: int, seed: int, temperature: float = 1.0,
+                 logit_std: float = 2.0, draft_noise: float = 1.0) -> SampledCase:
+    """A synthetic draft tree with the inputs the stochastic acceptance reads.
+
+    Target logits are i.i.d. N(0, logit_std^2).  The draft at node u is
+    proportional to exp(logits_u / temperature + N(0, draft_noise^2)), a
+    drafter correlated with the target.  Every node's children take tokens
+    drawn from its draft distribution without replacement (numpy's
+    generator), as a sampling drafter would; the shape is `random_tree`'s."""
+    shape, rng = random_tree(widths, vocab, seed)
+    T = shape.n
+    logits = rng.normal(0.0, logit_std, size=(T, vocab))
+    z = logits / temperature + rng.normal(0.0, draft_noise, size=(T, vocab))
+    q = np.exp(z - z.max(axis=1, keepdims=True))
+    q /= q.sum(axis=1, keepdims=True)
+    tokens = np.zeros(T, dtype=np.int32)
+    tokens[0] = rng.integers(0, vocab)
+    for u in range(T):
+        kids = [c for c in range(1, T) if shape.parents[c] == u]
+        if kids:
+            draws = rng.choice(vocab, size=len(kids), replace=False, p=q[u])
+            for c, t in zip(kids, draws):
+                tokens[c] = int(t)
+    return SampledCase(Tree(tokens, shape.parents.copy()), logits.astype(np.float32), q.astype(np.float32),
+                       rng.random(T).astype(np.float32), rng.random(T).astype(np.float32))
+
+
 def workload_tree(w: Workload, index: int, seq: int = 0) -> tuple[Tree, List[int]]:
     """The tree and the node path chosen for planting (possibly empty).
 
