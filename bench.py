@@ -128,6 +128,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-profile", action="store_true")
     ap.add_argument("--no-graphs", action="store_true", help="plain launches instead of graph replay")
+    ap.add_argument("--no-sampled", action="store_true", help="skip the temperature-1 (stochastic acceptance) leg")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on exactly one GPU; --gpus {args.gpus} is not supported", file=sys.stderr)
@@ -241,6 +242,46 @@ def main():
                     "bytes_per_launch": kernels[dom]["bytes_per_launch"],
                     "avg_launch_us": kernels[dom]["avg_launch_us"]}
 
+    # temperature-1 cycle: the same steps also writing the logits, then the
+    # stochastic acceptance with seeded draft distributions and uniforms
+    sampled = None
+    if not args.no_sampled:
+        R, V = w.batch * max_tree, m.vocab
+        logits = torch.empty((R, V), dtype=torch.float32, device=dev)
+        g = torch.Generator(device=dev)
+        g.manual_seed(1234)
+        qd = torch.rand((R, V), generator=g, device=dev)
+        qd /= qd.sum(dim=1, keepdim=True)
+        urng = np.random.default_rng(99)
+
+        def uniforms():
+            return urng.random((w.batch, max_tree)), urng.random((w.batch, max_tree))
+
+        def t1_step(i):
+            n, tok, par = packed[i % len(packed)]
+            v.step_arrays(prefix, n, tok, par, logits)
+            return v.accept_sampled(logits, qd, *uniforms(), 1.0)
+
+        ns = min(args.steps, 20)
+        for i in range(3):
+            t1_step(i)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        lens = []
+        for i in range(ns):
+            lens.extend(int(x) for x in t1_step(i).length)
+        t_cycle = (time.perf_counter() - t0) / ns
+        t0 = time.perf_counter()
+        for i in range(ns):
+            v.accept_sampled(logits, qd, *uniforms(), 1.0)
+        t_acc = (time.perf_counter() - t0) / ns
+        sampled = {"temperature": 1.0, "steps": ns, "ms_per_step": round(t_cycle * 1e3, 4),
+                   "accept_sampled_us": round(t_acc * 1e6, 1),
+                   "synthetic_mean_accept_len": round(float(np.mean(lens)) + 1.0, 3),
+                   "note": "step writing all logits + stochastic acceptance; draft distributions are "
+                           "seeded random rows, so acceptance is synthetic"}
+        log(f"T=1 cycle {t_cycle * 1e3:.3f} ms/step, stochastic acceptance {t_acc * 1e6:.1f} us")
+
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on a bounded sample")
@@ -268,6 +309,7 @@ def main():
         "synthetic_mean_accept_len": round(float(np.mean(accepted)) + 1.0, 3) if accepted else None,
         "roofline": roofline,
         "kernels": kernels,
+        "temperature_1": sampled,
         "cpu_baseline": cpu,
     }
     v.close()
