@@ -176,7 +176,9 @@ struct griffin_ctx {
   int32_t *route_ids = nullptr, *gather = nullptr, *count = nullptr, *slot = nullptr;
   // stochastic acceptance: residual rows [max_batch][2][vocab], uniforms
   // [2][max_batch * max_tree] (accept, final), results
-  float *samp_res = nullptr, *samp_u = nullptr;
+  char* samp_scratch = nullptr;  // sampled_scratch_bytes(max_batch, max_tree, vocab), zeroed
+  float* samp_u = nullptr;      // [5][max_batch * max_tree]: u_accept, u_final, work order, step children, tokens
+  float* samp_host = nullptr;   // pinned staging of samp_u
   int32_t* samp_result = nullptr;
 
   // metadata: one device buffer, double-buffered pinned staging
@@ -515,6 +517,7 @@ void griffin_verify_free(griffin_ctx* c) {
   for (auto& g : c->graphs) hipGraphExecDestroy(g.exec);
   if (c->result_host) hipHostFree(c->result_host);
   if (c->pred_host) hipHostFree(c->pred_host);
+  if (c->samp_host) hipHostFree(c->samp_host);
   delete c;
 }
 
@@ -614,8 +617,8 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
   ALLOC(c->pred, Mp);
   ALLOC(c->nan_row, Mp);
   ALLOC(c->result, (long long)d.max_batch * result_stride(d.max_depth));
-  ALLOC(c->samp_res, (long long)d.max_batch * 2 * d.vocab);
-  ALLOC(c->samp_u, 2LL * d.max_batch * d.max_tree);
+  ALLOC(c->samp_scratch, sampled_scratch_bytes(d.max_batch, d.max_tree, d.vocab));
+  ALLOC(c->samp_u, 5LL * d.max_batch * d.max_tree);
   ALLOC(c->samp_result, (long long)d.max_batch * result_stride(d.max_depth));
   ALLOC(c->rope_cos, (long long)d.kv_capacity * (d.head_dim / 2));
   ALLOC(c->rope_sin, (long long)d.kv_capacity * (d.head_dim / 2));
@@ -729,7 +732,9 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
   }
   if (hipHostMalloc((void**)&c->result_host, sizeof(int32_t) * d.max_batch * result_stride(d.max_depth),
                     hipHostMallocDefault) != hipSuccess ||
-      hipHostMalloc((void**)&c->pred_host, sizeof(int32_t) * Mp, hipHostMallocDefault) != hipSuccess) {
+      hipHostMalloc((void**)&c->pred_host, sizeof(int32_t) * Mp, hipHostMallocDefault) != hipSuccess ||
+      hipHostMalloc((void**)&c->samp_host, sizeof(float) * 5 * d.max_batch * d.max_tree, hipHostMallocDefault) !=
+          hipSuccess) {
     griffin_verify_free(c);
     return GRIFFIN_ENOMEM;
   }
@@ -829,6 +834,37 @@ int griffin_accept(griffin_ctx* c, int32_t* accept_len, int32_t* tokens_out, int
   return GRIFFIN_OK;
 }
 
+// Work list of the stochastic acceptance: every node's row b * max_tree + u,
+// sorted by child count (descending, ties by row); rows_with[j] = the number
+// of rows with at least j children; for k = 0, 1, .. in turn, the k-th child
+// (in id order) of each of the first rows_with[k + 1] rows and its token.
+// parents: root entries ignored.
+static void sampled_plan(int batch, int max_tree, const int32_t* n_nodes, const int32_t* parents,
+                         const int32_t* tokens, std::vector<int32_t>& order, std::vector<int>& rows_with,
+                         std::vector<int32_t>& step_child, std::vector<int32_t>& step_token) {
+  std::vector<std::vector<int32_t>> kids((size_t)batch * max_tree);
+  order.clear();
+  for (int b = 0; b < batch; ++b)
+    for (int i = 0; i < n_nodes[b]; ++i) {
+      order.push_back(b * max_tree + i);
+      if (i > 0) kids[(size_t)b * max_tree + parents[(size_t)b * max_tree + i]].push_back(i);
+    }
+  std::stable_sort(order.begin(), order.end(),
+                   [&](int32_t x, int32_t y) { return kids[x].size() > kids[y].size(); });
+  const int cmax = order.empty() ? 0 : (int)kids[order[0]].size();
+  rows_with.assign(cmax + 1, 0);
+  for (int32_t r : order)
+    for (int j = 0; j <= (int)kids[r].size(); ++j) ++rows_with[j];
+  step_child.clear();
+  step_token.clear();
+  for (int k = 0; k < cmax; ++k)
+    for (int i = 0; i < rows_with[k + 1]; ++i) {
+      const int32_t r = order[i], c = kids[r][k];
+      step_child.push_back(c);
+      step_token.push_back(tokens[(size_t)(r / max_tree) * max_tree + c]);
+    }
+}
+
 int griffin_accept_sampled(griffin_ctx* c, const float* logits, const float* q_draft, const float* u_accept,
                            const float* u_final, float temperature, int32_t* accept_len, int32_t* tokens_out,
                            int32_t* path_nodes) {
@@ -843,11 +879,21 @@ int griffin_accept_sampled(griffin_ctx* c, const float* logits, const float* q_d
   for (int r = 0; r < rows; ++r)
     if (!(u_accept[r] >= 0.f && u_accept[r] < 1.f) || !(u_final[r] >= 0.f && u_final[r] < 1.f))
       return set_err(c, GRIFFIN_EINVAL, "uniforms must lie in [0, 1)");
-  const size_t ub = sizeof(float) * rows;
-  float* ua = c->samp_u;
-  float* uf = c->samp_u + (size_t)d.max_batch * d.max_tree;
-  HIP_TRY(c, hipMemcpyAsync(ua, u_accept, ub, hipMemcpyHostToDevice, c->stream));
-  HIP_TRY(c, hipMemcpyAsync(uf, u_final, ub, hipMemcpyHostToDevice, c->stream));
+  std::vector<int32_t> order, step_child, step_token;
+  std::vector<int> rows_with;
+  const char* mh = c->meta_host[c->meta_cur];
+  sampled_plan(c->batch, d.max_tree, reinterpret_cast<const int32_t*>(mh + c->off_nodes),
+               reinterpret_cast<const int32_t*>(mh + c->off_parent), reinterpret_cast<const int32_t*>(mh + c->off_token),
+               order, rows_with, step_child, step_token);
+  // one copy from pinned staging (the previous call's copy ended at its synchronisation)
+  memcpy(c->samp_host, u_accept, sizeof(float) * rows);
+  memcpy(c->samp_host + rows, u_final, sizeof(float) * rows);
+  memcpy(c->samp_host + 2 * rows, order.data(), sizeof(int32_t) * order.size());
+  memcpy(c->samp_host + 3 * rows, step_child.data(), sizeof(int32_t) * step_child.size());
+  memcpy(c->samp_host + 4 * rows, step_token.data(), sizeof(int32_t) * step_token.size());
+  HIP_TRY(c, hipMemcpyAsync(c->samp_u, c->samp_host, sizeof(float) * 5 * rows, hipMemcpyHostToDevice, c->stream));
+  const float* ua = c->samp_u;
+  const float* uf = c->samp_u + rows;
   SampledArgs a{};
   a.n_nodes = c->meta.n_nodes;
   a.token = c->meta.token;
@@ -856,13 +902,18 @@ int griffin_accept_sampled(griffin_ctx* c, const float* logits, const float* q_d
   a.q = q_draft;
   a.u_accept = ua;
   a.u_final = uf;
-  a.res = c->samp_res;
+  a.order = reinterpret_cast<const int32_t*>(c->samp_u + 2 * rows);
+  a.step_child = reinterpret_cast<const int32_t*>(c->samp_u + 3 * rows);
+  a.step_token = reinterpret_cast<const int32_t*>(c->samp_u + 4 * rows);
+  a.scratch = c->samp_scratch;
   a.result = c->samp_result;
   a.inv_t = 1.f / temperature;
+  a.batch = c->batch;
+  a.scratch_batch = d.max_batch;
   a.max_tree = d.max_tree;
   a.max_depth = d.max_depth;
   a.vocab = d.vocab;
-  HIP_TRY(c, launch_sampled_accept(a, c->batch, c->stream));
+  HIP_TRY(c, launch_sampled_accept(a, rows_with.data(), (int)rows_with.size() - 1, c->stream));
   const int st = result_stride(d.max_depth);
   HIP_TRY(c, hipMemcpyAsync(c->result_host, c->samp_result, sizeof(int32_t) * c->batch * st, hipMemcpyDeviceToHost,
                             c->stream));
@@ -1013,8 +1064,14 @@ int griffin_accept_sampled_walk(void* hip_stream, int32_t batch, int32_t max_tre
   if (!(temperature > 0.f) || !std::isfinite(temperature)) return GRIFFIN_EINVAL;
   const int rows = batch * max_tree;
   std::vector<uint64_t> anc(rows, 0);
-  std::vector<int32_t> tok(rows, 0), par(rows, 0), dep(rows, 0), pos(rows, 0), nodes(batch);
-  std::vector<float> uu(2 * (size_t)rows, 0.f);
+  std::vector<int32_t> dep(rows, 0), pos(rows, 0);
+  // staging, one copy: tokens [rows], parents [rows], n_nodes [batch], u_accept [rows],
+  // u_final [rows] (float bits), work order, step children, step tokens [<= rows each]
+  std::vector<int32_t> stage(7 * (size_t)rows + batch, 0);
+  int32_t* tok = stage.data();
+  int32_t* par = tok + rows;
+  int32_t* nodes = par + rows;
+  float* uu = reinterpret_cast<float*>(nodes + batch);
   for (int b = 0; b < batch; ++b) {
     const size_t r0 = (size_t)b * max_tree;
     const int rc = prepare_tree(n_nodes[b], tokens + r0, parents + r0, 0, max_tree, max_depth, vocab,
@@ -1032,12 +1089,18 @@ int griffin_accept_sampled_walk(void* hip_stream, int32_t batch, int32_t max_tre
     uu[r] = u_accept[r];
     uu[rows + r] = u_final[r];
   }
+  std::vector<int32_t> order, step_child, step_token;
+  std::vector<int> rows_with;
+  sampled_plan(batch, max_tree, nodes, par, tok, order, rows_with, step_child, step_token);
+  int32_t* plan = reinterpret_cast<int32_t*>(uu + 2 * rows);
+  std::copy(order.begin(), order.end(), plan);
+  std::copy(step_child.begin(), step_child.end(), plan + rows);
+  std::copy(step_token.begin(), step_token.end(), plan + 2 * rows);
   hipStream_t s = static_cast<hipStream_t>(hip_stream);
   const int st = result_stride(max_depth);
-  const size_t n_int = sizeof(int32_t) * rows;
-  const size_t n_res = sizeof(float) * 2 * (size_t)batch * vocab;
-  const size_t total = 2 * n_int + sizeof(int32_t) * batch + sizeof(float) * 2 * rows + n_res +
-                       sizeof(int32_t) * batch * st + 6 * 256;
+  const size_t n_stage = sizeof(int32_t) * stage.size();
+  const size_t n_scratch = sampled_scratch_bytes(batch, max_tree, vocab);
+  const size_t total = n_stage + n_scratch + sizeof(int32_t) * batch * st + 3 * 256;
   char* dev = nullptr;
   if (hipMalloc((void**)&dev, total) != hipSuccess) return GRIFFIN_ENOMEM;
   char* p = dev;
@@ -1046,26 +1109,28 @@ int griffin_accept_sampled_walk(void* hip_stream, int32_t batch, int32_t max_tre
     p += (bytes + 255) / 256 * 256;
     return q;
   };
-  int32_t* d_tok = reinterpret_cast<int32_t*>(carve(n_int));
-  int32_t* d_par = reinterpret_cast<int32_t*>(carve(n_int));
-  int32_t* d_nodes = reinterpret_cast<int32_t*>(carve(sizeof(int32_t) * batch));
-  float* d_u = reinterpret_cast<float*>(carve(sizeof(float) * 2 * rows));
-  float* d_res = reinterpret_cast<float*>(carve(n_res));
+  int32_t* d_stage = reinterpret_cast<int32_t*>(carve(n_stage));
+  char* d_scratch = carve(n_scratch);
   int32_t* d_out = reinterpret_cast<int32_t*>(carve(sizeof(int32_t) * batch * st));
   int rc = GRIFFIN_OK;
   std::vector<int32_t> res((size_t)batch * st);
   hipError_t e = hipSuccess;
   SampledArgs a{};
-  a.n_nodes = d_nodes;
-  a.token = d_tok;
-  a.parent = d_par;
+  a.n_nodes = d_stage + 2 * rows;
+  a.token = d_stage;
+  a.parent = d_stage + rows;
   a.logits = logits;
   a.q = q_draft;
-  a.u_accept = d_u;
-  a.u_final = d_u + rows;
-  a.res = d_res;
+  a.u_accept = reinterpret_cast<const float*>(d_stage + 2 * rows + batch);
+  a.u_final = a.u_accept + rows;
+  a.order = d_stage + 4 * rows + batch;
+  a.step_child = a.order + rows;
+  a.step_token = a.order + 2 * rows;
+  a.scratch = d_scratch;
   a.result = d_out;
   a.inv_t = 1.f / temperature;
+  a.batch = batch;
+  a.scratch_batch = batch;
   a.max_tree = max_tree;
   a.max_depth = max_depth;
   a.vocab = vocab;
@@ -1073,11 +1138,8 @@ int griffin_accept_sampled_walk(void* hip_stream, int32_t batch, int32_t max_tre
     rc = GRIFFIN_ENOMEM;
     goto done;
   }
-  if ((e = hipMemcpyAsync(d_tok, tok.data(), n_int, hipMemcpyHostToDevice, s)) != hipSuccess ||
-      (e = hipMemcpyAsync(d_par, par.data(), n_int, hipMemcpyHostToDevice, s)) != hipSuccess ||
-      (e = hipMemcpyAsync(d_nodes, nodes.data(), sizeof(int32_t) * batch, hipMemcpyHostToDevice, s)) != hipSuccess ||
-      (e = hipMemcpyAsync(d_u, uu.data(), sizeof(float) * 2 * rows, hipMemcpyHostToDevice, s)) != hipSuccess ||
-      (e = launch_sampled_accept(a, batch, s)) != hipSuccess ||
+  if ((e = hipMemcpyAsync(d_stage, stage.data(), n_stage, hipMemcpyHostToDevice, s)) != hipSuccess ||
+      (e = launch_sampled_accept(a, rows_with.data(), (int)rows_with.size() - 1, s)) != hipSuccess ||
       (e = hipMemcpyAsync(res.data(), d_out, sizeof(int32_t) * batch * st, hipMemcpyDeviceToHost, s)) !=
           hipSuccess ||
       (e = hipStreamSynchronize(s)) != hipSuccess) {
