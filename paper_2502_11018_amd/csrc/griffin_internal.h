@@ -104,25 +104,6 @@ struct TreeKV32 {
   float* v;
 };
 
-// Stochastic acceptance (temperature > 0): every node's rejection chain
-// advances one child per launch, the vocabulary spread over workgroups.
-struct SampledArgs {
-  const int32_t* n_nodes;   // [B]
-  const int32_t* token;     // [B][max_tree]
-  const int32_t* parent;    // [B][max_tree] (the root's entry is not read)
-  const float* logits;      // [B][max_tree][vocab] target logits at every node
-  const float* q;           // [B][max_tree][vocab] draft distribution of each node's children
-  const float* u_accept;    // [B][max_tree] uniform for the test at each child
-  const float* u_final;     // [B][max_tree] uniform for the token drawn at each node
-  const int32_t* order;     // rows b * max_tree + u of every node, by child count, descending
-  const int32_t* step_child;  // for k = 0, 1, ..: the k-th child (node id) of each of the first
-  const int32_t* step_token;  // rows_with[k + 1] rows of `order`, and its token
-  void* scratch;             // sampled_scratch_bytes(scratch_batch, max_tree, vocab)
-  int32_t* result;          // [B][result_stride(max_depth)]: L, NaN flag, L + 1 tokens, L path nodes
-  float inv_t;              // 1 / temperature
-  int batch, scratch_batch, max_tree, max_depth, vocab;
-};
-
 // One layer's prefix cache (bf16): K [max_batch][Hkv][kv_cap][dh], V in
 // 32-slot transposed tiles [max_batch][Hkv][kv_cap / 32][dh][32].
 struct PrefixKV {
@@ -161,11 +142,6 @@ hipError_t launch_attn_combine(const float* part_o, const float* part_ml, StepMe
                                int splits, int qrows, int max_tree, int batch, const uint16_t* q,
                                const uint16_t* q_lo, TreeKV32 tree, PrefixKV prefix, float scale_log2,
                                uint16_t* o_out, int o_ks, hipStream_t s);
-int sampled_nslice(int vocab);
-size_t sampled_scratch_bytes(int batch, int max_tree, int vocab);
-// rows_with[j] = rows of `order` with >= j children (j = 0 .. max_children,
-// rows_with[0] = all nodes).
-hipError_t launch_sampled_accept(const SampledArgs& a, const int* rows_with, int max_children, hipStream_t s);
 hipError_t launch_argmax_reduce(const float* pmax, const int32_t* pidx, const int32_t* pnan, int n_tiles,
                                 int ld_part, int rows, int32_t* pred, int32_t* nan_row, hipStream_t s);
 hipError_t launch_commit(const int32_t* result, int max_depth, StepMeta meta, int batch, int n_layers, int Hkv,

@@ -12,6 +12,7 @@
 #include <vector>
 
 #include "griffin_internal.h"
+#include "sampling.h"
 #include "griffin_verify.h"
 
 using namespace griffin;

@@ -44,6 +44,7 @@
 
 #include "device_common.h"
 #include "griffin_internal.h"
+#include "sampling.h"
 
 namespace griffin {
 
@@ -139,22 +140,24 @@ __device__ __forceinline__ void slice_range(int V, int nslice, int s, int& lo, i
 }
 
 // f(x, y) for every element of [lo, hi) of a logits row and a q row that this
-// thread owns; VEC: 16-byte loads (V % 4 == 0, rows 16-byte aligned).
-template <bool VEC, typename F>
+// thread owns; VEC: 16-byte loads (V % 4 == 0, rows 16-byte aligned).  Q:
+// read the q row, else y = 0 (leaves: their q rows are not read).
+template <bool VEC, bool Q, typename F>
 __device__ __forceinline__ void for_slice(const float* lg, const float* qd, int lo, int hi, F&& f) {
   if constexpr (VEC) {
     const float4* l4 = reinterpret_cast<const float4*>(lg);
     const float4* q4 = reinterpret_cast<const float4*>(qd);
 #pragma unroll 2
     for (int i = (lo >> 2) + (int)threadIdx.x; i < (hi >> 2); i += SA_THREADS) {
-      const float4 x = l4[i], y = q4[i];
+      const float4 x = l4[i];
+      const float4 y = Q ? q4[i] : make_float4(0.f, 0.f, 0.f, 0.f);
       f(x.x, y.x);
       f(x.y, y.y);
       f(x.z, y.z);
       f(x.w, y.w);
     }
   } else {
-    for (int v = lo + (int)threadIdx.x; v < hi; v += SA_THREADS) f(lg[v], qd[v]);
+    for (int v = lo + (int)threadIdx.x; v < hi; v += SA_THREADS) f(lg[v], Q ? qd[v] : 0.f);
   }
 }
 
@@ -216,7 +219,7 @@ __device__ __forceinline__ float accept_prob(const SampState& st, const RmEntry&
 
 // ---- softmax normaliser and q's sum of every node --------------------------------
 template <bool VEC>
-__global__ __launch_bounds__(SA_THREADS) void sampled_norm_kernel(SampledArgs a, int nslice) {
+__global__ __launch_bounds__(SA_THREADS) void sampled_norm_kernel(SampledArgs a, int nslice, int n_parents) {
   __shared__ float red[8];
   const SampScratch sc = sa_carve(a.scratch, a.scratch_batch, a.max_tree, nslice);
   const int s = blockIdx.x, row = a.order[blockIdx.y], tid = threadIdx.x, V = a.vocab;
@@ -229,13 +232,17 @@ __global__ __launch_bounds__(SA_THREADS) void sampled_norm_kernel(SampledArgs a,
   // ones are flagged (fmaxf skips them)
   float m = -INFINITY, se = 0.f, sq = 0.f;
   int bad = 0;
-  for_slice<VEC>(lg, qd, lo, hi, [&](float x, float y) {
+  auto f = [&](float x, float y) {
     sq += y;
     bad |= x != x;
     const float mn = fmaxf(m, x);
     se = (mn == m ? se : se * expf((m - mn) * inv_t)) + (x > -INFINITY ? expf((x - mn) * inv_t) : 0.f);
     m = mn;
-  });
+  };
+  if ((int)blockIdx.y < n_parents)  // rows of `order` with children come first
+    for_slice<VEC, true>(lg, qd, lo, hi, f);
+  else
+    for_slice<VEC, false>(lg, qd, lo, hi, f);
   const float mb = block_max(m, red);
   const float seb = block_sum(m > -INFINITY ? se * expf((m - mb) * inv_t) : 0.f, red);
   const float sqb = block_sum(sq, red);
@@ -293,7 +300,8 @@ __global__ __launch_bounds__(SA_THREADS) void sampled_step_kernel(SampledArgs a,
   int lo, hi;
   slice_range(V, nslice, s, lo, hi);
   float g = 0.f;
-  if (!st.bad && st.S > 0.f) for_slice<VEC>(lg, qd, lo, hi, [&](float x, float y) { g += resid(x, y, an, nm); });
+  if (!st.bad && st.S > 0.f)
+    for_slice<VEC, true>(lg, qd, lo, hi, [&](float x, float y) { g += resid(x, y, an, nm); });
   g = block_sum(g, red);
   if (tid == 0) sc.gpart[((k & 1) * rows + row) * nslice + s] = g;
 }
@@ -380,7 +388,11 @@ __global__ __launch_bounds__(SA_THREADS) void sampled_draw_sums_kernel(SampledAr
     int lo, hi;
     slice_range(V, nslice, s, lo, hi);
     const float af = st.a;
-    for_slice<VEC>(a.logits + fr * V, a.q + fr * V, lo, hi, [&](float x, float y) { g += resid(x, y, af, nm); });
+    auto f = [&](float x, float y) { g += resid(x, y, af, nm); };
+    if (st.n_rm > 0)  // a node without children (or rejections) draws from p alone
+      for_slice<VEC, true>(a.logits + fr * V, a.q + fr * V, lo, hi, f);
+    else
+      for_slice<VEC, false>(a.logits + fr * V, a.q + fr * V, lo, hi, f);
     if (tid < st.n_rm) {  // rejected tokens in this slice: frozen value instead
       const RmEntry e = rml[tid];
       if (e.tok >= lo && e.tok < hi) g += e.f - resid_pq(e.p, e.q, af);
@@ -446,7 +458,7 @@ __global__ __launch_bounds__(SA_THREADS) void sampled_pick_kernel(SampledArgs a,
       const int nrm = st.n_rm;
       const float af = st.a;
       auto r_at = [&](int v) {
-        float r = resid(lg[v], qd[v], af, nm);
+        float r = resid(lg[v], nrm > 0 ? qd[v] : 0.f, af, nm);
         for (int j = 0; j < nrm; ++j) r = rml[j].tok == v ? rml[j].f : r;
         return r;
       };
@@ -492,7 +504,8 @@ __global__ __launch_bounds__(SA_THREADS) void sampled_pick_kernel(SampledArgs a,
 
 template <bool VEC>
 static void launch_all(const SampledArgs& a, const int* rows_with, int max_children, int ns, hipStream_t s) {
-  hipLaunchKernelGGL(sampled_norm_kernel<VEC>, dim3(ns, rows_with[0]), dim3(SA_THREADS), 0, s, a, ns);
+  hipLaunchKernelGGL(sampled_norm_kernel<VEC>, dim3(ns, rows_with[0]), dim3(SA_THREADS), 0, s, a, ns,
+                     max_children > 0 ? rows_with[1] : 0);
   for (int k = 0, base = 0, prev = 0; k < max_children; prev = base, base += rows_with[++k])
     hipLaunchKernelGGL(sampled_step_kernel<VEC>, dim3(ns, rows_with[k + 1]), dim3(SA_THREADS), 0, s, a, ns, k, base,
                        prev);

@@ -7,9 +7,10 @@
 
     python -m paper_2502_11018_amd.profiling stats RUN_kernel_trace.csv \\
             --stats RUN_kernel_stats.csv --steps K --out profiles/NAME.md \\
-            --title TITLE --command "CMD"
+            --title TITLE --command "CMD" [--include REGEX --step-end REGEX]
         Markdown summary of a `rocprofv3 --kernel-trace --stats -f csv` run of
-        bench.py: per-kernel durations over the last K timed steps.
+        bench.py: per-kernel durations over the last K steps (a step ends with
+        the kernel matching --step-end, by default the acceptance walk).
 
     python -m paper_2502_11018_amd.profiling traffic \\
             --kernel-regex REGEX --fetch BENCH_fetch.csv --write BENCH_write.csv \\
@@ -97,32 +98,37 @@ def _short(name: str) -> str:
 
 
 def cmd_stats(args):
-    """Per-kernel durations over the last `steps` verify steps (a step ends
-    with the acceptance-walk kernel), grouped by kernel and grid, plus the
-    library's rows of rocprofv3's own whole-run statistics."""
+    """Per-kernel durations over the last `steps` steps (a step ends with the
+    kernel matching --step-end: the acceptance walk for a verify step),
+    grouped by kernel and grid, plus the library's rows of rocprofv3's own
+    whole-run statistics."""
     rx = re.compile(args.include)
+    end_rx = re.compile(args.step_end)
     rows = [r for r in _rows(args.trace) if rx.search(_col(r, "Kernel_Name"))]
     rows.sort(key=lambda r: int(_col(r, "Start_Timestamp")))
-    ends = [int(_col(r, "End_Timestamp")) for r in rows if "accept_kernel" in _col(r, "Kernel_Name")]
+    ends = [int(_col(r, "End_Timestamp")) for r in rows if end_rx.search(_col(r, "Kernel_Name"))]
     if len(ends) < args.steps + 1:
         raise SystemExit(f"{args.trace}: fewer than {args.steps + 1} steps")
     t0 = ends[-args.steps - 1]
     win = [r for r in rows if int(_col(r, "Start_Timestamp")) > t0]
     groups = {}
-    for r in win:
-        key = (_short(_col(r, "Kernel_Name")),
-               tuple(int(_col(r, f"Grid_Size_{a}")) // int(_col(r, f"Workgroup_Size_{a}")) for a in "XYZ"))
+    prev = ""
+    for r in win:  # keyed by kernel, grid and the kernel launched before it (tells O from down)
+        name = _short(_col(r, "Kernel_Name"))
+        key = (name, tuple(int(_col(r, f"Grid_Size_{a}")) // int(_col(r, f"Workgroup_Size_{a}")) for a in "XYZ"),
+               prev)
         groups.setdefault(key, []).append((int(_col(r, "End_Timestamp")) - int(_col(r, "Start_Timestamp"))) / 1e3)
+        prev = name
     busy = sum(sum(v) for v in groups.values()) / args.steps
     span = (int(_col(win[-1], "End_Timestamp")) - int(_col(win[0], "Start_Timestamp"))) / 1e3 / args.steps
     out = [f"# {args.title}", "", "Command:", "", "```", args.command, "```", "",
            f"Last {args.steps} steps of the run: kernel busy time {busy:.1f} us per step, "
            f"first-kernel-start to last-kernel-end {span:.1f} us per step.", "",
-           "| kernel | workgroups | launches/step | avg us | min us | max us | us/step |",
-           "|---|---|---:|---:|---:|---:|---:|"]
-    for (name, grid), v in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
-        out.append(f"| `{name}` | {grid[0]}x{grid[1]}x{grid[2]} | {len(v) / args.steps:g} | {statistics.fmean(v):.2f} | "
-                   f"{min(v):.2f} | {max(v):.2f} | {sum(v) / args.steps:.1f} |")
+           "| kernel | workgroups | after | launches/step | avg us | min us | max us | us/step |",
+           "|---|---|---|---:|---:|---:|---:|---:|"]
+    for (name, grid, after), v in sorted(groups.items(), key=lambda kv: -sum(kv[1])):
+        out.append(f"| `{name}` | {grid[0]}x{grid[1]}x{grid[2]} | `{after}` | {len(v) / args.steps:g} | "
+                   f"{statistics.fmean(v):.2f} | {min(v):.2f} | {max(v):.2f} | {sum(v) / args.steps:.1f} |")
     if args.stats:
         out += ["", "rocprofv3 `--stats` rows of the library's kernels (whole run, including warm-up and the "
                 "chain steps that build the planted-tree pool):", "",
@@ -200,6 +206,7 @@ def main(argv=None):
     s.add_argument("--stats", default="", help="RUN_kernel_stats.csv")
     s.add_argument("--steps", type=int, required=True)
     s.add_argument("--include", default="griffin::")
+    s.add_argument("--step-end", default="accept_kernel", help="regex of the kernel that ends a step")
     s.add_argument("--out", required=True)
     s.add_argument("--title", required=True)
     s.add_argument("--command", required=True)

@@ -218,3 +218,28 @@ def test_accept_sampled_before_a_step_is_an_order_error():
         t = torch.zeros((8, w.model.vocab), device="cuda")
         with pytest.raises(P.GriffinError):
             v.accept_sampled(t, t, np.zeros((1, 8)), np.zeros((1, 8)), 1.0)
+
+
+def test_leaf_rows_of_q_are_not_read():
+    """The header's contract: rows of q_draft that belong to leaves are not
+    read (NaN there changes nothing), and a NaN logit at the root (always
+    visited) is reported as GRIFFIN_ENUMERIC."""
+    P = _lib()
+    V, max_tree, D, B = 3000, 64, 6, 4
+    cases = [gen.sampled_case((10,) * 6, V, 1300 + i) for i in range(B)]
+    lg, q, ua, uf = _pack(cases, max_tree, V)
+    say("sampled walk: NaN in the q rows of leaves")
+    ref = P.accept_sampled_walk([c.tree for c in cases], lg, q, ua, uf, 1.0, max_tree, D, V)
+    q2 = q.clone()
+    for b, c in enumerate(cases):
+        has_kids = set(int(x) for x in c.tree.parents[1:])
+        for u in range(c.tree.n):
+            if u not in has_kids:
+                q2[b * max_tree + u] = float("nan")
+    got = P.accept_sampled_walk([c.tree for c in cases], lg, q2, ua, uf, 1.0, max_tree, D, V)
+    assert (got.length == ref.length).all() and (got.tokens == ref.tokens).all() and (got.path == ref.path).all()
+    say("sampled walk: NaN logit at the root")
+    lg2 = lg.clone()
+    lg2[0, 17] = float("nan")
+    with pytest.raises(P.GriffinError):
+        P.accept_sampled_walk([c.tree for c in cases], lg2, q, ua, uf, 1.0, max_tree, D, V)
