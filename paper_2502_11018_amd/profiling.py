@@ -111,8 +111,9 @@ def cmd_stats(args):
         raise SystemExit(f"{args.trace}: fewer than {args.steps + 1} steps")
     t0 = ends[-args.steps - 1]
     win = [r for r in rows if int(_col(r, "Start_Timestamp")) > t0]
+    before = [r for r in rows if int(_col(r, "Start_Timestamp")) <= t0]
     groups = {}
-    prev = ""
+    prev = _short(_col(before[-1], "Kernel_Name")) if before else ""
     for r in win:  # keyed by kernel, grid and the kernel launched before it (tells O from down)
         name = _short(_col(r, "Kernel_Name"))
         key = (name, tuple(int(_col(r, f"Grid_Size_{a}")) // int(_col(r, f"Workgroup_Size_{a}")) for a in "XYZ"),

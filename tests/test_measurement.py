@@ -77,6 +77,7 @@ def test_stats_summary_groups_kernels_by_grid(tmp_path):
     rows, t = [], 0
     for step in range(3):
         for name, grid, dur in (("void griffin::gemm_kernel<0>(x)", 256, 1000), ("void griffin::gemm_kernel<0>(x)", 512, 3000),
+                                ("void griffin::norm(x)", 64, 200), ("void griffin::gemm_kernel<0>(x)", 512, 2000),
                                 ("void griffin::accept_kernel(x)", 64, 500)):
             rows.append([name, t, t + dur, grid, 1, 1, 64, 1, 1])
             t += dur + 100
@@ -85,5 +86,8 @@ def test_stats_summary_groups_kernels_by_grid(tmp_path):
     profiling.main(["stats", str(tmp_path / "trace.csv"), "--steps", "2", "--out", str(out), "--title", "t",
                     "--command", "c"])
     text = out.read_text()
-    assert "| `gemm_kernel<0>` | 8x1x1 | 1 | 3.00 |" in text
-    assert "| `gemm_kernel<0>` | 4x1x1 | 1 | 1.00 |" in text
+    # rows are keyed by kernel, grid and the kernel launched before it: the two
+    # 8-workgroup launches of one step stay apart
+    assert "| `gemm_kernel<0>` | 8x1x1 | `gemm_kernel<0>` | 1 | 3.00 |" in text
+    assert "| `gemm_kernel<0>` | 8x1x1 | `norm` | 1 | 2.00 |" in text
+    assert "| `gemm_kernel<0>` | 4x1x1 | `accept_kernel` | 1 | 1.00 |" in text
