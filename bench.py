@@ -34,9 +34,10 @@ def algorithmic_bytes(w, experts_touched=None):
     """Bytes a verify step must move: every weight once, the prefix KV read,
     the tree K/V written (SURVEY-style accounting; activations excluded)."""
     m = w.model
-    weights = m.weight_bytes(experts_touched) + 2 * w.tree_nodes * w.batch * m.d_model  # + embedding rows
-    kv_read = w.batch * w.prefix_len * m.kv_bytes_per_position()
-    kv_write = w.batch * w.tree_nodes * m.kv_bytes_per_position()
+    nodes = sum(1 + sum(w.widths_of(b)) for b in range(w.batch))
+    weights = m.weight_bytes(experts_touched) + 2 * nodes * m.d_model  # + embedding rows
+    kv_read = sum(w.prefixes()) * m.kv_bytes_per_position()
+    kv_write = nodes * m.kv_bytes_per_position()
     return weights + kv_read + kv_write, dict(weights=weights, kv_read=kv_read, kv_write=kv_write)
 
 
@@ -51,7 +52,7 @@ def class_bytes_per_launch(w):
         "gate_up_gemm": 2 * e * 2 * f * d,
         "down_gemm": 2 * e * d * f,
         "lm_head_gemm": 2 * m.vocab * d,
-        "tree_attention": w.batch * w.prefix_len * m.kv_bytes_per_position() // m.n_layers,
+        "tree_attention": sum(w.prefixes()) * m.kv_bytes_per_position() // m.n_layers,
     }
 
 
@@ -64,9 +65,11 @@ def class_mfma_flops_per_launch(w):
     batch-1 MoE shape every expert is assumed to receive rows (61 rows x top-2
     over 8 experts leave one idle with probability ~2e-7)."""
     m = w.model
-    rows = -(-w.batch * 64 // 64) * 64
+    rows = -(-w.batch * w.max_tree // 64) * 64
     d, f, e = m.d_model, m.d_ff, m.n_experts
-    keys = -(-w.prefix_len // 32) * 32   # prefix keys; tree keys are scored on the vector ALU in the merge
+    qrows = -(-w.max_tree // 32) * 32
+    # prefix keys in 32-key blocks; tree keys are scored on the vector ALU in the merge
+    keys = sum(-(-p // 32) * 32 for p in w.prefixes())
     return {
         "qkv_gemm": 2 * 2 * rows * m.qkv_rows * d,
         "o_gemm": 2 * 2 * rows * d * m.n_q_heads * m.head_dim,
@@ -74,16 +77,18 @@ def class_mfma_flops_per_launch(w):
         "gate_up_gemm": 2 * 2 * (e * 64 if e > 1 else rows) * 2 * f * d,
         "down_gemm": 2 * 2 * (e * 64 if e > 1 else rows) * d * f,
         "lm_head_gemm": 2 * 2 * rows * m.vocab * d,
-        "tree_attention": 2 * 2 * 2 * w.batch * m.n_q_heads * 64 * keys * m.head_dim,
+        "tree_attention": 2 * 2 * 2 * m.n_q_heads * qrows * keys * m.head_dim,
     }
 
 
 def cpu_baseline(w, weights_gpu, n_trees=2):
     """Time the fp64 oracle on a bounded sample of the same workload: the full
-    verify pass (all layers, LM head, argmax, acceptance) of the first
-    `n_trees` trees of the pool, one after another.  Copying the weights to
-    the host and generating the prefix KV are not timed; the oracle's per-use
-    upcast of each layer to fp64 is (it is part of how the oracle runs)."""
+    verify pass (all layers, LM head, argmax, acceptance) of `n_trees` trees,
+    one after another: the first trees of sequence 0 at batch 1, else the
+    first sequences' trees of one step (the value then scales to the whole
+    batch).  Copying the weights to the host and generating the prefix KV are
+    not timed; the oracle's per-use upcast of each layer to fp64 is (it is part
+    of how the oracle runs)."""
     import numpy as np
     import torch
     from threadpoolctl import threadpool_info
@@ -97,24 +102,32 @@ def cpu_baseline(w, weights_gpu, n_trees=2):
     mw = gen.ModelWeights(m, weights_gpu.embed.to("cpu"), weights_gpu.lm_head.to("cpu"),
                           weights_gpu.final_norm.to("cpu"), layers)
     ow = oracle.OracleWeights(mw, cache=False)
-    kv = []
-    for l in range(m.n_layers):
-        kk, vv = gen.synthetic_kv(m, l, 0, w.prefix_len, w.weight_seed, "cpu")
-        kv.append((kk.to(torch.float64).numpy(), vv.to(torch.float64).numpy()))
-    trees = [gen.workload_tree(w, i, 0)[0] for i in range(n_trees)]
+    seqs = [0] * n_trees if w.batch == 1 else list(range(min(n_trees, w.batch)))
+    idx = list(range(n_trees)) if w.batch == 1 else [0] * len(seqs)
+    kvs = {}
+    for b in set(seqs):
+        kvs[b] = []
+        for l in range(m.n_layers):
+            kk, vv = gen.synthetic_kv(m, l, b, w.prefix_of(b), w.weight_seed, "cpu")
+            kvs[b].append((kk.to(torch.float64).numpy(), vv.to(torch.float64).numpy()))
+    trees = [gen.workload_tree(w, i, b)[0] for i, b in zip(idx, seqs)]
     t0 = time.perf_counter()
-    for tree in trees:
-        res = oracle.verify_tree(ow, lambda l: kv[l], tree, w.prefix_len)
+    for tree, b in zip(trees, seqs):
+        res = oracle.verify_tree(ow, lambda l, b=b: kvs[b][l], tree, w.prefix_of(b))
         oracle.accept_dfs(tree, oracle.argmax_first(res.logits))
     elapsed = time.perf_counter() - t0
+    per_step = elapsed / len(trees) * w.batch
     threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    what = (f"{n_trees} {w.tree_nodes}-node trees at prefix {w.prefix_len} (batch 1)" if w.batch == 1 else
+            f"the trees of sequences 0..{len(seqs) - 1} of one batch-{w.batch} step (prefixes "
+            f"{[w.prefix_of(b) for b in seqs]}), scaled to the whole batch")
     return {
-        "value": round(n_trees / elapsed, 6),
+        "value": round(1.0 / per_step, 6),
         "unit": "verify_steps/s",
         "cores": int(threads),
         "kind": "oracle",
-        "sample": (f"fp64 oracle, full {m.n_layers}-layer verify pass + argmax + acceptance walk of {n_trees} "
-                   f"{w.tree_nodes}-node trees at prefix {w.prefix_len} (batch 1), {elapsed:.1f} s in total"),
+        "sample": (f"fp64 oracle, full {m.n_layers}-layer verify pass + argmax + acceptance walk of {what}, "
+                   f"{elapsed:.1f} s in total"),
     }
 
 
@@ -149,16 +162,17 @@ def main():
     weights = gen.make_weights(m, w.weight_seed, device=dev)
     torch.cuda.synchronize()
     log(f"weights {weights.nbytes() / 1e9:.2f} GB generated in {time.time() - t0:.1f} s")
-    max_tree = 64
+    max_tree = w.max_tree
+    prefix = w.prefixes()
     v = P.TreeVerifier(m, weights, max_batch=w.batch, max_tree=max_tree, max_depth=w.depth,
                        kv_capacity=w.kv_capacity())
     v.set_graphs(not args.no_graphs)
     for l in range(m.n_layers):
         for b in range(w.batch):
-            k, vv = gen.synthetic_kv(m, l, b, w.prefix_len, w.weight_seed, dev)
+            k, vv = gen.synthetic_kv(m, l, b, prefix[b], w.weight_seed, dev)
             v.write_prefix(l, b, k, vv)
     torch.cuda.synchronize()
-    log(f"prefix KV written ({w.batch} x {w.prefix_len} positions)")
+    log(f"prefix KV written ({w.batch} sequences, {sum(prefix)} positions)")
 
     # pool of draft trees; planted paths use the target's greedy continuation,
     # obtained from the verify path itself on chain trees
@@ -170,7 +184,7 @@ def main():
         if need:
             chains = [[int(t.tokens[0])] for t in trees]
             for _ in range(need):
-                v.step([w.prefix_len] * w.batch, [gen.chain_tree(c[0], c[1:]) for c in chains])
+                v.step(prefix, [gen.chain_tree(c[0], c[1:]) for c in chains])
                 v.accept()
                 pred = v.predictions()
                 for b, c in enumerate(chains):
@@ -179,7 +193,6 @@ def main():
         pool.append(trees)
     log(f"tree pool of {len(pool)} ready")
 
-    prefix = [w.prefix_len] * w.batch
     packed = [P.pack_trees(t, max_tree) for t in pool]
     accepted = []
 
@@ -205,6 +218,22 @@ def main():
     steps_per_s = 1e3 / ms_per_step
     total_bytes, parts = algorithmic_bytes(w)
     log(f"{ms_per_step:.3f} ms/step (events {ev_ms:.3f}), {steps_per_s:.1f} steps/s")
+
+    # plain decoding through the same pass: every tree is its root alone (one
+    # token per sequence per step), the cost a verify step is compared with
+    roots = P.pack_trees([gen.chain_tree(int(t.tokens[0]), []) for t in pool[0]], max_tree)
+    n_root = min(args.steps, 20)
+    for i in range(3):
+        v.step_arrays(prefix, *roots)
+        v.accept()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(n_root):
+        v.step_arrays(prefix, *roots)
+        v.accept()
+    torch.cuda.synchronize()
+    root_ms = (time.perf_counter() - t0) * 1e3 / n_root
+    log(f"root-only (plain decoding) {root_ms:.3f} ms/step")
 
     # per kernel class timing (separate pass: HIP events recorded on the
     # library's stream around every launch of the class)
@@ -301,8 +330,10 @@ def main():
         "dtype": "bf16",
         "data": "synthetic (random-init weights, seeded prefix KV and draft trees)",
         "config": {"workload": w.name, "batch": w.batch, "prefix_len": w.prefix_len,
-                   "tree_nodes": w.tree_nodes, "draft_tokens": w.n_draft, "depth": w.depth},
-        "draft_tree_tokens_per_s": round(steps_per_s * w.batch * w.n_draft, 1),
+                   "tree_nodes": w.tree_nodes, "draft_tokens": w.n_draft, "depth": w.depth,
+                   **({"prefix_lens": w.prefixes()} if w.prefix_lens else {})},
+        "draft_tree_tokens_per_s": round(steps_per_s * sum(sum(w.widths_of(b)) for b in range(w.batch)), 1),
+        "root_only_ms_per_step": round(root_ms, 4),
         "algorithmic_bytes_per_step": total_bytes,
         "step_hbm_GBs": round(total_bytes / (ms_per_step * 1e-3) / 1e9, 1),
         "step_hbm_frac": round(total_bytes / (ms_per_step * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),

@@ -85,7 +85,7 @@ def build_sequence(ow: oracle.OracleWeights, w: Workload, tree_index: int, seq: 
         if w.kv_source == "prefill":
             kv = prefix_kv_prefill(ow, toks)
         else:
-            kv = prefix_kv_synthetic(m, seq, w.prefix_len, w.weight_seed)
+            kv = prefix_kv_synthetic(m, seq, w.prefix_of(seq), w.weight_seed)
     tree, path = gen.workload_tree(w, tree_index, seq)
     greedy, margins = [], []
     if path:

@@ -176,3 +176,46 @@ def test_full_size_long_context_batch_matches_oracle():
         say(f"llama3-8b-longctx seq {b}: max rel err {st['max_rel']:.2e}, gated {st['gated']}/{st['total']}, "
             f"accept checked {st['accept_checked']}, L={st['L']}")
     v.close()
+
+
+def test_full_size_ragged_chain2_batch_matches_oracle():
+    """Llama-3-8B shape, a serving batch of 16 sequences with prefixes spread
+    over 256..2048 tokens and a chain of 2 drafts each, in 3-row slots (48
+    node rows in one call); sequences 0, 7 and 15 are checked against the
+    oracle."""
+    import paper_2502_11018_amd as P
+    w = get_workload("llama3-8b-chain2-b16")
+    m = w.model
+    B, prefix = w.batch, w.prefixes()
+    t0 = time.time()
+    say(f"llama3-8b-chain2-b16: generate weights on the GPU (prefixes {prefix})")
+    mw_gpu = gen.make_weights(m, w.weight_seed, device="cuda")
+    v = P.TreeVerifier(m, mw_gpu, max_batch=B, max_tree=w.max_tree, max_depth=w.depth,
+                       kv_capacity=w.kv_capacity())
+    checked = (0, 7, 15)
+    host_kv = {b: ([], []) for b in checked}
+    for l in range(m.n_layers):
+        for b in range(B):
+            k, vv = gen.synthetic_kv(m, l, b, prefix[b], w.weight_seed, "cuda")
+            v.write_prefix(l, b, k, vv)
+            if b in checked:
+                host_kv[b][0].append(k.to(torch.float64).cpu().numpy())
+                host_kv[b][1].append(vv.to(torch.float64).cpu().numpy())
+    trees = [gen.workload_tree(w, 0, b)[0] for b in range(B)]
+    say(f"llama3-8b-chain2-b16: GPU verify of {B} chains ({time.time() - t0:.0f}s)")
+    logits = torch.empty((B * w.max_tree, m.vocab), device="cuda")
+    v.step(prefix, trees, logits)
+    acc = v.accept()
+    pred = v.predictions()
+    lg_all = logits.view(B, w.max_tree, m.vocab)
+    say(f"llama3-8b-chain2-b16: host copy of the weights ({time.time() - t0:.0f}s)")
+    ow = oracle.OracleWeights(mw_gpu.to("cpu"), cache=True)
+    for b in checked:
+        say(f"llama3-8b-chain2-b16: oracle verify of sequence {b}, prefix {prefix[b]} ({time.time() - t0:.0f}s)")
+        kv = LoudKV(*host_kv[b])
+        os_ = H.oracle_sequence(ow, H.SeqCase(None, kv, trees[b], [], [], []))
+        lg = lg_all[b, : trees[b].n].cpu().numpy()
+        st = H.check_parity(os_, lg, pred[b, : trees[b].n], acc.sequence(b))
+        say(f"llama3-8b-chain2-b16 seq {b}: max rel err {st['max_rel']:.2e}, gated {st['gated']}/{st['total']}, "
+            f"accept checked {st['accept_checked']}, L={st['L']}")
+    v.close()

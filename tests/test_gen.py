@@ -47,16 +47,17 @@ def test_make_weights_shapes_and_layouts():
 @pytest.mark.parametrize("name", sorted(WORKLOADS))
 def test_workload_trees(name):
     w = WORKLOADS[name]
-    for b in range(min(w.batch, 2)):
+    for b in sorted({0, 1, w.batch - 1} & set(range(w.batch))) if not w.seq_widths else range(w.batch):
+        widths = w.widths_of(b)
         for i in range(4):
             tree, path = gen.workload_tree(w, i, b)
-            assert tree.n == w.tree_nodes
+            assert tree.n == 1 + sum(widths) <= w.tree_nodes <= w.max_tree
             assert tree.parents[0] == -1
             d = tree.depths()
             for j in range(1, tree.n):
                 assert 0 <= tree.parents[j] < j
             # breadth-first numbering with the configured widths
-            assert [int((d == k).sum()) for k in range(1, w.depth + 1)] == list(w.widths)
+            assert [int((d == k).sum()) for k in range(1, len(widths) + 1)] == list(widths)
             assert np.all(np.diff(d) >= 0)
             assert tree.tokens.min() >= 0 and tree.tokens.max() < w.model.vocab
             # the planting path is a root path
@@ -64,7 +65,7 @@ def test_workload_trees(name):
                 assert d[node] == k + 1
                 if k:
                     assert tree.parents[node] == path[k - 1]
-            if w.plant == "leaf":
+            if w.plant == "leaf" and tree.n > 1:
                 assert path and not any(tree.parents[j] == path[-1] for j in range(1, tree.n))
             tree2, path2 = gen.workload_tree(w, i, b)
             assert np.array_equal(tree.tokens, tree2.tokens) and path == path2
@@ -97,3 +98,20 @@ def test_synthetic_kv_scale_and_determinism():
     assert torch.equal(k, k2)
     assert not torch.equal(k, v)
     assert abs(k.float().std().item() - gen.kv_std(m)) < 0.03 * gen.kv_std(m)
+
+
+def test_ragged_batch_workloads():
+    """Per-sequence prefixes and tree sizes: prefix tokens and the KV capacity
+    follow each sequence's own length."""
+    w = WORKLOADS["small-chain2"]
+    P = w.prefixes()
+    assert len(P) == w.batch == 16 and len(set(P)) > 8 and min(P) >= 20 and max(P) <= 200
+    assert w.kv_capacity() >= max(P) + w.tree_nodes
+    sizes = [1 + sum(w.widths_of(b)) for b in range(w.batch)]
+    assert sorted(set(sizes)) == [1, 2, 3] and w.tree_nodes == 3 == w.max_tree
+    for b in (0, 3, 15):
+        assert len(gen.prefix_tokens(w, b)) == P[b]
+    for B in (2, 4, 8, 16):
+        c = WORKLOADS[f"llama3-8b-chain2-b{B}"]
+        assert c.batch == B and c.max_tree == 3 and c.depth == 2
+        assert all(256 <= p <= 2048 for p in c.prefixes())

@@ -91,3 +91,20 @@ def test_stats_summary_groups_kernels_by_grid(tmp_path):
     assert "| `gemm_kernel<0>` | 8x1x1 | `gemm_kernel<0>` | 1 | 3.00 |" in text
     assert "| `gemm_kernel<0>` | 8x1x1 | `norm` | 1 | 2.00 |" in text
     assert "| `gemm_kernel<0>` | 4x1x1 | `accept_kernel` | 1 | 1.00 |" in text
+
+
+def test_ragged_batch_accounting():
+    """A ragged batch counts each sequence's own prefix and tree: KV bytes
+    follow the sum of the prefixes, and 16 chains in 3-row slots are one
+    64-row tile for the GEMMs."""
+    w = get_workload("llama3-8b-chain2-b16")
+    m = w.model
+    total, parts = bench.algorithmic_bytes(w)
+    assert parts["kv_read"] == sum(w.prefixes()) * m.kv_bytes_per_position()
+    assert parts["kv_write"] == 16 * 3 * m.kv_bytes_per_position()
+    f = bench.class_mfma_flops_per_launch(w)
+    assert f["qkv_gemm"] == 2 * 2 * 64 * m.qkv_rows * m.d_model
+    keys = sum(-(-p // 32) * 32 for p in w.prefixes())
+    assert f["tree_attention"] == 2 * 2 * 2 * m.n_q_heads * 32 * keys * m.head_dim
+    assert bench.class_bytes_per_launch(w)["tree_attention"] == \
+        sum(w.prefixes()) * m.kv_bytes_per_position() // m.n_layers

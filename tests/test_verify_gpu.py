@@ -37,7 +37,7 @@ class Setup:
         self.mw_gpu = self.mw.to(self.dev)
         self.max_tree = max_tree
         self.max_depth = max_depth if max_depth is not None else max_tree - 1
-        self.cap = ((self.w.prefix_len + max_tree + kv_extra + 63) // 64) * 64
+        self.cap = ((max(self.w.prefixes()) + max_tree + kv_extra + 63) // 64) * 64
         self.kvs = []
         for b in range(self.w.batch):
             seq_case = H.build_sequence(self.ow, self.w, 0, b)
@@ -55,7 +55,7 @@ class Setup:
 
     def run(self, trees, prefix=None, logits=True):
         B = len(trees)
-        prefix = [self.w.prefix_len] * B if prefix is None else prefix
+        prefix = self.w.prefixes()[:B] if prefix is None else prefix
         out = torch.full((B * self.max_tree, self.w.model.vocab), float("nan"), device=self.dev) if logits else None
         self.v.step(prefix, trees, out)
         acc = self.v.accept(check=False)
@@ -91,9 +91,11 @@ def test_tiny_all_trees_match_oracle(tiny):
     assert sum(s["accept_checked"] for s in stats) >= 3
 
 
-@pytest.mark.parametrize("name", ["small-gqa", "small-mha", "small-moe"])
+@pytest.mark.parametrize("name", ["small-gqa", "small-mha", "small-moe", "small-chain2"])
 def test_small_workloads_match_oracle(name):
-    s = Setup(name, n_trees=3)
+    """small-chain2 is a ragged serving batch: 16 sequences with prefixes of
+    20..200 tokens and chains of 0..2 drafts in 3-row slots."""
+    s = Setup(name, n_trees=3, max_tree=get_workload(name).max_tree)
     try:
         checked = 0
         for i, cases in enumerate(s.cases):

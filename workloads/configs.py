@@ -69,22 +69,35 @@ class Workload:
     tree_seed: int = 1000
     n_trees: int = 16
     description: str = ""
+    max_tree: int = 64                                # node rows reserved per sequence
+    prefix_lens: Tuple[int, ...] = ()                 # ragged batch: per-sequence prefix (else prefix_len)
+    seq_widths: Tuple[Tuple[int, ...], ...] = ()      # ragged batch: per-sequence widths (else widths)
+
+    def prefix_of(self, seq: int) -> int:
+        return self.prefix_lens[seq] if self.prefix_lens else self.prefix_len
+
+    def widths_of(self, seq: int) -> Tuple[int, ...]:
+        return self.seq_widths[seq] if self.seq_widths else self.widths
+
+    def prefixes(self):
+        return [self.prefix_of(b) for b in range(self.batch)]
 
     @property
     def n_draft(self) -> int:
-        return int(sum(self.widths))
+        """Draft nodes of the largest tree of the batch."""
+        return max(int(sum(self.widths_of(b))) for b in range(self.batch))
 
     @property
     def tree_nodes(self) -> int:
-        """Nodes per tree including the root."""
+        """Nodes per tree including the root (the largest tree of the batch)."""
         return 1 + self.n_draft
 
     @property
     def depth(self) -> int:
-        return len(self.widths)
+        return max(len(self.widths_of(b)) for b in range(self.batch))
 
     def kv_capacity(self, align: int = 64) -> int:
-        need = self.prefix_len + self.tree_nodes
+        need = max(self.prefixes()) + self.tree_nodes
         return ((need + align - 1) // align) * align
 
 
@@ -110,6 +123,22 @@ SMALL_MHA = ModelShape("small-mha", n_layers=3, d_model=384, n_q_heads=3, n_kv_h
                        head_dim=128, d_ff=1000, vocab=4104, rms_eps=1e-5, rope_base=10000.0)
 
 D6 = (10, 10, 10, 10, 10, 10)
+
+
+def ragged_prefixes(batch: int, lo: int, hi: int, seed: int) -> Tuple[int, ...]:
+    """Per-sequence prefix lengths spread uniformly over [lo, hi] (a serving
+    batch of conversations at different points)."""
+    import numpy as np
+    rng = np.random.default_rng(seed)
+    return tuple(int(x) for x in rng.integers(lo, hi + 1, size=batch))
+
+
+def _chain2(batch: int) -> "Workload":
+    return Workload(f"llama3-8b-chain2-b{batch}", LLAMA3_8B, batch=batch, prefix_len=2048, widths=(1, 1),
+                    plant="half", kv_source="synthetic", max_tree=3,
+                    prefix_lens=ragged_prefixes(batch, 256, 2048, 4242 + batch),
+                    description=f"Llama-3-8B shape, B{batch}, ragged prefixes in [256, 2048], "
+                                "a chain of 2 drafts per sequence")
 
 WORKLOADS: Dict[str, Workload] = {
     w.name: w for w in [
@@ -138,6 +167,13 @@ WORKLOADS: Dict[str, Workload] = {
         Workload("small-mha", SMALL_MHA, batch=3, prefix_len=70, widths=(4, 6, 6, 6, 4, 2),
                  plant="leaf", kv_source="prefill",
                  description="3L d384 MHA 3x128 F1000 V4104, B3, P70, tree 28/6"),
+        # ragged serving batch: chains of 0-2 drafts, prefixes of different lengths
+        Workload("small-chain2", SMALL_GQA, batch=16, prefix_len=200, widths=(1, 1), plant="half",
+                 kv_source="prefill", max_tree=3, prefix_lens=ragged_prefixes(16, 20, 200, 77),
+                 seq_widths=tuple((1, 1) if b % 5 else ((1,) if b % 10 else ()) for b in range(16)),
+                 description="small-gqa model, B16, ragged prefixes in [20, 200], chains of 2 drafts "
+                             "(sequences 5 and 15: 1, sequences 0 and 10: the root alone)"),
+        *[_chain2(b) for b in (2, 4, 8, 16)],
     ]
 }
 

@@ -164,7 +164,7 @@ def make_weights(m: ModelShape, seed: int = 0, device="cpu") -> ModelWeights:
 
 def prefix_tokens(w: Workload, seq: int = 0) -> np.ndarray:
     rng = np.random.default_rng(w.prefix_seed + 7919 * seq)
-    return rng.integers(0, w.model.vocab, size=w.prefix_len, dtype=np.int64).astype(np.int32)
+    return rng.integers(0, w.model.vocab, size=w.prefix_of(seq), dtype=np.int64).astype(np.int32)
 
 
 def kv_std(m: ModelShape) -> float:
@@ -283,7 +283,10 @@ def workload_tree(w: Workload, index: int, seq: int = 0) -> tuple[Tree, List[int
     The planted tokens themselves are the target's greedy continuation, which
     the caller computes and writes with `apply_plant`.
     """
-    tree, rng = random_tree(w.widths, w.model.vocab, tree_seed(w, index, seq))
+    widths = w.widths_of(seq)
+    tree, rng = random_tree(widths, w.model.vocab, tree_seed(w, index, seq))
+    if tree.n == 1:
+        return tree, []
     children = np.zeros(tree.n, dtype=np.int32)
     for i in range(1, tree.n):
         children[tree.parents[i]] += 1
@@ -295,9 +298,9 @@ def workload_tree(w: Workload, index: int, seq: int = 0) -> tuple[Tree, List[int
         if rng.random() >= 0.5:
             return tree, []
         depth = tree.depths()
-        deepest = [i for i in range(1, tree.n) if depth[i] == w.depth]
+        deepest = [i for i in range(1, tree.n) if depth[i] == len(widths)]
         node = deepest[int(rng.integers(0, len(deepest)))]
-        length = int(rng.integers(0, w.depth + 1))
+        length = int(rng.integers(0, len(widths) + 1))
         return tree, tree.root_path(node)[:length]
     if w.plant == "none":
         return tree, []
