@@ -15,6 +15,7 @@ Prints one JSON line (rank 0).  Multi-GPU runs are not part of this build.
 from __future__ import annotations
 
 import argparse
+import gc
 import json
 import os
 import sys
@@ -201,6 +202,13 @@ def main():
         v.step_arrays(prefix, n, tok, par)
         return v.accept()
 
+    # Python's cyclic garbage collector stays off while steps are timed: one
+    # full collection over this process's heap takes about 30 ms, which would
+    # land in whichever timing window it happens to fall (reference counting
+    # still frees everything the steps allocate)
+    gc.collect()
+    gc.freeze()
+    gc.disable()
     for i in range(args.warmup):
         one_step(i)
     torch.cuda.synchronize()
@@ -311,6 +319,8 @@ def main():
                            "seeded random rows, so acceptance is synthetic"}
         log(f"T=1 cycle {t_cycle * 1e3:.3f} ms/step, stochastic acceptance {t_acc * 1e6:.1f} us")
 
+    gc.enable()
+    gc.unfreeze()
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on a bounded sample")

@@ -38,7 +38,7 @@
 
 namespace griffin {
 
-template <int DH, int NW>
+template <int DH, int NW, bool RAGGED>
 __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
   constexpr int CH = DH / 64;          // 64-dim chunks of Q/K per lane pair
   constexpr int DB = DH / 32;          // 32-dim blocks of the output
@@ -51,23 +51,33 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
 
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int col = lane & 31, hh = lane >> 5;
-  // XCD-aware decode: workgroups are dispatched round-robin over the 8 XCDs
-  // (id % 8), so every workgroup of one (sequence, KV head) stream gets the
-  // same id % 8 and the K/V blocks it re-reads are shared through that XCD's L2.
+  // Work units: the step's key-split table holds, per unit j, a sequence b,
+  // one of its key splits and that sequence's split count (sequences get
+  // splits in proportion to their prefix lengths).  XCD-aware decode:
+  // workgroups are dispatched round-robin over the 8 XCDs (id % 8), so every
+  // workgroup of one (unit, KV head) gets the same id % 8 and the K/V blocks
+  // it re-reads are shared through that XCD's L2.
   const int G = a.Hq / a.Hkv;
   const int chunks = (G + NW - 1) / NW;
-  const int per_stream = chunks * a.qblocks * a.splits;
+  const int per_unit = chunks * a.qblocks;
   const int id = blockIdx.x;
   const int rest = id >> 3;
-  const int stream = (rest / per_stream) * 8 + (id & 7);
-  if (stream >= a.batch * a.Hkv) return;  // uniform over the workgroup
-  int within = rest % per_stream;
-  const int split = within % a.splits;
-  within /= a.splits;
+  const int u = (rest / per_unit) * 8 + (id & 7);
+  if (u >= a.units * a.Hkv) return;  // uniform over the workgroup
+  const int within = rest % per_unit;
   const int qb = within % a.qblocks;
   const int chunk = within / a.qblocks;
-  const int b = stream / a.Hkv;
-  const int hk = stream % a.Hkv;
+  const int hk = u % a.Hkv;
+  // RAGGED: the unit comes from the step's split table; else every sequence
+  // has a.sp splits and unit j is split j % sp of sequence j / sp
+  int4 ent;
+  if constexpr (RAGGED) {
+    ent = a.meta.split_tab[u / a.Hkv];
+    if (ent.x < 0) return;  // a unit without work this step
+  } else {
+    ent = make_int4((u / a.Hkv / a.sp) | ((u / a.Hkv % a.sp) << 16), a.sp, 0, 0);
+  }
+  const int b = ent.x & 0xffff, split = ent.x >> 16, nsplit = ent.y;
   const int gh = chunk * NW + w;           // head within the group
   const bool head_live = gh < G;           // wave-uniform
   const int hq = hk * G + (head_live ? gh : 0);
@@ -91,13 +101,13 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
       }
   }
 
-  const int n_nodes = a.meta.n_nodes[b];
-  const int P = a.meta.prefix_len[b];
+  const int P = RAGGED ? ent.z : a.meta.prefix_len[b];
+  const int n_nodes = RAGGED ? ent.w : a.meta.n_nodes[b];
 
   // prefix key range of this split, in whole 32-key blocks
   const int nblk = (P + 31) >> 5;
-  const int kb0 = (int)((long long)nblk * split / a.splits);
-  const int kb1 = (int)((long long)nblk * (split + 1) / a.splits);
+  const int kb0 = (int)((long long)nblk * split / nsplit);
+  const int kb1 = (int)((long long)nblk * (split + 1) / nsplit);
   const int nb = kb1 - kb0;
 
   const long long head = ((long long)b * a.Hkv + hk) * a.kv_cap * DH;
@@ -308,8 +318,8 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
   static_assert(NW * 32 * DH * 4 <= (int)sizeof(ring), "transpose tiles fit in the ring");
   __builtin_amdgcn_s_barrier();
   if (!head_live) return;
-  float* po = a.part_o + ((((long long)b * a.Hq + hq) * a.splits + split) * qrows + qb * 32) * DH;
-  float* pml = a.part_ml + ((((long long)b * a.Hq + hq) * a.splits + split) * qrows + qb * 32) * 2;
+  float* po = a.part_o + ((((long long)b * a.Hq + hq) * a.sp + split) * qrows + qb * 32) * DH;
+  float* pml = a.part_ml + ((((long long)b * a.Hq + hq) * a.sp + split) * qrows + qb * 32) * 2;
   float* tile = reinterpret_cast<float*>(&ring[0][0][0]) + w * 32 * DH;
 #pragma unroll
   for (int d = 0; d < DB; ++d)
@@ -319,15 +329,26 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
       *reinterpret_cast<float4*>(tile + col * DH + 4 * (c ^ (col & 7))) =
           make_float4(oacc[d][4 * rg], oacc[d][4 * rg + 1], oacc[d][4 * rg + 2], oacc[d][4 * rg + 3]);
     }
+  // rows of absent nodes are not stored (the merge reads live rows only)
+  const int live_rows = min(32, n_nodes - qb * 32);
 #pragma unroll
   for (int n = 0; n < 32 / RPI; ++n) {
+    if (n * RPI >= live_rows) break;  // uniform
     const int r = n * RPI + lane / CHUNKS, c = lane % CHUNKS;
     *reinterpret_cast<float4*>(po + r * DH + 4 * c) =
         *reinterpret_cast<const float4*>(tile + r * DH + 4 * (c ^ (r & 7)));
   }
-  if (hh == 0) {
+  if (hh == 0 && col < live_rows) {
     pml[2 * col] = m_ref;
     pml[2 * col + 1] = l_run;
+    // the sequence's last split marks its unused slots empty, so that the
+    // merge reads all sp slots without knowing the split count
+    if (RAGGED && split == nsplit - 1)
+      for (int s2 = nsplit; s2 < a.sp; ++s2) {
+        float* pe = a.part_ml + ((((long long)b * a.Hq + hq) * a.sp + s2) * qrows + qb * 32 + col) * 2;
+        pe[0] = -INFINITY;
+        pe[1] = 0.f;
+      }
   }
 }
 
@@ -335,7 +356,10 @@ int attn_waves(int group) { return group >= 4 ? 4 : group >= 2 ? 2 : 1; }
 
 template <int DH, int NW>
 static void launch_attn_nw(const AttnArgs& a, dim3 grid, hipStream_t s) {
-  hipLaunchKernelGGL((tree_attention_kernel<DH, NW>), grid, dim3(64 * NW), 0, s, a);
+  if (a.meta.split_tab)
+    hipLaunchKernelGGL((tree_attention_kernel<DH, NW, true>), grid, dim3(64 * NW), 0, s, a);
+  else
+    hipLaunchKernelGGL((tree_attention_kernel<DH, NW, false>), grid, dim3(64 * NW), 0, s, a);
 }
 
 template <int DH>
@@ -349,9 +373,10 @@ hipError_t launch_attention(const AttnArgs& a, int batch, hipStream_t s) {
   if (a.batch != batch) return hipErrorInvalidValue;
   const int G = a.Hq / a.Hkv;
   const int nw = attn_waves(G);
-  const int streams = batch * a.Hkv;
-  const int per_stream = ((G + nw - 1) / nw) * a.qblocks * a.splits;
-  dim3 grid(((streams + 7) / 8) * 8 * per_stream);
+  if (a.units < 1 || a.sp < 1 || a.sp > 16) return hipErrorInvalidValue;
+  const int streams = a.units * a.Hkv;
+  const int per_unit = ((G + nw - 1) / nw) * a.qblocks;
+  dim3 grid(((streams + 7) / 8) * 8 * per_unit);
   if (a.dh == 128) launch_attn_dh<128>(a, nw, grid, s);
   else if (a.dh == 64) launch_attn_dh<64>(a, nw, grid, s);
   else return hipErrorInvalidValue;
@@ -368,7 +393,7 @@ hipError_t launch_attention(const AttnArgs& a, int batch, hipStream_t s) {
 // tree key reduce over the head's dh/4 threads with xor shuffles (a fixed
 // order).  The merged rows are written fragment-packed split bf16 (o_ks K
 // steps per tile) as the activation operand of the output projection.
-template <int MAXS>
+template <int MAXS, bool RAGGED>
 __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ part_o,
                                                            const float* __restrict__ part_ml, StepMeta meta,
                                                            int Hq, int Hkv, int dh, int qrows, int max_tree,
@@ -384,6 +409,8 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
   const int h = t / quads, d = (t % quads) * 4;
   float4 out = make_float4(0.f, 0.f, 0.f, 0.f);
   if (i < meta.n_nodes[b]) {  // uniform over the workgroup
+    // the sequence's key splits fill the first of the MAXS slots; the
+    // attention kernel marks the rest empty (m = -inf, l = 0)
     const long long base = ((long long)b * Hq + h) * MAXS;
     float ms[MAXS], ls[MAXS];
     float4 os[MAXS];
@@ -406,14 +433,15 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
     // an exact running maximum
     {
       const int P = meta.prefix_len[b];
+      const int ns = RAGGED ? meta.n_split[b] : MAXS;
       const int nblk = (P + 31) >> 5;
       const uint16_t* kh = prefix.k + ((long long)b * Hkv + hk) * prefix.kv_cap * dh + d;
       const uint16_t* vh = prefix.v + ((long long)b * Hkv + hk) * prefix.kv_cap * dh;
 #pragma unroll
       for (int s = 0; s < MAXS; ++s) {
         if (!(ls[s] < 0.f)) continue;  // uniform over the head's lanes
-        const int k0 = 32 * (int)((long long)nblk * s / MAXS);
-        const int k1 = min(P, 32 * (int)((long long)nblk * (s + 1) / MAXS));
+        const int k0 = 32 * (int)((long long)nblk * s / ns);
+        const int k1 = min(P, 32 * (int)((long long)nblk * (s + 1) / ns));
         float m = -INFINITY, l = 0.f;
         float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
         for (int key = k0; key < k1; ++key) {
@@ -505,8 +533,12 @@ hipError_t launch_attn_combine(const float* part_o, const float* part_ml, StepMe
   switch (splits) {
 #define GRIFFIN_COMB_CASE(n)                                                                                   \
   case n:                                                                                                     \
-    hipLaunchKernelGGL(attn_combine_kernel<n>, grid, dim3(256), 0, s, part_o, part_ml, meta, Hq, Hkv, dh, qrows,  \
-                       max_tree, q, q_lo, tree, prefix, scale_log2, o_out, o_ks);                             \
+    if (meta.split_tab)                                                                                       \
+      hipLaunchKernelGGL((attn_combine_kernel<n, true>), grid, dim3(256), 0, s, part_o, part_ml, meta, Hq, Hkv,   \
+                         dh, qrows, max_tree, q, q_lo, tree, prefix, scale_log2, o_out, o_ks);                \
+    else                                                                                                      \
+      hipLaunchKernelGGL((attn_combine_kernel<n, false>), grid, dim3(256), 0, s, part_o, part_ml, meta, Hq, Hkv,  \
+                         dh, qrows, max_tree, q, q_lo, tree, prefix, scale_log2, o_out, o_ks);                \
     break;
     GRIFFIN_COMB_CASE(1) GRIFFIN_COMB_CASE(2) GRIFFIN_COMB_CASE(3) GRIFFIN_COMB_CASE(4) GRIFFIN_COMB_CASE(5)
     GRIFFIN_COMB_CASE(6) GRIFFIN_COMB_CASE(7) GRIFFIN_COMB_CASE(8) GRIFFIN_COMB_CASE(9) GRIFFIN_COMB_CASE(10)

@@ -17,6 +17,9 @@ struct StepMeta {
   const int32_t* parent;      // [R]
   const int32_t* depth;       // [R]
   const uint64_t* anc;        // [R] ancestor-or-self bitmask over node ids
+  const int4* split_tab;      // [units] prefix-attention work: (b | split << 16, splits of b,
+                              // prefix_len[b], n_nodes[b]); x < 0: no work
+  const int32_t* n_split;     // [B] key splits of each sequence
 };
 
 enum GemmEpilogue : int {
@@ -117,10 +120,12 @@ struct AttnArgs {
   const uint16_t* q_lo;      // bf16 residual q - bf16(q), same layout
   const uint16_t* k_cache;   // this layer: [max_batch][Hkv][cap][dh]
   const uint16_t* v_cache;   // this layer: [max_batch][Hkv][cap / 32][dh][32]
-  float* part_o;             // [B][Hq][S][qrows][dh]
-  float* part_ml;            // [B][Hq][S][qrows][2]
+  float* part_o;             // [B][Hq][sp][qrows][dh]
+  float* part_ml;            // [B][Hq][sp][qrows][2]
   StepMeta meta;
-  int Hq, Hkv, dh, kv_cap, max_tree, qblocks, splits, batch;
+  int Hq, Hkv, dh, kv_cap, max_tree, qblocks, batch;
+  int units;                 // entries of meta.split_tab
+  int sp;                    // split slots per (sequence, head) in the partials (<= 16)
   float scale_log2;          // log2(e) / sqrt(dh)
 };
 

@@ -65,6 +65,44 @@ int prepare_tree(int32_t n, const int32_t* tokens, const int32_t* parents, int32
   return GRIFFIN_OK;
 }
 
+// Prefix-attention work of one step: batch * splits units, each sequence at
+// least one and at most min(sp, blocks / 2) (blocks = 32-key blocks of its
+// prefix), the rest dealt one at a time to the sequence with the most blocks
+// per split (ties: the lower index).  A sequence's result depends on the
+// batch only through its split count.  tab [batch * splits][4]: (b | split <<
+// 16, splits of b, prefix_len, n_nodes), b = -1 for units left unused;
+// nsplit [batch].
+void attn_split_plan(int batch, const int32_t* prefix_len, const int32_t* n_nodes, int splits, int sp,
+                     int32_t* tab, int32_t* nsplit) {
+  std::vector<int> blocks(batch), cap(batch), cnt(batch, 1);
+  for (int b = 0; b < batch; ++b) {
+    blocks[b] = (prefix_len[b] + 31) / 32;
+    cap[b] = std::max(1, std::min(sp, blocks[b] / 2));
+  }
+  for (int left = batch * splits - batch; left > 0; --left) {
+    int best = -1;
+    for (int b = 0; b < batch; ++b)
+      if (cnt[b] < cap[b] && (best < 0 || (long long)blocks[b] * cnt[best] > (long long)blocks[best] * cnt[b]))
+        best = b;
+    if (best < 0) break;
+    ++cnt[best];
+  }
+  int j = 0;
+  for (int b = 0; b < batch; ++b) {
+    nsplit[b] = cnt[b];
+    for (int s = 0; s < cnt[b]; ++s, ++j) {
+      tab[4 * j] = b | (s << 16);
+      tab[4 * j + 1] = cnt[b];
+      tab[4 * j + 2] = prefix_len[b];
+      tab[4 * j + 3] = n_nodes[b];
+    }
+  }
+  for (; j < batch * splits; ++j) {
+    tab[4 * j] = -1;
+    tab[4 * j + 1] = tab[4 * j + 2] = tab[4 * j + 3] = 0;
+  }
+}
+
 int validate_desc(const griffin_model_desc* d, std::string* why) {
   auto bad = [&](const char* m) {
     if (why) *why = m;
@@ -157,7 +195,7 @@ struct griffin_ctx {
   uint16_t *k_cache = nullptr, *v_cache = nullptr;
   hipStream_t stream = nullptr;
 
-  int R = 0, Mpad = 0, qkv_n = 0, attn_w = 0, attn_splits = 1, qblocks = 1;
+  int R = 0, Mpad = 0, qkv_n = 0, attn_w = 0, attn_splits = 1, attn_sp = 1, qblocks = 1;
   int E = 1, topk = 1;
   long long parts_elems = 0;
 
@@ -188,6 +226,7 @@ struct griffin_ctx {
   hipEvent_t meta_ev[2] = {nullptr, nullptr};
   size_t meta_bytes = 0;
   size_t off_prefix = 0, off_nodes = 0, off_token = 0, off_pos = 0, off_parent = 0, off_depth = 0, off_anc = 0;
+  size_t off_split = 0, off_nsplit = 0;
   int meta_cur = 0;
   StepMeta meta{};
 
@@ -340,13 +379,14 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
       a.kv_cap = d.kv_capacity;
       a.max_tree = d.max_tree;
       a.qblocks = c->qblocks;
-      a.splits = c->attn_splits;
+      a.units = B * c->attn_splits;
+      a.sp = c->attn_sp;
       a.batch = B;
       a.scale_log2 = scale_log2;
       LAUNCH(GRIFFIN_KC_ATTN, launch_attention(a, B, s));
     }
     LAUNCH(GRIFFIN_KC_MERGE, launch_attn_combine(c->attn_po, c->attn_pml, c->meta, d.n_q_heads, d.n_kv_heads,
-                                                d.head_dim, c->attn_splits, c->qblocks * 32, d.max_tree, B, c->q,
+                                                d.head_dim, c->attn_sp, c->qblocks * 32, d.max_tree, B, c->q,
                                                 c->q_lo, c->tree, PrefixKV{kc, vc, d.kv_capacity}, scale_log2, c->o,
                                                 c->p_o.ks_pad, s));
     {
@@ -567,13 +607,20 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
   c->attn_w = d.n_q_heads * d.head_dim;
   c->qblocks = cdiv(d.max_tree, 32);
   {
-    // key splits: about 256 attention workgroups (one per CU), at least two
-    // 32-key blocks per split
+    // key splits: about 256 attention workgroups (one per CU: the kernel
+    // holds one wave per SIMD, so more workgroups only add rounds), at
+    // least two 32-key blocks per split
     const int G = d.n_q_heads / d.n_kv_heads, nw = attn_waves(G);
     const int units = d.max_batch * d.n_kv_heads * cdiv(G, nw) * c->qblocks;
     const int by_par = cdiv(256, units);
     const int by_len = std::max(1, d.kv_capacity / 64);
     c->attn_splits = std::max(1, std::min(std::min(by_len, by_par), 16));
+    // With several sequences a step has batch * attn_splits split units,
+    // dealt to its sequences in proportion to their prefix lengths (a split
+    // table in the step's metadata); one sequence holds at most twice the
+    // even share (and 16), which bounds the slots the merge reads.  A
+    // single-sequence context gives its sequence all attn_splits, no table.
+    c->attn_sp = d.max_batch > 1 ? std::min(16, 2 * c->attn_splits) : c->attn_splits;
   }
   c->p_qkv = plan_gemm(EPI_STORE, c->qkv_n, d.d_model);
   c->p_o = plan_gemm(EPI_STORE, d.d_model, c->attn_w);
@@ -608,8 +655,8 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
   ALLOC(c->tree.k, (long long)d.max_batch * d.n_kv_heads * d.max_tree * d.head_dim);
   ALLOC(c->tree.v, (long long)d.max_batch * d.n_kv_heads * d.max_tree * d.head_dim);
   ALLOC(c->o, tiles * c->p_o.ks_pad * XPACK_STEP);
-  ALLOC(c->attn_po, (long long)d.max_batch * d.n_q_heads * c->attn_splits * qrows * d.head_dim);
-  ALLOC(c->attn_pml, (long long)d.max_batch * d.n_q_heads * c->attn_splits * qrows * 2);
+  ALLOC(c->attn_po, (long long)d.max_batch * d.n_q_heads * c->attn_sp * qrows * d.head_dim);
+  ALLOC(c->attn_pml, (long long)d.max_batch * d.n_q_heads * c->attn_sp * qrows * 2);
   ALLOC(c->act, (long long)c->E * tiles * c->p_down.ks_pad * XPACK_STEP);
   const long long lm_parts = (long long)c->p_lm.shape.n_wgs * c->p_lm.wn;
   ALLOC(c->pmax, Mp * lm_parts);
@@ -707,6 +754,8 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
     c->off_pos = take(sizeof(int32_t) * Mp);
     c->off_parent = take(sizeof(int32_t) * Mp);
     c->off_depth = take(sizeof(int32_t) * Mp);
+    c->off_split = take(4 * sizeof(int32_t) * d.max_batch * c->attn_splits);
+    c->off_nsplit = take(sizeof(int32_t) * d.max_batch);
     c->meta_bytes = off;
     hipError_t e = hipMalloc((void**)&c->meta_dev, c->meta_bytes);
     if (e != hipSuccess) {
@@ -730,6 +779,8 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
     c->meta.pos = reinterpret_cast<const int32_t*>(c->meta_dev + c->off_pos);
     c->meta.parent = reinterpret_cast<const int32_t*>(c->meta_dev + c->off_parent);
     c->meta.depth = reinterpret_cast<const int32_t*>(c->meta_dev + c->off_depth);
+    c->meta.split_tab = d.max_batch > 1 ? reinterpret_cast<const int4*>(c->meta_dev + c->off_split) : nullptr;
+    c->meta.n_split = reinterpret_cast<const int32_t*>(c->meta_dev + c->off_nsplit);
   }
   if (hipHostMalloc((void**)&c->result_host, sizeof(int32_t) * d.max_batch * result_stride(d.max_depth),
                     hipHostMallocDefault) != hipSuccess ||
@@ -787,6 +838,8 @@ int griffin_verify_step(griffin_ctx* c, int32_t batch, const int32_t* prefix_len
       h_parent[r0 + i] = i == 0 ? 0 : parents[r0 + i];
     }
   }
+  attn_split_plan(batch, prefix_len, n_nodes, c->attn_splits, c->attn_sp,
+                  reinterpret_cast<int32_t*>(h + c->off_split), reinterpret_cast<int32_t*>(h + c->off_nsplit));
   HIP_TRY(c, hipMemcpyAsync(c->meta_dev, h, c->meta_bytes, hipMemcpyHostToDevice, c->stream));
   HIP_TRY(c, hipEventRecord(c->meta_ev[k], c->stream));
   c->meta_cur = k;
