@@ -23,6 +23,8 @@ Modules
               brute-force acceptance over root-to-leaf paths
   latency.py  the paper's speedup model (appendix on decoding latency)
   sampling.py stochastic tree acceptance at temperature T > 0 (Sec. 5)
+  draft.py    the draft model's forward (TGF, decoder layer, TEH, Sec. 4.2)
+              and the dynamic draft-tree expansion
 
 Each function states which pins in ``tests/test_oracle_*.py`` hold it to the
 paper or to mathematics it does not share with itself.  Absolute logits of a
@@ -36,3 +38,5 @@ from .accept import argmax_first, top2_margin, accept_dfs, accept_trie  # noqa: 
 from .decode import DecodeCache, decode_step, prefill, greedy_chain, brute_force_accept  # noqa: F401
 from .latency import speedup_ratio  # noqa: F401
 from .sampling import softmax_t, draw, accept_sampled  # noqa: F401
+from .draft import (DraftOracleWeights, DraftResult, Expansion, draft_forward, expand_tree, layernorm,  # noqa: F401
+                    tgf, topk_logprobs)

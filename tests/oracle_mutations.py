@@ -7,11 +7,12 @@ import numpy as np
 
 import oracle.accept as oa
 import oracle.decode as od
+import oracle.draft as odr
 import oracle.model as om
 import oracle.sampling as osm
 import oracle.verify as ov
 
-_MODULES = (om, ov, od, oa, osm)
+_MODULES = (om, ov, od, oa, osm, odr)
 
 
 def _patch(name, fn):
@@ -248,12 +249,97 @@ def sampling_temperature_ignored():
     oracle.softmax_t = softmax_t
 
 
+def _patch_both(name, fn):
+    _patch(name, fn)
+    import oracle
+    setattr(oracle, name, fn)
+
+
+def draft_tgf_no_residual():
+    orig = odr.tgf
+
+    def tgf(dow, F, e):
+        h, o = orig(dow, F, e)
+        return h, o - h
+    _patch_both("tgf", tgf)
+
+
+def draft_layernorm_no_centring():
+    def layernorm(x, g, b, eps):
+        return x / np.sqrt((x * x).mean(axis=-1, keepdims=True) + eps) * g + b
+    _patch_both("layernorm", layernorm)
+
+
+def draft_heads_swapped():
+    orig = odr.draft_forward
+
+    def draft_forward(dow, tree, feats_in, prefix_kv, prefix_len):
+        r = orig(dow, tree, feats_in, prefix_kv, prefix_len)
+        m = dow.shape.target
+        logits = om.rmsnorm(r.regress, dow.target.final_norm, m.rms_eps) @ dow.target.lm_head().T
+        return odr.DraftResult(logits, r.regress, r.predict, r.h, r.o, r.y)
+    _patch_both("draft_forward", draft_forward)
+
+
+def draft_topk_probabilities():
+    orig = odr.topk_logprobs
+
+    def topk_logprobs(logits, k):
+        tok, lp = orig(logits, k)
+        return tok, np.exp(lp)
+    _patch_both("topk_logprobs", topk_logprobs)
+
+
+def draft_frontier_by_local_probability():
+    """The next frontier ranked by each candidate's own log-probability
+    instead of the cumulative score of its path."""
+    def expand_tree(root_token, root_feature, step, k, depth, n_total, tree_cls):
+        p_tok, p_par, p_cand, p_score = [int(root_token)], [-1], [-1], [0.0]
+        feats = [np.asarray(root_feature, dtype=np.float64)]
+        cands, local = [], []
+        frontier, passes = [0], []
+        for t in range(depth):
+            ptree = tree_cls(np.array(p_tok, dtype=np.int32), np.array(p_par, dtype=np.int32))
+            passes.append(ptree)
+            tok, logp, regress = step(ptree, np.stack(feats))
+            new = []
+            for r in frontier:
+                for j in range(k):
+                    cands.append((t + 1, r, int(tok[r, j]), p_score[r] + float(logp[r, j])))
+                    local.append(float(logp[r, j]))
+                    new.append(len(cands) - 1)
+            if t + 1 == depth:
+                break
+            best = sorted(new, key=lambda c: (-local[c], c))[:k]
+            frontier = []
+            for c in best:
+                _, r, token, score = cands[c]
+                p_tok.append(token)
+                p_par.append(r)
+                p_cand.append(c)
+                p_score.append(score)
+                feats.append(np.asarray(regress[r], dtype=np.float64))
+                frontier.append(len(p_tok) - 1)
+        chosen = sorted(range(len(cands)), key=lambda c: (-cands[c][3], c))[:n_total]
+        rank = {c: i for i, c in enumerate(chosen)}
+        order = sorted(chosen, key=lambda c: (cands[c][0], rank[c]))
+        index = {c: i + 1 for i, c in enumerate(order)}
+        tokens = [int(root_token)] + [cands[c][2] for c in order]
+        parents = [-1] + [0 if p_cand[cands[c][1]] < 0 else index.get(p_cand[cands[c][1]], 0) for c in order]
+        scores = np.array([0.0] + [cands[c][3] for c in order])
+        return odr.Expansion(tree_cls(np.array(tokens, dtype=np.int32), np.array(parents, dtype=np.int32)),
+                             scores, passes, np.array([c[3] for c in cands]))
+    _patch_both("expand_tree", expand_tree)
+
+
 MUTATIONS = {f.__name__: f for f in [
     rope_sign, rope_interleaved, rope_freq_exponent, rmsnorm_eps_outside, attention_unscaled,
     gqa_modulo, no_ancestor_mask, position_by_node_id, drop_attention_residual, swiglu_swapped,
     moe_unnormalised, qkv_kv_swapped, accept_no_bonus, accept_first_child_only,
     argmax_last_on_ties, latency_missing_depth, sampling_rejected_token_kept_in_q,
     sampling_residual_unnormalised, sampling_ratio_inverted, sampling_temperature_ignored,
+    draft_tgf_no_residual, draft_layernorm_no_centring, draft_heads_swapped, draft_topk_probabilities,
+    draft_frontier_by_local_probability,
 ]}
 
 

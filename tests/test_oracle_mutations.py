@@ -14,7 +14,7 @@ from tests.oracle_mutations import MUTATIONS
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 PIN_SUITES = ["tests/test_oracle_primitives.py", "tests/test_oracle_model.py",
-              "tests/test_oracle_golden.py", "tests/test_oracle_sampling.py"]
+              "tests/test_oracle_golden.py", "tests/test_oracle_sampling.py", "tests/test_oracle_draft.py"]
 
 
 def _run(name):

@@ -178,6 +178,43 @@ WORKLOADS: Dict[str, Workload] = {
 }
 
 
+@dataclass(frozen=True)
+class DraftShape:
+    """A GRIFFIN-style draft model for a target: Token-Guided Fusion (a 2d -> d
+    fusion, a 2d -> tgf_dim up projection, a tgf_dim -> d down projection),
+    one decoder layer of the target's shape, and the Token-Enhanced Head (two
+    d x d heads); it shares the target's embedding, final norm and LM head.
+    Expansion: `k` candidates per node and per depth, `depth` draft passes,
+    `n_total` draft tokens kept."""
+    target: ModelShape
+    tgf_dim: int
+    ln_eps: float = 1e-5
+    k: int = 10
+    depth: int = 6
+    n_total: int = 60
+
+    @property
+    def layer(self) -> ModelShape:
+        """The decoder layer as a one-layer model of the target's shape."""
+        return replace(self.target, name=self.target.name + "-draft", n_layers=1)
+
+    def param_count(self) -> int:
+        m, d, e = self.target, self.target.d_model, self.tgf_dim
+        tgf = 2 * d * d + d + 4 * d + 2 * d * e + e + e * d + d
+        layer = 2 * d + m.qkv_rows * d + d * m.n_q_heads * m.head_dim + 3 * d * m.d_ff
+        teh = 2 * (d * d + d)
+        return tgf + layer + teh
+
+
+DRAFTS: Dict[str, DraftShape] = {
+    # the expansion dimension is the value the paper's appendix gives (11008);
+    # with it the draft of the 8B target has 0.42B parameters, as published
+    "llama3-8b": DraftShape(LLAMA3_8B, tgf_dim=11008),
+    "tiny": DraftShape(TINY, tgf_dim=1000, k=4, depth=4, n_total=12),
+    "small-gqa": DraftShape(SMALL_GQA, tgf_dim=1800, k=5, depth=5, n_total=20),
+}
+
+
 def get_workload(name: str) -> Workload:
     try:
         return WORKLOADS[name]

@@ -160,6 +160,68 @@ def make_weights(m: ModelShape, seed: int = 0, device="cpu") -> ModelWeights:
     return ModelWeights(m, mat(_S_EMBED, m.vocab, d), mat(_S_LMHEAD, m.vocab, d), ones(), layers)
 
 
+# ------------------------------------------------------------ draft model ----
+
+_S_DRAFT_BASE = 500   # TGF / TEH tensors: _S_DRAFT_BASE + index below
+_S_DRAFT_LAYER = 600  # the draft's decoder layer (qkv, o, gate/up, down)
+_DRAFT_TENSORS = ("w_m", "b_m", "ln_h_g", "ln_h_b", "ln_x_g", "ln_x_b", "w_u", "b_u", "w_d", "b_d",
+                  "w_p", "b_p", "w_r", "b_r")
+
+
+@dataclass
+class DraftWeights:
+    """bf16 tensors of a draft model (matrices [out, in] like the target's):
+
+    w_m [d, 2d], b_m [d]            fusion of [feature, token embedding]
+    ln_h_g, ln_h_b, ln_x_g, ln_x_b  LayerNorm gains and biases [d]
+    w_u [e, 2d], b_u [e]            up projection of [LN(h), LN(embedding)]
+    w_d [d, e], b_d [d]             down projection
+    layer                           one decoder layer, keys as ModelWeights.layers[l]
+    w_p, w_r [d, d], b_p, b_r [d]   the two heads (predict, regress)
+    The embedding, final norm and LM head are the target's."""
+    shape: "DraftShape"
+    t: Dict[str, torch.Tensor]
+    layer: Dict[str, Optional[torch.Tensor]]
+
+    def to(self, device) -> "DraftWeights":
+        return DraftWeights(self.shape, {k: v.to(device) for k, v in self.t.items()},
+                            {k: None if v is None else v.to(device) for k, v in self.layer.items()})
+
+
+def make_draft_weights(ds, seed: int = 7, device="cpu") -> DraftWeights:
+    """Random-init draft weights: matrices and biases N(0, std^2) with the
+    target's std; LayerNorm gains 1 + N(0, 0.1^2) and biases N(0, 0.1^2)."""
+    m, d, e = ds.target, ds.target.d_model, ds.tgf_dim
+    std = m.weight_std
+    shapes = {"w_m": (d, 2 * d), "b_m": (d,), "ln_h_g": (d,), "ln_h_b": (d,), "ln_x_g": (d,), "ln_x_b": (d,),
+              "w_u": (e, 2 * d), "b_u": (e,), "w_d": (d, e), "b_d": (d,), "w_p": (d, d), "b_p": (d,),
+              "w_r": (d, d), "b_r": (d,)}
+    t = {}
+    for i, name in enumerate(_DRAFT_TENSORS):
+        shp = shapes[name]
+        n = int(np.prod(shp))
+        if name.startswith("ln_"):
+            v = hashed_normal_bf16(n, seed, _S_DRAFT_BASE + i, 0.1, device).float()
+            t[name] = (v + 1.0 if name.endswith("_g") else v).to(torch.bfloat16).view(*shp)
+        else:
+            t[name] = hashed_normal_bf16(n, seed, _S_DRAFT_BASE + i, std, device).view(*shp)
+    ones = torch.ones(d, dtype=torch.bfloat16, device=device)
+
+    def mat(which: int, *shape: int) -> torch.Tensor:
+        return hashed_normal_bf16(int(np.prod(shape)), seed, _S_DRAFT_LAYER + which, std, device).view(*shape)
+
+    layer = {"attn_norm": ones, "mlp_norm": ones.clone(), "w_qkv": mat(0, m.qkv_rows, d),
+             "w_o": mat(1, d, m.n_q_heads * m.head_dim), "w_gate_up": mat(2, 2 * m.d_ff, d),
+             "w_down": mat(3, d, m.d_ff), "w_router": None}
+    return DraftWeights(ds, t, layer)
+
+
+def draft_root_features(d: int, batch: int, seed: int = 11, device="cpu") -> torch.Tensor:
+    """Stand-in for the target's last hidden state at each sequence's root:
+    fp32 [batch, d], entries N(0, 1) rounded to bf16 (the same bits on both sides)."""
+    return hashed_normal_bf16(batch * d, seed, 0, 1.0, device).float().view(batch, d)
+
+
 # ------------------------------------------------------------------ prefix ----
 
 def prefix_tokens(w: Workload, seq: int = 0) -> np.ndarray:
