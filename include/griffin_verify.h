@@ -245,6 +245,79 @@ int griffin_accept_sampled_walk(void *hip_stream, int32_t batch, int32_t max_tre
                                 const float *u_accept, const float *u_final, float temperature,
                                 int32_t *accept_len, int32_t *tokens_out, int32_t *path_nodes);
 
+/* ------------------------------------------------------------ draft model
+ * A GRIFFIN-style draft model (Sec. 4.2): Token-Guided Fusion of an input
+ * feature F and the token embedding e,
+ *   h = [F, e] W_m + b_m,  z = [LN(h), LN(e)] W_u + b_u,  o = SiLU(z) W_d + b_d + h,
+ * one decoder layer of the target's shape over o (rotary attention over the
+ * draft's own cache of the prefix and the node's ancestors in the draft
+ * tree), and the Token-Enhanced Head, two heads on the layer output y:
+ * the predict feature F^P = y W_p + b_p, mapped to tokens by the target's final
+ * norm and LM head, and the regress feature F^R = y W_r + b_r, the input
+ * feature of the node's children in the next draft pass.  LN is LayerNorm
+ * with gain and bias.  The paper gives no equations for the decoder layer and
+ * the heads; the library takes these readings. */
+typedef struct griffin_draft griffin_draft;
+
+/* Device bf16 tensors of a draft model, row-major [out][in]:
+ *   w_m [d][2d], b_m [d]; ln_h_g, ln_h_b, ln_x_g, ln_x_b [d];
+ *   w_u [tgf_dim][2d], b_u [tgf_dim]; w_d [d][tgf_dim], b_d [d];
+ *   w_p, w_r [d][d], b_p, b_r [d];
+ *   the decoder layer as in griffin_weights (one layer, dense).
+ * The matrices are repacked at init (the caller may free them afterwards);
+ * biases, LayerNorm parameters and norm gains are borrowed. */
+typedef struct griffin_draft_weights {
+  const void *w_m, *b_m, *ln_h_g, *ln_h_b, *ln_x_g, *ln_x_b, *w_u, *b_u, *w_d, *b_d;
+  const void *w_p, *b_p, *w_r, *b_r;
+  const void *attn_norm, *w_qkv, *w_o, *mlp_norm, *w_gate_up, *w_down;
+} griffin_draft_weights;
+
+/* Create a draft context.  desc: the target's shape (its n_layers is ignored:
+ * the draft has one layer; n_experts must be 1) with the draft's own limits:
+ * max_batch, max_tree (>= 1 + k * (depth - 1) expanded nodes and >= n_total + 1
+ * drafted nodes), max_depth (>= depth - 1), kv_capacity.  embed, lm_head,
+ * final_norm: the target's (embed and final_norm borrowed, lm_head repacked).
+ * k_cache, v_cache: the draft layer's cache, laid out as for
+ * griffin_verify_init with one layer (prefix K/V of the draft layer).
+ * Errors: EINVAL, ESHAPE, ENOMEM, EHIP. */
+int griffin_draft_init(const griffin_model_desc *desc, int32_t tgf_dim, float ln_eps,
+                       const griffin_draft_weights *weights, const void *embed, const void *lm_head,
+                       const void *final_norm, void *k_cache, void *v_cache, void *hip_stream,
+                       griffin_draft **out);
+void griffin_draft_free(griffin_draft *draft);
+
+/* The draft's one-layer verify context (for griffin_write_prefix-style cache
+ * set-up, timing and error strings: griffin_last_error(griffin_draft_context(d))). */
+griffin_ctx *griffin_draft_context(griffin_draft *draft);
+
+/* One draft pass over `batch` trees laid out as for griffin_verify_step
+ * (node 0 the root at position prefix_len; a node's input feature is its
+ * parent's regress feature from the previous pass, the root's is
+ * root_features, device fp32 [batch][d]).  Writes, per node row
+ * b * max_tree + i, its k most probable next tokens (value descending, lower
+ * id first on ties) and their log-probabilities: host topk_tokens, topk_logp
+ * [batch * max_tree][k], 1 <= k <= 16 (rows of absent nodes untouched).
+ * Synchronises the stream.  Errors as griffin_verify_step, EINVAL. */
+int griffin_draft_step(griffin_draft *draft, int32_t batch, const int32_t *prefix_len, const int32_t *n_nodes,
+                       const int32_t *tokens, const int32_t *parents, const float *root_features, int32_t k,
+                       int32_t *topk_tokens, float *topk_logp);
+
+/* Draft a tree for each of `batch` sequences by dynamic expansion (the paper
+ * follows EAGLE-2's configuration: 60 draft tokens, depth 6): `depth` draft
+ * passes; every expanded node proposes its top-k tokens, scored by the
+ * cumulative log-probability of their path; the k best candidates of a
+ * depth are expanded in the next pass; the tree is the n_total best
+ * candidates of all depths (ties: the earlier candidate), numbered by depth,
+ * then by rank.  root_tokens host [batch]; root_features device fp32
+ * [batch][d].  Outputs, host, laid out for griffin_verify_step: n_nodes_out
+ * [batch], tokens_out and parents_out [batch][max_tree], scores_out (optional)
+ * [batch][max_tree] the cumulative log-probabilities (root 0).
+ * Errors: EINVAL, ETREE (k, depth or n_total do not fit max_tree/max_depth),
+ * and those of griffin_draft_step. */
+int griffin_draft_tree(griffin_draft *draft, int32_t batch, const int32_t *prefix_len, const int32_t *root_tokens,
+                       const float *root_features, int32_t k, int32_t depth, int32_t n_total,
+                       int32_t *n_nodes_out, int32_t *tokens_out, int32_t *parents_out, float *scores_out);
+
 /* Kernel classes of one verification pass, for griffin_profile_*. */
 #define GRIFFIN_KC_QKV 0     /* QKV projection GEMM */
 #define GRIFFIN_KC_ROPE 1    /* rotary embedding + tree K/V write */

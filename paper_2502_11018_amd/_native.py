@@ -39,6 +39,12 @@ class Weights(ctypes.Structure):
     ]
 
 
+class DraftWeights(ctypes.Structure):
+    _fields_ = [(n, c_void_p) for n in (
+        "w_m", "b_m", "ln_h_g", "ln_h_b", "ln_x_g", "ln_x_b", "w_u", "b_u", "w_d", "b_d", "w_p", "b_p", "w_r", "b_r",
+        "attn_norm", "w_qkv", "w_o", "mlp_norm", "w_gate_up", "w_down")]
+
+
 class GriffinError(RuntimeError):
     def __init__(self, code: int, what: str):
         self.code = code
@@ -75,6 +81,13 @@ def _load() -> ctypes.CDLL:
         "griffin_accept_sampled": (c_int32, [c_void_p, c_void_p, c_void_p, F32P, F32P, c_float, I32P, I32P, I32P]),
         "griffin_accept_sampled_walk": (c_int32, [c_void_p, c_int32, c_int32, c_int32, c_int32, I32P, I32P, I32P,
                                                   c_void_p, c_void_p, F32P, F32P, c_float, I32P, I32P, I32P]),
+        "griffin_draft_init": (c_int32, [POINTER(ModelDesc), c_int32, c_float, POINTER(DraftWeights), c_void_p,
+                                         c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, POINTER(c_void_p)]),
+        "griffin_draft_free": (None, [c_void_p]),
+        "griffin_draft_context": (c_void_p, [c_void_p]),
+        "griffin_draft_step": (c_int32, [c_void_p, c_int32, I32P, I32P, I32P, I32P, c_void_p, c_int32, I32P, F32P]),
+        "griffin_draft_tree": (c_int32, [c_void_p, c_int32, I32P, I32P, c_void_p, c_int32, c_int32, c_int32, I32P,
+                                         I32P, I32P, F32P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -87,6 +100,8 @@ lib = _load()
 EXPORTED = ("griffin_kv_cache_bytes", "griffin_verify_init", "griffin_verify_step", "griffin_accept",
             "griffin_read_predictions", "griffin_verify_free", "griffin_status_str", "griffin_last_error",
             "griffin_tree_prepare", "griffin_accept_walk", "griffin_profile_enable", "griffin_profile_read",
-            "griffin_set_graphs", "griffin_commit", "griffin_accept_sampled", "griffin_accept_sampled_walk")
+            "griffin_set_graphs", "griffin_commit", "griffin_accept_sampled", "griffin_accept_sampled_walk",
+            "griffin_draft_init", "griffin_draft_free", "griffin_draft_context", "griffin_draft_step",
+            "griffin_draft_tree")
 KERNEL_CLASSES = ("qkv_gemm", "rope_kv_write", "tree_attention", "o_gemm", "residual_rmsnorm", "gate_up_gemm",
                   "down_gemm", "lm_head_gemm", "argmax_accept_route", "attn_merge")

@@ -11,6 +11,9 @@
 #include <string>
 #include <vector>
 
+#include <functional>
+
+#include "draft.h"
 #include "griffin_internal.h"
 #include "sampling.h"
 #include "griffin_verify.h"
@@ -248,6 +251,11 @@ struct griffin_ctx {
   size_t prof_used = 0;                // pairs recorded since the last read
   int batch = 0;
   bool stepped = false;
+  // A draft model's one-layer context replaces the token embedding by its
+  // fusion module (front: writes x) and the final residual + norm by its
+  // heads (back: writes xn); it runs no argmax or acceptance.
+  std::function<int(griffin_ctx*, hipStream_t)> front;
+  std::function<int(griffin_ctx*, const ResidualAdd&, hipStream_t)> back;
   std::string err;
 };
 
@@ -345,7 +353,10 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
   const size_t layer_kv = (size_t)d.max_batch * d.n_kv_heads * d.kv_capacity * d.head_dim;
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.head_dim));  // log2(e) / sqrt(dh)
 
-  LAUNCH(GRIFFIN_KC_NORM, launch_embed(c->embed, c->meta.token, Mpad, d.d_model, c->x, s));
+  if (c->front)
+    TRY(c->front(c, s));
+  else
+    LAUNCH(GRIFFIN_KC_NORM, launch_embed(c->embed, c->meta.token, Mpad, d.d_model, c->x, s));
   ResidualAdd none{};
   ResidualAdd add_down{};
   for (int l = 0; l < d.n_layers; ++l) {
@@ -454,8 +465,11 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
     }
   }
   // ---- final norm, LM head with fused per-wave argmax, reduction, acceptance
-  LAUNCH(GRIFFIN_KC_NORM, launch_residual_rmsnorm(c->x, add_down, c->final_norm, d.rms_eps, Mpad, d.d_model, c->xn,
-                                                  c->xd_ks, s));
+  if (c->back)
+    TRY(c->back(c, add_down, s));
+  else
+    LAUNCH(GRIFFIN_KC_NORM, launch_residual_rmsnorm(c->x, add_down, c->final_norm, d.rms_eps, Mpad, d.d_model,
+                                                    c->xn, c->xd_ks, s));
   const int lm_parts = c->p_lm.shape.n_wgs * c->p_lm.wn;
   {
     GemmArgs a = gemm_args(c->p_lm, c->xn, c->xd_ks, c->pk_lm, m_tiles);
@@ -468,6 +482,7 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
     a.logit_rows = rows;
     LAUNCH(GRIFFIN_KC_LM_HEAD, launch_gemm(a, 1, s));
   }
+  if (c->front) return GRIFFIN_OK;  // a draft pass: the caller reads the logits
   LAUNCH(GRIFFIN_KC_OTHER, launch_argmax_reduce(c->pmax, c->pidx, c->pnan, lm_parts, lm_parts, rows, c->pred,
                                                 c->nan_row, s));
   LAUNCH(GRIFFIN_KC_OTHER, launch_accept(c->meta, c->pred, c->nan_row, B, d.max_tree, d.max_depth, c->result, s));
@@ -509,6 +524,88 @@ int run_pass(griffin_ctx* c, float* logits_out) {
   c->graphs.push_back({c->batch, logits_out, exec});
   HIP_TRY(c, hipGraphLaunch(exec, c->stream));
   return GRIFFIN_OK;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- draft model
+
+struct griffin_draft {
+  griffin_ctx* inner = nullptr;  // the decoder layer: a one-layer context with the draft's front and back
+  int d = 0, e = 0;
+  float ln_eps = 1e-5f;
+  GemmPlan p_m, p_u, p_d, p_h;
+  uint16_t *pk_m = nullptr, *pk_u = nullptr, *pk_d = nullptr, *pk_h = nullptr;
+  const uint16_t *b_m, *ln_h_g, *ln_h_b, *ln_x_g, *ln_x_b, *b_u, *b_d, *b_p, *b_r;
+  float *parts = nullptr, *h = nullptr, *feat_r = nullptr, *feat_p = nullptr, *root_feat = nullptr;
+  float* logits = nullptr;
+  uint16_t *x_m = nullptr, *x_u = nullptr, *x_d = nullptr, *x_h = nullptr;
+  int32_t* topk_tok = nullptr;
+  float* topk_lp = nullptr;
+  int32_t* topk_tok_host = nullptr;
+  float* topk_lp_host = nullptr;
+  std::vector<void*> allocs;
+};
+
+namespace {
+
+DraftArgs draft_args(griffin_draft* dc, griffin_ctx* c) {
+  const griffin_model_desc& d = c->d;
+  const int rows = c->batch * d.max_tree, mpad = round_up(rows, 64);
+  DraftArgs a{};
+  a.d = dc->d;
+  a.tgf_dim = dc->e;
+  a.rows = rows;
+  a.mpad = mpad;
+  a.max_tree = d.max_tree;
+  a.ln_eps = dc->ln_eps;
+  a.rms_eps = d.rms_eps;
+  a.embed = c->embed;
+  a.root_feat = dc->root_feat;
+  a.feat_r = dc->feat_r;
+  a.feat_p = dc->feat_p;
+  a.h = dc->h;
+  a.x = c->x;
+  a.parts = dc->parts;
+  a.n_parts_m = dc->p_m.out_splits();
+  a.n_parts_u = dc->p_u.out_splits();
+  a.n_parts_d = dc->p_d.out_splits();
+  a.n_parts_h = dc->p_h.out_splits();
+  a.stride_m = (long long)mpad * dc->d;
+  a.stride_u = (long long)mpad * dc->e;
+  a.stride_d = (long long)mpad * dc->d;
+  a.stride_h = (long long)mpad * 2 * dc->d;
+  a.x_m = dc->x_m;
+  a.x_u = dc->x_u;
+  a.x_d = dc->x_d;
+  a.x_h = dc->x_h;
+  a.xn = c->xn;
+  a.ks_m = dc->p_m.ks_pad;
+  a.ks_u = dc->p_u.ks_pad;
+  a.ks_d = dc->p_d.ks_pad;
+  a.ks_h = dc->p_h.ks_pad;
+  a.xn_ks = c->xd_ks;
+  a.b_m = dc->b_m;
+  a.ln_h_g = dc->ln_h_g;
+  a.ln_h_b = dc->ln_h_b;
+  a.ln_x_g = dc->ln_x_g;
+  a.ln_x_b = dc->ln_x_b;
+  a.b_u = dc->b_u;
+  a.b_d = dc->b_d;
+  a.b_p = dc->b_p;
+  a.b_r = dc->b_r;
+  a.final_norm = c->final_norm;
+  return a;
+}
+
+hipError_t draft_gemm(griffin_draft* dc, griffin_ctx* c, const GemmPlan& p, const uint16_t* X, const uint16_t* W,
+                      int N, hipStream_t s) {
+  const int mpad = round_up(c->batch * c->d.max_tree, 64);
+  GemmArgs a = gemm_args(p, X, p.ks_pad, W, mpad / 64);
+  a.out = dc->parts;
+  a.ldo = N;
+  a.out_split_stride = (long long)mpad * N;
+  return launch_gemm(a, 1, s);
 }
 
 }  // namespace
@@ -1212,6 +1309,258 @@ done:
   hipStreamSynchronize(s);
   hipFree(dev);
   return rc;
+}
+
+
+void griffin_draft_free(griffin_draft* dc) {
+  if (!dc) return;
+  if (dc->inner) griffin_verify_free(dc->inner);
+  for (void* p : dc->allocs) hipFree(p);
+  if (dc->topk_tok_host) hipHostFree(dc->topk_tok_host);
+  if (dc->topk_lp_host) hipHostFree(dc->topk_lp_host);
+  delete dc;
+}
+
+int griffin_draft_init(const griffin_model_desc* desc, int32_t tgf_dim, float ln_eps, const griffin_draft_weights* w,
+                       const void* embed, const void* lm_head, const void* final_norm, void* k_cache, void* v_cache,
+                       void* hip_stream, griffin_draft** out) {
+  if (!out) return GRIFFIN_EINVAL;
+  *out = nullptr;
+  if (!desc || !w || !embed || !lm_head || !final_norm || tgf_dim < 1 || !(ln_eps > 0.f)) return GRIFFIN_EINVAL;
+  if (desc->n_experts != 1) return GRIFFIN_ESHAPE;  // the draft's decoder layer is dense
+  const void* ptrs[] = {w->w_m, w->b_m, w->ln_h_g, w->ln_h_b, w->ln_x_g, w->ln_x_b, w->w_u, w->b_u, w->w_d,
+                        w->b_d, w->w_p, w->b_p, w->w_r, w->b_r, w->attn_norm, w->w_qkv, w->w_o, w->mlp_norm,
+                        w->w_gate_up, w->w_down};
+  for (const void* p : ptrs)
+    if (!p) return GRIFFIN_EINVAL;
+  griffin_model_desc ld = *desc;
+  ld.n_layers = 1;
+  griffin_weights lw{};
+  lw.embed = embed;
+  lw.lm_head = lm_head;
+  lw.final_norm = final_norm;
+  lw.attn_norm = &w->attn_norm;
+  lw.w_qkv = &w->w_qkv;
+  lw.w_o = &w->w_o;
+  lw.mlp_norm = &w->mlp_norm;
+  lw.w_gate_up = &w->w_gate_up;
+  lw.w_down = &w->w_down;
+  const void* no_router = nullptr;
+  lw.w_router = &no_router;
+  auto* dc = new griffin_draft();
+  int rc = griffin_verify_init(&ld, &lw, k_cache, v_cache, hip_stream, &dc->inner);
+  if (rc != GRIFFIN_OK) {
+    delete dc;
+    return rc;
+  }
+  griffin_ctx* c = dc->inner;
+  const int d = desc->d_model, e = tgf_dim;
+  dc->d = d;
+  dc->e = e;
+  dc->ln_eps = ln_eps;
+  dc->b_m = static_cast<const uint16_t*>(w->b_m);
+  dc->ln_h_g = static_cast<const uint16_t*>(w->ln_h_g);
+  dc->ln_h_b = static_cast<const uint16_t*>(w->ln_h_b);
+  dc->ln_x_g = static_cast<const uint16_t*>(w->ln_x_g);
+  dc->ln_x_b = static_cast<const uint16_t*>(w->ln_x_b);
+  dc->b_u = static_cast<const uint16_t*>(w->b_u);
+  dc->b_d = static_cast<const uint16_t*>(w->b_d);
+  dc->b_p = static_cast<const uint16_t*>(w->b_p);
+  dc->b_r = static_cast<const uint16_t*>(w->b_r);
+  dc->p_m = plan_gemm(EPI_STORE, d, 2 * d);
+  dc->p_u = plan_gemm(EPI_STORE, e, 2 * d);
+  dc->p_d = plan_gemm(EPI_STORE, d, e);
+  dc->p_h = plan_gemm(EPI_STORE, 2 * d, d);
+  const int rows = desc->max_batch * desc->max_tree, mpad = round_up(rows, 64), tiles = mpad / 64;
+  long long parts = 0;
+  for (const GemmPlan* p : {&dc->p_m, &dc->p_u, &dc->p_d, &dc->p_h})
+    parts = std::max(parts, (long long)p->out_splits() * mpad * p->n_out);
+  auto alloc = [&](void** p, size_t bytes) {
+    if (hipMalloc(p, std::max<size_t>(bytes, 256)) != hipSuccess) return false;
+    dc->allocs.push_back(*p);
+    return hipMemset(*p, 0, std::max<size_t>(bytes, 256)) == hipSuccess;
+  };
+  bool ok = alloc((void**)&dc->pk_m, 2 * dc->p_m.elems) && alloc((void**)&dc->pk_u, 2 * dc->p_u.elems) &&
+            alloc((void**)&dc->pk_d, 2 * dc->p_d.elems) && alloc((void**)&dc->pk_h, 2 * dc->p_h.elems) &&
+            alloc((void**)&dc->parts, 4 * parts) && alloc((void**)&dc->h, 4LL * mpad * d) &&
+            alloc((void**)&dc->feat_r, 4LL * rows * d) && alloc((void**)&dc->feat_p, 4LL * mpad * d) &&
+            alloc((void**)&dc->root_feat, 4LL * desc->max_batch * d) &&
+            alloc((void**)&dc->logits, 4LL * rows * desc->vocab) &&
+            alloc((void**)&dc->x_m, 2LL * tiles * dc->p_m.ks_pad * XPACK_STEP) &&
+            alloc((void**)&dc->x_u, 2LL * tiles * dc->p_u.ks_pad * XPACK_STEP) &&
+            alloc((void**)&dc->x_d, 2LL * tiles * dc->p_d.ks_pad * XPACK_STEP) &&
+            alloc((void**)&dc->x_h, 2LL * tiles * dc->p_h.ks_pad * XPACK_STEP) &&
+            alloc((void**)&dc->topk_tok, 4LL * rows * 16) && alloc((void**)&dc->topk_lp, 4LL * rows * 16) &&
+            hipHostMalloc((void**)&dc->topk_tok_host, 4LL * rows * 16, hipHostMallocDefault) == hipSuccess &&
+            hipHostMalloc((void**)&dc->topk_lp_host, 4LL * rows * 16, hipHostMallocDefault) == hipSuccess;
+  if (!ok) {
+    griffin_draft_free(dc);
+    return GRIFFIN_ENOMEM;
+  }
+  // pack the four matrices; the heads as one [2d][d] matrix (predict rows, then regress rows)
+  uint16_t* heads = nullptr;
+  hipError_t he = hipMalloc((void**)&heads, 2LL * 2 * d * d);
+  hipStream_t s = c->stream;
+  if (he == hipSuccess)
+    he = hipMemcpyAsync(heads, w->w_p, 2LL * d * d, hipMemcpyDeviceToDevice, s);
+  if (he == hipSuccess)
+    he = hipMemcpyAsync(heads + (size_t)d * d, w->w_r, 2LL * d * d, hipMemcpyDeviceToDevice, s);
+  if (he == hipSuccess)
+    he = launch_pack_weight(static_cast<const uint16_t*>(w->w_m), d, 2 * d, dc->p_m.shape, dc->pk_m, s);
+  if (he == hipSuccess)
+    he = launch_pack_weight(static_cast<const uint16_t*>(w->w_u), e, 2 * d, dc->p_u.shape, dc->pk_u, s);
+  if (he == hipSuccess)
+    he = launch_pack_weight(static_cast<const uint16_t*>(w->w_d), d, e, dc->p_d.shape, dc->pk_d, s);
+  if (he == hipSuccess) he = launch_pack_weight(heads, 2 * d, d, dc->p_h.shape, dc->pk_h, s);
+  if (he == hipSuccess) he = hipStreamSynchronize(s);
+  if (heads) hipFree(heads);
+  if (he != hipSuccess) {
+    griffin_draft_free(dc);
+    return GRIFFIN_EHIP;
+  }
+  c->front = [dc](griffin_ctx* cc, hipStream_t st) -> int {
+    const DraftArgs a = draft_args(dc, cc);
+    const int d2 = dc->d;
+    HIP_TRY(cc, launch_draft_front(a, cc->meta, 0, st));
+    HIP_TRY(cc, draft_gemm(dc, cc, dc->p_m, dc->x_m, dc->pk_m, d2, st));
+    HIP_TRY(cc, launch_draft_front(a, cc->meta, 1, st));
+    HIP_TRY(cc, draft_gemm(dc, cc, dc->p_u, dc->x_u, dc->pk_u, dc->e, st));
+    HIP_TRY(cc, launch_draft_front(a, cc->meta, 2, st));
+    HIP_TRY(cc, draft_gemm(dc, cc, dc->p_d, dc->x_d, dc->pk_d, d2, st));
+    HIP_TRY(cc, launch_draft_front(a, cc->meta, 3, st));
+    return GRIFFIN_OK;
+  };
+  c->back = [dc](griffin_ctx* cc, const ResidualAdd& add, hipStream_t st) -> int {
+    const DraftArgs a = draft_args(dc, cc);
+    HIP_TRY(cc, launch_draft_head(a, cc->meta, add, 0, st));
+    HIP_TRY(cc, draft_gemm(dc, cc, dc->p_h, dc->x_h, dc->pk_h, 2 * dc->d, st));
+    HIP_TRY(cc, launch_draft_head(a, cc->meta, add, 1, st));
+    return GRIFFIN_OK;
+  };
+  *out = dc;
+  return GRIFFIN_OK;
+}
+
+griffin_ctx* griffin_draft_context(griffin_draft* dc) { return dc ? dc->inner : nullptr; }
+
+int griffin_draft_step(griffin_draft* dc, int32_t batch, const int32_t* prefix_len, const int32_t* n_nodes,
+                       const int32_t* tokens, const int32_t* parents, const float* root_features, int32_t k,
+                       int32_t* topk_tokens, float* topk_logp) {
+  if (!dc) return GRIFFIN_EINVAL;
+  griffin_ctx* c = dc->inner;
+  const griffin_model_desc& d = c->d;
+  if (!root_features || !topk_tokens || !topk_logp || k < 1 || k > 16 || k > d.vocab || batch < 1 ||
+      batch > d.max_batch)
+    return set_err(c, GRIFFIN_EINVAL, "bad draft step arguments");
+  HIP_TRY(c, hipMemcpyAsync(dc->root_feat, root_features, sizeof(float) * batch * dc->d, hipMemcpyDeviceToDevice,
+                            c->stream));
+  TRY(griffin_verify_step(c, batch, prefix_len, n_nodes, tokens, parents, dc->logits));
+  const int rows = batch * d.max_tree;
+  HIP_TRY(c, launch_draft_topk(dc->logits, d.vocab, d.vocab, c->meta, rows, d.max_tree, k, dc->topk_tok,
+                               dc->topk_lp, c->stream));
+  HIP_TRY(c, hipMemcpyAsync(dc->topk_tok_host, dc->topk_tok, sizeof(int32_t) * rows * k, hipMemcpyDeviceToHost,
+                            c->stream));
+  HIP_TRY(c, hipMemcpyAsync(dc->topk_lp_host, dc->topk_lp, sizeof(float) * rows * k, hipMemcpyDeviceToHost,
+                            c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  memcpy(topk_tokens, dc->topk_tok_host, sizeof(int32_t) * rows * k);
+  memcpy(topk_logp, dc->topk_lp_host, sizeof(float) * rows * k);
+  c->stepped = false;  // a draft pass has no acceptance result
+  return GRIFFIN_OK;
+}
+
+int griffin_draft_tree(griffin_draft* dc, int32_t batch, const int32_t* prefix_len, const int32_t* root_tokens,
+                       const float* root_features, int32_t k, int32_t depth, int32_t n_total, int32_t* n_nodes_out,
+                       int32_t* tokens_out, int32_t* parents_out, float* scores_out) {
+  if (!dc) return GRIFFIN_EINVAL;
+  griffin_ctx* c = dc->inner;
+  const griffin_model_desc& d = c->d;
+  const int T = d.max_tree;
+  if (!prefix_len || !root_tokens || !root_features || !n_nodes_out || !tokens_out || !parents_out || batch < 1 ||
+      batch > d.max_batch || k < 1 || k > 16 || depth < 1 || n_total < 1)
+    return set_err(c, GRIFFIN_EINVAL, "bad draft tree arguments");
+  if (1 + (long long)k * (depth - 1) > T || depth - 1 > d.max_depth)
+    return set_err(c, GRIFFIN_ETREE, "1 + k * (depth - 1) expanded nodes must fit max_tree and max_depth");
+  if (n_total + 1 > T) return set_err(c, GRIFFIN_ETREE, "n_total + 1 must fit max_tree");
+  struct Cand {
+    int depth, parent;  // parent: node of the pass tree that proposed it
+    int token;
+    double score;
+  };
+  std::vector<std::vector<int>> p_tok(batch), p_par(batch), p_cand(batch), frontier(batch);
+  std::vector<std::vector<double>> p_score(batch);
+  std::vector<std::vector<Cand>> cands(batch);
+  for (int b = 0; b < batch; ++b) {
+    p_tok[b] = {root_tokens[b]};
+    p_par[b] = {-1};
+    p_cand[b] = {-1};
+    p_score[b] = {0.0};
+    frontier[b] = {0};
+  }
+  std::vector<int32_t> nn(batch), tok((size_t)batch * T, 0), par((size_t)batch * T, 0);
+  std::vector<int32_t> ktok((size_t)batch * T * k);
+  std::vector<float> klp((size_t)batch * T * k);
+  for (int t = 0; t < depth; ++t) {
+    for (int b = 0; b < batch; ++b) {
+      nn[b] = (int)p_tok[b].size();
+      for (int i = 0; i < nn[b]; ++i) {
+        tok[(size_t)b * T + i] = p_tok[b][i];
+        par[(size_t)b * T + i] = p_par[b][i];
+      }
+    }
+    TRY(griffin_draft_step(dc, batch, prefix_len, nn.data(), tok.data(), par.data(), root_features, k, ktok.data(),
+                           klp.data()));
+    for (int b = 0; b < batch; ++b) {
+      std::vector<int> fresh;
+      for (int r : frontier[b])
+        for (int j = 0; j < k; ++j) {
+          const size_t at = ((size_t)b * T + r) * k + j;
+          cands[b].push_back({t + 1, r, ktok[at], p_score[b][r] + (double)klp[at]});
+          fresh.push_back((int)cands[b].size() - 1);
+        }
+      if (t + 1 == depth) continue;
+      auto& cb = cands[b];
+      std::stable_sort(fresh.begin(), fresh.end(), [&](int x, int y) { return cb[x].score > cb[y].score; });
+      frontier[b].clear();
+      for (int i = 0; i < k && i < (int)fresh.size(); ++i) {
+        const Cand& q = cb[fresh[i]];
+        p_tok[b].push_back(q.token);
+        p_par[b].push_back(q.parent);
+        p_cand[b].push_back(fresh[i]);
+        p_score[b].push_back(q.score);
+        frontier[b].push_back((int)p_tok[b].size() - 1);
+      }
+    }
+  }
+  for (int b = 0; b < batch; ++b) {
+    auto& cb = cands[b];
+    std::vector<int> chosen(cb.size());
+    for (size_t i = 0; i < cb.size(); ++i) chosen[i] = (int)i;
+    std::stable_sort(chosen.begin(), chosen.end(), [&](int x, int y) { return cb[x].score > cb[y].score; });
+    chosen.resize(std::min<size_t>(chosen.size(), n_total));
+    std::vector<int> rank(cb.size(), -1);
+    for (size_t i = 0; i < chosen.size(); ++i) rank[chosen[i]] = (int)i;
+    std::vector<int> order = chosen;
+    std::stable_sort(order.begin(), order.end(), [&](int x, int y) {
+      return cb[x].depth != cb[y].depth ? cb[x].depth < cb[y].depth : rank[x] < rank[y];
+    });
+    std::vector<int> index(cb.size(), -1);
+    for (size_t i = 0; i < order.size(); ++i) index[order[i]] = (int)i + 1;
+    int32_t* to = tokens_out + (size_t)b * T;
+    int32_t* po = parents_out + (size_t)b * T;
+    n_nodes_out[b] = 1 + (int)order.size();
+    to[0] = root_tokens[b];
+    po[0] = -1;
+    if (scores_out) scores_out[(size_t)b * T] = 0.f;
+    for (size_t i = 0; i < order.size(); ++i) {
+      const Cand& q = cb[order[i]];
+      const int pc = p_cand[b][q.parent];
+      to[i + 1] = q.token;
+      po[i + 1] = pc < 0 ? 0 : index[pc];
+      if (scores_out) scores_out[(size_t)b * T + i + 1] = (float)q.score;
+    }
+  }
+  return GRIFFIN_OK;
 }
 
 }  // extern "C"

@@ -122,6 +122,23 @@ def accept_sampled_walk(trees: Sequence, logits: torch.Tensor, q_draft: torch.Te
     return AcceptResult(L, out, path[:, :max_depth])
 
 
+def write_prefix(k_cache: torch.Tensor, v_cache: torch.Tensor, shape, max_batch: int, kv_capacity: int, layer: int,
+                 seq: int, k: torch.Tensor, v: torch.Tensor, stream) -> None:
+    """Copy a prefix k, v bf16 [Hkv, P, dh] (k post-rotary) into the cache
+    layouts of griffin_verify_init: K [layers][batch][Hkv][cap][dh], V in
+    transposed 32-slot tiles [layers][batch][Hkv][cap / 32][dh][32]."""
+    Hkv, dh = shape.n_kv_heads, shape.head_dim
+    P = k.shape[1]
+    full, rem = divmod(P, 32)
+    tiles = v_cache.view(shape.n_layers, max_batch, Hkv, kv_capacity // 32, dh, 32)[layer, seq]
+    with torch.cuda.stream(stream):
+        k_cache.view(shape.n_layers, max_batch, Hkv, kv_capacity, dh)[layer, seq, :, :P, :].copy_(k)
+        if full:
+            tiles[:, :full].copy_(v[:, : full * 32].reshape(v.shape[0], full, 32, v.shape[2]).transpose(-1, -2))
+        if rem:
+            tiles[:, full, :, :rem].copy_(v[:, full * 32:].transpose(-1, -2))
+
+
 class TreeVerifier:
     """One verify context: borrowed weights, a KV cache, and the library's workspace.
 
@@ -179,16 +196,8 @@ class TreeVerifier:
 
     def write_prefix(self, layer: int, seq: int, k: torch.Tensor, v: torch.Tensor):
         """Place a cached prefix: k, v bf16 [Hkv, P, dh] (k post-rotary)."""
-        P = k.shape[1]
-        full, rem = divmod(P, 32)
-        tiles = self._v_tiles(layer, seq)                      # [Hkv, cap/32, dh, 32]
-        with torch.cuda.stream(self.stream):
-            self.k_cache.view(self.shape.n_layers, self.max_batch, self.shape.n_kv_heads, self.kv_capacity,
-                              self.shape.head_dim)[layer, seq, :, :P, :].copy_(k)
-            if full:
-                tiles[:, :full].copy_(v[:, : full * 32].reshape(v.shape[0], full, 32, v.shape[2]).transpose(-1, -2))
-            if rem:
-                tiles[:, full, :, :rem].copy_(v[:, full * 32:].transpose(-1, -2))
+        write_prefix(self.k_cache, self.v_cache, self.shape, self.max_batch, self.kv_capacity, layer, seq, k, v,
+                     self.stream)
 
     def read_v(self, layer: int, seq: int, n: int) -> torch.Tensor:
         """Cached values of slots [0, n) as [Hkv, n, dh]."""

@@ -1,0 +1,178 @@
+"""The draft model on the GPU, through the C ABI, against the fp64 oracle
+(oracle/draft.py) on the same seeded inputs.
+
+A draft pass: every live row's top-k tokens and log-probabilities.  Tokens
+are compared exactly where the oracle's k-th and (k+1)-th logits differ by
+more than TOKEN_GAP (fp32 / split-bf16 on the device, fp64 in the oracle);
+log-probabilities within LOGP_TOL.  A drafted tree: the set of root paths
+equals the oracle's expansion wherever none of its selections (the
+frontier of each depth, the final n_total) is decided by a score gap below
+SCORE_GAP; other cases are counted.  Every case prints its name first.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import draft as od
+from workloads import gen
+from workloads.configs import DRAFTS
+
+pytestmark = pytest.mark.gpu
+
+TOKEN_GAP = 2e-3
+LOGP_TOL = 2e-3
+SCORE_GAP = 2e-3
+
+
+def say(msg):
+    print(f"[gpu-case] {msg}", flush=True)
+
+
+class Draft:
+    def __init__(self, name, batch, prefix, max_tree=64):
+        import paper_2502_11018_amd as P
+        self.ds = DRAFTS[name]
+        m = self.ds.target
+        self.mw = gen.make_weights(m, 0)
+        self.dw = gen.make_draft_weights(self.ds, 3)
+        self.ow = oracle.OracleWeights(self.mw)
+        self.dow = od.DraftOracleWeights(self.dw, self.ow)
+        self.prefix = prefix
+        cap = ((max(prefix) + max_tree + 63) // 64) * 64
+        say(f"draft {name}: init batch {batch} cap {cap}")
+        self.dm = P.DraftModel(self.ds, self.dw.to("cuda"), self.mw.to("cuda"), max_batch=batch, max_tree=max_tree,
+                               max_depth=max_tree - 1, kv_capacity=cap)
+        self.kv = []
+        for b in range(batch):
+            k, v = gen.synthetic_kv(self.ds.layer, 0, b, prefix[b], 5)
+            self.kv.append((k.double().numpy(), v.double().numpy()))
+            self.dm.write_prefix(b, k.cuda(), v.cuda())
+        self.feat = gen.draft_root_features(m.d_model, batch, 11)
+        torch.cuda.synchronize()
+
+    def close(self):
+        self.dm.close()
+
+
+def _pass_feats(dr, tree, fr_prev, root_feat):
+    """Input features of a pass: the root's, then each node's parent's regress feature."""
+    f = np.zeros((tree.n, dr.ds.target.d_model))
+    f[0] = root_feat
+    for i in range(1, tree.n):
+        f[i] = fr_prev[tree.parents[i]]
+    return f
+
+
+@pytest.mark.parametrize("name", ["tiny", "small-gqa"])
+def test_draft_passes_match_oracle(name):
+    """Three passes over growing trees, as an expansion runs them: the root
+    alone, then its children, then grandchildren; each node reads its
+    parent's regress feature from the previous pass (the oracle's from its
+    own fp64 pass).  Top-k tokens and log-probabilities of every node."""
+    B = 2
+    dr = Draft(name, B, [37, 70])
+    try:
+        k, V, d = dr.ds.k, dr.ds.target.vocab, dr.ds.target.d_model
+        compared, total = 0, 0
+        fr_prev = [None] * B
+        for it, widths in enumerate([(), (3,), (3, 4)]):
+            trees = [gen.random_tree(widths, V, 50 + 7 * b)[0] for b in range(B)]
+            say(f"draft {name} pass {it}: {[t.n for t in trees]} nodes")
+            tok, lp = dr.dm.step(dr.prefix, trees, dr.feat.cuda(), k)
+            for b, t in enumerate(trees):
+                feats = np.zeros((t.n, d))
+                feats[0] = dr.feat[b].double().numpy()
+                for i in range(1, t.n):
+                    feats[i] = fr_prev[b][t.parents[i]]
+                r = od.draft_forward(dr.dow, t, feats, dr.kv[b], dr.prefix[b])
+                fr_prev[b] = r.regress
+                otok, _ = od.topk_logprobs(r.logits, k)
+                srt = np.sort(r.logits, axis=1)[:, ::-1]
+                for i in range(t.n):
+                    total += 1
+                    full = r.logits[i] - (srt[i, 0] + np.log(np.exp(r.logits[i] - srt[i, 0]).sum()))
+                    assert np.max(np.abs(lp[b, i] - full[tok[b, i]])) < LOGP_TOL, (b, i)
+                    if (-np.diff(srt[i, : k + 1])).min() > TOKEN_GAP:
+                        compared += 1
+                        assert list(tok[b, i]) == list(otok[i]), (b, i, tok[b, i], otok[i])
+        say(f"draft {name}: tokens compared on {compared}/{total} rows")
+        assert compared >= total // 2
+    finally:
+        dr.close()
+
+
+def _decided(ex, k, depth, n_total):
+    """True when every selection of the oracle's expansion clears SCORE_GAP:
+    the k-th vs (k+1)-th new candidate of each expanded depth, and the
+    n_total-th vs (n_total+1)-th candidate overall."""
+    sc = ex.candidate_scores
+    per = [k] + [k * k] * (depth - 1)
+    at = 0
+    for t in range(depth - 1):
+        new = np.sort(sc[at: at + per[t]])[::-1]
+        if len(new) > k and new[k - 1] - new[k] <= SCORE_GAP:
+            return False
+        at += per[t]
+    allc = np.sort(sc)[::-1]
+    return not (len(allc) > n_total and allc[n_total - 1] - allc[n_total] <= SCORE_GAP)
+
+
+def _path_set(n, tok, par):
+    out = set()
+    for i in range(1, n):
+        path, j = [], i
+        while j > 0:
+            path.append(int(tok[j]))
+            j = int(par[j])
+        out.add(tuple(path[::-1]))
+    return out
+
+
+@pytest.mark.parametrize("name", ["tiny", "small-gqa"])
+def test_drafted_tree_matches_oracle_expansion(name):
+    B = 3
+    dr = Draft(name, B, [20, 61, 90])
+    try:
+        ds = dr.ds
+        k, D, N, d = ds.k, ds.depth, ds.n_total, ds.target.d_model
+        roots = [5, 17, 29]
+        say(f"draft {name}: tree k={k} depth={D} n_total={N}")
+        n, tok, par, sc = dr.dm.tree(dr.prefix, roots, dr.feat.cuda(), k, D, N)
+        again = dr.dm.tree(dr.prefix, roots, dr.feat.cuda(), k, D, N)
+        assert all(np.array_equal(a, b) for a, b in zip((n, tok, par, sc), again)), "not deterministic"
+        compared = 0
+        for b in range(B):
+            assert n[b] == N + 1 and par[b, 0] == -1
+            assert all(0 <= par[b, i] < i for i in range(1, n[b]))
+
+            def step(ptree, feats, b=b):
+                r = od.draft_forward(dr.dow, ptree, feats, dr.kv[b], dr.prefix[b])
+                tk, lp = od.topk_logprobs(r.logits, k)
+                return tk, lp, r.regress
+
+            ex = od.expand_tree(roots[b], dr.feat[b].double().numpy(), step, k, D, N, gen.Tree)
+            assert np.max(np.abs(np.sort(sc[b, : n[b]]) - np.sort(ex.scores))) < 1e-2
+            if _decided(ex, k, D, N):
+                compared += 1
+                assert _path_set(n[b], tok[b], par[b]) == _path_set(ex.tree.n, ex.tree.tokens, ex.tree.parents)
+        say(f"draft {name}: trees compared {compared}/{B}")
+        assert compared >= 1
+    finally:
+        dr.close()
+
+
+def test_draft_errors():
+    import paper_2502_11018_amd as P
+    dr = Draft("tiny", 1, [30], max_tree=16)
+    try:
+        say("draft errors")
+        with pytest.raises(P.GriffinError):   # 1 + k (depth - 1) = 1 + 4 * 4 > 16
+            dr.dm.tree([30], [1], dr.feat[:1].cuda(), 4, 5, 12)
+        with pytest.raises(P.GriffinError):   # k > 16
+            dr.dm.step([30], [gen.chain_tree(1, [])], dr.feat[:1].cuda(), 17)
+        with pytest.raises(ValueError):        # features on the host
+            dr.dm.step([30], [gen.chain_tree(1, [])], dr.feat[:1], 4)
+    finally:
+        dr.close()
