@@ -143,6 +143,7 @@ def main():
     ap.add_argument("--no-profile", action="store_true")
     ap.add_argument("--no-graphs", action="store_true", help="plain launches instead of graph replay")
     ap.add_argument("--no-sampled", action="store_true", help="skip the temperature-1 (stochastic acceptance) leg")
+    ap.add_argument("--no-draft", action="store_true", help="skip the draft-model leg")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on exactly one GPU; --gpus {args.gpus} is not supported", file=sys.stderr)
@@ -319,6 +320,48 @@ def main():
                            "seeded random rows, so acceptance is synthetic"}
         log(f"T=1 cycle {t_cycle * 1e3:.3f} ms/step, stochastic acceptance {t_acc * 1e6:.1f} us")
 
+    # draft model of the same target: one pass (t-bar of the paper's latency
+    # model) and a whole 60-token depth-6 tree, then the modelled speedup
+    draft = None
+    from workloads.configs import DRAFTS
+    if not args.no_draft and m.name in DRAFTS:
+        ds = DRAFTS[m.name]
+        dw = gen.make_draft_weights(ds, 3, device=dev)
+        dm = P.DraftModel(ds, dw, weights, max_batch=w.batch, max_tree=64, max_depth=ds.depth,
+                          kv_capacity=w.kv_capacity())
+        for b in range(w.batch):
+            k, vv = gen.synthetic_kv(ds.layer, 0, b, prefix[b], 5, dev)
+            dm.write_prefix(b, k, vv)
+        feat = gen.draft_root_features(m.d_model, w.batch, 11, dev)
+        roots = [int(t.tokens[0]) for t in pool[0]]
+        biggest = [gen.random_tree((ds.k,) * (ds.depth - 1), m.vocab, 77 + b)[0] for b in range(w.batch)]
+        nd = min(args.steps, 20)
+        for _ in range(2):
+            dm.tree(prefix, roots, feat, ds.k, ds.depth, ds.n_total)
+            dm.step(prefix, biggest, feat, ds.k)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(nd):
+            dm.step(prefix, biggest, feat, ds.k)
+        t_pass = (time.perf_counter() - t0) * 1e3 / nd
+        t0 = time.perf_counter()
+        for _ in range(nd):
+            dn, _, _, _ = dm.tree(prefix, roots, feat, ds.k, ds.depth, ds.n_total)
+        t_tree = (time.perf_counter() - t0) * 1e3 / nd
+        dm.close()
+        sr = {str(tau): round(tau * ms_per_step / (ms_per_step + ds.depth * t_pass), 3) for tau in (4, 5, 6)}
+        cycle = {str(tau): round(tau * root_ms / (ms_per_step + t_tree), 3) for tau in (4, 5, 6)}
+        draft = {"params": ds.param_count(), "k": ds.k, "depth": ds.depth, "n_total": ds.n_total,
+                 "pass_ms": round(t_pass, 4), "pass_nodes": int(biggest[0].n), "tree_ms": round(t_tree, 4),
+                 "speedup_model": sr, "speedup_vs_plain_decoding": cycle,
+                 "note": "pass_ms = one draft pass over the largest expansion (1 + k (depth - 1) nodes), host "
+                         "round trip included; speedup_model = tau t / (t + depth * pass_ms) with t = ms_per_step "
+                         "(the paper's latency model); speedup_vs_plain_decoding = tau root_only_ms / (ms_per_step "
+                         "+ tree_ms); tau (tokens per cycle, bonus included) needs trained drafts and is a free "
+                         "parameter here"}
+        log(f"draft: pass {t_pass:.3f} ms ({biggest[0].n} nodes), tree {t_tree:.3f} ms, "
+            f"modelled speedup at tau 5: {sr['5']}x")
+
     gc.enable()
     gc.unfreeze()
     cpu = None
@@ -351,6 +394,7 @@ def main():
         "roofline": roofline,
         "kernels": kernels,
         "temperature_1": sampled,
+        "draft": draft,
         "cpu_baseline": cpu,
     }
     v.close()

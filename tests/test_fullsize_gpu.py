@@ -219,3 +219,67 @@ def test_full_size_ragged_chain2_batch_matches_oracle():
         say(f"llama3-8b-chain2-b16 seq {b}: max rel err {st['max_rel']:.2e}, gated {st['gated']}/{st['total']}, "
             f"accept checked {st['accept_checked']}, L={st['L']}")
     v.close()
+
+
+def test_full_size_draft_matches_oracle():
+    """The draft of the Llama-3-8B shape (TGF with expansion 11008, one
+    decoder layer, two heads: 0.42B parameters, the target's LM head), prefix
+    2048: the passes of a 60-token depth-6 expansion (k = 10) checked against
+    the oracle's draft pass on the same pass trees and input features."""
+    import paper_2502_11018_amd as P
+    from oracle import draft as od
+    from workloads.configs import DRAFTS
+    ds = DRAFTS["llama3-8b"]
+    m = ds.target
+    t0 = time.time()
+    say("llama3-8b draft: weights on the GPU")
+    mw_gpu = gen.make_weights(m, 0, device="cuda")
+    dw_gpu = gen.make_draft_weights(ds, 3, device="cuda")
+    P_len = 2048
+    dm = P.DraftModel(ds, dw_gpu, mw_gpu, max_batch=1, max_tree=64, max_depth=63, kv_capacity=P_len + 64)
+    k, v = gen.synthetic_kv(ds.layer, 0, 0, P_len, 5, "cuda")
+    dm.write_prefix(0, k, v)
+    kv = (k.double().cpu().numpy(), v.double().cpu().numpy())
+    feat = gen.draft_root_features(m.d_model, 1, 11, "cuda")
+    say(f"llama3-8b draft: GPU tree ({time.time() - t0:.0f}s)")
+    n, tok, par, sc = dm.tree([P_len], [7], feat, ds.k, ds.depth, ds.n_total)
+    assert n[0] == ds.n_total + 1
+    # replay the GPU's own pass trees on both sides: a pass tree is the root
+    # plus the nodes expanded so far; rebuild them from a fresh GPU expansion
+    # run pass by pass (the same code path as griffin_draft_tree)
+    say(f"llama3-8b draft: host copy for the oracle ({time.time() - t0:.0f}s)")
+    ow = oracle.OracleWeights(mw_gpu.to("cpu"), cache=True)
+    dow = od.DraftOracleWeights(dw_gpu.to("cpu"), ow)
+    fr = None
+    trees = [gen.Tree(np.array([7], np.int32), np.array([-1], np.int32))]
+    worst, compared, total = 0.0, 0, 0
+    for it in range(3):
+        t = trees[-1]
+        gtok, glp = dm.step([P_len], [t], feat, ds.k)
+        feats = np.zeros((t.n, m.d_model))
+        feats[0] = feat[0].double().cpu().numpy()
+        for i in range(1, t.n):
+            feats[i] = fr[t.parents[i]]
+        say(f"llama3-8b draft: oracle pass {it} over {t.n} nodes ({time.time() - t0:.0f}s)")
+        r = od.draft_forward(dow, t, feats, kv, P_len)
+        fr = r.regress
+        otok, _ = od.topk_logprobs(r.logits, ds.k)
+        srt = np.sort(r.logits, axis=1)[:, ::-1]
+        for i in range(t.n):
+            total += 1
+            full = r.logits[i] - (srt[i, 0] + np.log(np.exp(r.logits[i] - srt[i, 0]).sum()))
+            worst = max(worst, float(np.max(np.abs(glp[0, i] - full[gtok[0, i]]))))
+            if (-np.diff(srt[i, : ds.k + 1])).min() > 2e-3:
+                compared += 1
+                assert list(gtok[0, i]) == list(otok[i]), (it, i)
+        # next pass tree: the expansion's frontier from the GPU's own proposals
+        rows = [i for i in range(t.n) if t.depths()[i] == it]
+        cand = [(float(glp[0, r_, j]), r_, int(gtok[0, r_, j])) for r_ in rows for j in range(ds.k)]
+        best = sorted(range(len(cand)), key=lambda c: (-cand[c][0], c))[: ds.k]
+        toks = list(t.tokens) + [cand[c][2] for c in best]
+        pars = list(t.parents) + [cand[c][1] for c in best]
+        trees.append(gen.Tree(np.array(toks, np.int32), np.array(pars, np.int32)))
+    say(f"llama3-8b draft: log-prob error {worst:.2e}, tokens compared on {compared}/{total} rows "
+        f"({time.time() - t0:.0f}s)")
+    assert worst < 2e-3 and compared >= total // 2
+    dm.close()
