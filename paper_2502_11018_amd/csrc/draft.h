@@ -33,8 +33,10 @@ hipError_t launch_draft_front(const DraftArgs& a, const StepMeta& meta, int stag
 // TEH, stage 0: y = x + layer residual -> x_h; 1: F^R -> feat_r, RMSNorm(F^P) -> xn.
 hipError_t launch_draft_head(const DraftArgs& a, const StepMeta& meta, const ResidualAdd& add, int stage,
                              hipStream_t s);
-// Top-k (k <= 16) tokens and log-probabilities of every live row of logits [rows][ld].
+// Top-k (k <= 16) tokens and log-probabilities of every live row of logits
+// [rows][ld] (V <= 524288); `work` holds draft_topk_work_bytes(rows, V).
+size_t draft_topk_work_bytes(int rows, int V);
 hipError_t launch_draft_topk(const float* logits, long long ld, int V, const StepMeta& meta, int rows, int max_tree,
-                             int k, int32_t* tok, float* logp, hipStream_t s);
+                             int k, int32_t* tok, float* logp, float* work, hipStream_t s);
 
 }  // namespace griffin

@@ -145,144 +145,171 @@ __global__ __launch_bounds__(DR) void draft_head_out_kernel(DraftArgs a, StepMet
 }
 
 // Top-k tokens (value descending, lower id first on ties) and their
-// log-probabilities log softmax, one workgroup per live row.  One pass over
-// the row with several 16-byte loads in flight per thread: every thread keeps
-// a sorted list of its best DK candidates and a running maximum and sum of
-// exp (rescaled when the maximum grows); then k rounds of a block-wide argmax
-// over the list heads pick the winners (ties: lower id).
-constexpr int DK = 16;
-constexpr int TK = 1024;  // threads per row
-constexpr int TK_LOADS = 4;
+// log-probabilities log softmax.  Two launches, so that a handful of rows
+// still fills the chip: first every (row, vocabulary slice) workgroup holds
+// its slice in registers (32 logits a thread) and writes the slice's k best
+// candidates in order plus its maximum and sum of exp; then one wave per row
+// combines the slices' log-sum-exp and merges their sorted lists.
+constexpr int DK = 16;       // largest k
+constexpr int TS = 256;      // threads per slice workgroup
+constexpr int TE = 32;       // logits per thread
+constexpr int SLICE_MAX = TS * TE;
+constexpr int MAX_SLICES = 64;
+constexpr int PART_WORDS = 2 * DK + 2;  // values, ids, maximum, sum of exp
 
 __device__ __forceinline__ bool better(float va, int ia, float vb, int ib) {
   return va > vb || (va == vb && ia < ib);
 }
 
-struct TopList {
-  float v[DK];
-  int i[DK];
-  float m, s;  // running maximum, sum of exp(x - m)
+__host__ __device__ __forceinline__ int topk_slices(int V) { return (V + SLICE_MAX - 1) / SLICE_MAX; }
+__host__ __device__ __forceinline__ int topk_slice_len(int V) {
+  const int s = topk_slices(V);
+  return ((V + s - 1) / s + 3) & ~3;
+}
 
-  __device__ __forceinline__ void init() {
-#pragma unroll
-    for (int j = 0; j < DK; ++j) {
-      v[j] = -INFINITY;
-      i[j] = 0x7fffffff;
-    }
-    m = -INFINITY;
-    s = 0.f;
-  }
-  __device__ __forceinline__ void add(float x, int id) {
-    const float mn = fmaxf(m, x);
-    s = (mn == m ? s : s * expf(m - mn)) + (x > -INFINITY ? expf(x - mn) : 0.f);
-    m = mn;
-    if (better(x, id, v[DK - 1], i[DK - 1])) {  // insert, keeping the list sorted
-      float cv = x;
-      int ci = id;
-#pragma unroll
-      for (int j = 0; j < DK; ++j) {
-        const bool b = better(cv, ci, v[j], i[j]);
-        const float tv = v[j];
-        const int ti = i[j];
-        v[j] = b ? cv : tv;
-        i[j] = b ? ci : ti;
-        cv = b ? tv : cv;
-        ci = b ? ti : ci;
-      }
-    }
-  }
-};
-
-__global__ __launch_bounds__(TK) void draft_topk_kernel(const float* logits, long long ld, int V, StepMeta meta,
-                                                       int rows, int max_tree, int k, int32_t* tok_out,
-                                                       float* logp_out) {
-  __shared__ float wv[TK / 64], wm[TK / 64], wsum[TK / 64];
-  __shared__ int wi[TK / 64], ww[TK / 64];
-  __shared__ int win_thread;
-  const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+template <bool VEC>
+__global__ __launch_bounds__(TS) void draft_topk_slice_kernel(const float* logits, long long ld, int V, StepMeta meta,
+                                                             int rows, int max_tree, int k, float* part) {
+  __shared__ float wv[2][TS / 64], red[16];
+  __shared__ int wi[2][TS / 64];
+  const int r = blockIdx.x, slice = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   if (!draft_live(meta, r, rows, max_tree)) return;  // uniform
+  const int len = topk_slice_len(V), lo = slice * len, hi = min(V, lo + len);
   const float* lg = logits + (long long)r * ld;
-  TopList L;
-  L.init();
-  if ((V & 3) == 0) {
-    const float4* l4 = reinterpret_cast<const float4*>(lg);
-    const int n4 = V >> 2;
-    for (int base = tid; base < n4; base += TK * TK_LOADS) {
-      float4 x[TK_LOADS];
+  float x[TE];
+  unsigned taken = 0;  // bit j: element j is outside the slice or already chosen
+  auto id_of = [&](int j) { return VEC ? lo + 4 * (tid + (j >> 2) * TS) + (j & 3) : lo + tid + j * TS; };
+  if (VEC) {
+    const float4* l4 = reinterpret_cast<const float4*>(lg + lo);
 #pragma unroll
-      for (int u = 0; u < TK_LOADS; ++u) {
-        const int at = base + u * TK;
-        x[u] = at < n4 ? l4[at] : make_float4(-INFINITY, -INFINITY, -INFINITY, -INFINITY);
-      }
-#pragma unroll
-      for (int u = 0; u < TK_LOADS; ++u) {
-        const int id = 4 * (base + u * TK);
-        L.add(x[u].x, id);
-        L.add(x[u].y, id + 1);
-        L.add(x[u].z, id + 2);
-        L.add(x[u].w, id + 3);
-      }
+    for (int q = 0; q < TE / 4; ++q) {
+      const int at = lo + 4 * (tid + q * TS);
+      const float4 v = at < hi ? l4[tid + q * TS] : make_float4(0.f, 0.f, 0.f, 0.f);
+      x[4 * q] = v.x;
+      x[4 * q + 1] = v.y;
+      x[4 * q + 2] = v.z;
+      x[4 * q + 3] = v.w;
     }
   } else {
-    for (int v = tid; v < V; v += TK) L.add(lg[v], v);
+#pragma unroll
+    for (int j = 0; j < TE; ++j) {
+      const int at = lo + tid + j * TS;
+      x[j] = at < hi ? lg[at] : 0.f;
+    }
   }
-  // log-sum-exp over the row (fixed order: waves, then the waves' results)
-  float M = wave_max(L.m);
-  float S = wave_sum(L.m > -INFINITY ? L.s * expf(L.m - M) : 0.f);
-  if (lane == 0) {
-    wm[wave] = M;
-    wsum[wave] = S;
-  }
+#pragma unroll
+  for (int j = 0; j < TE; ++j)
+    if (id_of(j) >= hi) taken |= 1u << j;
+  // the slice's maximum and sum of exp (fixed order)
+  float m = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < TE; ++j)
+    if (!(taken >> j & 1)) m = fmaxf(m, x[j]);
+  m = wave_max(m);
   __syncthreads();
-  float gm = -INFINITY;
-  for (int w = 0; w < TK / 64; ++w) gm = fmaxf(gm, wm[w]);
-  float gs = 0.f;
-  for (int w = 0; w < TK / 64; ++w) gs += wm[w] > -INFINITY ? wsum[w] * expf(wm[w] - gm) : 0.f;
-  const float lse = gm + logf(gs);
+  if (lane == 0) red[wave] = m;
+  __syncthreads();
+  float M = red[0];
+  for (int w = 1; w < TS / 64; ++w) M = fmaxf(M, red[w]);
+  float e = 0.f;
+  if (M > -INFINITY) {
+#pragma unroll
+    for (int j = 0; j < TE; ++j)
+      if (!(taken >> j & 1)) e += expf(x[j] - M);
+  }
+  const float S = block_sum(e, red);
+  float* out = part + ((long long)r * gridDim.y + slice) * PART_WORDS;
+  if (tid == 0) {
+    out[2 * DK] = M;
+    out[2 * DK + 1] = S;
+  }
+  // k rounds of a block-wide argmax; the owner of the winner drops it
+  float bv = -INFINITY;
+  int bi = 0x7fffffff, bj = -1;
+  auto rescan = [&]() {
+    bv = -INFINITY;
+    bi = 0x7fffffff;
+    bj = -1;
+#pragma unroll
+    for (int j = 0; j < TE; ++j)
+      if (!(taken >> j & 1) && better(x[j], id_of(j), bv, bi)) {
+        bv = x[j];
+        bi = id_of(j);
+        bj = j;
+      }
+  };
+  rescan();
   for (int round = 0; round < k; ++round) {
-    // wave argmax of the list heads, then across the waves
-    float bv = L.v[0];
-    int bi = L.i[0], bt = tid;
+    float v = bv;
+    int i = bi;
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) {
-      const float ov = __shfl_xor(bv, o, 64);
-      const int oi = __shfl_xor(bi, o, 64), ot = __shfl_xor(bt, o, 64);
-      if (better(ov, oi, bv, bi)) {
-        bv = ov;
-        bi = oi;
-        bt = ot;
+      const float ov = __shfl_xor(v, o, 64);
+      const int oi = __shfl_xor(i, o, 64);
+      if (better(ov, oi, v, i)) {
+        v = ov;
+        i = oi;
       }
     }
-    __syncthreads();  // the previous round's readers of wv/wi/ww are done
+    const int buf = round & 1;  // two buffers: round r + 2 writes after every reader of round r passed round r + 1's barrier
     if (lane == 0) {
-      wv[wave] = bv;
-      wi[wave] = bi;
-      ww[wave] = bt;
+      wv[buf][wave] = v;
+      wi[buf][wave] = i;
     }
     __syncthreads();
-    if (tid == 0) {
-      float gv = wv[0];
-      int gi = wi[0], gt = ww[0];
-      for (int w = 1; w < TK / 64; ++w)
-        if (better(wv[w], wi[w], gv, gi)) {
-          gv = wv[w];
-          gi = wi[w];
-          gt = ww[w];
-        }
-      tok_out[(long long)r * k + round] = gi;
-      logp_out[(long long)r * k + round] = gv - lse;
-      win_thread = gt;
-    }
-    __syncthreads();
-    if (tid == win_thread) {  // pop the head
-#pragma unroll
-      for (int j = 0; j < DK - 1; ++j) {
-        L.v[j] = L.v[j + 1];
-        L.i[j] = L.i[j + 1];
+    float gv = wv[buf][0];
+    int gi = wi[buf][0];
+    for (int w = 1; w < TS / 64; ++w)
+      if (better(wv[buf][w], wi[buf][w], gv, gi)) {
+        gv = wv[buf][w];
+        gi = wi[buf][w];
       }
-      L.v[DK - 1] = -INFINITY;
-      L.i[DK - 1] = 0x7fffffff;
+    if (tid == 0) {
+      out[round] = gv;
+      out[DK + round] = __int_as_float(gi);
     }
+    if (bj >= 0 && bi == gi) {  // ids are unique: this thread held the winner
+      taken |= 1u << bj;
+      rescan();
+    }
+  }
+}
+
+__global__ __launch_bounds__(64) void draft_topk_merge_kernel(const float* part, int nslice, StepMeta meta, int rows,
+                                                             int max_tree, int k, int32_t* tok_out, float* logp_out) {
+  __shared__ float cv[MAX_SLICES * DK];
+  __shared__ int ci[MAX_SLICES * DK];
+  const int r = blockIdx.x, lane = threadIdx.x;
+  if (!draft_live(meta, r, rows, max_tree)) return;  // uniform
+  const float* pr = part + (long long)r * nslice * PART_WORDS;
+  const float Ms = lane < nslice ? pr[lane * PART_WORDS + 2 * DK] : -INFINITY;
+  const float Ss = lane < nslice ? pr[lane * PART_WORDS + 2 * DK + 1] : 0.f;
+  const float M = wave_max(Ms);
+  const float lse = M + logf(wave_sum(Ms > -INFINITY ? Ss * expf(Ms - M) : 0.f));
+  for (int q = lane; q < nslice * k; q += 64) {
+    cv[q] = pr[(q / k) * PART_WORDS + q % k];
+    ci[q] = __float_as_int(pr[(q / k) * PART_WORDS + DK + q % k]);
+  }
+  __syncthreads();
+  int head = 0;  // this lane's slice: next candidate of its sorted list
+  for (int round = 0; round < k; ++round) {
+    float v = lane < nslice && head < k ? cv[lane * k + head] : -INFINITY;
+    int i = lane < nslice && head < k ? ci[lane * k + head] : 0x7fffffff, w = lane;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const float ov = __shfl_xor(v, o, 64);
+      const int oi = __shfl_xor(i, o, 64), ow = __shfl_xor(w, o, 64);
+      if (better(ov, oi, v, i)) {
+        v = ov;
+        i = oi;
+        w = ow;
+      }
+    }
+    if (lane == 0) {
+      tok_out[(long long)r * k + round] = i;
+      logp_out[(long long)r * k + round] = v - lse;
+    }
+    if (lane == w) ++head;
   }
 }
 
@@ -308,11 +335,21 @@ hipError_t launch_draft_head(const DraftArgs& a, const StepMeta& meta, const Res
   return hipGetLastError();
 }
 
+size_t draft_topk_work_bytes(int rows, int V) {
+  return sizeof(float) * (size_t)rows * topk_slices(V) * PART_WORDS;
+}
+
 hipError_t launch_draft_topk(const float* logits, long long ld, int V, const StepMeta& meta, int rows, int max_tree,
-                             int k, int32_t* tok, float* logp, hipStream_t s) {
-  if (k < 1 || k > DK || V < k) return hipErrorInvalidValue;
-  if ((V & 3) == 0 && (ld & 3) != 0) return hipErrorInvalidValue;  // rows must stay 16-byte aligned
-  hipLaunchKernelGGL(draft_topk_kernel, dim3(rows), dim3(TK), 0, s, logits, ld, V, meta, rows, max_tree, k, tok,
+                             int k, int32_t* tok, float* logp, float* work, hipStream_t s) {
+  if (k < 1 || k > DK || V < k || topk_slices(V) > MAX_SLICES) return hipErrorInvalidValue;
+  const int ns = topk_slices(V);
+  if ((V & 3) == 0 && (ld & 3) == 0)  // 16-byte aligned rows and slices
+    hipLaunchKernelGGL(draft_topk_slice_kernel<true>, dim3(rows, ns), dim3(TS), 0, s, logits, ld, V, meta, rows,
+                       max_tree, k, work);
+  else
+    hipLaunchKernelGGL(draft_topk_slice_kernel<false>, dim3(rows, ns), dim3(TS), 0, s, logits, ld, V, meta, rows,
+                       max_tree, k, work);
+  hipLaunchKernelGGL(draft_topk_merge_kernel, dim3(rows), dim3(64), 0, s, work, ns, meta, rows, max_tree, k, tok,
                      logp);
   return hipGetLastError();
 }

@@ -542,6 +542,7 @@ struct griffin_draft {
   uint16_t *x_m = nullptr, *x_u = nullptr, *x_d = nullptr, *x_h = nullptr;
   int32_t* topk_tok = nullptr;
   float* topk_lp = nullptr;
+  float* topk_work = nullptr;
   int32_t* topk_tok_host = nullptr;
   float* topk_lp_host = nullptr;
   std::vector<void*> allocs;
@@ -1321,6 +1322,8 @@ void griffin_draft_free(griffin_draft* dc) {
   delete dc;
 }
 
+constexpr int kDraftMaxVocab = 64 * 8192;
+
 int griffin_draft_init(const griffin_model_desc* desc, int32_t tgf_dim, float ln_eps, const griffin_draft_weights* w,
                        const void* embed, const void* lm_head, const void* final_norm, void* k_cache, void* v_cache,
                        void* hip_stream, griffin_draft** out) {
@@ -1328,6 +1331,7 @@ int griffin_draft_init(const griffin_model_desc* desc, int32_t tgf_dim, float ln
   *out = nullptr;
   if (!desc || !w || !embed || !lm_head || !final_norm || tgf_dim < 1 || !(ln_eps > 0.f)) return GRIFFIN_EINVAL;
   if (desc->n_experts != 1) return GRIFFIN_ESHAPE;  // the draft's decoder layer is dense
+  if (desc->vocab > kDraftMaxVocab) return GRIFFIN_ESHAPE;  // the top-k's slice count
   const void* ptrs[] = {w->w_m, w->b_m, w->ln_h_g, w->ln_h_b, w->ln_x_g, w->ln_x_b, w->w_u, w->b_u, w->w_d,
                         w->b_d, w->w_p, w->b_p, w->w_r, w->b_r, w->attn_norm, w->w_qkv, w->w_o, w->mlp_norm,
                         w->w_gate_up, w->w_down};
@@ -1391,6 +1395,7 @@ int griffin_draft_init(const griffin_model_desc* desc, int32_t tgf_dim, float ln
             alloc((void**)&dc->x_d, 2LL * tiles * dc->p_d.ks_pad * XPACK_STEP) &&
             alloc((void**)&dc->x_h, 2LL * tiles * dc->p_h.ks_pad * XPACK_STEP) &&
             alloc((void**)&dc->topk_tok, 4LL * rows * 16) && alloc((void**)&dc->topk_lp, 4LL * rows * 16) &&
+            alloc((void**)&dc->topk_work, draft_topk_work_bytes(rows, desc->vocab)) &&
             hipHostMalloc((void**)&dc->topk_tok_host, 4LL * rows * 16, hipHostMallocDefault) == hipSuccess &&
             hipHostMalloc((void**)&dc->topk_lp_host, 4LL * rows * 16, hipHostMallocDefault) == hipSuccess;
   if (!ok) {
@@ -1457,7 +1462,7 @@ int griffin_draft_step(griffin_draft* dc, int32_t batch, const int32_t* prefix_l
   TRY(griffin_verify_step(c, batch, prefix_len, n_nodes, tokens, parents, dc->logits));
   const int rows = batch * d.max_tree;
   HIP_TRY(c, launch_draft_topk(dc->logits, d.vocab, d.vocab, c->meta, rows, d.max_tree, k, dc->topk_tok,
-                               dc->topk_lp, c->stream));
+                               dc->topk_lp, dc->topk_work, c->stream));
   HIP_TRY(c, hipMemcpyAsync(dc->topk_tok_host, dc->topk_tok, sizeof(int32_t) * rows * k, hipMemcpyDeviceToHost,
                             c->stream));
   HIP_TRY(c, hipMemcpyAsync(dc->topk_lp_host, dc->topk_lp, sizeof(float) * rows * k, hipMemcpyDeviceToHost,

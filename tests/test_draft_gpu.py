@@ -1,10 +1,12 @@
 """The draft model on the GPU, through the C ABI, against the fp64 oracle
 (oracle/draft.py) on the same seeded inputs.
 
-A draft pass: every live row's top-k tokens and log-probabilities.  Tokens
-are compared exactly where the oracle's k-th and (k+1)-th logits differ by
-more than TOKEN_GAP (fp32 / split-bf16 on the device, fp64 in the oracle);
-log-probabilities within LOGP_TOL.  A drafted tree: the set of root paths
+A draft pass: every live row's top-k tokens and log-probabilities.  The
+token of a rank is compared exactly where the oracle's logit of that rank
+is separated from both neighbouring ranks by more than TOKEN_GAP (fp32 /
+split-bf16 on the device, fp64 in the oracle); at every rank the token must
+carry that rank's oracle logit within TOKEN_GAP; log-probabilities within
+LOGP_TOL.  A drafted tree: the set of root paths
 equals the oracle's expansion wherever none of its selections (the
 frontier of each depth, the final n_total) is decided by a score gap below
 SCORE_GAP; other cases are counted.  Every case prints its name first.
@@ -65,7 +67,7 @@ def _pass_feats(dr, tree, fr_prev, root_feat):
     return f
 
 
-@pytest.mark.parametrize("name", ["tiny", "small-gqa"])
+@pytest.mark.parametrize("name", ["tiny", "small-gqa", "tiny-v20001", "tiny-v20000"])
 def test_draft_passes_match_oracle(name):
     """Three passes over growing trees, as an expansion runs them: the root
     alone, then its children, then grandchildren; each node reads its
@@ -91,13 +93,19 @@ def test_draft_passes_match_oracle(name):
                 otok, _ = od.topk_logprobs(r.logits, k)
                 srt = np.sort(r.logits, axis=1)[:, ::-1]
                 for i in range(t.n):
-                    total += 1
                     full = r.logits[i] - (srt[i, 0] + np.log(np.exp(r.logits[i] - srt[i, 0]).sum()))
                     assert np.max(np.abs(lp[b, i] - full[tok[b, i]])) < LOGP_TOL, (b, i)
-                    if (-np.diff(srt[i, : k + 1])).min() > TOKEN_GAP:
-                        compared += 1
-                        assert list(tok[b, i]) == list(otok[i]), (b, i, tok[b, i], otok[i])
-        say(f"draft {name}: tokens compared on {compared}/{total} rows")
+                    # valid at every rank: distinct tokens, each with its rank's value
+                    assert len(set(tok[b, i].tolist())) == k and tok[b, i].min() >= 0 and tok[b, i].max() < V
+                    assert np.max(np.abs(r.logits[i][tok[b, i]] - srt[i, :k])) <= TOKEN_GAP, (b, i)
+                    # unique where the rank's value is separated from both neighbours
+                    gap = -np.diff(srt[i, : k + 1])
+                    for j in range(k):
+                        total += 1
+                        if gap[j] > TOKEN_GAP and (j == 0 or gap[j - 1] > TOKEN_GAP):
+                            compared += 1
+                            assert tok[b, i, j] == otok[i, j], (b, i, j, tok[b, i], otok[i])
+        say(f"draft {name}: tokens compared at {compared}/{total} ranks")
         assert compared >= total // 2
     finally:
         dr.close()
@@ -130,7 +138,7 @@ def _path_set(n, tok, par):
     return out
 
 
-@pytest.mark.parametrize("name", ["tiny", "small-gqa"])
+@pytest.mark.parametrize("name", ["tiny", "small-gqa", "tiny-v20000"])
 def test_drafted_tree_matches_oracle_expansion(name):
     B = 3
     dr = Draft(name, B, [20, 61, 90])
@@ -153,9 +161,15 @@ def test_drafted_tree_matches_oracle_expansion(name):
                 return tk, lp, r.regress
 
             ex = od.expand_tree(roots[b], dr.feat[b].double().numpy(), step, k, D, N, gen.Tree)
-            assert np.max(np.abs(np.sort(sc[b, : n[b]]) - np.sort(ex.scores))) < 1e-2
+            # valid whatever near-ties decided: scores fall along every path, depth <= D
+            assert sc[b, 0] == 0 and all(sc[b, i] <= sc[b, par[b, i]] for i in range(1, n[b]))
+            depth = [0] * n[b]
+            for i in range(1, n[b]):
+                depth[i] = depth[par[b, i]] + 1
+            assert max(depth) <= D
             if _decided(ex, k, D, N):
                 compared += 1
+                assert np.max(np.abs(np.sort(sc[b, : n[b]]) - np.sort(ex.scores))) < 1e-2
                 assert _path_set(n[b], tok[b], par[b]) == _path_set(ex.tree.n, ex.tree.tokens, ex.tree.parents)
         say(f"draft {name}: trees compared {compared}/{B}")
         assert compared >= 1

@@ -212,6 +212,12 @@ DRAFTS: Dict[str, DraftShape] = {
     "llama3-8b": DraftShape(LLAMA3_8B, tgf_dim=11008),
     "tiny": DraftShape(TINY, tgf_dim=1000, k=4, depth=4, n_total=12),
     "small-gqa": DraftShape(SMALL_GQA, tgf_dim=1800, k=5, depth=5, n_total=20),
+    # vocabularies of several top-k slices (8192 logits each): one not a
+    # multiple of 4 (scalar loads), one with 16-byte loads and the largest k
+    "tiny-v20001": DraftShape(replace(TINY, name="tiny-v20001", vocab=20001), tgf_dim=1000, k=4, depth=4,
+                              n_total=12),
+    "tiny-v20000": DraftShape(replace(TINY, name="tiny-v20000", vocab=20000), tgf_dim=1000, k=16, depth=3,
+                              n_total=40),
 }
 
 
