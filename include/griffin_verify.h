@@ -273,10 +273,10 @@ typedef struct griffin_draft_weights {
 } griffin_draft_weights;
 
 /* Create a draft context.  desc: the target's shape (its n_layers is ignored:
- * the draft has one layer; n_experts must be 1; vocab at most 524288) with
- * the draft's own limits:
- * max_batch, max_tree (>= 1 + k * (depth - 1) expanded nodes and >= n_total + 1
- * drafted nodes), max_depth (>= depth - 1), kv_capacity.  embed, lm_head,
+ * the draft has one layer; n_experts must be 1; vocab at most 524288;
+ * d_model at most 8192) with the draft's own limits: max_batch, max_tree
+ * (>= 1 + k * (depth - 1) expanded nodes and >= n_total + 1 drafted nodes),
+ * max_depth (>= depth - 1), kv_capacity.  embed, lm_head,
  * final_norm: the target's (embed and final_norm borrowed, lm_head repacked).
  * k_cache, v_cache: the draft layer's cache, laid out as for
  * griffin_verify_init with one layer (prefix K/V of the draft layer).

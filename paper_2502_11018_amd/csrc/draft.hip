@@ -54,35 +54,94 @@ __global__ __launch_bounds__(DT) void draft_in_kernel(DraftArgs a, StepMeta meta
   }
 }
 
+// Per-row reductions hold a row in registers: RV values per thread.
+constexpr int RV = 8;  // d <= DR * RV
+
+// acc[j] += the split-K partials of column threadIdx.x + j * DR of the row at
+// `at`, in split order; four splits' loads are issued together.
+__device__ __forceinline__ void add_parts(float (&acc)[RV], const float* parts, int n, long long stride, long long at,
+                                          int d) {
+  for (int p0 = 0; p0 < n; p0 += 4) {
+    float t[4][RV];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int j = 0; j < RV; ++j) {
+        const int k = threadIdx.x + j * DR;
+        t[u][j] = p0 + u < n && k < d ? parts[(p0 + u) * stride + at + k] : 0.f;
+      }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+      for (int j = 0; j < RV; ++j) acc[j] += t[u][j];
+  }
+}
+
+// Two block-wide sums at once (fixed order).
+__device__ __forceinline__ float2 block_sum2(float x, float y, float* red /* >= 32 floats */) {
+  x = wave_sum(x);
+  y = wave_sum(y);
+  const int w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) {
+    red[w] = x;
+    red[16 + w] = y;
+  }
+  __syncthreads();
+  float sx = 0.f, sy = 0.f;
+  for (int i = 0; i < nw; ++i) {
+    sx += red[i];
+    sy += red[16 + i];
+  }
+  return make_float2(sx, sy);
+}
+
 // h = sum of the W_m partials + b_m (kept), then [LN(h), LN(e)] as the
 // operand of W_u (K = 2d).
 __global__ __launch_bounds__(DR) void draft_fuse_kernel(DraftArgs a, StepMeta meta) {
-  __shared__ float red[16];
+  __shared__ float red[32];
   const int r = blockIdx.x, d = a.d;
   const bool live = draft_live(meta, r, a.rows, a.max_tree);
-  float* h = a.h + (long long)r * d;
   const uint16_t* e = a.embed + (long long)meta.token[min(r, a.rows - 1)] * d;
+  float hv[RV], ev[RV];
+#pragma unroll
+  for (int j = 0; j < RV; ++j) {
+    const int k = threadIdx.x + j * DR;
+    hv[j] = 0.f;
+    ev[j] = k < d ? bf16_to_f32(e[k]) : 0.f;
+  }
+  if (live) add_parts(hv, a.parts, a.n_parts_m, a.stride_m, (long long)r * d, d);
   float sh = 0.f, se = 0.f;
-  for (int k = threadIdx.x; k < d; k += DR) {
-    const float v = live ? sum_parts(a.parts, a.n_parts_m, a.stride_m, (long long)r * d + k) + bf16_to_f32(a.b_m[k])
-                         : 0.f;
-    h[k] = v;
-    sh += v;
-    se += bf16_to_f32(e[k]);
+#pragma unroll
+  for (int j = 0; j < RV; ++j) {
+    const int k = threadIdx.x + j * DR;
+    if (k < d) {
+      hv[j] = live ? hv[j] + bf16_to_f32(a.b_m[k]) : 0.f;
+      a.h[(long long)r * d + k] = hv[j];
+      sh += hv[j];
+      se += ev[j];
+    }
   }
-  const float mh = dblock_sum(sh, red) / d, me = dblock_sum(se, red) / d;
+  const float2 mean = block_sum2(sh, se, red);
+  const float mh = mean.x / d, me = mean.y / d;
   float vh = 0.f, ve = 0.f;
-  for (int k = threadIdx.x; k < d; k += DR) {
-    const float dh = h[k] - mh, de = bf16_to_f32(e[k]) - me;
-    vh += dh * dh;
-    ve += de * de;
-  }
-  const float rh = rsqrtf(dblock_sum(vh, red) / d + a.ln_eps), re = rsqrtf(dblock_sum(ve, red) / d + a.ln_eps);
-  for (int k = threadIdx.x; k < d; k += DR) {
-    const float lh = (h[k] - mh) * rh * bf16_to_f32(a.ln_h_g[k]) + bf16_to_f32(a.ln_h_b[k]);
-    const float le = (bf16_to_f32(e[k]) - me) * re * bf16_to_f32(a.ln_x_g[k]) + bf16_to_f32(a.ln_x_b[k]);
-    put_split(a.x_u, xpack_off(r, k, a.ks_u), live ? lh : 0.f);
-    put_split(a.x_u, xpack_off(r, d + k, a.ks_u), live ? le : 0.f);
+#pragma unroll
+  for (int j = 0; j < RV; ++j)
+    if (threadIdx.x + j * DR < d) {
+      vh += (hv[j] - mh) * (hv[j] - mh);
+      ve += (ev[j] - me) * (ev[j] - me);
+    }
+  const float2 var = block_sum2(vh, ve, red);
+  const float rh = rsqrtf(var.x / d + a.ln_eps), re = rsqrtf(var.y / d + a.ln_eps);
+#pragma unroll
+  for (int j = 0; j < RV; ++j) {
+    const int k = threadIdx.x + j * DR;
+    if (k < d) {
+      const float lh = (hv[j] - mh) * rh * bf16_to_f32(a.ln_h_g[k]) + bf16_to_f32(a.ln_h_b[k]);
+      const float le = (ev[j] - me) * re * bf16_to_f32(a.ln_x_g[k]) + bf16_to_f32(a.ln_x_b[k]);
+      put_split(a.x_u, xpack_off(r, k, a.ks_u), live ? lh : 0.f);
+      put_split(a.x_u, xpack_off(r, d + k, a.ks_u), live ? le : 0.f);
+    }
   }
 }
 
@@ -125,23 +184,33 @@ __global__ __launch_bounds__(DT) void draft_head_in_kernel(DraftArgs a, StepMeta
 // F^P and F^R from the head partials; F^R is kept for the next pass, and
 // RMSNorm(F^P) times the final norm's gain becomes the LM head's operand.
 __global__ __launch_bounds__(DR) void draft_head_out_kernel(DraftArgs a, StepMeta meta) {
-  __shared__ float red[16];
+  __shared__ float red[32];
   const int r = blockIdx.x, d = a.d;
   const bool live = draft_live(meta, r, a.rows, a.max_tree);
-  float* fp = a.feat_p + (long long)r * d;
-  float* fr = a.feat_r + (long long)r * d;
-  float ss = 0.f;
-  for (int k = threadIdx.x; k < d; k += DR) {
-    const long long at = (long long)r * 2 * d + k;
-    const float p = live ? sum_parts(a.parts, a.n_parts_h, a.stride_h, at) + bf16_to_f32(a.b_p[k]) : 0.f;
-    const float q = live ? sum_parts(a.parts, a.n_parts_h, a.stride_h, at + d) + bf16_to_f32(a.b_r[k]) : 0.f;
-    fp[k] = p;
-    if (live) fr[k] = q;
-    ss += p * p;
+  float pv[RV], qv[RV];
+#pragma unroll
+  for (int j = 0; j < RV; ++j) pv[j] = qv[j] = 0.f;
+  if (live) {
+    add_parts(pv, a.parts, a.n_parts_h, a.stride_h, (long long)r * 2 * d, d);
+    add_parts(qv, a.parts, a.n_parts_h, a.stride_h, (long long)r * 2 * d + d, d);
   }
-  const float inv = rsqrtf(dblock_sum(ss, red) / d + a.rms_eps);
-  for (int k = threadIdx.x; k < d; k += DR)
-    put_split(a.xn, xpack_off(r, k, a.xn_ks), live ? fp[k] * inv * bf16_to_f32(a.final_norm[k]) : 0.f);
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < RV; ++j) {
+    const int k = threadIdx.x + j * DR;
+    if (k < d) {
+      pv[j] = live ? pv[j] + bf16_to_f32(a.b_p[k]) : 0.f;
+      a.feat_p[(long long)r * d + k] = pv[j];
+      if (live) a.feat_r[(long long)r * d + k] = qv[j] + bf16_to_f32(a.b_r[k]);
+      ss += pv[j] * pv[j];
+    }
+  }
+  const float inv = rsqrtf(block_sum2(ss, 0.f, red).x / d + a.rms_eps);
+#pragma unroll
+  for (int j = 0; j < RV; ++j) {
+    const int k = threadIdx.x + j * DR;
+    if (k < d) put_split(a.xn, xpack_off(r, k, a.xn_ks), live ? pv[j] * inv * bf16_to_f32(a.final_norm[k]) : 0.f);
+  }
 }
 
 // Top-k tokens (value descending, lower id first on ties) and their

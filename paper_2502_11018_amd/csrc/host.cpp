@@ -1323,6 +1323,7 @@ void griffin_draft_free(griffin_draft* dc) {
 }
 
 constexpr int kDraftMaxVocab = 64 * 8192;
+constexpr int kDraftMaxDim = 8192;
 
 int griffin_draft_init(const griffin_model_desc* desc, int32_t tgf_dim, float ln_eps, const griffin_draft_weights* w,
                        const void* embed, const void* lm_head, const void* final_norm, void* k_cache, void* v_cache,
@@ -1332,6 +1333,7 @@ int griffin_draft_init(const griffin_model_desc* desc, int32_t tgf_dim, float ln
   if (!desc || !w || !embed || !lm_head || !final_norm || tgf_dim < 1 || !(ln_eps > 0.f)) return GRIFFIN_EINVAL;
   if (desc->n_experts != 1) return GRIFFIN_ESHAPE;  // the draft's decoder layer is dense
   if (desc->vocab > kDraftMaxVocab) return GRIFFIN_ESHAPE;  // the top-k's slice count
+  if (desc->d_model > kDraftMaxDim) return GRIFFIN_ESHAPE;   // rows held in registers
   const void* ptrs[] = {w->w_m, w->b_m, w->ln_h_g, w->ln_h_b, w->ln_x_g, w->ln_x_b, w->w_u, w->b_u, w->w_d,
                         w->b_d, w->w_p, w->b_p, w->w_r, w->b_r, w->attn_norm, w->w_qkv, w->w_o, w->mlp_norm,
                         w->w_gate_up, w->w_down};
