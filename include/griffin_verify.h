@@ -54,7 +54,7 @@ extern "C" {
 #define GRIFFIN_ETREE (-3)     /* malformed tree: parents[0] != -1, parent not in [0,i), n out of [1,max_tree], depth > max_depth */
 #define GRIFFIN_ETOKEN (-4)    /* token id outside [0, vocab) */
 #define GRIFFIN_ECAPACITY (-5) /* prefix_len < 0 or prefix_len + n > kv_capacity */
-#define GRIFFIN_EORDER (-6)    /* griffin_accept / griffin_read_predictions before any step */
+#define GRIFFIN_EORDER (-6)    /* griffin_accept / griffin_read_predictions / griffin_read_features before any step */
 #define GRIFFIN_ENOMEM (-7)    /* device or pinned host allocation failed */
 #define GRIFFIN_EHIP (-8)      /* a HIP runtime call failed; griffin_last_error has the text */
 #define GRIFFIN_ENUMERIC (-9)  /* a NaN appeared in the logits of a valid tree node */
@@ -193,6 +193,17 @@ int griffin_commit(griffin_ctx *ctx);
  * Errors: EORDER, EHIP. */
 int griffin_read_predictions(griffin_ctx *ctx, int32_t *pred);
 
+/* The target's features of chosen nodes of the last step: the hidden state
+ * after the last layer, before the final norm, i.e. the feature that
+ * EAGLE-style drafting predicts and feeds back (Sec. 3; the draft of Sec. 4.2
+ * takes the feature of the token before each input token).  nodes host
+ * [batch][n], node ids of that step's trees, -1 for a zero row; out device
+ * fp32 [batch][n][d_model], written in stream order after the step (valid
+ * until the next step; no synchronisation).  1 <= batch <= the step's batch,
+ * 1 <= n <= max_tree.  Errors: EINVAL, EORDER (no step yet), ETREE (a node
+ * that is not in its sequence's tree), EHIP. */
+int griffin_read_features(griffin_ctx *ctx, int32_t batch, int32_t n, const int32_t *nodes, float *out);
+
 /* Replay the launch sequence of a step from a captured HIP graph (default:
  * enabled).  One graph is captured per (batch, logits_out) pair on its first
  * step and replayed afterwards (at most 8 are kept, the oldest is dropped);
@@ -302,6 +313,19 @@ griffin_ctx *griffin_draft_context(griffin_draft *draft);
 int griffin_draft_step(griffin_draft *draft, int32_t batch, const int32_t *prefix_len, const int32_t *n_nodes,
                        const int32_t *tokens, const int32_t *parents, const float *root_features, int32_t k,
                        int32_t *topk_tokens, float *topk_logp);
+
+/* Extend the draft's own cache by accepted tokens: for sequence b, the
+ * n_tokens[b] tokens tokens[b][0..n) (host [batch][max_tree]) at positions
+ * prefix_len[b] + j, with input features features (device fp32
+ * [batch][max_tree][d]; row j is the target's feature of the token before
+ * token j, see griffin_read_features).  One draft pass over each chain that
+ * stops once the decoder layer has written the chain's K/V to cache slots
+ * prefix_len[b] + j; the caller continues with prefix_len + n_tokens.
+ * Enqueued on the draft's stream, no synchronisation.  Errors: EINVAL, ETREE
+ * (n_tokens outside [1, min(max_tree, max_depth + 1)]), ETOKEN, ECAPACITY,
+ * EHIP. */
+int griffin_draft_extend(griffin_draft *draft, int32_t batch, const int32_t *prefix_len, const int32_t *n_tokens,
+                         const int32_t *tokens, const float *features);
 
 /* Draft a tree for each of `batch` sequences by dynamic expansion (the paper
  * follows EAGLE-2's configuration: 60 draft tokens, depth 6): `depth` draft

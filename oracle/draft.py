@@ -81,6 +81,8 @@ class DraftResult:
     h: np.ndarray         # TGF fusion [T, d]
     o: np.ndarray         # TGF output = decoder-layer input [T, d]
     y: np.ndarray         # decoder-layer output [T, d]
+    k: np.ndarray = None  # the decoder layer's K of the nodes [T, Hkv, dh], post-rotary
+    v: np.ndarray = None  # and V [T, Hkv, dh]: what the pass adds to the draft's cache
 
 
 def draft_forward(dow: DraftOracleWeights, tree, feats_in: np.ndarray, prefix_kv: Tuple[np.ndarray, np.ndarray],
@@ -109,7 +111,7 @@ def draft_forward(dow: DraftOracleWeights, tree, feats_in: np.ndarray, prefix_kv
     fp = y @ t["w_p"].T + t["b_p"]
     fr = y @ t["w_r"].T + t["b_r"]
     logits = rmsnorm(fp, dow.target.final_norm, m.rms_eps) @ dow.target.lm_head().T
-    return DraftResult(logits, fp, fr, h, o, y)
+    return DraftResult(logits, fp, fr, h, o, y, k, v)
 
 
 def topk_logprobs(logits: np.ndarray, k: int) -> Tuple[np.ndarray, np.ndarray]:

@@ -10,7 +10,7 @@ can run without it) and its absence raises ImportError.
 _EXPORTS = {
     "AcceptResult": "verifier", "TreeVerifier": "verifier", "accept_walk": "verifier", "accept_sampled_walk": "verifier", "pack_trees": "verifier",
     "tree_prepare": "verifier", "GriffinError": "_native", "STATUS": "_native", "KERNEL_CLASSES": "_native",
-    "DraftModel": "draft",
+    "DraftModel": "draft", "SpeculativeCycle": "cycle",
 }
 
 

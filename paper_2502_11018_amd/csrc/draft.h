@@ -15,6 +15,7 @@ struct DraftArgs {
   float ln_eps, rms_eps;
   const uint16_t* embed;     // target's embedding [V][d] (bf16)
   const float* root_feat;    // [batch][d] input feature of each root
+  const float* node_feat;    // [rows][d] input feature of every node, or null (then root_feat / feat_r)
   float* feat_r;             // [rows][d] regress features (input of the next pass)
   float* feat_p;             // [rows][d] predict features
   float* h;                  // [mpad][d] TGF fusion h

@@ -11,7 +11,8 @@
 // and write the next GEMM's split-bf16 operand.  Rows are b * max_tree + i;
 // rows of absent nodes get zero operands.  A node's input feature is its
 // parent's regress feature from the previous draft pass (the root's is the
-// caller's).
+// caller's), unless the caller gives every node's feature (a draft catching
+// up on accepted tokens with the target's features).
 
 #include "device_common.h"
 #include "draft.h"
@@ -45,8 +46,9 @@ __global__ __launch_bounds__(DT) void draft_in_kernel(DraftArgs a, StepMeta meta
   const int r = blockIdx.x, d = a.d;
   const bool live = draft_live(meta, r, a.rows, a.max_tree);
   const int b = r / a.max_tree, i = r % a.max_tree;
-  const float* f = i == 0 ? a.root_feat + (long long)b * d
-                          : a.feat_r + ((long long)b * a.max_tree + meta.parent[min(r, a.rows - 1)]) * d;
+  const float* f = a.node_feat ? a.node_feat + (long long)min(r, a.rows - 1) * d
+                  : i == 0    ? a.root_feat + (long long)b * d
+                              : a.feat_r + ((long long)b * a.max_tree + meta.parent[min(r, a.rows - 1)]) * d;
   const uint16_t* e = a.embed + (long long)meta.token[min(r, a.rows - 1)] * d;
   for (int k = blockIdx.y * DT + threadIdx.x; k < 2 * d; k += gridDim.y * DT) {
     const float v = !live ? 0.f : (k < d ? f[k] : bf16_to_f32(e[k - d]));

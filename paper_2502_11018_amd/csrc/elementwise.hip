@@ -444,6 +444,19 @@ hipError_t launch_commit(const int32_t* result, int max_depth, StepMeta meta, in
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------- row gather ----
+__global__ __launch_bounds__(256) void gather_rows_kernel(const float* __restrict__ x, int d,
+                                                          const int32_t* __restrict__ rows, float* __restrict__ out) {
+  const int j = blockIdx.x, r = rows[j];
+  float* o = out + (long long)j * d;
+  for (int k = threadIdx.x; k < d; k += 256) o[k] = r < 0 ? 0.f : x[(long long)r * d + k];
+}
+
+hipError_t launch_gather_rows(const float* x, int d, const int32_t* rows, int n, float* out, hipStream_t s) {
+  hipLaunchKernelGGL(gather_rows_kernel, dim3(n), dim3(256), 0, s, x, d, rows, out);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------ MoE router ----
 // For a valid row: h = RMSNorm(x) (fp32, from the fp32 residual), router
 // logits h . w_e in fp32, softmax, keep the top_k experts (ties to the lower

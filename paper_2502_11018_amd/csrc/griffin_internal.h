@@ -152,6 +152,8 @@ hipError_t launch_argmax_reduce(const float* pmax, const int32_t* pidx, const in
 hipError_t launch_commit(const int32_t* result, int max_depth, StepMeta meta, int batch, int n_layers, int Hkv,
                          int dh, int kv_cap, long long layer_kv, uint16_t* k_cache, uint16_t* v_cache,
                          hipStream_t s);
+// out[j] = row rows[j] of x ([*][d] fp32), or zeros where rows[j] < 0; n rows.
+hipError_t launch_gather_rows(const float* x, int d, const int32_t* rows, int n, float* out, hipStream_t s);
 hipError_t launch_accept(StepMeta meta, const int32_t* pred, const int32_t* nan_row, int batch,
                          int max_tree, int max_depth, int32_t* result, hipStream_t s);
 hipError_t launch_moe_route(const float* x, const uint16_t* gain, float eps, const uint16_t* w_router,

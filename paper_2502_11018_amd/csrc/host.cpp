@@ -242,6 +242,7 @@ struct griffin_ctx {
   struct GraphEntry {
     int batch;
     float* logits;
+    bool kv_only;
     hipGraphExec_t exec;
   };
   std::vector<GraphEntry> graphs;
@@ -256,6 +257,13 @@ struct griffin_ctx {
   // heads (back: writes xn); it runs no argmax or acceptance.
   std::function<int(griffin_ctx*, hipStream_t)> front;
   std::function<int(griffin_ctx*, const ResidualAdd&, hipStream_t)> back;
+  // a pass that ends once the last layer has written the nodes' K/V (a
+  // draft catching up on accepted tokens)
+  bool kv_only = false;
+  // griffin_read_features: rows of x to gather, staged through pinned memory
+  int32_t* feat_rows = nullptr;
+  int32_t* feat_rows_host = nullptr;
+  hipEvent_t feat_ev = nullptr;
   std::string err;
 };
 
@@ -375,6 +383,7 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
     LAUNCH(GRIFFIN_KC_ROPE, launch_qkv_rope(c->parts, c->p_qkv.out_splits(), ps * c->qkv_n, c->meta, c->rope_cos,
                                             c->rope_sin, d.n_q_heads, d.n_kv_heads, d.head_dim, d.max_tree, B,
                                             d.kv_capacity, c->q, c->q_lo, kc, vc, c->tree, s));
+    if (c->kv_only && l == d.n_layers - 1) return GRIFFIN_OK;
     {
       AttnArgs a{};
       a.q = c->q;
@@ -500,7 +509,7 @@ constexpr size_t kMaxGraphs = 8;
 int run_pass(griffin_ctx* c, float* logits_out) {
   if (!c->use_graphs || c->prof_mask != 0 || c->stream == nullptr) return enqueue_pass(c, logits_out);
   for (auto& g : c->graphs)
-    if (g.batch == c->batch && g.logits == logits_out) {
+    if (g.batch == c->batch && g.logits == logits_out && g.kv_only == c->kv_only) {
       HIP_TRY(c, hipGraphLaunch(g.exec, c->stream));
       return GRIFFIN_OK;
     }
@@ -521,7 +530,7 @@ int run_pass(griffin_ctx* c, float* logits_out) {
     hipGraphExecDestroy(c->graphs.front().exec);
     c->graphs.erase(c->graphs.begin());
   }
-  c->graphs.push_back({c->batch, logits_out, exec});
+  c->graphs.push_back({c->batch, logits_out, c->kv_only, exec});
   HIP_TRY(c, hipGraphLaunch(exec, c->stream));
   return GRIFFIN_OK;
 }
@@ -538,6 +547,7 @@ struct griffin_draft {
   uint16_t *pk_m = nullptr, *pk_u = nullptr, *pk_d = nullptr, *pk_h = nullptr;
   const uint16_t *b_m, *ln_h_g, *ln_h_b, *ln_x_g, *ln_x_b, *b_u, *b_d, *b_p, *b_r;
   float *parts = nullptr, *h = nullptr, *feat_r = nullptr, *feat_p = nullptr, *root_feat = nullptr;
+  float* node_feat = nullptr;  // [max_batch * max_tree][d]: griffin_draft_extend's features
   float* logits = nullptr;
   uint16_t *x_m = nullptr, *x_u = nullptr, *x_d = nullptr, *x_h = nullptr;
   int32_t* topk_tok = nullptr;
@@ -563,6 +573,7 @@ DraftArgs draft_args(griffin_draft* dc, griffin_ctx* c) {
   a.rms_eps = d.rms_eps;
   a.embed = c->embed;
   a.root_feat = dc->root_feat;
+  a.node_feat = c->kv_only ? dc->node_feat : nullptr;
   a.feat_r = dc->feat_r;
   a.feat_p = dc->feat_p;
   a.h = dc->h;
@@ -657,6 +668,8 @@ void griffin_verify_free(griffin_ctx* c) {
   if (c->result_host) hipHostFree(c->result_host);
   if (c->pred_host) hipHostFree(c->pred_host);
   if (c->samp_host) hipHostFree(c->samp_host);
+  if (c->feat_rows_host) hipHostFree(c->feat_rows_host);
+  if (c->feat_ev) hipEventDestroy(c->feat_ev);
   delete c;
 }
 
@@ -761,6 +774,7 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
   ALLOC(c->pidx, Mp * lm_parts);
   ALLOC(c->pnan, Mp * lm_parts);
   ALLOC(c->pred, Mp);
+  ALLOC(c->feat_rows, (long long)d.max_batch * d.max_tree);
   ALLOC(c->nan_row, Mp);
   ALLOC(c->result, (long long)d.max_batch * result_stride(d.max_depth));
   ALLOC(c->samp_scratch, sampled_scratch_bytes(d.max_batch, d.max_tree, d.vocab));
@@ -884,7 +898,10 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
                     hipHostMallocDefault) != hipSuccess ||
       hipHostMalloc((void**)&c->pred_host, sizeof(int32_t) * Mp, hipHostMallocDefault) != hipSuccess ||
       hipHostMalloc((void**)&c->samp_host, sizeof(float) * 5 * d.max_batch * d.max_tree, hipHostMallocDefault) !=
-          hipSuccess) {
+          hipSuccess ||
+      hipHostMalloc((void**)&c->feat_rows_host, sizeof(int32_t) * d.max_batch * d.max_tree, hipHostMallocDefault) !=
+          hipSuccess ||
+      hipEventCreateWithFlags(&c->feat_ev, hipEventDisableTiming) != hipSuccess) {
     griffin_verify_free(c);
     return GRIFFIN_ENOMEM;
   }
@@ -1094,6 +1111,28 @@ int griffin_read_predictions(griffin_ctx* c, int32_t* pred) {
     const int b = r / c->d.max_tree, i = r % c->d.max_tree;
     pred[r] = i < nodes[b] ? c->pred_host[r] : -1;
   }
+  return GRIFFIN_OK;
+}
+
+int griffin_read_features(griffin_ctx* c, int32_t batch, int32_t n, const int32_t* nodes, float* out) {
+  if (!c || !nodes || !out) return GRIFFIN_EINVAL;
+  if (!c->stepped) return set_err(c, GRIFFIN_EORDER, "no verification step has been enqueued");
+  if (batch < 1 || batch > c->batch || n < 1 || n > c->d.max_tree)
+    return set_err(c, GRIFFIN_EINVAL, "batch must be in [1, the last step's batch] and n in [1, max_tree]");
+  const int32_t* n_nodes = reinterpret_cast<const int32_t*>(c->meta_host[c->meta_cur] + c->off_nodes);
+  HIP_TRY(c, hipEventSynchronize(c->feat_ev));  // the previous call's upload has left the staging buffer
+  for (int b = 0; b < batch; ++b)
+    for (int j = 0; j < n; ++j) {
+      const int node = nodes[(size_t)b * n + j];
+      if (node < -1 || node >= n_nodes[b])
+        return set_err(c, GRIFFIN_ETREE, "sequence " + std::to_string(b) + ": node " + std::to_string(node) +
+                                             " is not a node of the last step");
+      c->feat_rows_host[(size_t)b * n + j] = node < 0 ? -1 : b * c->d.max_tree + node;
+    }
+  HIP_TRY(c, hipMemcpyAsync(c->feat_rows, c->feat_rows_host, sizeof(int32_t) * batch * n, hipMemcpyHostToDevice,
+                            c->stream));
+  HIP_TRY(c, hipEventRecord(c->feat_ev, c->stream));
+  HIP_TRY(c, launch_gather_rows(c->x, c->d.d_model, c->feat_rows, batch * n, out, c->stream));
   return GRIFFIN_OK;
 }
 
@@ -1391,6 +1430,7 @@ int griffin_draft_init(const griffin_model_desc* desc, int32_t tgf_dim, float ln
             alloc((void**)&dc->parts, 4 * parts) && alloc((void**)&dc->h, 4LL * mpad * d) &&
             alloc((void**)&dc->feat_r, 4LL * rows * d) && alloc((void**)&dc->feat_p, 4LL * mpad * d) &&
             alloc((void**)&dc->root_feat, 4LL * desc->max_batch * d) &&
+            alloc((void**)&dc->node_feat, 4LL * rows * d) &&
             alloc((void**)&dc->logits, 4LL * rows * desc->vocab) &&
             alloc((void**)&dc->x_m, 2LL * tiles * dc->p_m.ks_pad * XPACK_STEP) &&
             alloc((void**)&dc->x_u, 2LL * tiles * dc->p_u.ks_pad * XPACK_STEP) &&
@@ -1474,6 +1514,29 @@ int griffin_draft_step(griffin_draft* dc, int32_t batch, const int32_t* prefix_l
   memcpy(topk_logp, dc->topk_lp_host, sizeof(float) * rows * k);
   c->stepped = false;  // a draft pass has no acceptance result
   return GRIFFIN_OK;
+}
+
+int griffin_draft_extend(griffin_draft* dc, int32_t batch, const int32_t* prefix_len, const int32_t* n_tokens,
+                         const int32_t* tokens, const float* features) {
+  if (!dc) return GRIFFIN_EINVAL;
+  griffin_ctx* c = dc->inner;
+  const griffin_model_desc& d = c->d;
+  const int T = d.max_tree;
+  if (!prefix_len || !n_tokens || !tokens || !features || batch < 1 || batch > d.max_batch)
+    return set_err(c, GRIFFIN_EINVAL, "bad draft extend arguments");
+  std::vector<int32_t> par((size_t)batch * T, -1);
+  for (int b = 0; b < batch; ++b) {
+    if (n_tokens[b] < 1 || n_tokens[b] > T || n_tokens[b] - 1 > d.max_depth)
+      return set_err(c, GRIFFIN_ETREE, "n_tokens must be in [1, min(max_tree, max_depth + 1)]");
+    for (int i = 1; i < n_tokens[b]; ++i) par[(size_t)b * T + i] = i - 1;  // a chain: node i at prefix_len + i
+  }
+  HIP_TRY(c, hipMemcpyAsync(dc->node_feat, features, sizeof(float) * batch * T * dc->d, hipMemcpyDeviceToDevice,
+                            c->stream));
+  c->kv_only = true;
+  const int rc = griffin_verify_step(c, batch, prefix_len, n_tokens, tokens, par.data(), nullptr);
+  c->kv_only = false;
+  c->stepped = false;  // nothing to accept or commit: the chain's K/V already sit at their positions
+  return rc;
 }
 
 int griffin_draft_tree(griffin_draft* dc, int32_t batch, const int32_t* prefix_len, const int32_t* root_tokens,

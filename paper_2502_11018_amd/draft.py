@@ -76,6 +76,26 @@ class DraftModel:
         _check(rc, "griffin_draft_step", self._ctx())
         return ktok.reshape(B, self.max_tree, k), klp.reshape(B, self.max_tree, k)
 
+    def extend(self, prefix_len, tokens: Sequence, features: torch.Tensor):
+        """Write the draft layer's K/V of accepted tokens into its cache:
+        tokens[b] (a list) at positions prefix_len[b] + j, features a CUDA
+        float32 tensor [B, max_tree, d] whose row j is the target's feature of
+        the token before tokens[b][j].  The caller continues with
+        prefix_len[b] + len(tokens[b])."""
+        B, T, d = len(tokens), self.max_tree, self.shape.d_model
+        if (features.device.type != "cuda" or features.dtype != torch.float32 or not features.is_contiguous()
+                or tuple(features.shape) != (B, T, d)):
+            raise ValueError(f"features must be a contiguous CUDA float32 tensor of shape {(B, T, d)}")
+        if not all(1 <= len(t) <= T for t in tokens):
+            raise ValueError(f"every chain must hold 1 to {T} tokens")
+        n = _i32([len(t) for t in tokens])
+        tok = np.zeros((B, T), dtype=np.int32)
+        for b, t in enumerate(tokens):
+            tok[b, : len(t)] = t
+        rc = N.lib.griffin_draft_extend(self.h, B, _p32(_i32(prefix_len)), _p32(n), _p32(tok),
+                                        c_void_p(features.data_ptr()))
+        _check(rc, "griffin_draft_extend", self._ctx())
+
     def tree(self, prefix_len, root_tokens, root_features: torch.Tensor, k: int, depth: int, n_total: int):
         """Draft one tree per sequence; returns (n_nodes [B], tokens, parents, scores [B, max_tree])."""
         B = len(root_tokens)

@@ -258,6 +258,21 @@ class TreeVerifier:
         _check(rc, "griffin_read_predictions", self.ctx)
         return pred[: self._batch]
 
+    def features(self, nodes) -> torch.Tensor:
+        """The target's features (hidden state after the last layer, before the
+        final norm) of the last step's nodes: nodes[b] lists node ids of
+        sequence b (all lists of one length; -1 gives a zero row).  Returns a
+        CUDA float32 tensor [B, n, d_model], filled in stream order."""
+        ids = np.asarray(nodes, dtype=np.int32)
+        if ids.ndim != 2:
+            raise ValueError("nodes must be a [batch][n] array")
+        B, n = ids.shape
+        out = torch.empty((B, n, self.shape.d_model), dtype=torch.float32, device=self.k_cache.device)
+        ids = np.ascontiguousarray(ids)
+        rc = N.lib.griffin_read_features(self.ctx, B, n, _p32(ids), c_void_p(out.data_ptr()))
+        _check(rc, "griffin_read_features", self.ctx)
+        return out
+
     def close(self):
         if getattr(self, "ctx", None) is not None and self.ctx.value:
             N.lib.griffin_verify_free(self.ctx)

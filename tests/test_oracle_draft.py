@@ -232,3 +232,24 @@ def test_expansion_hand_worked_case():
     # final 4: (0) .5, (1) .3, (0,0) .2, (0,1) .175
     assert _paths(ex.tree) == {(0,), (1,), (0, 0), (0, 1)}
     assert list(ex.tree.parents) == [-1, 0, 0, 1, 1]
+
+
+def test_chain_kv_extends_the_prefix():
+    """A draft pass over a chain adds exactly the chain's K/V to the draft's
+    cache: passing the first tokens, appending their K/V to the prefix and
+    then passing the last token alone (at its position, with its feature)
+    reproduces the last row of the pass over the whole chain."""
+    ds, mw, ow, dw = _small()
+    dow = od.DraftOracleWeights(dw, ow)
+    P, d = 33, ds.target.d_model
+    Kp, Vp = _kv(ds, P)
+    toks = [7, 100, 3, 512, 9]
+    feats = np.random.default_rng(4).normal(size=(len(toks), d))
+    whole = od.draft_forward(dow, gen.chain_tree(toks[0], toks[1:]), feats, (Kp, Vp), P)
+    head = od.draft_forward(dow, gen.chain_tree(toks[0], toks[1:-1]), feats[:-1], (Kp, Vp), P)
+    K2 = np.concatenate([Kp, head.k.transpose(1, 0, 2)], axis=1)
+    V2 = np.concatenate([Vp, head.v.transpose(1, 0, 2)], axis=1)
+    last = od.draft_forward(dow, gen.chain_tree(toks[-1], []), feats[-1:], (K2, V2), P + len(toks) - 1)
+    assert np.allclose(last.logits[0], whole.logits[-1], rtol=0, atol=1e-9)
+    assert np.allclose(last.regress[0], whole.regress[-1], rtol=0, atol=1e-9)
+    assert np.allclose(head.k, whole.k[:-1], atol=1e-12) and np.allclose(head.v, whole.v[:-1], atol=1e-12)
