@@ -166,8 +166,9 @@ def main():
     log(f"weights {weights.nbytes() / 1e9:.2f} GB generated in {time.time() - t0:.1f} s")
     max_tree = w.max_tree
     prefix = w.prefixes()
+    cycle_room = 128  # positions the draft leg's speculative cycles append to the prefix
     v = P.TreeVerifier(m, weights, max_batch=w.batch, max_tree=max_tree, max_depth=w.depth,
-                       kv_capacity=w.kv_capacity())
+                       kv_capacity=w.kv_capacity() + cycle_room)
     v.set_graphs(not args.no_graphs)
     for l in range(m.n_layers):
         for b in range(w.batch):
@@ -328,7 +329,7 @@ def main():
         ds = DRAFTS[m.name]
         dw = gen.make_draft_weights(ds, 3, device=dev)
         dm = P.DraftModel(ds, dw, weights, max_batch=w.batch, max_tree=64, max_depth=ds.depth,
-                          kv_capacity=w.kv_capacity())
+                          kv_capacity=w.kv_capacity() + cycle_room)
         for b in range(w.batch):
             k, vv = gen.synthetic_kv(ds.layer, 0, b, prefix[b], 5, dev)
             dm.write_prefix(b, k, vv)
@@ -348,19 +349,48 @@ def main():
         for _ in range(nd):
             dn, _, _, _ = dm.tree(prefix, roots, feat, ds.k, ds.depth, ds.n_total)
         t_tree = (time.perf_counter() - t0) * 1e3 / nd
+        # whole cycles: draft tree, verify, accept, commit, the target's
+        # features, the draft's catch-up (random weights: about one token each)
+        t_cycle, cycle_tokens = None, None
+        if max_tree >= ds.n_total + 1 and w.depth >= ds.depth:
+            from paper_2502_11018_amd.cycle import SpeculativeCycle
+            cyc = SpeculativeCycle(v, dm, ds.k, ds.depth, ds.n_total)
+            cyc.start(prefix, roots, feat)
+            n_cyc = min(args.steps, 10)
+            assert (n_cyc + 2) * (ds.depth + 1) <= cycle_room
+            for _ in range(2):
+                cyc.cycle()
+            torch.cuda.synchronize()
+            emitted = 0
+            t0 = time.perf_counter()
+            for _ in range(n_cyc):
+                emitted += sum(len(t) for t in cyc.cycle())
+            torch.cuda.synchronize()
+            t_cycle = (time.perf_counter() - t0) * 1e3 / n_cyc
+            cycle_tokens = emitted / n_cyc
         dm.close()
         sr = {str(tau): round(tau * ms_per_step / (ms_per_step + ds.depth * t_pass), 3) for tau in (4, 5, 6)}
         cycle = {str(tau): round(tau * root_ms / (ms_per_step + t_tree), 3) for tau in (4, 5, 6)}
         draft = {"params": ds.param_count(), "k": ds.k, "depth": ds.depth, "n_total": ds.n_total,
                  "pass_ms": round(t_pass, 4), "pass_nodes": int(biggest[0].n), "tree_ms": round(t_tree, 4),
                  "speedup_model": sr, "speedup_vs_plain_decoding": cycle,
+                 "cycle_ms": None if t_cycle is None else round(t_cycle, 4),
+                 "cycle_tokens_measured": cycle_tokens,
+                 "speedup_from_measured_cycle": None if t_cycle is None else
+                 {str(tau): round(tau * root_ms / t_cycle, 3) for tau in (4, 5, 6)},
                  "note": "pass_ms = one draft pass over the largest expansion (1 + k (depth - 1) nodes), host "
                          "round trip included; speedup_model = tau t / (t + depth * pass_ms) with t = ms_per_step "
                          "(the paper's latency model); speedup_vs_plain_decoding = tau root_only_ms / (ms_per_step "
                          "+ tree_ms); tau (tokens per cycle, bonus included) needs trained drafts and is a free "
-                         "parameter here"}
+                         "parameter here; cycle_ms = one whole draft-and-verify cycle (SpeculativeCycle: tree, "
+                         "verify step, accept, commit, target features, draft catch-up) on the same context, "
+                         "cycle_tokens_measured its emitted tokens with random weights, "
+                         "speedup_from_measured_cycle = tau root_only_ms / cycle_ms"}
         log(f"draft: pass {t_pass:.3f} ms ({biggest[0].n} nodes), tree {t_tree:.3f} ms, "
             f"modelled speedup at tau 5: {sr['5']}x")
+        if t_cycle is not None:
+            log(f"cycle: {t_cycle:.3f} ms, {cycle_tokens:.2f} tokens per cycle measured (random weights); "
+                f"at tau 5: {5 * root_ms / t_cycle:.3f}x plain decoding")
 
     gc.enable()
     gc.unfreeze()
