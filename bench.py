@@ -144,6 +144,8 @@ def main():
     ap.add_argument("--no-graphs", action="store_true", help="plain launches instead of graph replay")
     ap.add_argument("--no-sampled", action="store_true", help="skip the temperature-1 (stochastic acceptance) leg")
     ap.add_argument("--no-draft", action="store_true", help="skip the draft-model leg")
+    ap.add_argument("--bf16-activations", action="store_true",
+                    help="GEMM activations rounded to bf16 instead of bf16 hi + lo parts")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on exactly one GPU; --gpus {args.gpus} is not supported", file=sys.stderr)
@@ -170,6 +172,7 @@ def main():
     v = P.TreeVerifier(m, weights, max_batch=w.batch, max_tree=max_tree, max_depth=w.depth,
                        kv_capacity=w.kv_capacity() + cycle_room)
     v.set_graphs(not args.no_graphs)
+    v.set_bf16_activations(args.bf16_activations)
     for l in range(m.n_layers):
         for b in range(w.batch):
             k, vv = gen.synthetic_kv(m, l, b, prefix[b], w.weight_seed, dev)

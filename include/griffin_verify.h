@@ -214,6 +214,16 @@ int griffin_read_features(griffin_ctx *ctx, int32_t batch, int32_t n, const int3
  * Errors: EINVAL (null context). */
 int griffin_set_graphs(griffin_ctx *ctx, int32_t enable);
 
+/* Precision of the GEMM operands.  Default (bf16_only = 0): each activation
+ * enters the projections as a bf16 high part plus a bf16 low part, two MFMAs
+ * per weight fragment, which keeps fp32-grade activations against bf16
+ * weights.  bf16_only = 1: the high part alone, i.e. activations rounded to
+ * bf16 as in a plain bf16 forward pass (the paper's setting), half the
+ * activation staging and MFMA work per weight byte.  Weights are bf16 either
+ * way; norms, RoPE, attention and reductions are unchanged.  Waits for the
+ * stream and drops captured graphs.  Errors: EINVAL, EHIP. */
+int griffin_set_activation_precision(griffin_ctx *ctx, int32_t bf16_only);
+
 /* Release the context (waits for its stream first).  NULL is a no-op. */
 void griffin_verify_free(griffin_ctx *ctx);
 

@@ -68,6 +68,7 @@ def _load() -> ctypes.CDLL:
         "griffin_accept": (c_int32, [c_void_p, I32P, I32P, I32P]),
         "griffin_read_predictions": (c_int32, [c_void_p, I32P]),
         "griffin_read_features": (c_int32, [c_void_p, c_int32, c_int32, I32P, c_void_p]),
+        "griffin_set_activation_precision": (c_int32, [c_void_p, c_int32]),
         "griffin_verify_free": (None, [c_void_p]),
         "griffin_status_str": (c_char_p, [c_int32]),
         "griffin_last_error": (c_char_p, [c_void_p]),
@@ -104,6 +105,7 @@ EXPORTED = ("griffin_kv_cache_bytes", "griffin_verify_init", "griffin_verify_ste
             "griffin_tree_prepare", "griffin_accept_walk", "griffin_profile_enable", "griffin_profile_read",
             "griffin_set_graphs", "griffin_commit", "griffin_accept_sampled", "griffin_accept_sampled_walk",
             "griffin_draft_init", "griffin_draft_free", "griffin_draft_context", "griffin_draft_step",
-            "griffin_draft_tree", "griffin_read_features", "griffin_draft_extend")
+            "griffin_draft_tree", "griffin_read_features", "griffin_draft_extend",
+            "griffin_set_activation_precision")
 KERNEL_CLASSES = ("qkv_gemm", "rope_kv_write", "tree_attention", "o_gemm", "residual_rmsnorm", "gate_up_gemm",
                   "down_gemm", "lm_head_gemm", "argmax_accept_route", "attn_merge")

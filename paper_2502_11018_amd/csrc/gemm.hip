@@ -34,14 +34,16 @@
 
 namespace griffin {
 
-template <int EPI, int NB, int WN, int PF, int KS>
+template <int EPI, int NB, int WN, int PF, int KS, bool XLO>
 __global__ __launch_bounds__(64 * WN * KS) void gemm_kernel(GemmArgs a) {
-  constexpr int XPIECES = 16;          // per step: {hi, lo} x {rows 0-31, 32-63} x 4 pieces of 1 KB
+  // per step: {hi, lo} (XLO) or {hi} x {rows 0-31, 32-63} x 4 pieces of 1 KB
+  constexpr int XH = XLO ? 2 : 1;
+  constexpr int XPIECES = 8 * XH;
   constexpr int XP = XPIECES / WN;     // activation pieces each wave stages per step
   constexpr int LOADS = NB * 4 + XP;   // vector-memory instructions per stage per wave
   static_assert(LOADS * (PF - 2) < 64, "wait count out of range");
   static_assert(PF >= 2 && XPIECES % WN == 0, "pipeline shape");
-  static_assert(WN * NB * 8 <= PF * KS * 16 || KS == 1, "K-split merge buffer");
+  static_assert(WN * NB * 8 <= PF * KS * XPIECES || KS == 1, "K-split merge buffer");
   __shared__ u32x4 xs[PF][KS][XPIECES][64];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -99,11 +101,11 @@ __global__ __launch_bounds__(64 * WN * KS) void gemm_kernel(GemmArgs a) {
     }
   };
   // Consume stage t from slot u: the weights times the activation's bf16 high
-  // part plus its bf16 low part (two MFMAs into the same accumulator).
+  // part plus, with XLO, its bf16 low part (two MFMAs into one accumulator).
   auto compute = [&](int u) {
-    u32x4 xv[2][2][4];
+    u32x4 xv[XH][2][4];
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int h = 0; h < XH; ++h)
 #pragma unroll
       for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
@@ -111,7 +113,7 @@ __global__ __launch_bounds__(64 * WN * KS) void gemm_kernel(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
+      for (int h = 0; h < XH; ++h)
 #pragma unroll
         for (int b = 0; b < NB; ++b)
 #pragma unroll
@@ -255,19 +257,20 @@ __global__ __launch_bounds__(64 * WN * KS) void gemm_kernel(GemmArgs a) {
   }
 }
 
-template <int EPI, int NB, int WN, int PF, int KS>
+template <int EPI, int NB, int WN, int PF, int KS, bool XLO>
 static hipError_t launch_one(const GemmArgs& a, int experts, hipStream_t s) {
   const int gx = a.m_tiles > 1 ? (a.n_wgs + 7) / 8 * 8 * a.m_tiles : a.n_wgs;
   dim3 grid(gx, experts, a.splits / KS);
-  hipLaunchKernelGGL((gemm_kernel<EPI, NB, WN, PF, KS>), grid, dim3(64 * WN * KS), 0, s, a);
+  hipLaunchKernelGGL((gemm_kernel<EPI, NB, WN, PF, KS, XLO>), grid, dim3(64 * WN * KS), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_gemm(const GemmArgs& a, int experts, hipStream_t s) {
   const int epi = a.epi, nb = a.nb, wn = a.wn, pf = a.pf, ks = a.kslices;
   if (ks < 1 || a.splits % ks != 0) return hipErrorInvalidValue;
-#define GRIFFIN_GEMM_CASE(E, B, N_, P, K_)                                                        \
-  if (epi == (E) && nb == (B) && wn == (N_) && pf == (P) && ks == (K_)) return launch_one<E, B, N_, P, K_>(a, experts, s);
+#define GRIFFIN_GEMM_CASE(E, B, N_, P, K_)                                                          \
+  if (epi == (E) && nb == (B) && wn == (N_) && pf == (P) && ks == (K_))                            \
+    return a.xlo ? launch_one<E, B, N_, P, K_, true>(a, experts, s) : launch_one<E, B, N_, P, K_, false>(a, experts, s);
   GRIFFIN_GEMM_CASE(EPI_STORE, 1, 4, 4, 1)
   GRIFFIN_GEMM_CASE(EPI_STORE, 1, 4, 2, 1)
   GRIFFIN_GEMM_CASE(EPI_SWIGLU, 2, 2, 3, 2)

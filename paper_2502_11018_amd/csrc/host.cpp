@@ -260,6 +260,8 @@ struct griffin_ctx {
   // a pass that ends once the last layer has written the nodes' K/V (a
   // draft catching up on accepted tokens)
   bool kv_only = false;
+  // GEMM operands: bf16 hi + lo activations (default) or the bf16 hi part alone
+  bool act_bf16 = false;
   // griffin_read_features: rows of x to gather, staged through pinned memory
   int32_t* feat_rows = nullptr;
   int32_t* feat_rows_host = nullptr;
@@ -303,7 +305,7 @@ int dev_alloc(griffin_ctx* c, T** p, size_t count) {
   return GRIFFIN_OK;
 }
 
-GemmArgs gemm_args(const GemmPlan& p, const uint16_t* X, int x_ks, const uint16_t* W, int m_tiles) {
+GemmArgs gemm_args(const GemmPlan& p, const uint16_t* X, int x_ks, const uint16_t* W, int m_tiles, bool xlo) {
   GemmArgs a{};
   a.epi = p.epi;
   a.nb = p.nb;
@@ -317,6 +319,7 @@ GemmArgs gemm_args(const GemmPlan& p, const uint16_t* X, int x_ks, const uint16_
   a.m_tiles = m_tiles;
   a.X = X;
   a.x_ks = x_ks;
+  a.xlo = xlo ? 1 : 0;
   a.W = W;
   return a;
 }
@@ -372,7 +375,7 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
     LAUNCH(GRIFFIN_KC_NORM, launch_residual_rmsnorm(c->x, l == 0 ? none : add_down, c->attn_norm[l], d.rms_eps,
                                                     Mpad, d.d_model, c->xn, c->xd_ks, s));
     {
-      GemmArgs a = gemm_args(c->p_qkv, c->xn, c->xd_ks, c->pk_qkv[l], m_tiles);
+      GemmArgs a = gemm_args(c->p_qkv, c->xn, c->xd_ks, c->pk_qkv[l], m_tiles, !c->act_bf16);
       a.out = c->parts;
       a.ldo = c->qkv_n;
       a.out_split_stride = ps * c->qkv_n;
@@ -410,7 +413,7 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
                                                 c->q_lo, c->tree, PrefixKV{kc, vc, d.kv_capacity}, scale_log2, c->o,
                                                 c->p_o.ks_pad, s));
     {
-      GemmArgs a = gemm_args(c->p_o, c->o, c->p_o.ks_pad, c->pk_o[l], m_tiles);
+      GemmArgs a = gemm_args(c->p_o, c->o, c->p_o.ks_pad, c->pk_o[l], m_tiles, !c->act_bf16);
       a.out = c->parts;
       a.ldo = d.d_model;
       a.out_split_stride = ps * d.d_model;
@@ -425,11 +428,11 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
 
     // ---- MLP block
     if (c->E == 1) {
-      GemmArgs g = gemm_args(c->p_gu, c->xn, c->xd_ks, c->pk_gu[l], m_tiles);
+      GemmArgs g = gemm_args(c->p_gu, c->xn, c->xd_ks, c->pk_gu[l], m_tiles, !c->act_bf16);
       g.act = c->act;
       g.act_ks = c->p_down.ks_pad;
       LAUNCH(GRIFFIN_KC_GATE_UP, launch_gemm(g, 1, s));
-      GemmArgs dn = gemm_args(c->p_down, c->act, c->p_down.ks_pad, c->pk_down[l], m_tiles);
+      GemmArgs dn = gemm_args(c->p_down, c->act, c->p_down.ks_pad, c->pk_down[l], m_tiles, !c->act_bf16);
       dn.out = c->parts;
       dn.ldo = d.d_model;
       dn.out_split_stride = ps * d.d_model;
@@ -447,7 +450,7 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
                                                 c->slot, s));
       LAUNCH(GRIFFIN_KC_OTHER, launch_moe_gather(c->xn, c->xd_ks, c->gather, c->count, c->E, Mpad, d.d_model,
                                                  c->xe, xe_tiles, s));
-      GemmArgs g = gemm_args(c->p_gu, c->xe, c->xd_ks, c->pk_gu[l], m_tiles);
+      GemmArgs g = gemm_args(c->p_gu, c->xe, c->xd_ks, c->pk_gu[l], m_tiles, !c->act_bf16);
       g.x_etiles = xe_tiles;
       g.count = c->count;
       g.o_erows = Mpad;
@@ -455,7 +458,7 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
       g.act = c->act;
       g.act_ks = c->p_down.ks_pad;
       LAUNCH(GRIFFIN_KC_GATE_UP, launch_gemm(g, c->E, s));
-      GemmArgs dn = gemm_args(c->p_down, c->act, c->p_down.ks_pad, c->pk_down[l], m_tiles);
+      GemmArgs dn = gemm_args(c->p_down, c->act, c->p_down.ks_pad, c->pk_down[l], m_tiles, !c->act_bf16);
       dn.x_etiles = xe_tiles;
       dn.count = c->count;
       dn.o_erows = Mpad;
@@ -481,7 +484,7 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
                                                     c->xn, c->xd_ks, s));
   const int lm_parts = c->p_lm.shape.n_wgs * c->p_lm.wn;
   {
-    GemmArgs a = gemm_args(c->p_lm, c->xn, c->xd_ks, c->pk_lm, m_tiles);
+    GemmArgs a = gemm_args(c->p_lm, c->xn, c->xd_ks, c->pk_lm, m_tiles, !c->act_bf16);
     a.pmax = c->pmax;
     a.pidx = c->pidx;
     a.pnan = c->pnan;
@@ -613,7 +616,7 @@ DraftArgs draft_args(griffin_draft* dc, griffin_ctx* c) {
 hipError_t draft_gemm(griffin_draft* dc, griffin_ctx* c, const GemmPlan& p, const uint16_t* X, const uint16_t* W,
                       int N, hipStream_t s) {
   const int mpad = round_up(c->batch * c->d.max_tree, 64);
-  GemmArgs a = gemm_args(p, X, p.ks_pad, W, mpad / 64);
+  GemmArgs a = gemm_args(p, X, p.ks_pad, W, mpad / 64, !c->act_bf16);
   a.out = dc->parts;
   a.ldo = N;
   a.out_split_stride = (long long)mpad * N;
@@ -973,6 +976,15 @@ int griffin_commit(griffin_ctx* c) {
   const long long layer_kv = (long long)d.max_batch * d.n_kv_heads * d.kv_capacity * d.head_dim;
   HIP_TRY(c, launch_commit(c->result, d.max_depth, c->meta, c->batch, d.n_layers, d.n_kv_heads, d.head_dim,
                            d.kv_capacity, layer_kv, c->k_cache, c->v_cache, c->stream));
+  return GRIFFIN_OK;
+}
+
+int griffin_set_activation_precision(griffin_ctx* c, int32_t bf16_only) {
+  if (!c) return GRIFFIN_EINVAL;
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  c->act_bf16 = bf16_only != 0;
+  for (auto& g : c->graphs) hipGraphExecDestroy(g.exec);  // captured launches carry the GEMM variant
+  c->graphs.clear();
   return GRIFFIN_OK;
 }
 

@@ -258,6 +258,12 @@ class TreeVerifier:
         _check(rc, "griffin_read_predictions", self.ctx)
         return pred[: self._batch]
 
+    def set_bf16_activations(self, enable: bool):
+        """GEMM activations as bf16 alone (True) or bf16 high + low parts
+        (False, the default); see griffin_set_activation_precision."""
+        rc = N.lib.griffin_set_activation_precision(self.ctx, 1 if enable else 0)
+        _check(rc, "griffin_set_activation_precision", self.ctx)
+
     def features(self, nodes) -> torch.Tensor:
         """The target's features (hidden state after the last layer, before the
         final norm) of the last step's nodes: nodes[b] lists node ids of

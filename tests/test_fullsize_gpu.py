@@ -62,13 +62,28 @@ def _planted(w, ow, kv, max_index=64):
 
 @pytest.mark.parametrize("name", ["llama3-8b", "llama2-7b"])
 def test_full_size_verify_matches_oracle(name):
+    _full_size_verify(name, bf16_activations=False)
+
+
+def test_full_size_bf16_activations_error_bound():
+    """The opt-in mode with GEMM activations rounded to bf16 (a plain bf16
+    forward pass, the paper's setting) instead of bf16 hi + lo.  It does not
+    meet the acceptance gate: over 32 layers the logits drift by ~2e-2 of the
+    row range and the argmax flips at nodes whose oracle margin is several
+    times 1e-2.  Measured here, with a bound on the drift, so that the
+    default's need for the low parts stays documented."""
+    _full_size_verify("llama3-8b", bf16_activations=True)
+
+
+def _full_size_verify(name, bf16_activations):
     import paper_2502_11018_amd as P
     w = get_workload(name)
     m = w.model
     t0 = time.time()
-    say(f"{name}: generate weights on the GPU")
+    say(f"{name}: generate weights on the GPU (bf16 activations: {bf16_activations})")
     mw_gpu = gen.make_weights(m, w.weight_seed, device="cuda")
     v = P.TreeVerifier(m, mw_gpu, max_batch=1, max_tree=64, max_depth=w.depth, kv_capacity=w.kv_capacity())
+    v.set_bf16_activations(bf16_activations)
     Ks, Vs = [], []
     for l in range(m.n_layers):
         k, vv = gen.synthetic_kv(m, l, 0, w.prefix_len, w.weight_seed, "cuda")
@@ -90,6 +105,15 @@ def test_full_size_verify_matches_oracle(name):
         lg = logits[: tree.n].cpu().numpy()
         say(f"{name}: oracle verify {label} ({time.time() - t0:.0f}s)")
         os_ = H.oracle_sequence(ow, H.SeqCase(None, kv, tree, [], [], []))
+        if bf16_activations:
+            span = os_.logits.max(axis=1) - os_.logits.min(axis=1)
+            drift = (np.abs(lg - os_.logits).max(axis=1) / span).max()
+            gated = [i for i in range(tree.n) if os_.margin[i] > 1e-2]
+            flips = [i for i in gated if pred[i] != np.argmax(os_.logits[i])]
+            say(f"{name} {label} (bf16 activations): logit drift {drift:.2e} of the range, argmax flips at "
+                f"{len(flips)}/{len(gated)} gated nodes (largest margin {max([os_.margin[i] for i in flips], default=0):.3f})")
+            assert drift < 5e-2
+            continue
         st = H.check_parity(os_, lg, pred[: tree.n], acc.sequence(0))
         rel = np.abs(lg - os_.logits).max(axis=1)
         say(f"{name} {label}: max rel err {st['max_rel']:.2e}, max abs err {rel.max():.3e}, "
