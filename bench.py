@@ -144,6 +144,7 @@ def main():
     ap.add_argument("--no-graphs", action="store_true", help="plain launches instead of graph replay")
     ap.add_argument("--no-sampled", action="store_true", help="skip the temperature-1 (stochastic acceptance) leg")
     ap.add_argument("--no-draft", action="store_true", help="skip the draft-model leg")
+    ap.add_argument("--no-cycle", action="store_true", help="skip the whole-cycle part of the draft leg")
     ap.add_argument("--bf16-activations", action="store_true",
                     help="GEMM activations rounded to bf16 instead of bf16 hi + lo parts")
     args = ap.parse_args()
@@ -355,7 +356,7 @@ def main():
         # whole cycles: draft tree, verify, accept, commit, the target's
         # features, the draft's catch-up (random weights: about one token each)
         t_cycle, cycle_tokens = None, None
-        if max_tree >= ds.n_total + 1 and w.depth >= ds.depth:
+        if not args.no_cycle and max_tree >= ds.n_total + 1 and w.depth >= ds.depth:
             from paper_2502_11018_amd.cycle import SpeculativeCycle
             cyc = SpeculativeCycle(v, dm, ds.k, ds.depth, ds.n_total)
             cyc.start(prefix, roots, feat)
