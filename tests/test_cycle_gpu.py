@@ -165,8 +165,16 @@ def test_draft_extend_matches_oracle():
                 compared += 1
                 assert list(tok[b, 0]) == list(otok[0])
         say(f"extend: top-k compared on {compared}/2 roots")
-        with pytest.raises(ValueError):           # a chain longer than max_tree
+        with pytest.raises(ValueError):           # a chain longer than max_tree (caught by the binding)
             pr.d.extend(pr.prefixes, [[1] * (T + 1), [2]], feats.cuda())
+        # the library's own check, called directly: ETREE, nothing enqueued
+        import paper_2502_11018_amd._native as N
+        from paper_2502_11018_amd.verifier import _i32, _p32
+        from ctypes import c_void_p
+        tok = np.zeros((2, T), dtype=np.int32)
+        rc = N.lib.griffin_draft_extend(pr.d.h, 2, _p32(_i32(P2)), _p32(_i32([T + 1, 1])), _p32(tok),
+                                        c_void_p(feats.cuda().data_ptr()))
+        assert rc == N.CODES["GRIFFIN_ETREE"]
     finally:
         pr.close()
 

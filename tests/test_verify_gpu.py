@@ -409,3 +409,30 @@ def test_speculative_loop_is_lossless(name):
         assert accepted > cycle  # the planted parts were accepted (more than one token per cycle on average)
     finally:
         s.v.close()
+
+
+def test_activation_precision_switch_drops_stale_graphs(tiny):
+    """Switching the GEMM activations to bf16 alone changes the logits (a
+    different kernel variant runs, not a stale graph), and switching back
+    gives the default's bits again, with graph replay on throughout."""
+    m = tiny.w.model
+    trees = [tiny.cases[0][0].tree]
+    out = torch.empty((tiny.max_tree, m.vocab), device=tiny.dev)
+
+    def logits():
+        out.fill_(float("nan"))
+        tiny.v.step([tiny.w.prefix_len], trees, out)
+        tiny.v.accept(check=False)
+        return out[: trees[0].n].cpu().numpy().copy()
+
+    say("tiny: activation precision switch")
+    ref = logits()
+    assert np.array_equal(logits(), ref)            # graph replay of the default
+    try:
+        tiny.v.set_bf16_activations(True)
+        alt = logits()
+        assert np.isfinite(alt).all() and not np.array_equal(alt, ref)
+        assert np.array_equal(logits(), alt)        # its own graph replays the same bits
+    finally:
+        tiny.v.set_bf16_activations(False)
+    assert np.array_equal(logits(), ref)
