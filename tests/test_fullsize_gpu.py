@@ -307,3 +307,54 @@ def test_full_size_draft_matches_oracle():
         f"({time.time() - t0:.0f}s)")
     assert worst < 2e-3 and compared >= total // 2
     dm.close()
+
+
+def test_full_size_cycle_is_lossless():
+    """Whole draft-and-verify cycles at the Llama-3-8B shape (prefix 2048,
+    the 0.42B draft with random weights, k 10, depth 6, 60 tokens): the
+    emitted tokens equal the oracle's greedy continuation as far as its
+    margins exceed the acceptance gate's 1e-2."""
+    import paper_2502_11018_amd as P
+    from paper_2502_11018_amd.cycle import SpeculativeCycle
+    from workloads.configs import DRAFTS
+    w = get_workload("llama3-8b")
+    m, ds = w.model, DRAFTS["llama3-8b"]
+    n_tokens, P_len = 8, w.prefix_len
+    t0 = time.time()
+    say("llama3-8b cycle: weights on the GPU")
+    mw_gpu = gen.make_weights(m, w.weight_seed, device="cuda")
+    cap = P_len + 64 + 64
+    v = P.TreeVerifier(m, mw_gpu, max_batch=1, max_tree=64, max_depth=ds.depth, kv_capacity=cap)
+    Ks, Vs = [], []
+    for l in range(m.n_layers):
+        k, vv = gen.synthetic_kv(m, l, 0, P_len, w.weight_seed, "cuda")
+        v.write_prefix(l, 0, k, vv)
+        Ks.append(k.to(torch.float64).cpu().numpy())
+        Vs.append(vv.to(torch.float64).cpu().numpy())
+    kv = H.PrefixKV(Ks, Vs)
+    dm = P.DraftModel(ds, gen.make_draft_weights(ds, 3, device="cuda"), mw_gpu, max_batch=1, max_tree=64,
+                      max_depth=ds.depth, kv_capacity=cap)
+    dk, dv = gen.synthetic_kv(ds.layer, 0, 0, P_len, 5, "cuda")
+    dm.write_prefix(0, dk, dv)
+    root = 1234
+    cyc = SpeculativeCycle(v, dm, ds.k, ds.depth, ds.n_total)
+    cyc.start([P_len], [root], gen.draft_root_features(m.d_model, 1, 11, "cuda"))
+    out = []
+    while len(out) < n_tokens:
+        say(f"llama3-8b cycle at prefix {cyc.prefix[0]} ({time.time() - t0:.0f}s)")
+        out += cyc.cycle()[0]
+    dm.close()
+    v.close()
+    say(f"llama3-8b cycle: oracle greedy continuation ({time.time() - t0:.0f}s)")
+    ow = oracle.OracleWeights(mw_gpu.to("cpu"), cache=True)
+    cache, tok, greedy, margins = kv.decode_cache(m), root, [], []
+    for j in range(n_tokens):                       # oracle.greedy_chain, one token at a time (progress)
+        logits = oracle.decode_step(ow, cache, tok, P_len + j)
+        tok = int(oracle.argmax_first(logits))
+        greedy.append(tok)
+        margins.append(float(oracle.top2_margin(logits)))
+        say(f"llama3-8b cycle: oracle token {j}: {tok} (margin {margins[-1]:.3f}, {time.time() - t0:.0f}s)")
+    decided = next((i for i, mg in enumerate(margins) if mg <= H.MARGIN_GATE), n_tokens)
+    say(f"llama3-8b cycle: {decided} tokens decided beyond the margin gate ({time.time() - t0:.0f}s)")
+    assert decided >= 3
+    assert out[:decided] == [int(t) for t in greedy[:decided]]
