@@ -12,6 +12,12 @@
         bench.py: per-kernel durations over the last K steps (a step ends with
         the kernel matching --step-end, by default the acceptance walk).
 
+    python -m paper_2502_11018_amd.profiling counters --pmc RUN_counter_collection.csv ... \\
+            --trace RUN_kernel_trace.csv --group LABEL=REGEX ... --out profiles/NAME.md ...
+        Per kernel group, the mean per dispatch of every counter of the --pmc
+        passes (MFMA flops and utilisation, FETCH_SIZE) beside the mean
+        kernel duration of a --kernel-trace run of the same command.
+
     python -m paper_2502_11018_amd.profiling traffic \\
             --kernel-regex REGEX --fetch BENCH_fetch.csv --write BENCH_write.csv \\
             --copy-fetch COPY_fetch.csv --copy-write COPY_write.csv --copy-bytes N \\
@@ -174,6 +180,50 @@ def cmd_traffic(args):
     print("\n".join(out))
 
 
+def _mean_duration_us(trace_csv: str, rx):
+    durs = [(int(_col(r, "End_Timestamp")) - int(_col(r, "Start_Timestamp"))) / 1e3
+            for r in _rows(trace_csv) if rx.search(_col(r, "Kernel_Name"))]
+    return (statistics.fmean(durs), len(durs)) if durs else (None, 0)
+
+
+def cmd_counters(args):
+    """Per kernel group: the mean per dispatch of every counter in the given
+    rocprofv3 --pmc CSVs, with the mean kernel-trace duration of the same
+    group; MfmaFlopsBF16 becomes TFLOP/s against the bf16 dense peak and
+    FETCH_SIZE (KiB) bytes scaled by the copy kernel's reading."""
+    scale = 1.0
+    if args.copy_fetch:
+        cf, _ = counter_per_dispatch(args.copy_fetch, "FETCH_SIZE", args.copy_regex)
+        scale = args.copy_bytes / (cf * 1024.0)
+    out = [f"# {args.title}", "", "Commands (each a separate rocprofv3 pass):", "", "```", args.command, "```", "",
+           "| kernel group | dispatches | mean us (trace) | counter | per dispatch | derived |",
+           "|---|---:|---:|---|---:|---|"]
+    for g in args.group:
+        label, regex = g.split("=", 1)
+        rx = re.compile(regex)
+        dur, nd = _mean_duration_us(args.trace, rx)
+        for path in args.pmc:
+            names = sorted({_col(r, "Counter_Name") for r in _rows(path) if rx.search(_col(r, "Kernel_Name"))})
+            for name in names:
+                val, n = counter_per_dispatch(path, name, regex)
+                derived = ""
+                if name == "MfmaFlopsBF16" and dur:
+                    derived = f"{val / (dur * 1e-6) / 1e12:.1f} TFLOP/s = {val / (dur * 1e-6) / 2.5e15:.1%} of 2.5 PFLOP/s"
+                elif name == "MfmaUtil":
+                    derived = "% of SIMD cycles with the MFMA unit busy"
+                elif name == "FETCH_SIZE" and dur:
+                    b = val * 1024.0 * scale
+                    derived = f"{b / 1e6:.2f} MB (x{scale:.3f}), {b / (dur * 1e-6) / 1e9:.0f} GB/s = {b / (dur * 1e-6) / 8e12:.1%} of 8 TB/s"
+                shown = f"{val:.4g}" if name != "MfmaFlopsBF16" else f"{val / 1e9:.2f} GFLOP"
+                out.append(f"| {label} | {n} | {dur:.2f} | {name} | {shown} | {derived} |" if dur else
+                           f"| {label} | {n} | — | {name} | {shown} | {derived} |")
+    if args.note:
+        out += ["", args.note]
+    with open(args.out, "w") as f:
+        f.write("\n".join(out) + "\n")
+    print("\n".join(out))
+
+
 def read_traffic_record(profiles_dir: str, label: str, workload: str, repo_root: str):
     """Scaled HBM bytes per dispatch from a committed summary, or None when
     there is none or the kernel source changed since the counters were taken."""
@@ -212,6 +262,17 @@ def main(argv=None):
     s.add_argument("--title", required=True)
     s.add_argument("--command", required=True)
     s.add_argument("--note", default="")
+    k = sub.add_parser("counters")
+    k.add_argument("--pmc", nargs="+", required=True, help="rocprofv3 --pmc counter_collection CSVs")
+    k.add_argument("--trace", required=True, help="kernel_trace CSV of the same command (durations)")
+    k.add_argument("--group", nargs="+", required=True, help="LABEL=REGEX of kernel names")
+    k.add_argument("--copy-fetch", default="")
+    k.add_argument("--copy-regex", default="copy|Copy")
+    k.add_argument("--copy-bytes", type=int, default=1 << 30)
+    k.add_argument("--title", required=True)
+    k.add_argument("--command", required=True)
+    k.add_argument("--note", default="")
+    k.add_argument("--out", required=True)
     t = sub.add_parser("traffic")
     t.add_argument("--kernel-regex", required=True)
     t.add_argument("--copy-regex", default="copy|Copy")
@@ -226,7 +287,7 @@ def main(argv=None):
     t.add_argument("--out", required=True)
     t.add_argument("--command", required=True)
     args = ap.parse_args(argv)
-    {"copy": cmd_copy, "stats": cmd_stats, "traffic": cmd_traffic}[args.cmd](args)
+    {"copy": cmd_copy, "stats": cmd_stats, "counters": cmd_counters, "traffic": cmd_traffic}[args.cmd](args)
 
 
 if __name__ == "__main__":
