@@ -20,7 +20,8 @@ Readings (the paper gives no equations for these; listed in the design doc):
   the published 0.42B parameters).
 * The decoder layer is one layer of the target's architecture (RMSNorm,
   rotary attention over the draft's own cache of the prefix plus the node's
-  ancestors in the draft tree, SwiGLU MLP).
+  ancestors in the draft tree, SwiGLU MLP); for an MoE target its MLP is
+  dense, of the experts' width.
 * TEH is two linear heads with bias on the layer output y: F^P = y W_p + b_p
   and F^R = y W_r + b_r.  Logits = RMSNorm(F^P) (the target's final norm)
   times the target's LM head.
@@ -105,7 +106,7 @@ def draft_forward(dow: DraftOracleWeights, tree, feats_in: np.ndarray, prefix_kv
     k = rope(k, pos[:, None], m.rope_base)
     att = tree_attention(q, k, v, prefix_kv[0], prefix_kv[1], visible)
     x = x + att.reshape(T, Hq * dh) @ L["w_o"].T
-    y2, _ = mlp(rmsnorm(x, L["mlp_norm"], m.rms_eps), L, m)
+    y2, _ = mlp(rmsnorm(x, L["mlp_norm"], m.rms_eps), L, dow.shape.layer)
     y = x + y2
     t = dow.t
     fp = y @ t["w_p"].T + t["b_p"]

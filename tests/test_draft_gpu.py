@@ -67,7 +67,7 @@ def _pass_feats(dr, tree, fr_prev, root_feat):
     return f
 
 
-@pytest.mark.parametrize("name", ["tiny", "small-gqa", "tiny-v20001", "tiny-v20000"])
+@pytest.mark.parametrize("name", ["tiny", "small-gqa", "small-moe", "tiny-v20001", "tiny-v20000"])
 def test_draft_passes_match_oracle(name):
     """Three passes over growing trees, as an expansion runs them: the root
     alone, then its children, then grandchildren; each node reads its

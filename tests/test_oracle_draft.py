@@ -253,3 +253,25 @@ def test_chain_kv_extends_the_prefix():
     assert np.allclose(last.logits[0], whole.logits[-1], rtol=0, atol=1e-9)
     assert np.allclose(last.regress[0], whole.regress[-1], rtol=0, atol=1e-9)
     assert np.allclose(head.k, whole.k[:-1], atol=1e-12) and np.allclose(head.v, whole.v[:-1], atol=1e-12)
+
+
+def test_draft_layer_of_an_moe_target_is_dense():
+    """The draft of an MoE target has one dense SwiGLU layer of the experts'
+    width: its pass equals that of a draft whose target is the same model made
+    dense (the weights are the same tensors)."""
+    from dataclasses import replace
+    ds = DRAFTS["small-moe"]
+    assert ds.layer.n_experts == 1 and ds.layer.d_ff == ds.target.d_ff
+    mw = gen.make_weights(ds.target, 0)
+    dw = gen.make_draft_weights(ds, 3)
+    dense = replace(ds.target, n_experts=1, top_k=1)
+    dw_dense = gen.DraftWeights(replace(ds, target=dense), dw.t, dw.layer)
+    mw_dense = gen.ModelWeights(dense, mw.embed, mw.lm_head, mw.final_norm, [])
+    P = 25
+    k, v = gen.synthetic_kv(ds.layer, 0, 0, P, 5)
+    kv = (k.double().numpy(), v.double().numpy())
+    tree, _ = gen.random_tree((2, 3), ds.target.vocab, 8)
+    feats = np.random.default_rng(3).normal(size=(tree.n, ds.target.d_model))
+    a = od.draft_forward(od.DraftOracleWeights(dw, oracle.OracleWeights(mw)), tree, feats, kv, P)
+    b = od.draft_forward(od.DraftOracleWeights(dw_dense, oracle.OracleWeights(mw_dense)), tree, feats, kv, P)
+    assert np.array_equal(a.logits, b.logits) and np.array_equal(a.regress, b.regress)

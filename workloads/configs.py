@@ -195,8 +195,9 @@ class DraftShape:
 
     @property
     def layer(self) -> ModelShape:
-        """The decoder layer as a one-layer model of the target's shape."""
-        return replace(self.target, name=self.target.name + "-draft", n_layers=1)
+        """The decoder layer as a one-layer model of the target's shape, with a
+        dense SwiGLU MLP of the target's (expert) width also for MoE targets."""
+        return replace(self.target, name=self.target.name + "-draft", n_layers=1, n_experts=1, top_k=1)
 
     def param_count(self) -> int:
         m, d, e = self.target, self.target.d_model, self.tgf_dim
@@ -214,6 +215,8 @@ DRAFTS: Dict[str, DraftShape] = {
     "small-gqa": DraftShape(SMALL_GQA, tgf_dim=1800, k=5, depth=5, n_total=20),
     # vocabularies of several top-k slices (8192 logits each): one not a
     # multiple of 4 (scalar loads), one with 16-byte loads and the largest k
+    # an MoE target: the draft's decoder layer is dense (expert width)
+    "small-moe": DraftShape(SMALL_MOE, tgf_dim=900, k=4, depth=4, n_total=12),
     "tiny-v20001": DraftShape(replace(TINY, name="tiny-v20001", vocab=20001), tgf_dim=1000, k=4, depth=4,
                               n_total=12),
     "tiny-v20000": DraftShape(replace(TINY, name="tiny-v20000", vocab=20000), tgf_dim=1000, k=16, depth=3,
