@@ -119,6 +119,12 @@ def cpu_baseline(w, weights_gpu, n_trees=2):
     elapsed = time.perf_counter() - t0
     per_step = elapsed / len(trees) * w.batch
     threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    cpu_model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next((ln.split(":", 1)[1].strip() for ln in f if ln.startswith("model name")), None)
+    except OSError:
+        pass
     what = (f"{n_trees} {w.tree_nodes}-node trees at prefix {w.prefix_len} (batch 1)" if w.batch == 1 else
             f"the trees of sequences 0..{len(seqs) - 1} of one batch-{w.batch} step (prefixes "
             f"{[w.prefix_of(b) for b in seqs]}), scaled to the whole batch")
@@ -126,6 +132,7 @@ def cpu_baseline(w, weights_gpu, n_trees=2):
         "value": round(1.0 / per_step, 6),
         "unit": "verify_steps/s",
         "cores": int(threads),
+        "cpu_model": cpu_model,
         "kind": "oracle",
         "sample": (f"fp64 oracle, full {m.n_layers}-layer verify pass + argmax + acceptance walk of {what}, "
                    f"{elapsed:.1f} s in total"),

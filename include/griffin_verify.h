@@ -176,22 +176,45 @@ int griffin_accept_sampled(griffin_ctx *ctx, const float *logits, const float *q
                            const float *u_accept, const float *u_final, float temperature,
                            int32_t *accept_len, int32_t *tokens_out, int32_t *path_nodes);
 
-/* Commit the last step's accepted path into the KV cache (asynchronous, on
- * the context's stream; needs no host round trip).  For every sequence b of
- * that step, with L accepted draft nodes n_1..n_L at depths 1..L: their K/V,
+/* Commit the accepted path of the last step into the KV cache (asynchronous,
+ * on the context's stream).  The path is the one the last acceptance call
+ * since that step returned: griffin_accept (greedy) or griffin_accept_sampled
+ * (temperature > 0), whichever ran last.  For every sequence b of that step,
+ * with L accepted draft nodes n_1..n_L at depths 1..L: their K/V,
  * already rotated at positions prefix_len + k, move from scratch slots
  * prefix_len + n_k to slots prefix_len + k, so that slots [0, prefix_len + L]
  * hold the plain causal cache of prefix + root + accepted tokens.  The caller
  * continues with prefix_len + L + 1 and the target's extra token (tokens_out
- * entry L of griffin_accept) as the next root.  The paper's losslessness: a
- * loop of step / accept / commit emits exactly the target's greedy tokens.
- * Errors: EINVAL, EORDER (no step yet), EHIP. */
+ * entry L of the acceptance call) as the next root.  The paper's
+ * losslessness: a loop of step / accept / commit emits exactly the target's
+ * greedy tokens (and, with griffin_accept_sampled, samples of the target's
+ * distribution).
+ * Errors: EINVAL, EORDER (no step yet, or no acceptance call since the last
+ * step), EHIP. */
 int griffin_commit(griffin_ctx *ctx);
 
 /* Wait for the last step and copy the target's greedy prediction (argmax of
  * the logits) of every node: pred [batch][max_tree] host, -1 for absent nodes.
  * Errors: EORDER, EHIP. */
 int griffin_read_predictions(griffin_ctx *ctx, int32_t *pred);
+
+/* Wait for the last step and copy every node's top-2 logit margin: the
+ * largest logit minus the second largest (0 when the largest value occurs
+ * twice), over the non-NaN entries of the node's row: margin [batch][max_tree]
+ * host fp32, -1 for absent nodes, NaN for a row with fewer than two non-NaN
+ * logits.  A greedy choice whose margin is within the logits' rounding error
+ * is a near tie (Sec. 5: greedy decoding is decided by the argmax alone).
+ * Errors: EORDER, EHIP. */
+int griffin_read_margins(griffin_ctx *ctx, float *margin);
+
+/* Mixture-of-experts models only (the Mixtral targets of Sec. 5): wait for
+ * the last step and copy the fp32 router logits its pass computed, before the
+ * softmax and top-k, for every layer and node: out [n_layers][batch][max_tree]
+ * [n_experts] host, zeros for absent nodes.  A diagnostic of the routing
+ * decisions (a near tie between the last kept and first dropped expert is
+ * where a rounding difference can change a token's experts).
+ * Errors: EINVAL (dense model), EORDER (no step yet), EHIP. */
+int griffin_read_router_logits(griffin_ctx *ctx, float *out);
 
 /* The target's features of chosen nodes of the last step: the hidden state
  * after the last layer, before the final norm, i.e. the feature that

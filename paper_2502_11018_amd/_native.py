@@ -68,6 +68,8 @@ def _load() -> ctypes.CDLL:
         "griffin_accept": (c_int32, [c_void_p, I32P, I32P, I32P]),
         "griffin_read_predictions": (c_int32, [c_void_p, I32P]),
         "griffin_read_features": (c_int32, [c_void_p, c_int32, c_int32, I32P, c_void_p]),
+        "griffin_read_router_logits": (c_int32, [c_void_p, F32P]),
+        "griffin_read_margins": (c_int32, [c_void_p, F32P]),
         "griffin_set_activation_precision": (c_int32, [c_void_p, c_int32]),
         "griffin_verify_free": (None, [c_void_p]),
         "griffin_status_str": (c_char_p, [c_int32]),
@@ -106,6 +108,6 @@ EXPORTED = ("griffin_kv_cache_bytes", "griffin_verify_init", "griffin_verify_ste
             "griffin_set_graphs", "griffin_commit", "griffin_accept_sampled", "griffin_accept_sampled_walk",
             "griffin_draft_init", "griffin_draft_free", "griffin_draft_context", "griffin_draft_step",
             "griffin_draft_tree", "griffin_read_features", "griffin_draft_extend",
-            "griffin_set_activation_precision")
+            "griffin_set_activation_precision", "griffin_read_router_logits", "griffin_read_margins")
 KERNEL_CLASSES = ("qkv_gemm", "rope_kv_write", "tree_attention", "o_gemm", "residual_rmsnorm", "gate_up_gemm",
                   "down_gemm", "lm_head_gemm", "argmax_accept_route", "attn_merge")

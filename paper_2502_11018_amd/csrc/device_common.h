@@ -85,4 +85,27 @@ __device__ __forceinline__ float block_sum(float v, float* smem /* >= 16 floats 
 
 __device__ __forceinline__ float silu_f32(float z) { return z / (1.0f + __expf(-z)); }
 
+// Top-2 of (value, index) candidates, NaN-free: best with the lowest index
+// among equal maxima, and the second largest value of the union counted with
+// multiplicity (equal maxima at two indices give second == best).  Merging
+// two such summaries gives the summary of the union, in any order.
+__device__ __forceinline__ void top2_push(float& best, int& bidx, float& second, float v, int id) {
+  if (v > best || (v == best && id < bidx)) {
+    second = best;
+    best = v;
+    bidx = id;
+  } else if (v > second) {
+    second = v;
+  }
+}
+__device__ __forceinline__ void top2_merge(float& best, int& bidx, float& second, float ob, int oi, float os) {
+  if (ob > best || (ob == best && oi < bidx)) {
+    second = fmaxf(best, os);
+    best = ob;
+    bidx = oi;
+  } else {
+    second = fmaxf(second, ob);
+  }
+}
+
 }  // namespace griffin

@@ -275,42 +275,46 @@ hipError_t launch_qkv_rope(const float* qkv_parts, int n_parts, long long part_s
 // ------------------------------------------------------ argmax reduction ----
 // pred[r] = argmax over the LM-head column groups' partial maxima; ties keep
 // the lowest token id.
-__device__ __forceinline__ void argmax_merge(float& best, int& bidx, float v, int id) {
-  if (v > best || (v == best && id < bidx)) { best = v; bidx = id; }
-}
 
 // One 256-thread workgroup per row; each thread issues all loads of its
 // entries of a 4096-entry chunk before comparing any.  (max, lowest index) is
-// a total order, so the result does not depend on the reduction order.
+// a total order and the second largest value of a union does not depend on
+// how it is split, so the result does not depend on the reduction order.
+// margin[r] = max - second max (0 for a tie at the top; NaN when the row has
+// fewer than two non-NaN entries).
 constexpr int AR_THREADS = 256, AR_PER = 16;
 __global__ __launch_bounds__(AR_THREADS) void argmax_reduce_kernel(const float* __restrict__ pmax,
+                                                                   const float* __restrict__ pmax2,
                                                                    const int32_t* __restrict__ pidx,
                                                                    const int32_t* __restrict__ pnan, int n_tiles,
-                                                                   int ld_part, int32_t* pred, int32_t* nan_row) {
-  __shared__ float sb[AR_THREADS / 64];
+                                                                   int ld_part, int32_t* pred, float* margin,
+                                                                   int32_t* nan_row) {
+  __shared__ float sb[AR_THREADS / 64], s2[AR_THREADS / 64];
   __shared__ int si[AR_THREADS / 64], sn[AR_THREADS / 64];
   const int r = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const float* pm = pmax + (long long)r * ld_part;
+  const float* pm2 = pmax2 + (long long)r * ld_part;
   const int32_t* pi = pidx + (long long)r * ld_part;
   const int32_t* pn = pnan + (long long)r * ld_part;
-  float best = -INFINITY;
+  float best = -INFINITY, second = -INFINITY;
   int bidx = 0x7fffffff;
   int nan_cnt = 0;
   for (int base = 0; base < n_tiles; base += AR_THREADS * AR_PER) {
-    float v[AR_PER];
+    float v[AR_PER], v2[AR_PER];
     int id[AR_PER], nn[AR_PER];
 #pragma unroll
     for (int k = 0; k < AR_PER; ++k) {
       const int t = min(base + k * AR_THREADS + tid, n_tiles - 1);  // clamped: loads stay unconditional
       v[k] = pm[t];
+      v2[k] = pm2[t];
       id[k] = pi[t];
       nn[k] = pn[t];
     }
 #pragma unroll
     for (int k = 0; k < AR_PER; ++k) {
       if (base + k * AR_THREADS + tid < n_tiles) {
-        argmax_merge(best, bidx, v[k], id[k]);
+        top2_merge(best, bidx, second, v[k], id[k], v2[k]);
         nan_cnt += nn[k];
       }
     }
@@ -319,30 +323,34 @@ __global__ __launch_bounds__(AR_THREADS) void argmax_reduce_kernel(const float* 
   for (int o = 32; o > 0; o >>= 1) {
     const float ob = __shfl_xor(best, o, 64);
     const int oi = __shfl_xor(bidx, o, 64);
+    const float os = __shfl_xor(second, o, 64);
     nan_cnt += __shfl_xor(nan_cnt, o, 64);
-    argmax_merge(best, bidx, ob, oi);
+    top2_merge(best, bidx, second, ob, oi, os);
   }
   if (lane == 0) {
     sb[w] = best;
+    s2[w] = second;
     si[w] = bidx;
     sn[w] = nan_cnt;
   }
   __syncthreads();
   if (tid == 0) {
     for (int k = 1; k < AR_THREADS / 64; ++k) {
-      argmax_merge(best, bidx, sb[k], si[k]);
+      top2_merge(best, bidx, second, sb[k], si[k], s2[k]);
       nan_cnt += sn[k];
     }
     pred[r] = bidx;
+    margin[r] = second == -INFINITY ? __builtin_nanf("") : best - second;
     nan_row[r] = nan_cnt;
   }
 }
 
-hipError_t launch_argmax_reduce(const float* pmax, const int32_t* pidx, const int32_t* pnan, int n_tiles,
-                                int ld_part, int rows, int32_t* pred, int32_t* nan_row, hipStream_t s) {
+hipError_t launch_argmax_reduce(const float* pmax, const float* pmax2, const int32_t* pidx, const int32_t* pnan,
+                                int n_tiles, int ld_part, int rows, int32_t* pred, float* margin, int32_t* nan_row,
+                                hipStream_t s) {
   if (n_tiles < 1) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(argmax_reduce_kernel, dim3(rows), dim3(AR_THREADS), 0, s, pmax, pidx, pnan, n_tiles, ld_part,
-                     pred, nan_row);
+  hipLaunchKernelGGL(argmax_reduce_kernel, dim3(rows), dim3(AR_THREADS), 0, s, pmax, pmax2, pidx, pnan, n_tiles,
+                     ld_part, pred, margin, nan_row);
   return hipGetLastError();
 }
 
@@ -465,7 +473,8 @@ __global__ __launch_bounds__(256) void moe_route_kernel(const float* __restrict_
                                                         const uint16_t* __restrict__ gain, float eps,
                                                         const uint16_t* __restrict__ wr, int d, int n_experts,
                                                         int top_k, const int32_t* n_nodes, int max_tree,
-                                                        int32_t* route_ids, float* route_w) {
+                                                        int32_t* route_ids, float* route_w,
+                                                        float* __restrict__ logits_out) {
   __shared__ float red[16];
   __shared__ float logit[64];
   const int r = blockIdx.x;
@@ -488,6 +497,8 @@ __global__ __launch_bounds__(256) void moe_route_kernel(const float* __restrict_
     const float t = block_sum(acc, red);
     if (threadIdx.x == 0) logit[e] = t;
   }
+  __syncthreads();
+  if (threadIdx.x < n_experts) logits_out[(long long)r * n_experts + threadIdx.x] = logit[threadIdx.x];
   __syncthreads();
   if (threadIdx.x == 0) {
     float mx = -INFINITY;
@@ -516,10 +527,10 @@ __global__ __launch_bounds__(256) void moe_route_kernel(const float* __restrict_
 
 hipError_t launch_moe_route(const float* x, const uint16_t* gain, float eps, const uint16_t* w_router, int rows,
                             int d, int n_experts, int top_k, const int32_t* n_nodes, int max_tree,
-                            int32_t* route_ids, float* route_w, hipStream_t s) {
+                            int32_t* route_ids, float* route_w, float* logits_out, hipStream_t s) {
   if (n_experts > 64 || top_k > 4) return hipErrorInvalidValue;
   hipLaunchKernelGGL(moe_route_kernel, dim3(rows), dim3(256), 0, s, x, gain, eps, w_router, d, n_experts, top_k,
-                     n_nodes, max_tree, route_ids, route_w);
+                     n_nodes, max_tree, route_ids, route_w, logits_out);
   return hipGetLastError();
 }
 

@@ -214,8 +214,8 @@ __global__ __launch_bounds__(64 * WN * KS) void gemm_kernel(GemmArgs a) {
           *reinterpret_cast<uint2*>(dst + XPACK_LO) = make_uint2(p0.lo, p1.lo);
         }
       }
-    } else {  // EPI_ARGMAX: partial (max, argmax, NaN count) over this wave's columns
-      float best = -INFINITY;
+    } else {  // EPI_ARGMAX: partial (max, argmax, second max, NaN count) over this wave's columns
+      float best = -INFINITY, second = -INFINITY;
       int bidx = 0x7fffffff;
       int nan_cnt = 0;
 #pragma unroll
@@ -228,16 +228,18 @@ __global__ __launch_bounds__(64 * WN * KS) void gemm_kernel(GemmArgs a) {
             const float v = acc[b][mb][4 * rg + i];
             if (n < a.N) {
               if (v != v) ++nan_cnt;
-              else if (v > best || (v == best && n < bidx)) { best = v; bidx = n; }
+              else top2_push(best, bidx, second, v, n);
             }
           }
       const float ob = __shfl_xor(best, 32, 64);
       const int oi = __shfl_xor(bidx, 32, 64);
+      const float os = __shfl_xor(second, 32, 64);
       nan_cnt += __shfl_xor(nan_cnt, 32, 64);
-      if (ob > best || (ob == best && oi < bidx)) { best = ob; bidx = oi; }
+      top2_merge(best, bidx, second, ob, oi, os);
       const int part = wg * WN + wc;
       if (g == 0) {
         a.pmax[orow * a.ld_part + part] = best;
+        a.pmax2[orow * a.ld_part + part] = second;
         a.pidx[orow * a.ld_part + part] = bidx;
         a.pnan[orow * a.ld_part + part] = nan_cnt;
       }

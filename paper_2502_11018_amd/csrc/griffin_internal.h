@@ -79,6 +79,7 @@ struct GemmArgs {
   int act_ks;
   // EPI_ARGMAX
   float* pmax;
+  float* pmax2;              // second largest value of the same columns (top-2 margin)
   int32_t* pidx;
   int32_t* pnan;
   int ld_part;
@@ -148,8 +149,9 @@ hipError_t launch_attn_combine(const float* part_o, const float* part_ml, StepMe
                                int splits, int qrows, int max_tree, int batch, const uint16_t* q,
                                const uint16_t* q_lo, TreeKV32 tree, PrefixKV prefix, float scale_log2,
                                uint16_t* o_out, int o_ks, hipStream_t s);
-hipError_t launch_argmax_reduce(const float* pmax, const int32_t* pidx, const int32_t* pnan, int n_tiles,
-                                int ld_part, int rows, int32_t* pred, int32_t* nan_row, hipStream_t s);
+hipError_t launch_argmax_reduce(const float* pmax, const float* pmax2, const int32_t* pidx, const int32_t* pnan,
+                                int n_tiles, int ld_part, int rows, int32_t* pred, float* margin, int32_t* nan_row,
+                                hipStream_t s);
 hipError_t launch_commit(const int32_t* result, int max_depth, StepMeta meta, int batch, int n_layers, int Hkv,
                          int dh, int kv_cap, long long layer_kv, uint16_t* k_cache, uint16_t* v_cache,
                          hipStream_t s);
@@ -159,7 +161,8 @@ hipError_t launch_accept(StepMeta meta, const int32_t* pred, const int32_t* nan_
                          int max_tree, int max_depth, int32_t* result, hipStream_t s);
 hipError_t launch_moe_route(const float* x, const uint16_t* gain, float eps, const uint16_t* w_router,
                             int rows, int d, int n_experts, int top_k, const int32_t* n_nodes,
-                            int max_tree, int32_t* route_ids, float* route_w, hipStream_t s);
+                            int max_tree, int32_t* route_ids, float* route_w, float* logits_out,
+                            hipStream_t s);
 hipError_t launch_moe_lists(const int32_t* route_ids, int rows, int padded_rows, int n_experts, int top_k,
                             int cap, int32_t* gather, int32_t* count, int32_t* slot, hipStream_t s);
 hipError_t launch_moe_gather(const uint16_t* xn, int xn_ks, const int32_t* gather, const int32_t* count,

@@ -15,10 +15,12 @@
 
 #include "draft.h"
 #include "griffin_internal.h"
+#include "plan.h"
 #include "sampling.h"
 #include "griffin_verify.h"
 
 using namespace griffin;
+using namespace griffin_plan;
 
 namespace {
 
@@ -29,102 +31,6 @@ int round_up(int x, int m) { return (x + m - 1) / m * m; }
 int cdiv(int x, int m) { return (x + m - 1) / m; }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
-
-// Validate one tree and, optionally, fill depth / position / ancestor masks.
-int prepare_tree(int32_t n, const int32_t* tokens, const int32_t* parents, int32_t prefix_len, int32_t max_tree,
-                 int32_t max_depth, int32_t vocab, int32_t kv_capacity, int32_t* depth, int32_t* pos,
-                 uint64_t* anc, std::string* why) {
-  auto fail = [&](int code, const char* fmt, long a = 0, long b = 0) {
-    if (why) {
-      char buf[256];
-      snprintf(buf, sizeof buf, fmt, a, b);
-      *why = buf;
-    }
-    return code;
-  };
-  if (!tokens || !parents) return fail(GRIFFIN_EINVAL, "null tree array");
-  if (n < 1 || n > max_tree || n > kMaxTree) return fail(GRIFFIN_ETREE, "tree size %ld outside [1, %ld]", n, max_tree);
-  if (prefix_len < 0 || (long)prefix_len + n > kv_capacity)
-    return fail(GRIFFIN_ECAPACITY, "prefix_len %ld + nodes %ld exceeds kv_capacity", prefix_len, n);
-  if (parents[0] != -1) return fail(GRIFFIN_ETREE, "parents[0] = %ld, must be -1", parents[0]);
-  int32_t dep[kMaxTree];
-  uint64_t an[kMaxTree];
-  dep[0] = 0;
-  an[0] = 1ull;
-  for (int i = 0; i < n; ++i) {
-    if (tokens[i] < 0 || tokens[i] >= vocab) return fail(GRIFFIN_ETOKEN, "token %ld of node %ld out of range", tokens[i], i);
-    if (i == 0) continue;
-    const int p = parents[i];
-    if (p < 0 || p >= i) return fail(GRIFFIN_ETREE, "parent %ld of node %ld not in [0, i)", p, i);
-    dep[i] = dep[p] + 1;
-    if (dep[i] > max_depth) return fail(GRIFFIN_ETREE, "node %ld has depth %ld > max_depth", i, dep[i]);
-    an[i] = an[p] | (1ull << i);
-  }
-  for (int i = 0; i < n; ++i) {
-    if (depth) depth[i] = dep[i];
-    if (pos) pos[i] = prefix_len + dep[i];
-    if (anc) anc[i] = an[i];
-  }
-  return GRIFFIN_OK;
-}
-
-// Prefix-attention work of one step: batch * splits units, each sequence at
-// least one and at most min(sp, blocks / 2) (blocks = 32-key blocks of its
-// prefix), the rest dealt one at a time to the sequence with the most blocks
-// per split (ties: the lower index).  A sequence's result depends on the
-// batch only through its split count.  tab [batch * splits][4]: (b | split <<
-// 16, splits of b, prefix_len, n_nodes), b = -1 for units left unused;
-// nsplit [batch].
-void attn_split_plan(int batch, const int32_t* prefix_len, const int32_t* n_nodes, int splits, int sp,
-                     int32_t* tab, int32_t* nsplit) {
-  std::vector<int> blocks(batch), cap(batch), cnt(batch, 1);
-  for (int b = 0; b < batch; ++b) {
-    blocks[b] = (prefix_len[b] + 31) / 32;
-    cap[b] = std::max(1, std::min(sp, blocks[b] / 2));
-  }
-  for (int left = batch * splits - batch; left > 0; --left) {
-    int best = -1;
-    for (int b = 0; b < batch; ++b)
-      if (cnt[b] < cap[b] && (best < 0 || (long long)blocks[b] * cnt[best] > (long long)blocks[best] * cnt[b]))
-        best = b;
-    if (best < 0) break;
-    ++cnt[best];
-  }
-  int j = 0;
-  for (int b = 0; b < batch; ++b) {
-    nsplit[b] = cnt[b];
-    for (int s = 0; s < cnt[b]; ++s, ++j) {
-      tab[4 * j] = b | (s << 16);
-      tab[4 * j + 1] = cnt[b];
-      tab[4 * j + 2] = prefix_len[b];
-      tab[4 * j + 3] = n_nodes[b];
-    }
-  }
-  for (; j < batch * splits; ++j) {
-    tab[4 * j] = -1;
-    tab[4 * j + 1] = tab[4 * j + 2] = tab[4 * j + 3] = 0;
-  }
-}
-
-int validate_desc(const griffin_model_desc* d, std::string* why) {
-  auto bad = [&](const char* m) {
-    if (why) *why = m;
-    return GRIFFIN_ESHAPE;
-  };
-  if (d->n_layers < 1 || d->d_model < 8 || d->vocab < 2 || d->d_ff < 8) return bad("non-positive dimension");
-  if (d->head_dim != 64 && d->head_dim != 128) return bad("head_dim must be 64 or 128");
-  if (d->n_kv_heads < 1 || d->n_q_heads < 1 || d->n_q_heads % d->n_kv_heads) return bad("n_q_heads must be a multiple of n_kv_heads");
-  if (d->d_model % 8 || d->d_ff % 8 || (d->n_q_heads * d->head_dim) % 8) return bad("d_model, d_ff, n_q_heads*head_dim must be multiples of 8");
-  if (d->d_model > 8192) return bad("d_model above 8192");
-  if (d->n_experts < 1 || d->n_experts > 64) return bad("n_experts must be in [1, 64]");
-  if (d->n_experts > 1 && (d->top_k < 1 || d->top_k > 4 || d->top_k > d->n_experts)) return bad("top_k must be in [1, min(n_experts, 4)]");
-  if (d->max_batch < 1) return bad("max_batch < 1");
-  if (d->max_tree < 1 || d->max_tree > kMaxTree) return bad("max_tree must be in [1, 64]");
-  if (d->max_depth < 0 || d->max_depth >= d->max_tree) return bad("max_depth must be in [0, max_tree - 1]");
-  if (d->kv_capacity < 32 || d->kv_capacity % 32) return bad("kv_capacity must be a positive multiple of 32");
-  if (!(d->rms_eps > 0.f) || !(d->rope_base > 1.0)) return bad("rms_eps must be > 0 and rope_base > 1");
-  return GRIFFIN_OK;
-}
 
 // Launch shape of one weight matrix (fixed at init; the packing follows it).
 struct GemmPlan {
@@ -211,7 +117,11 @@ struct griffin_ctx {
 
   std::vector<void*> allocs;
   float *x = nullptr, *parts = nullptr, *attn_po = nullptr, *attn_pml = nullptr;
-  float *rope_cos = nullptr, *rope_sin = nullptr, *pmax = nullptr, *route_w = nullptr, *yslots = nullptr;
+  float *rope_cos = nullptr, *rope_sin = nullptr, *pmax = nullptr, *pmax2 = nullptr, *route_w = nullptr,
+        *yslots = nullptr;
+  float* margin = nullptr;         // [Mpad] top-2 logit margin of every row
+  float* margin_host = nullptr;    // pinned copy for griffin_read_margins
+  float* router_logits = nullptr;  // MoE: [n_layers][max_batch * max_tree][E] fp32, the last pass's
   uint16_t *xn = nullptr, *q = nullptr, *q_lo = nullptr, *o = nullptr, *act = nullptr, *xe = nullptr;
   TreeKV32 tree{};  // fp32 tree K/V of the layer being computed (reused by every layer)
   int32_t *pidx = nullptr, *pnan = nullptr, *pred = nullptr, *nan_row = nullptr, *result = nullptr;
@@ -252,6 +162,9 @@ struct griffin_ctx {
   size_t prof_used = 0;                // pairs recorded since the last read
   int batch = 0;
   bool stepped = false;
+  // the accepted paths griffin_commit moves: the result buffer of the last
+  // acceptance (greedy walk or stochastic) since the last step, else null
+  const int32_t* accepted = nullptr;
   // A draft model's one-layer context replaces the token embedding by its
   // fusion module (front: writes x) and the final residual + norm by its
   // heads (back: writes xn); it runs no argmax or acceptance.
@@ -445,7 +358,7 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
       const int xe_tiles = Mpad / 64;
       LAUNCH(GRIFFIN_KC_OTHER, launch_moe_route(c->x, c->mlp_norm[l], d.rms_eps, c->w_router[l], rows, d.d_model,
                                                 c->E, c->topk, c->meta.n_nodes, d.max_tree, c->route_ids,
-                                                c->route_w, s));
+                                                c->route_w, c->router_logits + (long long)l * rows * c->E, s));
       LAUNCH(GRIFFIN_KC_OTHER, launch_moe_lists(c->route_ids, rows, Mpad, c->E, c->topk, Mpad, c->gather, c->count,
                                                 c->slot, s));
       LAUNCH(GRIFFIN_KC_OTHER, launch_moe_gather(c->xn, c->xd_ks, c->gather, c->count, c->E, Mpad, d.d_model,
@@ -486,6 +399,7 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
   {
     GemmArgs a = gemm_args(c->p_lm, c->xn, c->xd_ks, c->pk_lm, m_tiles, !c->act_bf16);
     a.pmax = c->pmax;
+    a.pmax2 = c->pmax2;
     a.pidx = c->pidx;
     a.pnan = c->pnan;
     a.ld_part = lm_parts;
@@ -495,8 +409,8 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
     LAUNCH(GRIFFIN_KC_LM_HEAD, launch_gemm(a, 1, s));
   }
   if (c->front) return GRIFFIN_OK;  // a draft pass: the caller reads the logits
-  LAUNCH(GRIFFIN_KC_OTHER, launch_argmax_reduce(c->pmax, c->pidx, c->pnan, lm_parts, lm_parts, rows, c->pred,
-                                                c->nan_row, s));
+  LAUNCH(GRIFFIN_KC_OTHER, launch_argmax_reduce(c->pmax, c->pmax2, c->pidx, c->pnan, lm_parts, lm_parts, rows,
+                                                c->pred, c->margin, c->nan_row, s));
   LAUNCH(GRIFFIN_KC_OTHER, launch_accept(c->meta, c->pred, c->nan_row, B, d.max_tree, d.max_depth, c->result, s));
   return GRIFFIN_OK;
 }
@@ -670,6 +584,7 @@ void griffin_verify_free(griffin_ctx* c) {
   for (auto& g : c->graphs) hipGraphExecDestroy(g.exec);
   if (c->result_host) hipHostFree(c->result_host);
   if (c->pred_host) hipHostFree(c->pred_host);
+  if (c->margin_host) hipHostFree(c->margin_host);
   if (c->samp_host) hipHostFree(c->samp_host);
   if (c->feat_rows_host) hipHostFree(c->feat_rows_host);
   if (c->feat_ev) hipEventDestroy(c->feat_ev);
@@ -774,6 +689,8 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
   ALLOC(c->act, (long long)c->E * tiles * c->p_down.ks_pad * XPACK_STEP);
   const long long lm_parts = (long long)c->p_lm.shape.n_wgs * c->p_lm.wn;
   ALLOC(c->pmax, Mp * lm_parts);
+  ALLOC(c->pmax2, Mp * lm_parts);
+  ALLOC(c->margin, Mp);
   ALLOC(c->pidx, Mp * lm_parts);
   ALLOC(c->pnan, Mp * lm_parts);
   ALLOC(c->pred, Mp);
@@ -788,6 +705,7 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
   if (moe) {
     ALLOC(c->route_ids, Mp * c->topk);
     ALLOC(c->route_w, Mp * c->topk);
+    ALLOC(c->router_logits, (long long)d.n_layers * d.max_batch * d.max_tree * c->E);
     ALLOC(c->gather, (long long)c->E * Mp);
     ALLOC(c->count, c->E);
     ALLOC(c->slot, Mp * c->topk);
@@ -900,6 +818,7 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
   if (hipHostMalloc((void**)&c->result_host, sizeof(int32_t) * d.max_batch * result_stride(d.max_depth),
                     hipHostMallocDefault) != hipSuccess ||
       hipHostMalloc((void**)&c->pred_host, sizeof(int32_t) * Mp, hipHostMallocDefault) != hipSuccess ||
+      hipHostMalloc((void**)&c->margin_host, sizeof(float) * Mp, hipHostMallocDefault) != hipSuccess ||
       hipHostMalloc((void**)&c->samp_host, sizeof(float) * 5 * d.max_batch * d.max_tree, hipHostMallocDefault) !=
           hipSuccess ||
       hipHostMalloc((void**)&c->feat_rows_host, sizeof(int32_t) * d.max_batch * d.max_tree, hipHostMallocDefault) !=
@@ -963,6 +882,7 @@ int griffin_verify_step(griffin_ctx* c, int32_t batch, const int32_t* prefix_len
   c->meta_cur = k;
   c->batch = batch;
   c->stepped = false;
+  c->accepted = nullptr;
   const int rc = run_pass(c, logits_out);
   if (rc != GRIFFIN_OK) return rc;
   c->stepped = true;
@@ -972,9 +892,11 @@ int griffin_verify_step(griffin_ctx* c, int32_t batch, const int32_t* prefix_len
 int griffin_commit(griffin_ctx* c) {
   if (!c) return GRIFFIN_EINVAL;
   if (!c->stepped) return set_err(c, GRIFFIN_EORDER, "no verification step has been enqueued");
+  if (!c->accepted)
+    return set_err(c, GRIFFIN_EORDER, "no griffin_accept or griffin_accept_sampled since the last step");
   const griffin_model_desc& d = c->d;
   const long long layer_kv = (long long)d.max_batch * d.n_kv_heads * d.kv_capacity * d.head_dim;
-  HIP_TRY(c, launch_commit(c->result, d.max_depth, c->meta, c->batch, d.n_layers, d.n_kv_heads, d.head_dim,
+  HIP_TRY(c, launch_commit(c->accepted, d.max_depth, c->meta, c->batch, d.n_layers, d.n_kv_heads, d.head_dim,
                            d.kv_capacity, layer_kv, c->k_cache, c->v_cache, c->stream));
   return GRIFFIN_OK;
 }
@@ -1002,6 +924,7 @@ int griffin_accept(griffin_ctx* c, int32_t* accept_len, int32_t* tokens_out, int
   HIP_TRY(c, hipMemcpyAsync(c->result_host, c->result, sizeof(int32_t) * c->batch * st, hipMemcpyDeviceToHost,
                             c->stream));
   HIP_TRY(c, hipStreamSynchronize(c->stream));
+  c->accepted = c->result;
   bool nan = false;
   for (int b = 0; b < c->batch; ++b) {
     const int32_t* r = c->result_host + (size_t)b * st;
@@ -1013,37 +936,6 @@ int griffin_accept(griffin_ctx* c, int32_t* accept_len, int32_t* tokens_out, int
   }
   if (nan) return set_err(c, GRIFFIN_ENUMERIC, "NaN in the logits of a tree node");
   return GRIFFIN_OK;
-}
-
-// Work list of the stochastic acceptance: every node's row b * max_tree + u,
-// sorted by child count (descending, ties by row); rows_with[j] = the number
-// of rows with at least j children; for k = 0, 1, .. in turn, the k-th child
-// (in id order) of each of the first rows_with[k + 1] rows and its token.
-// parents: root entries ignored.
-static void sampled_plan(int batch, int max_tree, const int32_t* n_nodes, const int32_t* parents,
-                         const int32_t* tokens, std::vector<int32_t>& order, std::vector<int>& rows_with,
-                         std::vector<int32_t>& step_child, std::vector<int32_t>& step_token) {
-  std::vector<std::vector<int32_t>> kids((size_t)batch * max_tree);
-  order.clear();
-  for (int b = 0; b < batch; ++b)
-    for (int i = 0; i < n_nodes[b]; ++i) {
-      order.push_back(b * max_tree + i);
-      if (i > 0) kids[(size_t)b * max_tree + parents[(size_t)b * max_tree + i]].push_back(i);
-    }
-  std::stable_sort(order.begin(), order.end(),
-                   [&](int32_t x, int32_t y) { return kids[x].size() > kids[y].size(); });
-  const int cmax = order.empty() ? 0 : (int)kids[order[0]].size();
-  rows_with.assign(cmax + 1, 0);
-  for (int32_t r : order)
-    for (int j = 0; j <= (int)kids[r].size(); ++j) ++rows_with[j];
-  step_child.clear();
-  step_token.clear();
-  for (int k = 0; k < cmax; ++k)
-    for (int i = 0; i < rows_with[k + 1]; ++i) {
-      const int32_t r = order[i], c = kids[r][k];
-      step_child.push_back(c);
-      step_token.push_back(tokens[(size_t)(r / max_tree) * max_tree + c]);
-    }
 }
 
 int griffin_accept_sampled(griffin_ctx* c, const float* logits, const float* q_draft, const float* u_accept,
@@ -1099,6 +991,7 @@ int griffin_accept_sampled(griffin_ctx* c, const float* logits, const float* q_d
   HIP_TRY(c, hipMemcpyAsync(c->result_host, c->samp_result, sizeof(int32_t) * c->batch * st, hipMemcpyDeviceToHost,
                             c->stream));
   HIP_TRY(c, hipStreamSynchronize(c->stream));
+  c->accepted = c->samp_result;
   bool nan = false;
   for (int b = 0; b < c->batch; ++b) {
     const int32_t* r = c->result_host + (size_t)b * st;
@@ -1123,6 +1016,38 @@ int griffin_read_predictions(griffin_ctx* c, int32_t* pred) {
     const int b = r / c->d.max_tree, i = r % c->d.max_tree;
     pred[r] = i < nodes[b] ? c->pred_host[r] : -1;
   }
+  return GRIFFIN_OK;
+}
+
+int griffin_read_margins(griffin_ctx* c, float* margin) {
+  if (!c || !margin) return GRIFFIN_EINVAL;
+  if (!c->stepped) return set_err(c, GRIFFIN_EORDER, "no verification step has been enqueued");
+  const int rows = c->batch * c->d.max_tree;
+  HIP_TRY(c, hipMemcpyAsync(c->margin_host, c->margin, sizeof(float) * rows, hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  const int32_t* nodes = reinterpret_cast<const int32_t*>(c->meta_host[c->meta_cur] + c->off_nodes);
+  for (int r = 0; r < rows; ++r) {
+    const int b = r / c->d.max_tree, i = r % c->d.max_tree;
+    margin[r] = i < nodes[b] ? c->margin_host[r] : -1.f;
+  }
+  return GRIFFIN_OK;
+}
+
+int griffin_read_router_logits(griffin_ctx* c, float* out) {
+  if (!c || !out) return GRIFFIN_EINVAL;
+  if (c->E == 1) return set_err(c, GRIFFIN_EINVAL, "the model has no router (n_experts = 1)");
+  if (!c->stepped) return set_err(c, GRIFFIN_EORDER, "no verification step has been enqueued");
+  const griffin_model_desc& d = c->d;
+  const int rows = c->batch * d.max_tree;
+  // the pass writes layer l's rows at l * rows * E (rows of this step's batch)
+  const size_t n = (size_t)d.n_layers * rows * c->E;
+  HIP_TRY(c, hipMemcpyAsync(out, c->router_logits, sizeof(float) * n, hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  const int32_t* nodes = reinterpret_cast<const int32_t*>(c->meta_host[c->meta_cur] + c->off_nodes);
+  for (int l = 0; l < d.n_layers; ++l)
+    for (int r = 0; r < rows; ++r)
+      if (r % d.max_tree >= nodes[r / d.max_tree])
+        std::fill(out + ((size_t)l * rows + r) * c->E, out + ((size_t)l * rows + r + 1) * c->E, 0.f);
   return GRIFFIN_OK;
 }
 

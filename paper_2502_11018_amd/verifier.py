@@ -258,6 +258,23 @@ class TreeVerifier:
         _check(rc, "griffin_read_predictions", self.ctx)
         return pred[: self._batch]
 
+    def margins(self) -> np.ndarray:
+        """Top-2 logit margin of every node of the last step: [batch, max_tree]
+        fp32, -1 for absent nodes."""
+        out = np.zeros((max(self._batch, 1), self.max_tree), dtype=np.float32)
+        rc = N.lib.griffin_read_margins(self.ctx, _pf32(out))
+        _check(rc, "griffin_read_margins", self.ctx)
+        return out[: self._batch]
+
+    def router_logits(self) -> np.ndarray:
+        """MoE models: the fp32 router logits of the last step's pass,
+        [n_layers, batch, max_tree, n_experts] (zeros for absent nodes)."""
+        out = np.zeros((self.shape.n_layers, max(self._batch, 1), self.max_tree, self.shape.n_experts),
+                       dtype=np.float32)
+        rc = N.lib.griffin_read_router_logits(self.ctx, _pf32(out))
+        _check(rc, "griffin_read_router_logits", self.ctx)
+        return out[:, : self._batch]
+
     def set_bf16_activations(self, enable: bool):
         """GEMM activations as bf16 alone (True) or bf16 high + low parts
         (False, the default); see griffin_set_activation_precision."""

@@ -9,7 +9,9 @@ carry that rank's oracle logit within TOKEN_GAP; log-probabilities within
 LOGP_TOL.  A drafted tree: the set of root paths
 equals the oracle's expansion wherever none of its selections (the
 frontier of each depth, the final n_total) is decided by a score gap below
-SCORE_GAP; other cases are counted.  Every case prints its name first.
+SCORE_GAP; every drafted tree, decided or not, must be a correct expansion
+of the oracle's draft (scores, top-k membership, nothing dropped that beats
+the kept nodes by more than SCORE_GAP).  Every case prints its name first.
 """
 
 import numpy as np
@@ -138,6 +140,61 @@ def _path_set(n, tok, par):
     return out
 
 
+def _oracle_scores(dr, b, n, tok, par, D):
+    """The oracle's view of a drafted tree: every node's path log-probability
+    and every node's full log-softmax row.  A node's outputs depend only on
+    its root path (the ancestor mask) and its input feature, its parent's
+    regress feature from the previous pass, so D passes over the whole tree
+    make every node of depth <= p exact after pass p."""
+    t = gen.Tree(np.asarray(tok[:n], np.int32), np.asarray(par[:n], np.int32))
+    depth = t.depths()
+    feats = np.zeros((n, dr.ds.target.d_model))
+    feats[0] = dr.feat[b].double().numpy()
+    logp = [None] * n
+    prev = None
+    for p in range(D):
+        if prev is not None:
+            for i in range(1, n):
+                feats[i] = prev[t.parents[i]]
+        r = od.draft_forward(dr.dow, t, feats, dr.kv[b], dr.prefix[b])
+        for i in range(n):
+            if depth[i] == p:
+                row = r.logits[i]
+                mx = row.max()
+                logp[i] = row - (mx + np.log(np.exp(row - mx).sum()))
+        prev = r.regress
+    score = np.zeros(n)
+    for i in range(1, n):
+        score[i] = score[t.parents[i]] + logp[t.parents[i]][t.tokens[i]]
+    return t, depth, score, logp
+
+
+def _check_valid_expansion(dr, b, n, tok, par, sc, k, D, N):
+    """A drafted tree that near-ties may have decided differently from the
+    oracle's expansion must still be a correct expansion of the oracle's
+    draft: each kept node's score is its path log-probability (within
+    LOGP_TOL per level), each kept child is one of its parent's top-k
+    tokens (within TOKEN_GAP), and no candidate proposed by a node that kept
+    children but itself dropped scores above the worst kept node by more than
+    SCORE_GAP."""
+    t, depth, score, logp = _oracle_scores(dr, b, n, tok, par, D)
+    for i in range(1, n):
+        assert abs(sc[i] - score[i]) <= LOGP_TOL * depth[i], (b, i, sc[i], score[i])
+    worst = min(score[1:])
+    kids = {}
+    for i in range(1, n):
+        kids.setdefault(int(t.parents[i]), []).append(i)
+    for u, ch in kids.items():
+        top = np.argsort(-logp[u], kind="stable")[:k]
+        kth = logp[u][top[-1]]
+        kept = {int(t.tokens[c]) for c in ch}
+        for c in ch:
+            assert logp[u][t.tokens[c]] >= kth - TOKEN_GAP, (b, u, c)
+        for v in top:
+            if int(v) not in kept:
+                assert score[u] + logp[u][v] <= worst + SCORE_GAP, (b, u, int(v), score[u] + logp[u][v], worst)
+
+
 @pytest.mark.parametrize("name", ["tiny", "small-gqa", "tiny-v20000"])
 def test_drafted_tree_matches_oracle_expansion(name):
     B = 3
@@ -167,6 +224,7 @@ def test_drafted_tree_matches_oracle_expansion(name):
             for i in range(1, n[b]):
                 depth[i] = depth[par[b, i]] + 1
             assert max(depth) <= D
+            _check_valid_expansion(dr, b, n[b], tok[b], par[b], sc[b], k, D, N)
             if _decided(ex, k, D, N):
                 compared += 1
                 assert np.max(np.abs(np.sort(sc[b, : n[b]]) - np.sort(ex.scores))) < 1e-2

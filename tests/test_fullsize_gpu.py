@@ -125,8 +125,10 @@ def _full_size_verify(name, bf16_activations):
 
 def test_full_size_moe_verify_matches_oracle():
     """Mixtral-8x7B shape (about 94 GB of bf16 weights, 8 experts, top-2): one
-    unplanted tree through all 32 layers; nodes whose routing has an oracle
-    near-tie on their ancestry are left out of the gates and counted."""
+    unplanted tree through all 32 layers.  The device's router logits are
+    compared with the oracle's; nodes whose root path chose other experts
+    than the oracle (each such choice must be a near tie within the measured
+    router-logit error) are left out of the gates and counted."""
     import paper_2502_11018_amd as P
     w = get_workload("mixtral-8x7b")
     m = w.model
@@ -148,17 +150,20 @@ def test_full_size_moe_verify_matches_oracle():
     acc = v.accept()
     pred = v.predictions()[0]
     lg = logits[: tree.n].cpu().numpy()
+    rl = v.router_logits()[:, 0]
     v.close()
     say(f"mixtral-8x7b: host copy of the weights ({time.time() - t0:.0f}s)")
     ow = oracle.OracleWeights(mw_gpu.to("cpu"), cache=False)
     del mw_gpu
     say(f"mixtral-8x7b: oracle verify ({time.time() - t0:.0f}s)")
     os_ = H.oracle_sequence(ow, H.SeqCase(None, kv, tree, [], [], []))
-    ex = H.router_near_tie_nodes(os_, m.top_k, H.ROUTER_GAP)
+    err, gap, ex, near = H.router_check(os_, rl, m.top_k)
     st = H.check_parity(os_, lg, pred[: tree.n], acc.sequence(0), exclude=ex)
     say(f"mixtral-8x7b: max rel err {st['max_rel']:.2e}, gated {st['gated']}/{st['total']}, "
-        f"router near-tie nodes {len(ex)}, accept checked {st['accept_checked']} ({time.time() - t0:.0f}s)")
-    assert len(ex) < tree.n
+        f"router logit error {err:.2e}, near-tie gap {gap:.2e}, nodes with other experts on their path "
+        f"{len(ex)} (with a near tie: {len(near)}), accept checked {st['accept_checked']} ({time.time() - t0:.0f}s)")
+    # the MoE path is checked on almost every node, not on the few a wide gap leaves
+    assert len(ex) <= tree.n // 10
 
 
 def test_full_size_long_context_batch_matches_oracle():

@@ -39,7 +39,15 @@ def test_make_weights_shapes_and_layouts():
     assert L["w_down"].shape == (w.n_experts, w.d_model, w.d_ff)
     assert L["w_router"].shape == (w.n_experts, w.d_model)
     assert mw.embed.dtype == torch.bfloat16
-    assert torch.all(L["attn_norm"] == 1)
+    # RMSNorm gains: 1 + N(0, 0.1^2), bounded, and different per layer and norm
+    gains = [L["attn_norm"], L["mlp_norm"], mw.layers[1]["attn_norm"], mw.final_norm]
+    for g in gains:
+        assert g.shape == (w.d_model,) and g.dtype == torch.bfloat16
+        dev = g.float() - 1.0
+        assert 0.08 < dev.std().item() < 0.12 and dev.abs().max().item() <= 0.1 * 3.47
+    for i in range(len(gains)):
+        for j in range(i):
+            assert not torch.equal(gains[i], gains[j])
     # storage = what a pass streams + the embedding table (only T rows of it are read)
     assert mw.nbytes() == w.weight_bytes() + 2 * w.vocab * w.d_model
 

@@ -176,8 +176,10 @@ def test_zero_layers_pass_embedding_through_residual():
     out = _verify(ow, kv, tree).logits
     E = mw.embed.to(torch.float64).numpy()
     W = mw.lm_head.to(torch.float64).numpy()
+    g = mw.final_norm.to(torch.float64).numpy()
+    assert np.ptp(g) > 0          # a non-unit final gain, applied per column
     x = E[[7, 8, 9]]
-    want = x / np.sqrt(np.mean(x * x, axis=1, keepdims=True) + shape.rms_eps) @ W.T
+    want = (x / np.sqrt(np.mean(x * x, axis=1, keepdims=True) + shape.rms_eps) * g) @ W.T
     np.testing.assert_allclose(out, want, rtol=1e-12, atol=1e-12)
 
 

@@ -243,3 +243,93 @@ def test_leaf_rows_of_q_are_not_read():
     lg2[0, 17] = float("nan")
     with pytest.raises(P.GriffinError):
         P.accept_sampled_walk([c.tree for c in cases], lg2, q, ua, uf, 1.0, max_tree, D, V)
+
+
+def _sampled_draft(ow, cache, prefix_len, root, widths, V, T, rng, noise=0.5):
+    """A draft tree as a sampling drafter builds it: each expanded node's
+    children are drawn without replacement from q = the target's distribution
+    at that node (the oracle's, over the tree built so far) perturbed by
+    exp(N(0, noise^2)); the first child of each expanded node is expanded
+    next.  Returns the tree and q [n, V] (uniform rows at leaves, not read)."""
+    tokens, parents, q_rows = [root], [-1], {}
+    expand = [0]
+    for w in widths:
+        lg = oracle.verify_tree(ow, lambda l: (cache.K[l], cache.V[l]),
+                                gen.Tree(np.array(tokens, np.int32), np.array(parents, np.int32)),
+                                prefix_len).logits
+        nxt = []
+        for u in expand:
+            z = lg[u] / T + rng.normal(0.0, noise, size=V)
+            q = np.exp(z - z.max())
+            q /= q.sum()
+            q_rows[u] = q
+            kids = rng.choice(V, size=w, replace=False, p=q)
+            first = len(tokens)
+            for t in kids:
+                tokens.append(int(t))
+                parents.append(u)
+            nxt.append(first)
+        expand = nxt
+    n = len(tokens)
+    q = np.full((n, V), 1.0 / V)
+    for u, row in q_rows.items():
+        q[u] = row
+    return gen.Tree(np.array(tokens, np.int32), np.array(parents, np.int32)), q
+
+
+def test_sampled_loop_commits_the_sampled_path():
+    """Cycles of step / accept_sampled / commit at T = 1: each commit must move
+    the stochastic acceptance's path (not the greedy walk's) into the cache.
+    The oracle keeps its own causal cache of every emitted token (the cache
+    is bf16 on both sides) and verifies each new tree from it: every cycle's
+    logits must match it, and every cycle's decisions must equal the oracle's
+    where they clear their margins (else the oracle follows the device's
+    valid choice)."""
+    from tests.test_verify_gpu import Setup
+    from tests import harness as H
+    N_TOK, T = 24, 1.0
+    s = Setup("tiny", n_trees=1, kv_extra=N_TOK + 16)
+    try:
+        m = s.w.model
+        V = m.vocab
+        rng = np.random.default_rng(41)
+        cache = s.kvs[0].decode_cache(m)
+        P_len = s.w.prefix_len
+        root = int(s.cases[0][0].tree.tokens[0])
+        emitted, compared, cycles, moved = [], 0, 0, 0
+        while len(emitted) < N_TOK:
+            tree, q = _sampled_draft(s.ow, cache, P_len, root, (3, 2, 2, 2), V, T, rng)
+            ua = rng.random((1, s.max_tree)).astype(np.float32)
+            uf = rng.random((1, s.max_tree)).astype(np.float32)
+            qd = np.zeros((s.max_tree, V), np.float32)
+            qd[: tree.n] = q
+            say(f"sampled loop: cycle {cycles} prefix {P_len} nodes {tree.n}")
+            out = torch.zeros((s.max_tree, V), device="cuda")
+            s.v.step([P_len], [tree], out)
+            res = s.v.accept_sampled(out, torch.from_numpy(qd).cuda(), ua, uf, T)
+            s.v.commit()
+            ol = oracle.verify_tree(s.ow, lambda l: (cache.K[l], cache.V[l]), tree, P_len).logits
+            gl = out[: tree.n].cpu().numpy().astype(np.float64)
+            rel = (np.abs(gl - ol).max(axis=1) / (ol.max(axis=1) - ol.min(axis=1))).max()
+            assert rel < H.REGRESS_REL_TOL, f"cycle {cycles}: logits off by {rel:.2e} of the range"
+            ok, _ = _compare(tree, ol, q, ua[0, : tree.n], uf[0, : tree.n], T, res, 0,
+                             accept_margin=1e-3, draw_margin=1e-3, draw_tol=2e-3)
+            compared += ok
+            L, toks, path = res.sequence(0)
+            assert [int(tree.tokens[n]) for n in path] == toks[:L]
+            moved += L >= 2 or (L == 1 and path[0] != 1)   # a commit the greedy buffer would get wrong
+            # the oracle's cache follows: root and accepted tokens, stored as bf16
+            for k, t in enumerate([root] + toks[:L]):
+                oracle.decode_step(s.ow, cache, int(t), P_len + k)
+                for l in range(m.n_layers):
+                    cache.K[l][:, -1] = H.bf16_round(cache.K[l][:, -1])
+                    cache.V[l][:, -1] = H.bf16_round(cache.V[l][:, -1])
+            emitted += toks
+            P_len += L + 1
+            root = toks[-1]
+            cycles += 1
+        say(f"sampled loop: {cycles} cycles, {len(emitted)} tokens, decisions compared {compared}/{cycles}, "
+            f"commits of a non-trivial sampled path {moved}")
+        assert compared >= cycles - 2 and moved >= 2
+    finally:
+        s.v.close()

@@ -80,6 +80,13 @@ def test_tiny_all_trees_match_oracle(tiny):
         lg, pred, acc = tiny.run([c.tree])
         assert acc.status == 0
         st = H.check_parity(os_, lg[0, : c.tree.n], pred[0, : c.tree.n], acc.sequence(0))
+        # the device's top-2 margin: exact for its own logits, within twice their error of the oracle's
+        mg = tiny.v.margins()[0]
+        own = np.sort(lg[0, : c.tree.n].astype(np.float64), axis=1)
+        assert np.allclose(mg[: c.tree.n], own[:, -1] - own[:, -2], rtol=0, atol=1e-6)
+        err = np.abs(lg[0, : c.tree.n] - os_.logits).max(axis=1)
+        assert np.all(np.abs(mg[: c.tree.n] - os_.margin) <= 2 * err + 1e-7)
+        assert np.all(mg[c.tree.n:] == -1)
         # planted root-to-leaf greedy paths are accepted in full
         assert int(acc.length[0]) >= len(c.plant_path) or not st["accept_checked"]
         stats.append(st)
@@ -101,10 +108,17 @@ def test_small_workloads_match_oracle(name):
         for i, cases in enumerate(s.cases):
             say(f"{name} step {i} batch {len(cases)}")
             lg, pred, acc = s.run([c.tree for c in cases])
+            moe = s.w.model.n_experts > 1
+            rl = s.v.router_logits() if moe else None       # [L, B, max_tree, E]
             for b, c in enumerate(cases):
                 os_ = H.oracle_sequence(s.ow, c)
-                excl = (H.router_near_tie_nodes(os_, s.w.model.top_k, H.ROUTER_GAP)
-                        if s.w.model.n_experts > 1 else set())
+                excl = set()
+                if moe:
+                    err, gap, excl, near = H.router_check(os_, rl[:, b], s.w.model.top_k)
+                    say(f"{name} step {i} seq {b}: router logit error {err:.2e}, gap {gap:.2e}, "
+                        f"nodes with other experts on their path {len(excl)}, with a near tie {len(near)}")
+                    # at this size the gap is the 1e-4 floor and no routing is that close
+                    assert not excl and not near
                 st = H.check_parity(os_, lg[b, : c.tree.n], pred[b, : c.tree.n], acc.sequence(b), excl)
                 checked += st["accept_checked"]
                 if st["accept_checked"]:
@@ -231,7 +245,9 @@ def test_scores_past_the_attention_cap_match_oracle():
         out = torch.empty((16, m.vocab), device="cuda")
         v.step([plen], [tree], out)
         acc = v.accept()
-        st = H.check_parity(os_, out[: tree.n].cpu().numpy(), v.predictions()[0], acc.sequence(0))
+        # the merge recomputes the capped splits from the bf16 cache: a larger, bounded error
+        st = H.check_parity(os_, out[: tree.n].cpu().numpy(), v.predictions()[0], acc.sequence(0),
+                            regress_tol=5e-3)
     say(f"scores past the attention cap: max rel err {st['max_rel']:.2e}")
 
 
@@ -436,3 +452,43 @@ def test_activation_precision_switch_drops_stale_graphs(tiny):
     finally:
         tiny.v.set_bf16_activations(False)
     assert np.array_equal(logits(), ref)
+
+
+def test_nan_in_the_lm_head_is_reported(tiny):
+    """A NaN in one row of the LM head makes that vocabulary entry NaN at every
+    node: griffin_accept reports GRIFFIN_ENUMERIC and still writes its
+    outputs, which are the walk over the argmax of the remaining entries."""
+    P = _lib()
+    m = tiny.w.model
+    c = tiny.cases[0][0]
+    os_ = H.oracle_sequence(tiny.ow, c)
+    bad = int(os_.pred[0])          # the root's own argmax, so the NaN hides the winner there
+    lm = tiny.mw.lm_head.clone()
+    lm[bad, 7] = float("nan")
+    w_nan = gen.ModelWeights(m, tiny.mw.embed, lm, tiny.mw.final_norm, tiny.mw.layers).to("cuda")
+    say("tiny: NaN in one LM-head row")
+    with P.TreeVerifier(m, w_nan, max_batch=1, max_tree=tiny.max_tree, max_depth=tiny.max_depth,
+                        kv_capacity=tiny.cap) as v:
+        for l in range(m.n_layers):
+            v.write_prefix(l, 0, torch.from_numpy(c.kv.K[l]).to(torch.bfloat16).cuda(),
+                           torch.from_numpy(c.kv.V[l]).to(torch.bfloat16).cuda())
+        out = torch.empty((tiny.max_tree, m.vocab), device="cuda")
+        v.step([tiny.w.prefix_len], [c.tree], out)
+        with pytest.raises(P.GriffinError) as ei:
+            v.accept()
+        assert ei.value.name == "GRIFFIN_ENUMERIC"
+        acc = v.accept(check=False)
+        assert P.STATUS[acc.status] == "GRIFFIN_ENUMERIC"
+        lg = out[: c.tree.n].cpu().numpy()
+        pred = v.predictions()[0][: c.tree.n]
+    assert np.isnan(lg[:, bad]).all()
+    # the argmax skips the NaN entry: the oracle's argmax with that entry removed
+    ol = os_.logits.copy()
+    ol[:, bad] = -np.inf
+    srt = np.sort(ol, axis=1)
+    for i in range(c.tree.n):
+        if srt[i, -1] - srt[i, -2] > H.MARGIN_GATE:
+            assert pred[i] == int(np.argmax(ol[i])), i
+    assert pred[0] != bad
+    own = oracle.accept_dfs(c.tree, pred)
+    assert acc.sequence(0) == (own.length, own.tokens, own.path)

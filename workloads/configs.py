@@ -32,6 +32,7 @@ class ModelShape:
     rms_eps: float = 1e-5
     rope_base: float = 10000.0
     weight_std: float = 0.02    # std of every matrix and embedding entry
+    gain_std: float = 0.1       # RMSNorm gains are 1 + N(0, gain_std^2), different per layer and norm
 
     @property
     def qkv_rows(self) -> int:

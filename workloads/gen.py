@@ -90,7 +90,8 @@ def hashed_normal_bf16(numel: int, seed: int, stream: int, std: float,
 # stream ids
 _S_EMBED, _S_LMHEAD = 1, 3
 _S_LAYER_BASE, _S_LAYER_STRIDE = 1000, 16
-_S_QKV, _S_O, _S_GU, _S_DOWN, _S_ROUTER = 0, 1, 2, 3, 4
+_S_QKV, _S_O, _S_GU, _S_DOWN, _S_ROUTER, _S_ATTN_NORM, _S_MLP_NORM = 0, 1, 2, 3, 4, 5, 6
+_S_FINAL_NORM = 5
 _S_KV_BASE = 1 << 20
 
 
@@ -131,6 +132,13 @@ class ModelWeights:
         return 2 * n
 
 
+def norm_gain(d: int, seed: int, stream: int, gain_std: float, device="cpu") -> torch.Tensor:
+    """RMSNorm gain [d]: bf16(1 + N(0, gain_std^2)) from its own stream, so a
+    dropped, swapped or mis-indexed gain changes the result."""
+    v = hashed_normal_bf16(d, seed, stream, gain_std, device).float()
+    return (v + 1.0).to(torch.bfloat16)
+
+
 def make_weights(m: ModelShape, seed: int = 0, device="cpu") -> ModelWeights:
     d, f, E = m.d_model, m.d_ff, m.n_experts
     std = m.weight_std
@@ -139,12 +147,11 @@ def make_weights(m: ModelShape, seed: int = 0, device="cpu") -> ModelWeights:
         n = int(np.prod(shape))
         return hashed_normal_bf16(n, seed, stream, std, device).view(*shape)
 
-    ones = lambda: torch.ones(d, dtype=torch.bfloat16, device=device)  # noqa: E731
     layers = []
     for l in range(m.n_layers):
         L: Dict[str, Optional[torch.Tensor]] = {
-            "attn_norm": ones(),
-            "mlp_norm": ones(),
+            "attn_norm": norm_gain(d, seed, _layer_stream(l, _S_ATTN_NORM), m.gain_std, device),
+            "mlp_norm": norm_gain(d, seed, _layer_stream(l, _S_MLP_NORM), m.gain_std, device),
             "w_qkv": mat(_layer_stream(l, _S_QKV), m.qkv_rows, d),
             "w_o": mat(_layer_stream(l, _S_O), d, m.n_q_heads * m.head_dim),
         }
@@ -157,7 +164,8 @@ def make_weights(m: ModelShape, seed: int = 0, device="cpu") -> ModelWeights:
             L["w_down"] = mat(_layer_stream(l, _S_DOWN), E, d, f)
             L["w_router"] = mat(_layer_stream(l, _S_ROUTER), E, d)
         layers.append(L)
-    return ModelWeights(m, mat(_S_EMBED, m.vocab, d), mat(_S_LMHEAD, m.vocab, d), ones(), layers)
+    return ModelWeights(m, mat(_S_EMBED, m.vocab, d), mat(_S_LMHEAD, m.vocab, d),
+                        norm_gain(d, seed, _S_FINAL_NORM, m.gain_std, device), layers)
 
 
 # ------------------------------------------------------------ draft model ----
@@ -190,7 +198,8 @@ class DraftWeights:
 
 def make_draft_weights(ds, seed: int = 7, device="cpu") -> DraftWeights:
     """Random-init draft weights: matrices and biases N(0, std^2) with the
-    target's std; LayerNorm gains 1 + N(0, 0.1^2) and biases N(0, 0.1^2)."""
+    target's std; LayerNorm gains 1 + N(0, 0.1^2) and biases N(0, 0.1^2); the
+    decoder layer's RMSNorm gains 1 + N(0, gain_std^2) like the target's."""
     m, d, e = ds.target, ds.target.d_model, ds.tgf_dim
     std = m.weight_std
     shapes = {"w_m": (d, 2 * d), "b_m": (d,), "ln_h_g": (d,), "ln_h_b": (d,), "ln_x_g": (d,), "ln_x_b": (d,),
@@ -205,12 +214,12 @@ def make_draft_weights(ds, seed: int = 7, device="cpu") -> DraftWeights:
             t[name] = (v + 1.0 if name.endswith("_g") else v).to(torch.bfloat16).view(*shp)
         else:
             t[name] = hashed_normal_bf16(n, seed, _S_DRAFT_BASE + i, std, device).view(*shp)
-    ones = torch.ones(d, dtype=torch.bfloat16, device=device)
-
     def mat(which: int, *shape: int) -> torch.Tensor:
         return hashed_normal_bf16(int(np.prod(shape)), seed, _S_DRAFT_LAYER + which, std, device).view(*shape)
 
-    layer = {"attn_norm": ones, "mlp_norm": ones.clone(), "w_qkv": mat(0, m.qkv_rows, d),
+    layer = {"attn_norm": norm_gain(d, seed, _S_DRAFT_LAYER + 4, m.gain_std, device),
+             "mlp_norm": norm_gain(d, seed, _S_DRAFT_LAYER + 5, m.gain_std, device),
+             "w_qkv": mat(0, m.qkv_rows, d),
              "w_o": mat(1, d, m.n_q_heads * m.head_dim), "w_gate_up": mat(2, 2 * m.d_ff, d),
              "w_down": mat(3, d, m.d_ff), "w_router": None}
     return DraftWeights(ds, t, layer)
