@@ -289,6 +289,30 @@ int griffin_accept_sampled_walk(void *hip_stream, int32_t batch, int32_t max_tre
                                 const float *u_accept, const float *u_final, float temperature,
                                 int32_t *accept_len, int32_t *tokens_out, int32_t *path_nodes);
 
+/* griffin_accept_sampled_walk without any device allocation, for callers that
+ * cannot allocate (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments, same kernels and the
+ * same results as griffin_accept_sampled_walk.  Its device memory (the
+ * staged tree and uniforms, the kernels' scratch and the result) is a fixed
+ * 4 MiB block (4194304 bytes) that the library holds on every GPU it runs on
+ * until the process ends; a call needs
+ *   4 * (7 * batch * max_tree + batch) + sampled scratch + 4 * batch * (3 + 2 * max_depth) + 768
+ * bytes, the sampled scratch being about 1.3 MB for batch 8, max_tree 64,
+ * vocab 128256 (about 24 such sequences fit).  Calls that need more return
+ * GRIFFIN_ENOMEM before any device work.  Every call on one GPU shares that
+ * GPU's block: calls that overlap in time on the same GPU (two host threads,
+ * or two streams whose work interleaves) race and must be serialised by the
+ * caller.  The block keeps the last call's contents; the kernels read nothing
+ * they have not written in the same call.  Host-side bookkeeping uses
+ * ordinary host memory.  Synchronises hip_stream.
+ * Errors: EINVAL, ETREE, ETOKEN, ENOMEM (beyond the fixed block), EHIP,
+ * ENUMERIC (outputs still written). */
+int griffin_accept_sampled_walk_noalloc(void *hip_stream, int32_t batch, int32_t max_tree, int32_t max_depth,
+                                        int32_t vocab, const int32_t *n_nodes, const int32_t *tokens,
+                                        const int32_t *parents, const float *logits, const float *q_draft,
+                                        const float *u_accept, const float *u_final, float temperature,
+                                        int32_t *accept_len, int32_t *tokens_out, int32_t *path_nodes);
+
 /* ------------------------------------------------------------ draft model
  * A GRIFFIN-style draft model (Sec. 4.2): Token-Guided Fusion of an input
  * feature F and the token embedding e,

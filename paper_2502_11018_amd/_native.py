@@ -85,6 +85,9 @@ def _load() -> ctypes.CDLL:
         "griffin_accept_sampled": (c_int32, [c_void_p, c_void_p, c_void_p, F32P, F32P, c_float, I32P, I32P, I32P]),
         "griffin_accept_sampled_walk": (c_int32, [c_void_p, c_int32, c_int32, c_int32, c_int32, I32P, I32P, I32P,
                                                   c_void_p, c_void_p, F32P, F32P, c_float, I32P, I32P, I32P]),
+        "griffin_accept_sampled_walk_noalloc": (c_int32, [c_void_p, c_int32, c_int32, c_int32, c_int32, I32P, I32P,
+                                                          I32P, c_void_p, c_void_p, F32P, F32P, c_float, I32P, I32P,
+                                                          I32P]),
         "griffin_draft_init": (c_int32, [POINTER(ModelDesc), c_int32, c_float, POINTER(DraftWeights), c_void_p,
                                          c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, POINTER(c_void_p)]),
         "griffin_draft_free": (None, [c_void_p]),
@@ -108,6 +111,7 @@ EXPORTED = ("griffin_kv_cache_bytes", "griffin_verify_init", "griffin_verify_ste
             "griffin_set_graphs", "griffin_commit", "griffin_accept_sampled", "griffin_accept_sampled_walk",
             "griffin_draft_init", "griffin_draft_free", "griffin_draft_context", "griffin_draft_step",
             "griffin_draft_tree", "griffin_read_features", "griffin_draft_extend",
-            "griffin_set_activation_precision", "griffin_read_router_logits", "griffin_read_margins")
+            "griffin_set_activation_precision", "griffin_read_router_logits", "griffin_read_margins",
+            "griffin_accept_sampled_walk_noalloc")
 KERNEL_CLASSES = ("qkv_gemm", "rope_kv_write", "tree_attention", "o_gemm", "residual_rmsnorm", "gate_up_gemm",
                   "down_gemm", "lm_head_gemm", "argmax_accept_route", "attn_merge")

@@ -1181,20 +1181,28 @@ done:
   return rc;
 }
 
-int griffin_accept_sampled_walk(void* hip_stream, int32_t batch, int32_t max_tree, int32_t max_depth, int32_t vocab,
-                                const int32_t* n_nodes, const int32_t* tokens, const int32_t* parents,
-                                const float* logits, const float* q_draft, const float* u_accept,
-                                const float* u_final, float temperature, int32_t* accept_len, int32_t* tokens_out,
-                                int32_t* path_nodes) {
+// The stochastic walk for trees given directly.  Its device memory (staged
+// inputs, kernel scratch, result) is one block: hipMalloc'ed for this call
+// when `fixed` is null, else the caller's fixed block of `fixed_bytes`.
+static int sampled_walk(void* hip_stream, int32_t batch, int32_t max_tree, int32_t max_depth, int32_t vocab,
+                        const int32_t* n_nodes, const int32_t* tokens, const int32_t* parents, const float* logits,
+                        const float* q_draft, const float* u_accept, const float* u_final, float temperature,
+                        int32_t* accept_len, int32_t* tokens_out, int32_t* path_nodes, char* fixed,
+                        size_t fixed_bytes) {
   if (batch < 1 || max_tree < 1 || max_tree > kMaxTree || max_depth < 0 || max_depth >= max_tree || vocab < 1 ||
       !n_nodes || !tokens || !parents || !logits || !q_draft || !u_accept || !u_final)
     return GRIFFIN_EINVAL;
   if (!(temperature > 0.f) || !std::isfinite(temperature)) return GRIFFIN_EINVAL;
   const int rows = batch * max_tree;
-  std::vector<uint64_t> anc(rows, 0);
-  std::vector<int32_t> dep(rows, 0), pos(rows, 0);
+  const int st = result_stride(max_depth);
   // staging, one copy: tokens [rows], parents [rows], n_nodes [batch], u_accept [rows],
   // u_final [rows] (float bits), work order, step children, step tokens [<= rows each]
+  const size_t n_stage = sizeof(int32_t) * (7 * (size_t)rows + batch);
+  const size_t n_scratch = sampled_scratch_bytes(batch, max_tree, vocab);
+  const size_t total = n_stage + n_scratch + sizeof(int32_t) * batch * st + 3 * 256;
+  if (fixed && total > fixed_bytes) return GRIFFIN_ENOMEM;  // before any device work
+  std::vector<uint64_t> anc(rows, 0);
+  std::vector<int32_t> dep(rows, 0), pos(rows, 0);
   std::vector<int32_t> stage(7 * (size_t)rows + batch, 0);
   int32_t* tok = stage.data();
   int32_t* par = tok + rows;
@@ -1225,12 +1233,8 @@ int griffin_accept_sampled_walk(void* hip_stream, int32_t batch, int32_t max_tre
   std::copy(step_child.begin(), step_child.end(), plan + rows);
   std::copy(step_token.begin(), step_token.end(), plan + 2 * rows);
   hipStream_t s = static_cast<hipStream_t>(hip_stream);
-  const int st = result_stride(max_depth);
-  const size_t n_stage = sizeof(int32_t) * stage.size();
-  const size_t n_scratch = sampled_scratch_bytes(batch, max_tree, vocab);
-  const size_t total = n_stage + n_scratch + sizeof(int32_t) * batch * st + 3 * 256;
-  char* dev = nullptr;
-  if (hipMalloc((void**)&dev, total) != hipSuccess) return GRIFFIN_ENOMEM;
+  char* dev = fixed;
+  if (!dev && hipMalloc((void**)&dev, total) != hipSuccess) return GRIFFIN_ENOMEM;
   char* p = dev;
   auto carve = [&](size_t bytes) {
     char* q = p;
@@ -1284,8 +1288,30 @@ int griffin_accept_sampled_walk(void* hip_stream, int32_t batch, int32_t max_tre
   }
 done:
   hipStreamSynchronize(s);
-  hipFree(dev);
+  if (!fixed) hipFree(dev);
   return rc;
+}
+
+int griffin_accept_sampled_walk(void* hip_stream, int32_t batch, int32_t max_tree, int32_t max_depth, int32_t vocab,
+                                const int32_t* n_nodes, const int32_t* tokens, const int32_t* parents,
+                                const float* logits, const float* q_draft, const float* u_accept,
+                                const float* u_final, float temperature, int32_t* accept_len, int32_t* tokens_out,
+                                int32_t* path_nodes) {
+  return sampled_walk(hip_stream, batch, max_tree, max_depth, vocab, n_nodes, tokens, parents, logits, q_draft,
+                      u_accept, u_final, temperature, accept_len, tokens_out, path_nodes, nullptr, 0);
+}
+
+int griffin_accept_sampled_walk_noalloc(void* hip_stream, int32_t batch, int32_t max_tree, int32_t max_depth,
+                                        int32_t vocab, const int32_t* n_nodes, const int32_t* tokens,
+                                        const int32_t* parents, const float* logits, const float* q_draft,
+                                        const float* u_accept, const float* u_final, float temperature,
+                                        int32_t* accept_len, int32_t* tokens_out, int32_t* path_nodes) {
+  void* block = nullptr;
+  size_t bytes = 0;
+  if (static_scratch(&block, &bytes) != hipSuccess) return GRIFFIN_EHIP;
+  return sampled_walk(hip_stream, batch, max_tree, max_depth, vocab, n_nodes, tokens, parents, logits, q_draft,
+                      u_accept, u_final, temperature, accept_len, tokens_out, path_nodes, static_cast<char*>(block),
+                      bytes);
 }
 
 

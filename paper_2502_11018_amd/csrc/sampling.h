@@ -32,4 +32,10 @@ size_t sampled_scratch_bytes(int batch, int max_tree, int vocab);
 // rows_with[0] = all nodes).
 hipError_t launch_sampled_accept(const SampledArgs& a, const int* rows_with, int max_children, hipStream_t s);
 
+// The current device's copy of the library's fixed scratch block (a
+// file-scope device array of kStaticScratchBytes, looked up once per device):
+// *ptr is its device address, *bytes its size.
+constexpr size_t kStaticScratchBytes = 4u << 20;
+hipError_t static_scratch(void** ptr, size_t* bytes);
+
 }  // namespace griffin

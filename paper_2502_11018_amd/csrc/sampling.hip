@@ -41,6 +41,7 @@
 // Kernel boundaries order every hand-over; no counters, fences or atomics.
 
 #include <algorithm>
+#include <mutex>
 
 #include "device_common.h"
 #include "griffin_internal.h"
@@ -526,6 +527,32 @@ hipError_t launch_sampled_accept(const SampledArgs& a, const int* rows_with, int
   else
     launch_all<false>(a, rows_with, max_children, ns, s);
   return hipGetLastError();
+}
+
+// Fixed scratch of the allocation-free walk.  Host code never uses the
+// array's name as an address (on the host it names a stand-in, not device
+// memory): the device address comes from hipGetSymbolAddress, once per device
+// with that device current, and is kept per device.
+static __device__ __align__(256) char scratch[kStaticScratchBytes];
+
+hipError_t static_scratch(void** ptr, size_t* bytes) {
+  constexpr int kMaxDevices = 64;
+  static void* addr[kMaxDevices] = {};
+  static std::mutex mu;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  *bytes = kStaticScratchBytes;
+  return hipSuccess;
 }
 
 }  // namespace griffin

@@ -103,10 +103,11 @@ def _device_rows(t: torch.Tensor, rows: int, vocab: int, what: str):
 
 def accept_sampled_walk(trees: Sequence, logits: torch.Tensor, q_draft: torch.Tensor, u_accept, u_final,
                         temperature: float, max_tree: int, max_depth: int, vocab: int,
-                        stream: Optional[torch.cuda.Stream] = None) -> AcceptResult:
+                        stream: Optional[torch.cuda.Stream] = None, noalloc: bool = False) -> AcceptResult:
     """Device stochastic acceptance (temperature > 0) on given logits and
     draft distributions, both fp32 [B*max_tree, vocab] CUDA tensors; the
-    uniforms are [B, max_tree] arrays in [0, 1)."""
+    uniforms are [B, max_tree] arrays in [0, 1).  noalloc: the entry point
+    that uses the library's fixed device block instead of allocating."""
     n, tok, par = pack_trees(trees, max_tree)
     B = len(trees)
     ua, uf = _f32(u_accept).reshape(B, max_tree), _f32(u_final).reshape(B, max_tree)
@@ -114,11 +115,12 @@ def accept_sampled_walk(trees: Sequence, logits: torch.Tensor, q_draft: torch.Te
     out = np.zeros((B, max_depth + 1), dtype=np.int32)
     path = np.zeros((B, max(max_depth, 1)), dtype=np.int32)
     s = (stream or torch.cuda.current_stream()).cuda_stream
-    rc = N.lib.griffin_accept_sampled_walk(
+    name = "griffin_accept_sampled_walk_noalloc" if noalloc else "griffin_accept_sampled_walk"
+    rc = getattr(N.lib, name)(
         c_void_p(s), B, max_tree, max_depth, vocab, _p32(n), _p32(tok), _p32(par),
         _device_rows(logits, B * max_tree, vocab, "logits"), _device_rows(q_draft, B * max_tree, vocab, "q_draft"),
         _pf32(ua), _pf32(uf), float(temperature), _p32(L), _p32(out), _p32(path))
-    _check(rc, "griffin_accept_sampled_walk")
+    _check(rc, name)
     return AcceptResult(L, out, path[:, :max_depth])
 
 
