@@ -256,8 +256,10 @@ def main():
     root_ms = (time.perf_counter() - t0) * 1e3 / n_root
     log(f"root-only (plain decoding) {root_ms:.3f} ms/step")
 
-    # per kernel class timing (separate pass: HIP events recorded on the
-    # library's stream around every launch of the class)
+    # per kernel class timing (separate pass with plain launches): the GEMM
+    # classes time themselves on the device wall clock (earliest workgroup
+    # start to latest wave end of each launch); the other classes by HIP
+    # events recorded on the library's stream around every launch
     kernels, roofline = {}, None
     if not args.no_profile:
         v.profile_enable()
@@ -290,7 +292,9 @@ def main():
                     "traffic": None if traffic is None else int(round(traffic)),
                     "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-scaled)",
                     "bytes_per_launch": kernels[dom]["bytes_per_launch"],
-                    "avg_launch_us": kernels[dom]["avg_launch_us"]}
+                    "avg_launch_us": kernels[dom]["avg_launch_us"],
+                    "timing": "the kernel's own device wall-clock stamps (earliest workgroup start to latest "
+                              "wave end) over every launch of the profiled steps"}
 
     # temperature-1 cycle: the same steps also writing the logits, then the
     # stochastic acceptance with seeded draft distributions and uniforms

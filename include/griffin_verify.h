@@ -413,9 +413,15 @@ int griffin_draft_tree(griffin_draft *draft, int32_t batch, const int32_t *prefi
 #define GRIFFIN_KC_MERGE 9   /* split merge + ancestor (tree-key) attention */
 #define GRIFFIN_KC_COUNT 10
 
-/* Per-class timing with HIP events recorded on the context's stream around
- * every launch of the classes in `class_mask` (bit k = class k); 0 disables.
- * Timing adds two event records per launch, so time the pass without it. */
+/* Per-class timing of the launches of the classes in `class_mask` (bit k =
+ * class k); 0 disables.  The GEMM classes (QKV, O, gate/up, down, LM head)
+ * time themselves: each launch records, on the device wall clock, the start
+ * of its earliest workgroup and the end of its latest wave (after its stores
+ * complete), so the dispatch gap before the kernel is not counted (up to
+ * 16384 launches between reads).  The other classes are timed with HIP
+ * events recorded on the context's stream around every launch, which include
+ * that gap.  Timing disables graph replay and adds work per launch, so time
+ * the pass itself without it.  Errors: EINVAL, ENOMEM, EHIP. */
 int griffin_profile_enable(griffin_ctx *ctx, uint32_t class_mask);
 
 /* Wait for the stream, then return per class the summed launch durations in

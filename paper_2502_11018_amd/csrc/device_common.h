@@ -108,4 +108,18 @@ __device__ __forceinline__ void top2_merge(float& best, int& bidx, float& second
   }
 }
 
+// Launch timing by the kernel itself: the earliest workgroup start (stored
+// complemented, so that one zero fill initialises both words and a max
+// atomic takes the minimum) and the latest wave end, on the device wall
+// clock.  A null pointer (the untimed case) skips both.
+__device__ __forceinline__ void stamp_begin(unsigned long long* st) {
+  if (st && threadIdx.x == 0) atomicMax(st, ~(unsigned long long)__builtin_amdgcn_s_memrealtime());
+}
+__device__ __forceinline__ void stamp_end(unsigned long long* st) {
+  if (st) {
+    __builtin_amdgcn_s_waitcnt(0);  // this wave's stores have completed
+    if ((threadIdx.x & 63) == 0) atomicMax(st + 1, (unsigned long long)__builtin_amdgcn_s_memrealtime());
+  }
+}
+
 }  // namespace griffin

@@ -42,11 +42,132 @@ __device__ __forceinline__ void add4(float4& a, const float4& p) {
   a.x += p.x; a.y += p.y; a.z += p.z; a.w += p.w;
 }
 
+// The router epilogue of the norm kernel (Router): this thread's GPT groups
+// of 4 normed values h, 8 experts per reduction round.
+constexpr int ROUTE_EC = 8;  // experts per reduction round of the router epilogue
+
+// Router weights of this thread's elements for experts e0 .. e0 + 7 (zero
+// past n_experts), loaded early so that their latency overlaps the norm.
+template <int GPT>
+__device__ __forceinline__ void route_load(const Router& rt, int e0, int d, const int (&gi)[GPT],
+                                           uint2 (&ww)[ROUTE_EC][GPT]) {
+#pragma unroll
+  for (int q = 0; q < ROUTE_EC; ++q)
+#pragma unroll
+    for (int u = 0; u < GPT; ++u)
+      ww[q][u] = e0 + q < rt.n_experts ? *reinterpret_cast<const uint2*>(rt.w + (long long)(e0 + q) * d + 4 * gi[u])
+                                       : make_uint2(0u, 0u);
+}
+
+// Sum 8 values over the 64 lanes of a wave with 10 shuffles: each exchange
+// halves the values a lane carries; lane l ends with the sum of value
+// (l >> 3) & 7 (as the 3 bits of lane l's positions 32, 16, 8 select it).
+__device__ __forceinline__ float wave_sum8(const float (&v)[8]) {
+  const int lane = threadIdx.x & 63;
+  float a4[4];
+  const bool h32 = lane & 32;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float send = h32 ? v[i] : v[i + 4], keep = h32 ? v[i + 4] : v[i];
+    a4[i] = keep + __shfl_xor(send, 32, 64);
+  }
+  float a2[2];
+  const bool h16 = lane & 16;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const float send = h16 ? a4[i] : a4[i + 2], keep = h16 ? a4[i + 2] : a4[i];
+    a2[i] = keep + __shfl_xor(send, 16, 64);
+  }
+  const bool h8 = lane & 8;
+  float a1 = (h8 ? a2[1] : a2[0]) + __shfl_xor(h8 ? a2[0] : a2[1], 8, 64);
+  a1 += __shfl_xor(a1, 4, 64);
+  a1 += __shfl_xor(a1, 2, 64);
+  a1 += __shfl_xor(a1, 1, 64);
+  return a1;  // lane l: value index 4 * [l & 32] + 2 * [l & 16] + [l & 8]
+}
+
+template <int GPT>
+__device__ __forceinline__ void route_row(const Router& rt, int r, const float4 (&h)[GPT], const int (&gi)[GPT],
+                                          const bool (&ok)[GPT], int d, const uint2 (&w0)[ROUTE_EC][GPT]) {
+  constexpr int EC = ROUTE_EC;
+  __shared__ float part[RN_THREADS / 64][EC];
+  __shared__ float logit[64];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int b = r / rt.max_tree, i = r % rt.max_tree;
+  if (r >= rt.rows) return;  // padding row (uniform)
+  if (i >= rt.n_nodes[b]) {  // absent node (uniform)
+    if (tid < rt.top_k) {
+      rt.ids[r * rt.top_k + tid] = -1;
+      rt.weights[r * rt.top_k + tid] = 0.f;
+    }
+    return;
+  }
+  for (int e0 = 0; e0 < rt.n_experts; e0 += EC) {
+    uint2 wl[EC][GPT];
+    if (e0 == 0) {
+#pragma unroll
+      for (int q = 0; q < EC; ++q)
+#pragma unroll
+        for (int u = 0; u < GPT; ++u) wl[q][u] = w0[q][u];
+    } else {
+      route_load<GPT>(rt, e0, d, gi, wl);
+    }
+    float acc[EC];
+#pragma unroll
+    for (int q = 0; q < EC; ++q) {
+      acc[q] = 0.f;
+#pragma unroll
+      for (int u = 0; u < GPT; ++u)
+        if (ok[u]) {
+          const uint2 ww = wl[q][u];
+          acc[q] += h[u].x * bf16_to_f32(ww.x & 0xffff) + h[u].y * bf16_to_f32(ww.x >> 16) +
+                    h[u].z * bf16_to_f32(ww.y & 0xffff) + h[u].w * bf16_to_f32(ww.y >> 16);
+        }
+    }
+    const float wsum = wave_sum8(acc);
+    __syncthreads();
+    if ((lane & 7) == 0) part[w][((lane >> 5) & 1) * 4 + ((lane >> 4) & 1) * 2 + ((lane >> 3) & 1)] = wsum;
+    __syncthreads();
+    if (tid < EC && e0 + tid < rt.n_experts) {
+      float t = 0.f;
+      for (int k = 0; k < RN_THREADS / 64; ++k) t += part[k][tid];  // fixed order
+      logit[e0 + tid] = t;
+    }
+  }
+  __syncthreads();
+  if (tid < rt.n_experts) rt.logits[(long long)r * rt.n_experts + tid] = logit[tid];
+  __syncthreads();
+  if (tid == 0) {
+    float mx = -INFINITY;
+    for (int e = 0; e < rt.n_experts; ++e) mx = fmaxf(mx, logit[e]);
+    float* p = logit;  // probabilities (unnormalised) in place
+    for (int e = 0; e < rt.n_experts; ++e) p[e] = __expf(logit[e] - mx);
+    int chosen[4];
+    float ps[4], tot = 0.f;
+    for (int k = 0; k < rt.top_k; ++k) {
+      int best = -1;
+      for (int e = 0; e < rt.n_experts; ++e) {
+        bool used = false;
+        for (int q = 0; q < k; ++q) used |= chosen[q] == e;
+        if (!used && (best < 0 || p[e] > p[best])) best = e;
+      }
+      chosen[k] = best;
+      ps[k] = p[best];
+      tot += p[best];
+    }
+    for (int k = 0; k < rt.top_k; ++k) {
+      rt.ids[r * rt.top_k + k] = chosen[k];
+      rt.weights[r * rt.top_k + k] = ps[k] / tot;
+    }
+  }
+}
+
 template <int NP, int GPT>
 __global__ __launch_bounds__(RN_THREADS) void residual_rmsnorm_kernel(float* __restrict__ x, ResidualAdd add,
                                                                       const uint16_t* __restrict__ gain,
                                                                       float eps, int d,
-                                                                      uint16_t* __restrict__ xn, int xn_ks) {
+                                                                      uint16_t* __restrict__ xn, int xn_ks,
+                                                                      Router rt) {
   __shared__ float red[16];
   const int r = blockIdx.x;
   float* __restrict__ xr = x + (long long)r * d;
@@ -62,6 +183,8 @@ __global__ __launch_bounds__(RN_THREADS) void residual_rmsnorm_kernel(float* __r
     gi[u] = ok[u] ? g : groups - 1;  // clamped: loads stay unconditional
     v[u] = reinterpret_cast<const float4*>(xr)[gi[u]];
   }
+  uint2 w0[ROUTE_EC][GPT];  // MoE: the first router weights, in flight during the norm
+  if (rt.w) route_load<GPT>(rt, 0, d, gi, w0);
   if constexpr (NP > 0) {
     // dense: K-split partial sums, all loaded first, added in split order
     float4 p[NP][GPT];
@@ -117,29 +240,40 @@ __global__ __launch_bounds__(RN_THREADS) void residual_rmsnorm_kernel(float* __r
       *reinterpret_cast<uint2*>(dst + XPACK_LO) = make_uint2(p0.lo, p1.lo);
     }
   }
+  if (rt.w) {  // MoE: route the row from its normed fp32 values (uniform branch)
+    float4 h[GPT];
+#pragma unroll
+    for (int u = 0; u < GPT; ++u) {
+      const uint2 gg = *reinterpret_cast<const uint2*>(gain + 4 * gi[u]);
+      h[u] = make_float4(v[u].x * rs * bf16_to_f32(gg.x & 0xffff), v[u].y * rs * bf16_to_f32(gg.x >> 16),
+                         v[u].z * rs * bf16_to_f32(gg.y & 0xffff), v[u].w * rs * bf16_to_f32(gg.y >> 16));
+    }
+    route_row<GPT>(rt, r, h, gi, ok, d, w0);
+  }
 }
 
 template <int NP>
 static hipError_t launch_rn(float* x, const ResidualAdd& add, const uint16_t* gain, float eps, int rows, int d,
-                            uint16_t* xn, int xn_ks, hipStream_t s) {
+                            uint16_t* xn, int xn_ks, hipStream_t s, const Router& rt) {
   const int groups = d / 4;
   if (groups <= RN_THREADS)
     hipLaunchKernelGGL((residual_rmsnorm_kernel<NP, 1>), dim3(rows), dim3(RN_THREADS), 0, s, x, add, gain, eps, d,
-                       xn, xn_ks);
+                       xn, xn_ks, rt);
   else
     hipLaunchKernelGGL((residual_rmsnorm_kernel<NP, 2>), dim3(rows), dim3(RN_THREADS), 0, s, x, add, gain, eps, d,
-                       xn, xn_ks);
+                       xn, xn_ks, rt);
   return hipGetLastError();
 }
 
 hipError_t launch_residual_rmsnorm(float* x, const ResidualAdd& add, const uint16_t* gain, float eps, int rows,
-                                   int d, uint16_t* xn, int xn_ks, hipStream_t s) {
+                                   int d, uint16_t* xn, int xn_ks, hipStream_t s, const Router& rt) {
   if (d % 4 != 0 || d > 8 * RN_THREADS || add.n_parts > RN_SPLITS) return hipErrorInvalidValue;
-  if (add.parts == nullptr) return launch_rn<0>(x, add, gain, eps, rows, d, xn, xn_ks, s);
-  if (add.slot != nullptr) return launch_rn<-1>(x, add, gain, eps, rows, d, xn, xn_ks, s);
+  if (rt.w && (rt.n_experts < 1 || rt.n_experts > 64 || rt.top_k < 1 || rt.top_k > 4)) return hipErrorInvalidValue;
+  if (add.parts == nullptr) return launch_rn<0>(x, add, gain, eps, rows, d, xn, xn_ks, s, rt);
+  if (add.slot != nullptr) return launch_rn<-1>(x, add, gain, eps, rows, d, xn, xn_ks, s, rt);
   switch (add.n_parts) {
 #define GRIFFIN_RN_CASE(n) \
-  case n: return launch_rn<n>(x, add, gain, eps, rows, d, xn, xn_ks, s);
+  case n: return launch_rn<n>(x, add, gain, eps, rows, d, xn, xn_ks, s, rt);
     GRIFFIN_RN_CASE(1) GRIFFIN_RN_CASE(2) GRIFFIN_RN_CASE(3) GRIFFIN_RN_CASE(4) GRIFFIN_RN_CASE(5)
     GRIFFIN_RN_CASE(6) GRIFFIN_RN_CASE(7) GRIFFIN_RN_CASE(8) GRIFFIN_RN_CASE(9) GRIFFIN_RN_CASE(10)
     GRIFFIN_RN_CASE(11) GRIFFIN_RN_CASE(12) GRIFFIN_RN_CASE(13) GRIFFIN_RN_CASE(14) GRIFFIN_RN_CASE(15)
@@ -147,31 +281,6 @@ hipError_t launch_residual_rmsnorm(float* x, const ResidualAdd& add, const uint1
 #undef GRIFFIN_RN_CASE
     default: return hipErrorInvalidValue;
   }
-}
-
-// ----------------------------------------------------- MoE input gather ----
-// Copy the rows routed to each expert into that expert's activation tiles
-// (both fragment-packed with ks steps): expert e, row c <- xn row gather[e][c].
-__global__ __launch_bounds__(256) void moe_gather_kernel(const uint16_t* __restrict__ xn, int ks,
-                                                         const int32_t* __restrict__ gather,
-                                                         const int32_t* __restrict__ count, int cap, int d,
-                                                         uint16_t* __restrict__ xe, int xe_tiles) {
-  const int e = blockIdx.y, c = blockIdx.x;
-  if (c >= count[e]) return;
-  const int src = gather[e * cap + c];
-  const long long dst_row = (long long)e * xe_tiles * 64 + c;
-  for (int k = threadIdx.x * 8; k < d; k += blockDim.x * 8) {
-    const long long o = xpack_off(dst_row, k, ks), i = xpack_off(src, k, ks);
-    *reinterpret_cast<u32x4*>(xe + o) = *reinterpret_cast<const u32x4*>(xn + i);
-    *reinterpret_cast<u32x4*>(xe + o + XPACK_LO) = *reinterpret_cast<const u32x4*>(xn + i + XPACK_LO);
-  }
-}
-
-hipError_t launch_moe_gather(const uint16_t* xn, int xn_ks, const int32_t* gather, const int32_t* count,
-                             int n_experts, int cap, int d, uint16_t* xe, int xe_tiles, hipStream_t s) {
-  hipLaunchKernelGGL(moe_gather_kernel, dim3(cap, n_experts), dim3(256), 0, s, xn, xn_ks, gather, count, cap, d,
-                     xe, xe_tiles);
-  return hipGetLastError();
 }
 
 // ------------------------------------------------ rotary + tree K/V write ----
@@ -469,101 +578,72 @@ hipError_t launch_gather_rows(const float* x, int d, const int32_t* rows, int n,
 // For a valid row: h = RMSNorm(x) (fp32, from the fp32 residual), router
 // logits h . w_e in fp32, softmax, keep the top_k experts (ties to the lower
 // id), renormalise their probabilities.  Absent rows get expert id -1.
-__global__ __launch_bounds__(256) void moe_route_kernel(const float* __restrict__ x,
-                                                        const uint16_t* __restrict__ gain, float eps,
-                                                        const uint16_t* __restrict__ wr, int d, int n_experts,
-                                                        int top_k, const int32_t* n_nodes, int max_tree,
-                                                        int32_t* route_ids, float* route_w,
-                                                        float* __restrict__ logits_out) {
-  __shared__ float red[16];
-  __shared__ float logit[64];
-  const int r = blockIdx.x;
-  const int b = r / max_tree, i = r % max_tree;
-  if (i >= n_nodes[b]) {
-    if (threadIdx.x < top_k) {
-      route_ids[r * top_k + threadIdx.x] = -1;
-      route_w[r * top_k + threadIdx.x] = 0.f;
+// Per-expert row lists and the gather of the routed rows, in one launch.  The
+// c-th row routed to expert e (rows in ascending order: deterministic) is
+// found by every workgroup (e, c) itself from wave ballots over the route
+// ids, and its packed split-bf16 activations are copied to row c of expert
+// e's tiles.  Workgroup (e, 0) also writes count[e] and, for every (row, k)
+// routed to e, slot[row][k] = e * cap + the row's place in the list; expert
+// 0's writes slot = -1 for absent entries and for the padding rows.
+__global__ __launch_bounds__(256) void moe_dispatch_kernel(const int32_t* __restrict__ route_ids, int rows,
+                                                           int padded_rows, int top_k, int cap,
+                                                           const uint16_t* __restrict__ xn, int ks, int d,
+                                                           uint16_t* __restrict__ xe, int xe_tiles, int32_t* count,
+                                                           int32_t* slot) {
+  __shared__ int src_row;
+  const int e = blockIdx.y, c = blockIdx.x, tid = threadIdx.x;
+  if (tid < 64) {
+    const int lane = tid;
+    int base = 0, found = -1;
+    for (int q0 = 0; q0 < padded_rows; q0 += 64) {
+      const int r = q0 + lane;
+      int hit_k = -1;
+      bool absent = false;
+      if (r < rows) {
+        for (int k = 0; k < top_k; ++k) {
+          const int id = route_ids[r * top_k + k];
+          if (id == e) hit_k = k;
+          if (id < 0) absent = true;
+        }
+      }
+      const uint64_t m = __ballot(hit_k >= 0);
+      const int n = __popcll(m);
+      if (c == 0) {
+        const int pos = base + __popcll(m & ((1ull << lane) - 1ull));
+        if (hit_k >= 0) slot[r * top_k + hit_k] = e * cap + pos;
+        if (e == 0 && r < padded_rows && (r >= rows || absent))
+          for (int k = 0; k < top_k; ++k) slot[r * top_k + k] = -1;
+      }
+      if (found < 0 && c >= base && c < base + n) {
+        // the (c - base)-th set bit of m
+        uint64_t mm = m;
+        for (int j = 0; j < c - base; ++j) mm &= mm - 1ull;
+        found = q0 + __ffsll((unsigned long long)mm) - 1;
+      }
+      base += n;
     }
-    return;
-  }
-  const float* xr = x + (long long)r * d;
-  float ss = 0.f;
-  for (int j = threadIdx.x; j < d; j += blockDim.x) ss += xr[j] * xr[j];
-  const float rs = rsqrtf(block_sum(ss, red) / (float)d + eps);
-  for (int e = 0; e < n_experts; ++e) {
-    const uint16_t* w = wr + (long long)e * d;
-    float acc = 0.f;
-    for (int j = threadIdx.x; j < d; j += blockDim.x) acc += xr[j] * rs * bf16_to_f32(gain[j]) * bf16_to_f32(w[j]);
-    const float t = block_sum(acc, red);
-    if (threadIdx.x == 0) logit[e] = t;
+    if (lane == 0) {
+      src_row = found;
+      if (c == 0) count[e] = base;
+    }
   }
   __syncthreads();
-  if (threadIdx.x < n_experts) logits_out[(long long)r * n_experts + threadIdx.x] = logit[threadIdx.x];
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    float mx = -INFINITY;
-    for (int e = 0; e < n_experts; ++e) mx = fmaxf(mx, logit[e]);
-    float* p = logit;  // probabilities (unnormalised) in place
-    for (int e = 0; e < n_experts; ++e) p[e] = __expf(logit[e] - mx);
-    int chosen[4];
-    float ps[4], tot = 0.f;
-    for (int k = 0; k < top_k; ++k) {
-      int best = -1;
-      for (int e = 0; e < n_experts; ++e) {
-        bool used = false;
-        for (int q = 0; q < k; ++q) used |= chosen[q] == e;
-        if (!used && (best < 0 || p[e] > p[best])) best = e;
-      }
-      chosen[k] = best;
-      ps[k] = p[best];
-      tot += p[best];
-    }
-    for (int k = 0; k < top_k; ++k) {
-      route_ids[r * top_k + k] = chosen[k];
-      route_w[r * top_k + k] = ps[k] / tot;
-    }
+  const int src = src_row;
+  if (src < 0) return;  // fewer than c + 1 rows routed to e (uniform)
+  const long long dst_row = (long long)e * xe_tiles * 64 + c;
+  for (int k = tid * 8; k < d; k += blockDim.x * 8) {
+    const long long o = xpack_off(dst_row, k, ks), i = xpack_off(src, k, ks);
+    *reinterpret_cast<u32x4*>(xe + o) = *reinterpret_cast<const u32x4*>(xn + i);
+    *reinterpret_cast<u32x4*>(xe + o + XPACK_LO) = *reinterpret_cast<const u32x4*>(xn + i + XPACK_LO);
   }
 }
 
-hipError_t launch_moe_route(const float* x, const uint16_t* gain, float eps, const uint16_t* w_router, int rows,
-                            int d, int n_experts, int top_k, const int32_t* n_nodes, int max_tree,
-                            int32_t* route_ids, float* route_w, float* logits_out, hipStream_t s) {
-  if (n_experts > 64 || top_k > 4) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(moe_route_kernel, dim3(rows), dim3(256), 0, s, x, gain, eps, w_router, d, n_experts, top_k,
-                     n_nodes, max_tree, route_ids, route_w, logits_out);
-  return hipGetLastError();
-}
-
-// Per-expert row lists in ascending row order (deterministic): gather[e][c]
-// is the c-th row routed to expert e, slot[r][k] = e * cap + c for the k-th
-// kept expert of row r (-1 for absent rows, including padding rows).
-__global__ __launch_bounds__(64) void moe_lists_kernel(const int32_t* __restrict__ route_ids, int rows,
-                                                       int padded_rows, int n_experts, int top_k, int cap,
-                                                       int32_t* gather, int32_t* count, int32_t* slot) {
-  const int e = threadIdx.x;
-  for (int r = e; r < padded_rows; r += blockDim.x)
-    if (r >= rows)
-      for (int k = 0; k < top_k; ++k) slot[r * top_k + k] = -1;
-  if (e >= n_experts) return;
-  int c = 0;
-  for (int r = 0; r < rows; ++r)
-    for (int k = 0; k < top_k; ++k) {
-      const int id = route_ids[r * top_k + k];
-      if (id < 0) {
-        if (e == 0) slot[r * top_k + k] = -1;
-      } else if (id == e) {
-        gather[e * cap + c] = r;
-        slot[r * top_k + k] = e * cap + c;
-        ++c;
-      }
-    }
-  count[e] = c;
-}
-
-hipError_t launch_moe_lists(const int32_t* route_ids, int rows, int padded_rows, int n_experts, int top_k,
-                            int cap, int32_t* gather, int32_t* count, int32_t* slot, hipStream_t s) {
-  hipLaunchKernelGGL(moe_lists_kernel, dim3(1), dim3(64), 0, s, route_ids, rows, padded_rows, n_experts, top_k,
-                     cap, gather, count, slot);
+hipError_t launch_moe_dispatch(const int32_t* route_ids, int rows, int padded_rows, int n_experts, int top_k,
+                               int cap, const uint16_t* xn, int xn_ks, int d, uint16_t* xe, int xe_tiles,
+                               int32_t* count, int32_t* slot, hipStream_t s) {
+  if (padded_rows > cap) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(moe_dispatch_kernel, dim3(cap, n_experts), dim3(256), 0, s, route_ids, rows, padded_rows,
+                     top_k, cap, xn, xn_ks, d, xe, xe_tiles, count, slot);
   return hipGetLastError();
 }
 

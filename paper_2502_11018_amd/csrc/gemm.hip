@@ -34,6 +34,122 @@
 
 namespace griffin {
 
+// Merge the KS K slices of a workgroup in slice order through LDS (red: at
+// least WN * NB * 8 KB, free: every wave's reads of it have returned).  Every
+// wave of the workgroup calls it (its barriers are uniform); waves whose kh
+// is not a slice index only take part in the barriers.  Slice 0 ends with the
+// sum.
+template <int NB, int WN, int KS>
+__device__ __forceinline__ void ks_merge(f32x16 (&acc)[NB][2], float* red, int kh, int wc, int lane) {
+  wait_vmcnt_lds<0>();
+  __builtin_amdgcn_s_barrier();
+  for (int k = 1; k < KS; ++k) {
+    if (kh == k) {
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) red[(((wc * NB + b) * 2 + mb) * 16 + i) * 64 + lane] = acc[b][mb][i];
+    }
+    wait_vmcnt_lds<0>();
+    __builtin_amdgcn_s_barrier();
+    if (kh == 0) {
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) acc[b][mb][i] += red[(((wc * NB + b) * 2 + mb) * 16 + i) * 64 + lane];
+    }
+    wait_vmcnt_lds<0>();
+    __builtin_amdgcn_s_barrier();
+  }
+}
+
+// The epilogues, every wave for its own NB column blocks of one 64-row tile.
+template <int EPI, int NB, int WN>
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, f32x16 (&acc)[NB][2], int e, int m_tile, int wg,
+                                              int wc, int zsplit, int rows_e, int lane) {
+  const int lr = lane & 31, g = lane >> 5;
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb) {
+    const int ml = m_tile * 64 + mb * 32 + lr;  // tile row
+    const bool row_ok = ml < rows_e;
+    const long long orow = (long long)e * a.o_erows + ml;
+    if constexpr (EPI == EPI_STORE) {
+      if (!row_ok) continue;
+      float* out = a.out + (long long)zsplit * a.out_split_stride + orow * a.ldo;
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int rg = 0; rg < 4; ++rg) {
+          const int n = ((wg * WN + wc) * NB + b) * 32 + 8 * rg + 4 * g;
+          if (n < a.N)
+            *reinterpret_cast<float4*>(out + n) = make_float4(acc[b][mb][4 * rg], acc[b][mb][4 * rg + 1],
+                                                              acc[b][mb][4 * rg + 2], acc[b][mb][4 * rg + 3]);
+        }
+    } else if constexpr (EPI == EPI_SWIGLU) {
+      static_assert(EPI != EPI_SWIGLU || NB == 2, "SwiGLU pairs one gate and one up block");
+      if (!row_ok) continue;
+#pragma unroll
+      for (int rg = 0; rg < 4; ++rg) {
+        const int n = (wg * WN + wc) * 32 + 8 * rg + 4 * g;
+        if (n < a.N) {
+          float h[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) h[i] = silu_f32(acc[0][mb][4 * rg + i]) * acc[NB - 1][mb][4 * rg + i];
+          uint16_t* dst = a.act + xpack_off(orow, n, a.act_ks);
+          const Hilo2 p0 = pack_hilo2(h[0], h[1]), p1 = pack_hilo2(h[2], h[3]);
+          *reinterpret_cast<uint2*>(dst) = make_uint2(p0.hi, p1.hi);
+          *reinterpret_cast<uint2*>(dst + XPACK_LO) = make_uint2(p0.lo, p1.lo);
+        }
+      }
+    } else {  // EPI_ARGMAX: partial (max, argmax, second max, NaN count) over this wave's columns
+      float best = -INFINITY, second = -INFINITY;
+      int bidx = 0x7fffffff;
+      int nan_cnt = 0;
+#pragma unroll
+      for (int b = 0; b < NB; ++b)
+#pragma unroll
+        for (int rg = 0; rg < 4; ++rg)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int n = ((wg * WN + wc) * NB + b) * 32 + 8 * rg + 4 * g + i;
+            const float v = acc[b][mb][4 * rg + i];
+            if (n < a.N) {
+              if (v != v) ++nan_cnt;
+              else top2_push(best, bidx, second, v, n);
+            }
+          }
+      const float ob = __shfl_xor(best, 32, 64);
+      const int oi = __shfl_xor(bidx, 32, 64);
+      const float os = __shfl_xor(second, 32, 64);
+      nan_cnt += __shfl_xor(nan_cnt, 32, 64);
+      top2_merge(best, bidx, second, ob, oi, os);
+      const int part = wg * WN + wc;
+      if (g == 0) {
+        a.pmax[orow * a.ld_part + part] = best;
+        a.pmax2[orow * a.ld_part + part] = second;
+        a.pidx[orow * a.ld_part + part] = bidx;
+        a.pnan[orow * a.ld_part + part] = nan_cnt;
+      }
+      if (a.logits && orow < a.logit_rows) {
+        float* out = a.logits + orow * a.ld_logits;
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+          for (int rg = 0; rg < 4; ++rg) {
+            const int n = ((wg * WN + wc) * NB + b) * 32 + 8 * rg + 4 * g;
+            if (n < a.N)
+              *reinterpret_cast<float4*>(out + n) = make_float4(acc[b][mb][4 * rg], acc[b][mb][4 * rg + 1],
+                                                                acc[b][mb][4 * rg + 2], acc[b][mb][4 * rg + 3]);
+          }
+      }
+    }
+  }
+}
+
 template <int EPI, int NB, int WN, int PF, int KS, bool XLO>
 __global__ __launch_bounds__(64 * WN * KS) void gemm_kernel(GemmArgs a) {
   // per step: {hi, lo} (XLO) or {hi} x {rows 0-31, 32-63} x 4 pieces of 1 KB
@@ -46,6 +162,7 @@ __global__ __launch_bounds__(64 * WN * KS) void gemm_kernel(GemmArgs a) {
   static_assert(WN * NB * 8 <= PF * KS * XPIECES || KS == 1, "K-split merge buffer");
   __shared__ u32x4 xs[PF][KS][XPIECES][64];
 
+  stamp_begin(a.stamp);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wc = wave % WN;            // column group of this wave
   const int kh = wave / WN;            // K slice of this wave inside the workgroup
@@ -150,113 +267,11 @@ __global__ __launch_bounds__(64 * WN * KS) void gemm_kernel(GemmArgs a) {
     if (u < rem) compute(u);
 
   if constexpr (KS > 1) {
-    // merge the K slices in slice order through LDS (the ring is free once
-    // every wave's reads have returned)
-    float* red = reinterpret_cast<float*>(&xs[0][0][0][0]);
-    wait_vmcnt_lds<0>();
-    __builtin_amdgcn_s_barrier();
-    for (int k = 1; k < KS; ++k) {
-      if (kh == k) {
-#pragma unroll
-        for (int b = 0; b < NB; ++b)
-#pragma unroll
-          for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) red[(((wc * NB + b) * 2 + mb) * 16 + i) * 64 + lane] = acc[b][mb][i];
-      }
-      wait_vmcnt_lds<0>();
-      __builtin_amdgcn_s_barrier();
-      if (kh == 0) {
-#pragma unroll
-        for (int b = 0; b < NB; ++b)
-#pragma unroll
-          for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-            for (int i = 0; i < 16; ++i) acc[b][mb][i] += red[(((wc * NB + b) * 2 + mb) * 16 + i) * 64 + lane];
-      }
-      wait_vmcnt_lds<0>();
-      __builtin_amdgcn_s_barrier();
-    }
+    ks_merge<NB, WN, KS>(acc, reinterpret_cast<float*>(&xs[0][0][0][0]), kh, wc, lane);
     if (kh != 0) return;
   }
-
-  // ---- epilogues, every wave for its own NB blocks
-#pragma unroll
-  for (int mb = 0; mb < 2; ++mb) {
-    const int ml = m_tile * 64 + mb * 32 + lr;  // tile row
-    const bool row_ok = ml < rows_e;
-    const long long orow = (long long)e * a.o_erows + ml;
-    if constexpr (EPI == EPI_STORE) {
-      if (!row_ok) continue;
-      float* out = a.out + (long long)zsplit * a.out_split_stride + orow * a.ldo;
-#pragma unroll
-      for (int b = 0; b < NB; ++b)
-#pragma unroll
-        for (int rg = 0; rg < 4; ++rg) {
-          const int n = ((wg * WN + wc) * NB + b) * 32 + 8 * rg + 4 * g;
-          if (n < a.N)
-            *reinterpret_cast<float4*>(out + n) = make_float4(acc[b][mb][4 * rg], acc[b][mb][4 * rg + 1],
-                                                              acc[b][mb][4 * rg + 2], acc[b][mb][4 * rg + 3]);
-        }
-    } else if constexpr (EPI == EPI_SWIGLU) {
-      static_assert(EPI != EPI_SWIGLU || NB == 2, "SwiGLU pairs one gate and one up block");
-      if (!row_ok) continue;
-#pragma unroll
-      for (int rg = 0; rg < 4; ++rg) {
-        const int n = (wg * WN + wc) * 32 + 8 * rg + 4 * g;
-        if (n < a.N) {
-          float h[4];
-#pragma unroll
-          for (int i = 0; i < 4; ++i) h[i] = silu_f32(acc[0][mb][4 * rg + i]) * acc[NB - 1][mb][4 * rg + i];
-          uint16_t* dst = a.act + xpack_off(orow, n, a.act_ks);
-          const Hilo2 p0 = pack_hilo2(h[0], h[1]), p1 = pack_hilo2(h[2], h[3]);
-          *reinterpret_cast<uint2*>(dst) = make_uint2(p0.hi, p1.hi);
-          *reinterpret_cast<uint2*>(dst + XPACK_LO) = make_uint2(p0.lo, p1.lo);
-        }
-      }
-    } else {  // EPI_ARGMAX: partial (max, argmax, second max, NaN count) over this wave's columns
-      float best = -INFINITY, second = -INFINITY;
-      int bidx = 0x7fffffff;
-      int nan_cnt = 0;
-#pragma unroll
-      for (int b = 0; b < NB; ++b)
-#pragma unroll
-        for (int rg = 0; rg < 4; ++rg)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int n = ((wg * WN + wc) * NB + b) * 32 + 8 * rg + 4 * g + i;
-            const float v = acc[b][mb][4 * rg + i];
-            if (n < a.N) {
-              if (v != v) ++nan_cnt;
-              else top2_push(best, bidx, second, v, n);
-            }
-          }
-      const float ob = __shfl_xor(best, 32, 64);
-      const int oi = __shfl_xor(bidx, 32, 64);
-      const float os = __shfl_xor(second, 32, 64);
-      nan_cnt += __shfl_xor(nan_cnt, 32, 64);
-      top2_merge(best, bidx, second, ob, oi, os);
-      const int part = wg * WN + wc;
-      if (g == 0) {
-        a.pmax[orow * a.ld_part + part] = best;
-        a.pmax2[orow * a.ld_part + part] = second;
-        a.pidx[orow * a.ld_part + part] = bidx;
-        a.pnan[orow * a.ld_part + part] = nan_cnt;
-      }
-      if (a.logits && orow < a.logit_rows) {
-        float* out = a.logits + orow * a.ld_logits;
-#pragma unroll
-        for (int b = 0; b < NB; ++b)
-#pragma unroll
-          for (int rg = 0; rg < 4; ++rg) {
-            const int n = ((wg * WN + wc) * NB + b) * 32 + 8 * rg + 4 * g;
-            if (n < a.N)
-              *reinterpret_cast<float4*>(out + n) = make_float4(acc[b][mb][4 * rg], acc[b][mb][4 * rg + 1],
-                                                                acc[b][mb][4 * rg + 2], acc[b][mb][4 * rg + 3]);
-          }
-      }
-    }
-  }
+  gemm_epilogue<EPI, NB, WN>(a, acc, e, m_tile, wg, wc, zsplit, rows_e, lane);
+  stamp_end(a.stamp);
 }
 
 template <int EPI, int NB, int WN, int PF, int KS, bool XLO>

@@ -86,6 +86,9 @@ struct GemmArgs {
   float* logits;             // optional fp32 [rows][ld_logits], rows < logit_rows
   long long ld_logits;
   int logit_rows;
+  // per-launch timing (null when not timed): [0] = ~(earliest workgroup
+  // start), [1] = latest wave end, device wall clock; both start at 0
+  unsigned long long* stamp;
 };
 
 // Residual update folded into the normalisation kernel:
@@ -98,6 +101,20 @@ struct ResidualAdd {
   const int32_t* slot;       // MoE: [rows][top_k] slot of each kept expert output, NULL for dense
   const float* slot_w;       // MoE: [rows][top_k] renormalised router weights
   int top_k;
+};
+
+// MoE routing folded into the RMSNorm before the experts: from the normed fp32
+// row h = RMSNorm(x) * gain, router logits h . w_e (fp32), softmax over the
+// experts, the top_k kept (ties to the lower id) with renormalised weights.
+// w == NULL: no routing.
+struct Router {
+  const uint16_t* w;         // [n_experts][d] bf16
+  int n_experts, top_k;
+  const int32_t* n_nodes;    // [B]: rows of absent nodes get id -1
+  int max_tree, rows;        // live row slots B * max_tree (padding rows beyond are left alone)
+  int32_t* ids;              // [rows][top_k]
+  float* weights;            // [rows][top_k]
+  float* logits;             // [rows][n_experts], the fp32 router logits (diagnostic)
 };
 
 // fp32 copies of the tree nodes' K (after rotation) and V for the layer being
@@ -137,7 +154,8 @@ hipError_t launch_pack_weight(const uint16_t* src, int rows, int K, const PackSh
                               hipStream_t s);
 hipError_t launch_embed(const uint16_t* embed, const int32_t* token, int rows, int d, float* x, hipStream_t s);
 hipError_t launch_residual_rmsnorm(float* x, const ResidualAdd& add, const uint16_t* gain, float eps,
-                                   int rows, int d, uint16_t* xn, int xn_ks, hipStream_t s);
+                                   int rows, int d, uint16_t* xn, int xn_ks, hipStream_t s,
+                                   const Router& route = Router{});
 hipError_t launch_qkv_rope(const float* qkv_parts, int n_parts, long long part_stride, StepMeta meta,
                            const float* rope_cos, const float* rope_sin, int Hq, int Hkv, int dh,
                            int max_tree, int batch, int kv_cap, uint16_t* q_out, uint16_t* q_lo,
@@ -159,14 +177,11 @@ hipError_t launch_commit(const int32_t* result, int max_depth, StepMeta meta, in
 hipError_t launch_gather_rows(const float* x, int d, const int32_t* rows, int n, float* out, hipStream_t s);
 hipError_t launch_accept(StepMeta meta, const int32_t* pred, const int32_t* nan_row, int batch,
                          int max_tree, int max_depth, int32_t* result, hipStream_t s);
-hipError_t launch_moe_route(const float* x, const uint16_t* gain, float eps, const uint16_t* w_router,
-                            int rows, int d, int n_experts, int top_k, const int32_t* n_nodes,
-                            int max_tree, int32_t* route_ids, float* route_w, float* logits_out,
-                            hipStream_t s);
-hipError_t launch_moe_lists(const int32_t* route_ids, int rows, int padded_rows, int n_experts, int top_k,
-                            int cap, int32_t* gather, int32_t* count, int32_t* slot, hipStream_t s);
-hipError_t launch_moe_gather(const uint16_t* xn, int xn_ks, const int32_t* gather, const int32_t* count,
-                             int n_experts, int cap, int d, uint16_t* xe, int xe_tiles, hipStream_t s);
+// Per-expert row lists (count[e], slot[row][k]) and the gather of the routed
+// rows' packed activations into each expert's tiles, in one launch.
+hipError_t launch_moe_dispatch(const int32_t* route_ids, int rows, int padded_rows, int n_experts, int top_k,
+                               int cap, const uint16_t* xn, int xn_ks, int d, uint16_t* xe, int xe_tiles,
+                               int32_t* count, int32_t* slot, hipStream_t s);
 
 // Result block written by the acceptance kernel, per sequence b:
 // [0] accept_len, [1] nan flag, [2 .. 2+max_depth] tokens_out (max_depth+1),

@@ -125,7 +125,7 @@ struct griffin_ctx {
   uint16_t *xn = nullptr, *q = nullptr, *q_lo = nullptr, *o = nullptr, *act = nullptr, *xe = nullptr;
   TreeKV32 tree{};  // fp32 tree K/V of the layer being computed (reused by every layer)
   int32_t *pidx = nullptr, *pnan = nullptr, *pred = nullptr, *nan_row = nullptr, *result = nullptr;
-  int32_t *route_ids = nullptr, *gather = nullptr, *count = nullptr, *slot = nullptr;
+  int32_t *route_ids = nullptr, *count = nullptr, *slot = nullptr;
   // stochastic acceptance: residual rows [max_batch][2][vocab], uniforms
   // [2][max_batch * max_tree] (accept, final), results
   char* samp_scratch = nullptr;  // sampled_scratch_bytes(max_batch, max_tree, vocab), zeroed
@@ -160,6 +160,11 @@ struct griffin_ctx {
   std::vector<hipEvent_t> prof_ev;     // pairs: start, stop
   std::vector<int> prof_cls;           // class of each pair
   size_t prof_used = 0;                // pairs recorded since the last read
+  // GEMM launches time themselves on the device wall clock: slots of
+  // (~start, end), zeroed when timing is enabled or read
+  unsigned long long* prof_stamp = nullptr;
+  std::vector<int> stamp_cls;          // class of each used slot
+  double wall_khz = 0.0;               // device wall clock rate
   int batch = 0;
   bool stepped = false;
   // the accepted paths griffin_commit moves: the result buffer of the last
@@ -254,6 +259,16 @@ int prof_pair(griffin_ctx* c, int cls, hipEvent_t* a, hipEvent_t* b) {
   return GRIFFIN_OK;
 }
 
+constexpr size_t kStampSlots = 16384;
+
+// A stamp slot for a timed GEMM launch of class cls (null when the class is
+// not timed or the slots are used up; the launch then carries events only).
+unsigned long long* stamp_slot(griffin_ctx* c, int cls) {
+  if (!((c->prof_mask >> cls) & 1u) || !c->prof_stamp || c->stamp_cls.size() >= kStampSlots) return nullptr;
+  c->stamp_cls.push_back(cls);
+  return c->prof_stamp + 2 * (c->stamp_cls.size() - 1);
+}
+
 #define LAUNCH(cls, call)                                                   \
   do {                                                                      \
     hipEvent_t ev0_ = nullptr, ev1_ = nullptr;                              \
@@ -292,6 +307,7 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
       a.out = c->parts;
       a.ldo = c->qkv_n;
       a.out_split_stride = ps * c->qkv_n;
+      a.stamp = stamp_slot(c, GRIFFIN_KC_QKV);
       LAUNCH(GRIFFIN_KC_QKV, launch_gemm(a, 1, s));
     }
     uint16_t* kc = c->k_cache + (size_t)l * layer_kv;
@@ -330,25 +346,40 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
       a.out = c->parts;
       a.ldo = d.d_model;
       a.out_split_stride = ps * d.d_model;
+      a.stamp = stamp_slot(c, GRIFFIN_KC_O);
       LAUNCH(GRIFFIN_KC_O, launch_gemm(a, 1, s));
     }
     ResidualAdd add_o{};
     add_o.parts = c->parts;
     add_o.n_parts = c->p_o.out_splits();
     add_o.part_stride = ps * d.d_model;
+    Router route{};
+    if (c->E > 1) {  // MoE: the MLP norm also routes every row
+      route.w = c->w_router[l];
+      route.n_experts = c->E;
+      route.top_k = c->topk;
+      route.n_nodes = c->meta.n_nodes;
+      route.max_tree = d.max_tree;
+      route.rows = rows;
+      route.ids = c->route_ids;
+      route.weights = c->route_w;
+      route.logits = c->router_logits + (long long)l * rows * c->E;
+    }
     LAUNCH(GRIFFIN_KC_NORM, launch_residual_rmsnorm(c->x, add_o, c->mlp_norm[l], d.rms_eps, Mpad, d.d_model, c->xn,
-                                                    c->xd_ks, s));
+                                                    c->xd_ks, s, route));
 
     // ---- MLP block
     if (c->E == 1) {
       GemmArgs g = gemm_args(c->p_gu, c->xn, c->xd_ks, c->pk_gu[l], m_tiles, !c->act_bf16);
       g.act = c->act;
       g.act_ks = c->p_down.ks_pad;
+      g.stamp = stamp_slot(c, GRIFFIN_KC_GATE_UP);
       LAUNCH(GRIFFIN_KC_GATE_UP, launch_gemm(g, 1, s));
       GemmArgs dn = gemm_args(c->p_down, c->act, c->p_down.ks_pad, c->pk_down[l], m_tiles, !c->act_bf16);
       dn.out = c->parts;
       dn.ldo = d.d_model;
       dn.out_split_stride = ps * d.d_model;
+      dn.stamp = stamp_slot(c, GRIFFIN_KC_DOWN);
       LAUNCH(GRIFFIN_KC_DOWN, launch_gemm(dn, 1, s));
       add_down = ResidualAdd{};
       add_down.parts = c->parts;
@@ -356,13 +387,8 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
       add_down.part_stride = ps * d.d_model;
     } else {
       const int xe_tiles = Mpad / 64;
-      LAUNCH(GRIFFIN_KC_OTHER, launch_moe_route(c->x, c->mlp_norm[l], d.rms_eps, c->w_router[l], rows, d.d_model,
-                                                c->E, c->topk, c->meta.n_nodes, d.max_tree, c->route_ids,
-                                                c->route_w, c->router_logits + (long long)l * rows * c->E, s));
-      LAUNCH(GRIFFIN_KC_OTHER, launch_moe_lists(c->route_ids, rows, Mpad, c->E, c->topk, Mpad, c->gather, c->count,
-                                                c->slot, s));
-      LAUNCH(GRIFFIN_KC_OTHER, launch_moe_gather(c->xn, c->xd_ks, c->gather, c->count, c->E, Mpad, d.d_model,
-                                                 c->xe, xe_tiles, s));
+      LAUNCH(GRIFFIN_KC_OTHER, launch_moe_dispatch(c->route_ids, rows, Mpad, c->E, c->topk, Mpad, c->xn, c->xd_ks,
+                                                   d.d_model, c->xe, xe_tiles, c->count, c->slot, s));
       GemmArgs g = gemm_args(c->p_gu, c->xe, c->xd_ks, c->pk_gu[l], m_tiles, !c->act_bf16);
       g.x_etiles = xe_tiles;
       g.count = c->count;
@@ -370,6 +396,7 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
       g.w_estride = c->p_gu.elems;
       g.act = c->act;
       g.act_ks = c->p_down.ks_pad;
+      g.stamp = stamp_slot(c, GRIFFIN_KC_GATE_UP);
       LAUNCH(GRIFFIN_KC_GATE_UP, launch_gemm(g, c->E, s));
       GemmArgs dn = gemm_args(c->p_down, c->act, c->p_down.ks_pad, c->pk_down[l], m_tiles, !c->act_bf16);
       dn.x_etiles = xe_tiles;
@@ -379,6 +406,7 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
       dn.out = c->yslots;
       dn.ldo = d.d_model;
       dn.out_split_stride = (long long)c->E * Mpad * d.d_model;
+      dn.stamp = stamp_slot(c, GRIFFIN_KC_DOWN);
       LAUNCH(GRIFFIN_KC_DOWN, launch_gemm(dn, c->E, s));
       add_down = ResidualAdd{};
       add_down.parts = c->yslots;
@@ -406,6 +434,7 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
     a.logits = logits_out;
     a.ld_logits = d.vocab;
     a.logit_rows = rows;
+    a.stamp = stamp_slot(c, GRIFFIN_KC_LM_HEAD);
     LAUNCH(GRIFFIN_KC_LM_HEAD, launch_gemm(a, 1, s));
   }
   if (c->front) return GRIFFIN_OK;  // a draft pass: the caller reads the logits
@@ -581,6 +610,7 @@ void griffin_verify_free(griffin_ctx* c) {
     if (c->meta_ev[k]) hipEventDestroy(c->meta_ev[k]);
   }
   for (hipEvent_t e : c->prof_ev) hipEventDestroy(e);
+  if (c->prof_stamp) hipFree(c->prof_stamp);
   for (auto& g : c->graphs) hipGraphExecDestroy(g.exec);
   if (c->result_host) hipHostFree(c->result_host);
   if (c->pred_host) hipHostFree(c->pred_host);
@@ -706,7 +736,6 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
     ALLOC(c->route_ids, Mp * c->topk);
     ALLOC(c->route_w, Mp * c->topk);
     ALLOC(c->router_logits, (long long)d.n_layers * d.max_batch * d.max_tree * c->E);
-    ALLOC(c->gather, (long long)c->E * Mp);
     ALLOC(c->count, c->E);
     ALLOC(c->slot, Mp * c->topk);
     ALLOC(c->yslots, (long long)c->p_down.out_splits() * c->E * Mp * d.d_model);
@@ -1078,6 +1107,20 @@ int griffin_profile_enable(griffin_ctx* c, uint32_t class_mask) {
   HIP_TRY(c, hipStreamSynchronize(c->stream));
   c->prof_mask = class_mask & ((1u << GRIFFIN_KC_COUNT) - 1);
   c->prof_used = 0;
+  c->stamp_cls.clear();
+  if (c->prof_mask && !c->prof_stamp) {
+    int dev = 0, khz = 0;
+    HIP_TRY(c, hipGetDevice(&dev));
+    HIP_TRY(c, hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev));
+    if (khz <= 0) return set_err(c, GRIFFIN_EHIP, "device wall clock rate unavailable");
+    c->wall_khz = khz;
+    void* p = nullptr;
+    if (hipMalloc(&p, kStampSlots * 2 * sizeof(unsigned long long)) != hipSuccess)
+      return set_err(c, GRIFFIN_ENOMEM, "launch timing slots");
+    c->prof_stamp = static_cast<unsigned long long*>(p);
+  }
+  if (c->prof_stamp)
+    HIP_TRY(c, hipMemsetAsync(c->prof_stamp, 0, kStampSlots * 2 * sizeof(unsigned long long), c->stream));
   return GRIFFIN_OK;
 }
 
@@ -1088,12 +1131,29 @@ int griffin_profile_read(griffin_ctx* c, double* ms, int64_t* launches) {
     ms[k] = 0.0;
     launches[k] = 0;
   }
+  // classes timed on the device clock replace their event intervals
+  uint32_t stamped = 0;
+  for (int k : c->stamp_cls) stamped |= 1u << k;
   for (size_t i = 0; i < c->prof_used; ++i) {
+    if ((stamped >> c->prof_cls[i]) & 1u) continue;
     float t = 0.f;
     HIP_TRY(c, hipEventElapsedTime(&t, c->prof_ev[2 * i], c->prof_ev[2 * i + 1]));
     ms[c->prof_cls[i]] += t;
     launches[c->prof_cls[i]] += 1;
   }
+  if (!c->stamp_cls.empty()) {
+    std::vector<unsigned long long> st(2 * c->stamp_cls.size());
+    HIP_TRY(c, hipMemcpy(st.data(), c->prof_stamp, st.size() * sizeof(unsigned long long), hipMemcpyDeviceToHost));
+    for (size_t i = 0; i < c->stamp_cls.size(); ++i) {
+      if (st[2 * i] == 0 || st[2 * i + 1] == 0) continue;  // a launch whose workgroups all returned early
+      const unsigned long long t0 = ~st[2 * i], t1 = st[2 * i + 1];
+      ms[c->stamp_cls[i]] += t1 > t0 ? (double)(t1 - t0) / c->wall_khz : 0.0;
+      launches[c->stamp_cls[i]] += 1;
+    }
+    HIP_TRY(c, hipMemsetAsync(c->prof_stamp, 0, st.size() * sizeof(unsigned long long), c->stream));
+    HIP_TRY(c, hipStreamSynchronize(c->stream));
+  }
+  c->stamp_cls.clear();
   c->prof_used = 0;
   return GRIFFIN_OK;
 }

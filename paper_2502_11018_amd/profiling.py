@@ -113,10 +113,12 @@ def cmd_stats(args):
     rows = [r for r in _rows(args.trace) if rx.search(_col(r, "Kernel_Name"))]
     rows.sort(key=lambda r: int(_col(r, "Start_Timestamp")))
     ends = [int(_col(r, "End_Timestamp")) for r in rows if end_rx.search(_col(r, "Kernel_Name"))]
-    if len(ends) < args.steps + 1:
-        raise SystemExit(f"{args.trace}: fewer than {args.steps + 1} steps")
-    t0 = ends[-args.steps - 1]
-    win = [r for r in rows if int(_col(r, "Start_Timestamp")) > t0]
+    skip = args.skip_last
+    if len(ends) < args.steps + skip + 1:
+        raise SystemExit(f"{args.trace}: fewer than {args.steps + skip + 1} steps")
+    t0 = ends[-args.steps - skip - 1]
+    t1 = ends[-skip - 1] if skip else ends[-1]
+    win = [r for r in rows if t0 < int(_col(r, "Start_Timestamp")) <= t1]
     before = [r for r in rows if int(_col(r, "Start_Timestamp")) <= t0]
     groups = {}
     prev = _short(_col(before[-1], "Kernel_Name")) if before else ""
@@ -129,7 +131,9 @@ def cmd_stats(args):
     busy = sum(sum(v) for v in groups.values()) / args.steps
     span = (int(_col(win[-1], "End_Timestamp")) - int(_col(win[0], "Start_Timestamp"))) / 1e3 / args.steps
     out = [f"# {args.title}", "", "Command:", "", "```", args.command, "```", "",
-           f"Last {args.steps} steps of the run: kernel busy time {busy:.1f} us per step, "
+           (f"Last {args.steps} steps of the run" if not skip else
+            f"{args.steps} steps of the run, ending {skip} steps before its last") +
+           f": kernel busy time {busy:.1f} us per step, "
            f"first-kernel-start to last-kernel-end {span:.1f} us per step.", "",
            "| kernel | workgroups | after | launches/step | avg us | min us | max us | us/step |",
            "|---|---|---|---:|---:|---:|---:|---:|"]
@@ -258,6 +262,8 @@ def main(argv=None):
     s.add_argument("--steps", type=int, required=True)
     s.add_argument("--include", default="griffin::")
     s.add_argument("--step-end", default="accept_kernel", help="regex of the kernel that ends a step")
+    s.add_argument("--skip-last", type=int, default=0,
+                   help="steps at the end of the run left out of the window (e.g. a later profiling pass)")
     s.add_argument("--out", required=True)
     s.add_argument("--title", required=True)
     s.add_argument("--command", required=True)
