@@ -150,58 +150,68 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, f32x16 (&acc)[N
   }
 }
 
-template <int EPI, int NB, int WN, int PF, int KS, bool XLO>
+template <int EPI, int NB, int WN, int PF, int KS, bool XLO, int TG>
 __global__ __launch_bounds__(64 * WN * KS) void gemm_kernel(GemmArgs a) {
-  // per step: {hi, lo} (XLO) or {hi} x {rows 0-31, 32-63} x 4 pieces of 1 KB
+  // per step: {hi, lo} (XLO) or {hi} x {rows 0-31, 32-63} x 4 pieces of 1 KB,
+  // for each of the TG 64-row tiles of the workgroup
   constexpr int XH = XLO ? 2 : 1;
   constexpr int XPIECES = 8 * XH;
-  constexpr int XP = XPIECES / WN;     // activation pieces each wave stages per step
-  constexpr int LOADS = NB * 4 + XP;   // vector-memory instructions per stage per wave
+  constexpr int XP = XPIECES / WN;          // activation pieces each wave stages per step and tile
+  constexpr int LOADS = NB * 4 + TG * XP;   // vector-memory instructions per stage per wave
   static_assert(LOADS * (PF - 2) < 64, "wait count out of range");
   static_assert(PF >= 2 && XPIECES % WN == 0, "pipeline shape");
   static_assert(WN * NB * 8 <= PF * KS * XPIECES || KS == 1, "K-split merge buffer");
-  __shared__ u32x4 xs[PF][KS][XPIECES][64];
+  static_assert(TG == 1 || KS == 1, "several tiles per workgroup merge no K slices");
+  __shared__ u32x4 xs[PF][KS][TG][XPIECES][64];
 
   stamp_begin(a.stamp);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wc = wave % WN;            // column group of this wave
   const int kh = wave / WN;            // K slice of this wave inside the workgroup
-  const int lr = lane & 31, g = lane >> 5;
   const int e = blockIdx.y;
   // XCD-aware decode: workgroups are dispatched round-robin over the 8 XCDs
   // (linear id % 8, and the grid's x extent is a multiple of 8), so the
-  // m_tiles workgroups that stream the same weights get the same id % 8 and
-  // the re-reads of those weights hit that XCD's L2.
-  int m_tile = 0, wg = blockIdx.x;
-  if (a.m_tiles > 1) {
-    const int grp = blockIdx.x / (8 * a.m_tiles), r = blockIdx.x % (8 * a.m_tiles);
-    m_tile = r >> 3;
+  // workgroups of the groups of TG row tiles that stream the same weights
+  // get the same id % 8 and the re-reads of those weights hit that XCD's L2.
+  const int groups = (a.m_tiles + TG - 1) / TG;
+  int tgrp = 0, wg = blockIdx.x;
+  if (groups > 1) {
+    const int grp = blockIdx.x / (8 * groups), r = blockIdx.x % (8 * groups);
+    tgrp = r >> 3;
     wg = grp * 8 + (r & 7);
     if (wg >= a.n_wgs) return;  // padding of the grid to a multiple of 8 (uniform)
   }
   const int zsplit = blockIdx.z;       // output split (its KS slices are merged in the workgroup)
   const int split = zsplit * KS + kh;  // K slice of this wave's weight stream
   const int rows_e = a.count ? a.count[e] : a.m_tiles * 64;
-  if (m_tile * 64 >= rows_e) return;  // uniform over the workgroup
+  const int tile0 = tgrp * TG;         // first row tile of the workgroup
+  if (tile0 * 64 >= rows_e) return;    // uniform over the workgroup
 
   const long long Q = (long long)a.n_wgs * a.splits * WN;
   const long long q = ((long long)split * a.n_wgs + wg) * WN + wc;
   const uint16_t* W = a.W + (long long)e * a.w_estride + q * NB * 2048 + lane * 8;
   const long long wstep = Q * NB * 2048;  // elements between consecutive steps of a stream
-  const uint16_t* X = a.X + ((long long)(e * a.x_etiles + m_tile) * a.x_ks + (long long)zsplit * KS * a.len) *
-                                XPACK_STEP + lane * 8;
+  // activation tiles of the group, the last one repeated where the group
+  // runs past the tiles (their results are not stored)
+  const uint16_t* X[TG];
+#pragma unroll
+  for (int g = 0; g < TG; ++g)
+    X[g] = a.X + ((long long)(e * a.x_etiles + min(tile0 + g, a.m_tiles - 1)) * a.x_ks +
+                  (long long)zsplit * KS * a.len) * XPACK_STEP + lane * 8;
 
-  f32x16 acc[NB][2];
+  f32x16 acc[TG][NB][2];
 #pragma unroll
-  for (int b = 0; b < NB; ++b)
+  for (int g = 0; g < TG; ++g)
 #pragma unroll
-    for (int mb = 0; mb < 2; ++mb)
+    for (int b = 0; b < NB; ++b)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) acc[b][mb][i] = 0.f;
+      for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[g][b][mb][i] = 0.f;
 
   // Stage t: this wave's weight blocks into registers, its share of the
-  // activation stage straight into LDS slot t % PF (lane l's 16 bytes land at
-  // the piece base + 16 l, which is the fragment order).
+  // activation stage of every tile straight into LDS slot t % PF (lane l's 16
+  // bytes land at the piece base + 16 l, which is the fragment order).
   u32x4 wb[PF][NB][4];
   auto issue = [&](u32x4 (&wv)[NB][4], int slot, int t) {
     const uint16_t* wp = W + t * wstep;
@@ -210,33 +220,39 @@ __global__ __launch_bounds__(64 * WN * KS) void gemm_kernel(GemmArgs a) {
 #pragma unroll
       for (int b = 0; b < NB; ++b) wv[b][j] = ld_u4(wp + b * 2048 + j * 512);
 #pragma unroll
-    for (int p = 0; p < XP; ++p) {
-      const int pp = wave * XP + p, sk = pp / XPIECES, pc = pp % XPIECES;  // slice, piece
-      __builtin_amdgcn_global_load_lds(
-          (const void*)(X + ((long long)sk * a.len + t) * XPACK_STEP + pc * 512),
-          (lds_void*)&xs[slot][sk][pc][0], 16, 0, 0);
-    }
+    for (int g = 0; g < TG; ++g)
+#pragma unroll
+      for (int p = 0; p < XP; ++p) {
+        const int pp = wave * XP + p, sk = pp / XPIECES, pc = pp % XPIECES;  // slice, piece
+        __builtin_amdgcn_global_load_lds(
+            (const void*)(X[g] + ((long long)sk * a.len + t) * XPACK_STEP + pc * 512),
+            (lds_void*)&xs[slot][sk][g][pc][0], 16, 0, 0);
+      }
   };
   // Consume stage t from slot u: the weights times the activation's bf16 high
-  // part plus, with XLO, its bf16 low part (two MFMAs into one accumulator).
+  // part plus, with XLO, its bf16 low part (two MFMAs into one accumulator),
+  // for every tile with the same weight registers.
   auto compute = [&](int u) {
-    u32x4 xv[XH][2][4];
 #pragma unroll
-    for (int h = 0; h < XH; ++h)
-#pragma unroll
-      for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) xv[h][mb][j] = xs[u][kh][h * 8 + mb * 4 + j][lane];
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int g = 0; g < TG; ++g) {
+      u32x4 xv[XH][2][4];
 #pragma unroll
       for (int h = 0; h < XH; ++h)
 #pragma unroll
-        for (int b = 0; b < NB; ++b)
+        for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-          for (int mb = 0; mb < 2; ++mb)
-            acc[b][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(wb[u][b][j]), as_bf16x8(xv[h][mb][j]),
-                                                                 acc[b][mb], 0, 0, 0);
+          for (int j = 0; j < 4; ++j) xv[h][mb][j] = xs[u][kh][g][h * 8 + mb * 4 + j][lane];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int h = 0; h < XH; ++h)
+#pragma unroll
+          for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb)
+              acc[g][b][mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                  as_bf16x8(wb[u][b][j]), as_bf16x8(xv[h][mb][j]), acc[g][b][mb], 0, 0, 0);
+    }
   };
 
   // Pipeline: stages t+1 .. t+PF-2 stay in flight while stage t is consumed.
@@ -267,34 +283,43 @@ __global__ __launch_bounds__(64 * WN * KS) void gemm_kernel(GemmArgs a) {
     if (u < rem) compute(u);
 
   if constexpr (KS > 1) {
-    ks_merge<NB, WN, KS>(acc, reinterpret_cast<float*>(&xs[0][0][0][0]), kh, wc, lane);
+    ks_merge<NB, WN, KS>(acc[0], reinterpret_cast<float*>(&xs[0][0][0][0][0]), kh, wc, lane);
     if (kh != 0) return;
   }
-  gemm_epilogue<EPI, NB, WN>(a, acc, e, m_tile, wg, wc, zsplit, rows_e, lane);
+#pragma unroll
+  for (int g = 0; g < TG; ++g)
+    if (tile0 + g < a.m_tiles && (tile0 + g) * 64 < rows_e)
+      gemm_epilogue<EPI, NB, WN>(a, acc[g], e, tile0 + g, wg, wc, zsplit, rows_e, lane);
   stamp_end(a.stamp);
 }
 
-template <int EPI, int NB, int WN, int PF, int KS, bool XLO>
+template <int EPI, int NB, int WN, int PF, int KS, bool XLO, int TG>
 static hipError_t launch_one(const GemmArgs& a, int experts, hipStream_t s) {
-  const int gx = a.m_tiles > 1 ? (a.n_wgs + 7) / 8 * 8 * a.m_tiles : a.n_wgs;
+  const int groups = (a.m_tiles + TG - 1) / TG;
+  const int gx = groups > 1 ? (a.n_wgs + 7) / 8 * 8 * groups : a.n_wgs;
   dim3 grid(gx, experts, a.splits / KS);
-  hipLaunchKernelGGL((gemm_kernel<EPI, NB, WN, PF, KS, XLO>), grid, dim3(64 * WN * KS), 0, s, a);
+  hipLaunchKernelGGL((gemm_kernel<EPI, NB, WN, PF, KS, XLO, TG>), grid, dim3(64 * WN * KS), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_gemm(const GemmArgs& a, int experts, hipStream_t s) {
   const int epi = a.epi, nb = a.nb, wn = a.wn, pf = a.pf, ks = a.kslices;
   if (ks < 1 || a.splits % ks != 0) return hipErrorInvalidValue;
-#define GRIFFIN_GEMM_CASE(E, B, N_, P, K_)                                                          \
-  if (epi == (E) && nb == (B) && wn == (N_) && pf == (P) && ks == (K_))                            \
-    return a.xlo ? launch_one<E, B, N_, P, K_, true>(a, experts, s) : launch_one<E, B, N_, P, K_, false>(a, experts, s);
-  GRIFFIN_GEMM_CASE(EPI_STORE, 1, 4, 4, 1)
-  GRIFFIN_GEMM_CASE(EPI_STORE, 1, 4, 2, 1)
-  GRIFFIN_GEMM_CASE(EPI_SWIGLU, 2, 2, 3, 2)
-  GRIFFIN_GEMM_CASE(EPI_SWIGLU, 2, 2, 2, 2)
-  GRIFFIN_GEMM_CASE(EPI_SWIGLU, 2, 2, 2, 1)
-  GRIFFIN_GEMM_CASE(EPI_ARGMAX, 2, 4, 4, 1)
-  GRIFFIN_GEMM_CASE(EPI_ARGMAX, 2, 4, 2, 1)
+  const int tg = a.tg < 1 ? 1 : a.tg;
+#define GRIFFIN_GEMM_CASE(E, B, N_, P, K_, T_)                                                         \
+  if (epi == (E) && nb == (B) && wn == (N_) && pf == (P) && ks == (K_) && tg == (T_))                 \
+    return a.xlo ? launch_one<E, B, N_, P, K_, true, T_>(a, experts, s)                               \
+                 : launch_one<E, B, N_, P, K_, false, T_>(a, experts, s);
+  // one 64-row tile per workgroup
+  GRIFFIN_GEMM_CASE(EPI_STORE, 1, 4, 4, 1, 1)
+  GRIFFIN_GEMM_CASE(EPI_STORE, 1, 4, 2, 1, 1)
+  GRIFFIN_GEMM_CASE(EPI_SWIGLU, 2, 2, 3, 2, 1)
+  GRIFFIN_GEMM_CASE(EPI_SWIGLU, 2, 2, 2, 2, 1)
+  GRIFFIN_GEMM_CASE(EPI_SWIGLU, 2, 2, 2, 1, 1)
+  GRIFFIN_GEMM_CASE(EPI_ARGMAX, 2, 4, 4, 1, 1)
+  GRIFFIN_GEMM_CASE(EPI_ARGMAX, 2, 4, 2, 1, 1)
+  // four row tiles per workgroup sharing each weight fragment (batched rows)
+  GRIFFIN_GEMM_CASE(EPI_SWIGLU, 2, 4, 2, 1, 4)
 #undef GRIFFIN_GEMM_CASE
   return hipErrorInvalidValue;
 }

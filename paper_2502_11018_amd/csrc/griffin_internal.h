@@ -60,6 +60,7 @@ struct GemmArgs {
   int epi, nb, wn, pf;       // kernel variant
   int n_wgs, splits, len;    // launch shape (matches the weight packing): splits = K slices
   int kslices;               // K slices merged inside one workgroup (output splits = splits / kslices)
+  int tg;                    // 64-row tiles per workgroup sharing each weight fragment (1 or 4)
   int N;                     // output columns (SwiGLU: d_ff)
   int m_tiles;               // 64-row activation tiles
   const uint16_t* X;         // packed activations

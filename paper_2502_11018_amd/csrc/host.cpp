@@ -35,6 +35,7 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 // Launch shape of one weight matrix (fixed at init; the packing follows it).
 struct GemmPlan {
   int epi = 0, nb = 1, wn = 4, pf = 4;
+  int tg = 1;       // 64-row tiles per workgroup
   int kslices = 1;  // K slices merged inside a workgroup (shape.splits / kslices output splits)
   int out_splits() const { return shape.splits / kslices; }
   int n_out = 0;   // output columns
@@ -44,12 +45,32 @@ struct GemmPlan {
   long long elems = 0;  // packed elements of one matrix (one expert)
 };
 
-GemmPlan plan_gemm(int epi, int n_out, int K, int experts = 1) {
+// m_tiles: the most 64-row tiles a step of the context can have.  In a dense
+// context of several tiles the gate/up GEMM shares each weight fragment
+// between four tiles per workgroup (batched rows: re-streaming the weights
+// per tile, even from L2, bounds it).  The other GEMMs keep one tile per
+// workgroup: four tiles' activation stages leave LDS for only a two-stage
+// pipeline, which measured slower for them (down 129 -> 169 us, LM head
+// 0.90 -> 1.19 ms at 8 x 61 rows).
+GemmPlan plan_gemm(int epi, int n_out, int K, int experts = 1, int m_tiles = 1) {
   GemmPlan p;
   p.epi = epi;
   p.n_out = n_out;
   p.K = K;
   p.ks = cdiv(K, 64);
+  if (m_tiles >= 2 && experts == 1 && epi == EPI_SWIGLU) {
+    p.tg = 4;
+    p.kslices = 1;
+    p.pf = 2;
+    p.nb = 2;
+    p.wn = 4;
+    p.rows = 2 * n_out;
+    const int n_wgs = cdiv(cdiv(n_out, 32), p.wn);
+    p.ks_pad = p.ks;
+    p.shape = PackShape{p.nb, p.wn, 1, p.ks, n_wgs, 1, n_out};
+    p.elems = packed_elems(p.shape);
+    return p;
+  }
   int splits = 1;
   if (epi == EPI_SWIGLU) {
     p.nb = 2;
@@ -232,6 +253,7 @@ GemmArgs gemm_args(const GemmPlan& p, const uint16_t* X, int x_ks, const uint16_
   a.n_wgs = p.shape.n_wgs;
   a.splits = p.shape.splits;
   a.kslices = p.kslices;
+  a.tg = p.tg;
   a.len = p.shape.len;
   a.N = p.n_out;
   a.m_tiles = m_tiles;
@@ -681,11 +703,12 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
     // single-sequence context gives its sequence all attn_splits, no table.
     c->attn_sp = d.max_batch > 1 ? std::min(16, 2 * c->attn_splits) : c->attn_splits;
   }
-  c->p_qkv = plan_gemm(EPI_STORE, c->qkv_n, d.d_model);
-  c->p_o = plan_gemm(EPI_STORE, d.d_model, c->attn_w);
-  c->p_gu = plan_gemm(EPI_SWIGLU, d.d_ff, d.d_model, c->E);
-  c->p_down = plan_gemm(EPI_STORE, d.d_model, d.d_ff, c->E);
-  c->p_lm = plan_gemm(EPI_ARGMAX, d.vocab, d.d_model);
+  const int max_tiles = c->Mpad / 64;
+  c->p_qkv = plan_gemm(EPI_STORE, c->qkv_n, d.d_model, 1, max_tiles);
+  c->p_o = plan_gemm(EPI_STORE, d.d_model, c->attn_w, 1, max_tiles);
+  c->p_gu = plan_gemm(EPI_SWIGLU, d.d_ff, d.d_model, c->E, max_tiles);
+  c->p_down = plan_gemm(EPI_STORE, d.d_model, d.d_ff, c->E, max_tiles);
+  c->p_lm = plan_gemm(EPI_ARGMAX, d.vocab, d.d_model, 1, max_tiles);
   c->xd_ks = std::max({c->p_qkv.ks_pad, c->p_gu.ks_pad, c->p_lm.ks_pad});
   const long long Mp = c->Mpad;
   const long long tiles = Mp / 64;
@@ -1435,11 +1458,11 @@ int griffin_draft_init(const griffin_model_desc* desc, int32_t tgf_dim, float ln
   dc->b_d = static_cast<const uint16_t*>(w->b_d);
   dc->b_p = static_cast<const uint16_t*>(w->b_p);
   dc->b_r = static_cast<const uint16_t*>(w->b_r);
-  dc->p_m = plan_gemm(EPI_STORE, d, 2 * d);
-  dc->p_u = plan_gemm(EPI_STORE, e, 2 * d);
-  dc->p_d = plan_gemm(EPI_STORE, d, e);
-  dc->p_h = plan_gemm(EPI_STORE, 2 * d, d);
   const int rows = desc->max_batch * desc->max_tree, mpad = round_up(rows, 64), tiles = mpad / 64;
+  dc->p_m = plan_gemm(EPI_STORE, d, 2 * d, 1, tiles);
+  dc->p_u = plan_gemm(EPI_STORE, e, 2 * d, 1, tiles);
+  dc->p_d = plan_gemm(EPI_STORE, d, e, 1, tiles);
+  dc->p_h = plan_gemm(EPI_STORE, 2 * d, d, 1, tiles);
   long long parts = 0;
   for (const GemmPlan* p : {&dc->p_m, &dc->p_u, &dc->p_d, &dc->p_h})
     parts = std::max(parts, (long long)p->out_splits() * mpad * p->n_out);
