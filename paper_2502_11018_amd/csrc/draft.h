@@ -41,3 +41,38 @@ hipError_t launch_draft_topk(const float* logits, long long ld, int V, const Ste
                              int k, int32_t* tok, float* logp, float* work, hipStream_t s);
 
 }  // namespace griffin
+
+namespace griffin {
+
+// Device-side expansion of a draft tree (Sec. 3.1, the EAGLE-2 style dynamic
+// tree the draft builds): after pass t's top-k, one workgroup per sequence
+// scores the candidates of the pass's frontier, and either writes the next
+// pass tree (the k best of them, appended to the pass tree in the step
+// metadata, plus the next pass's fixed metadata) or, after the last pass,
+// selects the n_total best of all candidates.  Candidate scores are fp64
+// sums of fp32 log-probabilities, ranked by score (NaN lowest), ties to the
+// earlier candidate.
+constexpr int DRAFT_SEL_MAX = 1024;  // candidates per sequence: k (1 + k (depth - 1)) <= 16 * 64
+struct DraftSelectArgs {
+  int t, k, depth, n_total, max_tree;
+  const int32_t* topk_tok;  // [batch * max_tree][k] of pass t
+  const float* topk_lp;
+  int32_t* c_tok;           // [batch][DRAFT_SEL_MAX] candidates: token, proposing pass-tree node, score
+  int32_t* c_node;
+  double* c_score;
+  int32_t* n_cand;          // [batch * max_tree] pass-tree node -> its candidate
+  double* n_score;          // [batch * max_tree] pass-tree node -> its score
+  int32_t* m_token;         // the step metadata's tree rows [batch * max_tree]
+  int32_t* m_parent;
+  uint64_t* m_anc;
+  const uint4* tail_src;    // next pass's fixed metadata (prefix, sizes, positions, depths, split table)
+  uint4* tail_dst;
+  int tail_words;
+  int32_t* o_nodes;         // last pass: [batch] node counts, [batch][max_tree] tokens, parents, scores
+  int32_t* o_tok;
+  int32_t* o_par;
+  float* o_score;
+};
+hipError_t launch_draft_select(const DraftSelectArgs& a, int batch, hipStream_t s);
+
+}  // namespace griffin

@@ -425,4 +425,102 @@ hipError_t launch_draft_topk(const float* logits, long long ld, int V, const Ste
   return hipGetLastError();
 }
 
+// ------------------------------------------------------------ tree expansion
+
+// Ranking key of a candidate score: NaN counts as the lowest score.
+__device__ __forceinline__ double sel_key(double s) { return s != s ? -INFINITY : s; }
+// Candidate a (score sa) ranks before candidate b: higher score, then lower index.
+__device__ __forceinline__ bool sel_before(double sa, int a, double sb, int b) {
+  return sa > sb || (sa == sb && a < b);
+}
+
+constexpr int SEL_T = 256;
+
+__global__ __launch_bounds__(SEL_T) void draft_select_kernel(DraftSelectArgs a) {
+  __shared__ double sc[DRAFT_SEL_MAX];  // ranking keys of the candidates
+  __shared__ int rank[DRAFT_SEL_MAX], slot[DRAFT_SEL_MAX];
+  const int b = blockIdx.x, tid = threadIdx.x, k = a.k, T = a.max_tree, t = a.t;
+  // the frontier of pass t: the root, or the k nodes the previous pass added
+  const int f0 = t == 0 ? 0 : 1 + k * (t - 1), nf = (t == 0 ? 1 : k) * k;
+  const int c0 = t == 0 ? 0 : k + k * k * (t - 1);  // index of the first fresh candidate
+  const long long cb = (long long)b * DRAFT_SEL_MAX, nb = (long long)b * T;
+  for (int q = tid; q < nf; q += SEL_T) {
+    const int r = f0 + q / k;
+    const long long at = (nb + r) * k + q % k;
+    const double s = (r == 0 ? 0.0 : a.n_score[nb + r]) + (double)a.topk_lp[at];
+    a.c_tok[cb + c0 + q] = a.topk_tok[at];
+    a.c_node[cb + c0 + q] = r;
+    a.c_score[cb + c0 + q] = s;
+    sc[c0 + q] = sel_key(s);
+  }
+  if (t + 1 < a.depth) {
+    __syncthreads();
+    // the k best fresh candidates become pass-tree nodes 1 + k t + rank
+    for (int q = tid; q < nf; q += SEL_T) {
+      const double s = sc[c0 + q];
+      int rk = 0;
+      for (int o = 0; o < nf; ++o) rk += sel_before(sc[c0 + o], o, s, q);
+      if (rk < k) {
+        const int node = 1 + k * t + rk, r = f0 + q / k;
+        a.n_cand[nb + node] = c0 + q;
+        a.n_score[nb + node] = a.c_score[cb + c0 + q];
+        a.m_token[nb + node] = a.c_tok[cb + c0 + q];
+        a.m_parent[nb + node] = r;
+        a.m_anc[nb + node] = a.m_anc[nb + r] | (1ull << node);
+      }
+    }
+    for (int w = b * SEL_T + tid; w < a.tail_words; w += gridDim.x * SEL_T) a.tail_dst[w] = a.tail_src[w];
+    return;
+  }
+  // last pass: the n_total best of all candidates, numbered by depth, then rank
+  const int nc = c0 + nf;
+  for (int q = tid; q < c0; q += SEL_T) sc[q] = sel_key(a.c_score[cb + q]);
+  __syncthreads();
+  for (int q = tid; q < nc; q += SEL_T) {
+    const double s = sc[q];
+    int rk = 0;
+    for (int o = 0; o < nc; ++o) rk += sel_before(sc[o], o, s, q);
+    rank[q] = rk;
+  }
+  __syncthreads();
+  const int keep = min(nc, a.n_total);
+  auto depth_of = [&](int q) { return q < k ? 1 : 2 + (q - k) / (k * k); };
+  for (int q = tid; q < nc; q += SEL_T) {
+    int at = -1;
+    if (rank[q] < keep) {
+      const int dq = depth_of(q), rq = rank[q];
+      at = 0;
+      for (int o = 0; o < nc; ++o) {
+        const int ro = rank[o], dout = depth_of(o);
+        at += ro < keep && (dout < dq || (dout == dq && ro < rq));
+      }
+    }
+    slot[q] = at;
+  }
+  __syncthreads();
+  for (int q = tid; q < nc; q += SEL_T) {
+    const int at = slot[q];
+    if (at < 0) continue;
+    const int r = a.c_node[cb + q];
+    const int pc = r == 0 ? -1 : a.n_cand[nb + r];
+    a.o_tok[nb + at + 1] = a.c_tok[cb + q];
+    a.o_par[nb + at + 1] = pc < 0 ? 0 : slot[pc] + 1;
+    a.o_score[nb + at + 1] = (float)a.c_score[cb + q];
+  }
+  if (tid == 0) {
+    a.o_nodes[b] = 1 + keep;
+    a.o_tok[nb] = a.m_token[nb];
+    a.o_par[nb] = -1;
+    a.o_score[nb] = 0.f;
+  }
+}
+
+hipError_t launch_draft_select(const DraftSelectArgs& a, int batch, hipStream_t s) {
+  if (a.k < 1 || a.k > DK || a.t < 0 || a.t >= a.depth || a.max_tree > 64 || 1 + a.k * (a.depth - 1) > a.max_tree ||
+      a.k * (1 + a.k * (a.depth - 1)) > DRAFT_SEL_MAX || batch < 1)
+    return hipErrorInvalidValue;
+  hipLaunchKernelGGL(draft_select_kernel, dim3(batch), dim3(SEL_T), 0, s, a);
+  return hipGetLastError();
+}
+
 }  // namespace griffin

@@ -169,11 +169,13 @@ struct griffin_ctx {
   // per-class launch timing (griffin_profile_*)
   uint32_t prof_mask = 0;
 
-  // captured launch sequences of a pass, keyed by (batch, logits_out)
+  // captured launch sequences of a pass, keyed by (batch, logits_out,
+  // kv_only), and of a whole draft tree (also keyed by k, depth, n_total)
   struct GraphEntry {
     int batch;
     float* logits;
     bool kv_only;
+    int tree_k, tree_depth, tree_n;  // 0: one pass
     hipGraphExec_t exec;
   };
   std::vector<GraphEntry> graphs;
@@ -466,23 +468,24 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
   return GRIFFIN_OK;
 }
 
-// Enqueue one pass: replay a captured HIP graph of the launch sequence when
-// possible (one per batch size and logits_out pointer, at most kMaxGraphs
-// kept, captured on first use), otherwise launch kernel by kernel.  Every
-// per-step input lives in device buffers whose addresses are fixed for the
-// context, so a graph stays valid for its key.  Per-class timing and the
-// legacy null stream use the plain launches.
+// Enqueue a launch sequence: replay the HIP graph captured for its key when
+// there is one (at most kMaxGraphs kept, captured on first use), otherwise
+// launch kernel by kernel.  Every per-step input lives in device buffers whose
+// addresses are fixed for the context, so a graph stays valid for its key.
+// Per-class timing and the legacy null stream use the plain launches.
 constexpr size_t kMaxGraphs = 8;
 
-int run_pass(griffin_ctx* c, float* logits_out) {
-  if (!c->use_graphs || c->prof_mask != 0 || c->stream == nullptr) return enqueue_pass(c, logits_out);
+template <class Body>
+int run_graph(griffin_ctx* c, const griffin_ctx::GraphEntry& key, Body body) {
+  if (!c->use_graphs || c->prof_mask != 0 || c->stream == nullptr) return body();
   for (auto& g : c->graphs)
-    if (g.batch == c->batch && g.logits == logits_out && g.kv_only == c->kv_only) {
+    if (g.batch == key.batch && g.logits == key.logits && g.kv_only == key.kv_only && g.tree_k == key.tree_k &&
+        g.tree_depth == key.tree_depth && g.tree_n == key.tree_n) {
       HIP_TRY(c, hipGraphLaunch(g.exec, c->stream));
       return GRIFFIN_OK;
     }
   HIP_TRY(c, hipStreamBeginCapture(c->stream, hipStreamCaptureModeThreadLocal));
-  const int rc = enqueue_pass(c, logits_out);
+  const int rc = body();
   hipGraph_t graph = nullptr;
   const hipError_t e = hipStreamEndCapture(c->stream, &graph);
   if (rc != GRIFFIN_OK) {
@@ -498,9 +501,17 @@ int run_pass(griffin_ctx* c, float* logits_out) {
     hipGraphExecDestroy(c->graphs.front().exec);
     c->graphs.erase(c->graphs.begin());
   }
-  c->graphs.push_back({c->batch, logits_out, c->kv_only, exec});
+  griffin_ctx::GraphEntry g = key;
+  g.exec = exec;
+  c->graphs.push_back(g);
   HIP_TRY(c, hipGraphLaunch(exec, c->stream));
   return GRIFFIN_OK;
+}
+
+// One pass (batch, logits_out, kv_only from the context).
+int run_pass(griffin_ctx* c, float* logits_out) {
+  return run_graph(c, {c->batch, logits_out, c->kv_only, 0, 0, 0, nullptr},
+                   [&]() { return enqueue_pass(c, logits_out); });
 }
 
 }  // namespace
@@ -523,6 +534,17 @@ struct griffin_draft {
   float* topk_work = nullptr;
   int32_t* topk_tok_host = nullptr;
   float* topk_lp_host = nullptr;
+  // griffin_draft_tree's device-side expansion: candidate and pass-tree
+  // state, the fixed metadata of every pass (host staging and device copy)
+  // and the output rows
+  int32_t *c_tok = nullptr, *c_node = nullptr, *n_cand = nullptr;
+  double *c_score = nullptr, *n_score = nullptr;
+  char* stage_host = nullptr;
+  char* stage_dev = nullptr;
+  int max_passes = 0;
+  hipEvent_t stage_ev = nullptr;  // the staging buffer's last copy
+  int32_t* out_dev = nullptr;   // [max_batch] node counts, then tokens, parents, scores [max_batch * max_tree]
+  int32_t* out_host = nullptr;
   std::vector<void*> allocs;
 };
 
@@ -832,12 +854,14 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
       off += (bytes + 255) / 256 * 256;
       return o;
     };
+    // the rows that depend on the tree's shape first, the rest (fixed for a
+    // given batch, prefix and size) after them from off_prefix on
     c->off_anc = take(sizeof(uint64_t) * Mp);
+    c->off_token = take(sizeof(int32_t) * Mp);
+    c->off_parent = take(sizeof(int32_t) * Mp);
     c->off_prefix = take(sizeof(int32_t) * d.max_batch);
     c->off_nodes = take(sizeof(int32_t) * d.max_batch);
-    c->off_token = take(sizeof(int32_t) * Mp);
     c->off_pos = take(sizeof(int32_t) * Mp);
-    c->off_parent = take(sizeof(int32_t) * Mp);
     c->off_depth = take(sizeof(int32_t) * Mp);
     c->off_split = take(4 * sizeof(int32_t) * d.max_batch * c->attn_splits);
     c->off_nsplit = take(sizeof(int32_t) * d.max_batch);
@@ -1404,6 +1428,9 @@ void griffin_draft_free(griffin_draft* dc) {
   for (void* p : dc->allocs) hipFree(p);
   if (dc->topk_tok_host) hipHostFree(dc->topk_tok_host);
   if (dc->topk_lp_host) hipHostFree(dc->topk_lp_host);
+  if (dc->stage_host) hipHostFree(dc->stage_host);
+  if (dc->stage_ev) hipEventDestroy(dc->stage_ev);
+  if (dc->out_host) hipHostFree(dc->out_host);
   delete dc;
 }
 
@@ -1486,6 +1513,17 @@ int griffin_draft_init(const griffin_model_desc* desc, int32_t tgf_dim, float ln
             alloc((void**)&dc->topk_work, draft_topk_work_bytes(rows, desc->vocab)) &&
             hipHostMalloc((void**)&dc->topk_tok_host, 4LL * rows * 16, hipHostMallocDefault) == hipSuccess &&
             hipHostMalloc((void**)&dc->topk_lp_host, 4LL * rows * 16, hipHostMallocDefault) == hipSuccess;
+  dc->max_passes = std::min(desc->max_tree, desc->max_depth + 1);
+  const size_t tail = c->meta_bytes - c->off_prefix, out_words = desc->max_batch + 3LL * rows;
+  ok = ok && alloc((void**)&dc->c_tok, 4LL * desc->max_batch * DRAFT_SEL_MAX) &&
+       alloc((void**)&dc->c_node, 4LL * desc->max_batch * DRAFT_SEL_MAX) &&
+       alloc((void**)&dc->c_score, 8LL * desc->max_batch * DRAFT_SEL_MAX) &&
+       alloc((void**)&dc->n_cand, 4LL * rows) && alloc((void**)&dc->n_score, 8LL * rows) &&
+       alloc((void**)&dc->stage_dev, tail * dc->max_passes) && alloc((void**)&dc->out_dev, 4 * out_words) &&
+       hipHostMalloc((void**)&dc->stage_host, c->meta_bytes + tail * dc->max_passes, hipHostMallocDefault) ==
+           hipSuccess &&
+       hipHostMalloc((void**)&dc->out_host, 4 * out_words, hipHostMallocDefault) == hipSuccess &&
+       hipEventCreateWithFlags(&dc->stage_ev, hipEventDisableTiming) == hipSuccess;
   if (!ok) {
     griffin_draft_free(dc);
     return GRIFFIN_ENOMEM;
@@ -1593,88 +1631,113 @@ int griffin_draft_tree(griffin_draft* dc, int32_t batch, const int32_t* prefix_l
   const griffin_model_desc& d = c->d;
   const int T = d.max_tree;
   if (!prefix_len || !root_tokens || !root_features || !n_nodes_out || !tokens_out || !parents_out || batch < 1 ||
-      batch > d.max_batch || k < 1 || k > 16 || depth < 1 || n_total < 1)
+      batch > d.max_batch || k < 1 || k > 16 || k > d.vocab || depth < 1 || n_total < 1)
     return set_err(c, GRIFFIN_EINVAL, "bad draft tree arguments");
   if (1 + (long long)k * (depth - 1) > T || depth - 1 > d.max_depth)
     return set_err(c, GRIFFIN_ETREE, "1 + k * (depth - 1) expanded nodes must fit max_tree and max_depth");
   if (n_total + 1 > T) return set_err(c, GRIFFIN_ETREE, "n_total + 1 must fit max_tree");
-  struct Cand {
-    int depth, parent;  // parent: node of the pass tree that proposed it
-    int token;
-    double score;
-  };
-  std::vector<std::vector<int>> p_tok(batch), p_par(batch), p_cand(batch), frontier(batch);
-  std::vector<std::vector<double>> p_score(batch);
-  std::vector<std::vector<Cand>> cands(batch);
-  for (int b = 0; b < batch; ++b) {
-    p_tok[b] = {root_tokens[b]};
-    p_par[b] = {-1};
-    p_cand[b] = {-1};
-    p_score[b] = {0.0};
-    frontier[b] = {0};
+  // Pass t's tree has 1 + k t nodes: the root, then k nodes per depth (node
+  // i >= 1 at depth 1 + (i - 1) / k), whichever candidates they hold, so
+  // every pass's sizes, positions and attention split table are known here;
+  // only the tokens, parents and ancestor masks come from the device.
+  auto depth_of = [k](int i) { return i == 0 ? 0 : 1 + (i - 1) / k; };
+  const int n_last = 1 + k * (depth - 1);
+  {
+    std::vector<int32_t> tok(n_last, 0), par(n_last, -1);
+    for (int i = 1; i < n_last; ++i) par[i] = depth_of(i) == 1 ? 0 : 1 + k * (depth_of(i) - 2);
+    for (int b = 0; b < batch; ++b) {
+      tok[0] = root_tokens[b];
+      std::string why;
+      const int rc = prepare_tree(n_last, tok.data(), par.data(), prefix_len[b], T, d.max_depth, d.vocab,
+                                  d.kv_capacity, nullptr, nullptr, nullptr, &why);
+      if (rc != GRIFFIN_OK) return set_err(c, rc, "sequence " + std::to_string(b) + ": " + why);
+    }
   }
-  std::vector<int32_t> nn(batch), tok((size_t)batch * T, 0), par((size_t)batch * T, 0);
-  std::vector<int32_t> ktok((size_t)batch * T * k);
-  std::vector<float> klp((size_t)batch * T * k);
+  const size_t mb = c->meta_bytes, tail = mb - c->off_prefix;
+  HIP_TRY(c, hipEventSynchronize(dc->stage_ev));  // the previous call's copies out of the staging buffer
+  char* h0 = dc->stage_host;
+  memset(h0, 0, mb + tail * (depth - 1));
+  std::vector<int32_t> nn(batch);
   for (int t = 0; t < depth; ++t) {
+    // h + off_x addresses field x of pass t's metadata (fields from off_prefix on, for t > 0)
+    char* h = t == 0 ? h0 : h0 + mb + tail * (t - 1) - c->off_prefix;
+    auto* prefix = reinterpret_cast<int32_t*>(h + c->off_prefix);
+    auto* nodes = reinterpret_cast<int32_t*>(h + c->off_nodes);
+    auto* pos = reinterpret_cast<int32_t*>(h + c->off_pos);
+    auto* dep = reinterpret_cast<int32_t*>(h + c->off_depth);
     for (int b = 0; b < batch; ++b) {
-      nn[b] = (int)p_tok[b].size();
+      nn[b] = 1 + k * t;
+      prefix[b] = prefix_len[b];
+      nodes[b] = nn[b];
       for (int i = 0; i < nn[b]; ++i) {
-        tok[(size_t)b * T + i] = p_tok[b][i];
-        par[(size_t)b * T + i] = p_par[b][i];
+        dep[(size_t)b * T + i] = depth_of(i);
+        pos[(size_t)b * T + i] = prefix_len[b] + depth_of(i);
+      }
+      if (t == 0) {
+        reinterpret_cast<int32_t*>(h + c->off_token)[(size_t)b * T] = root_tokens[b];
+        reinterpret_cast<int32_t*>(h + c->off_parent)[(size_t)b * T] = 0;
+        reinterpret_cast<uint64_t*>(h + c->off_anc)[(size_t)b * T] = 1ull;
       }
     }
-    TRY(griffin_draft_step(dc, batch, prefix_len, nn.data(), tok.data(), par.data(), root_features, k, ktok.data(),
-                           klp.data()));
-    for (int b = 0; b < batch; ++b) {
-      std::vector<int> fresh;
-      for (int r : frontier[b])
-        for (int j = 0; j < k; ++j) {
-          const size_t at = ((size_t)b * T + r) * k + j;
-          cands[b].push_back({t + 1, r, ktok[at], p_score[b][r] + (double)klp[at]});
-          fresh.push_back((int)cands[b].size() - 1);
-        }
-      if (t + 1 == depth) continue;
-      auto& cb = cands[b];
-      std::stable_sort(fresh.begin(), fresh.end(), [&](int x, int y) { return cb[x].score > cb[y].score; });
-      frontier[b].clear();
-      for (int i = 0; i < k && i < (int)fresh.size(); ++i) {
-        const Cand& q = cb[fresh[i]];
-        p_tok[b].push_back(q.token);
-        p_par[b].push_back(q.parent);
-        p_cand[b].push_back(fresh[i]);
-        p_score[b].push_back(q.score);
-        frontier[b].push_back((int)p_tok[b].size() - 1);
-      }
-    }
+    attn_split_plan(batch, prefix_len, nn.data(), c->attn_splits, c->attn_sp,
+                    reinterpret_cast<int32_t*>(h + c->off_split), reinterpret_cast<int32_t*>(h + c->off_nsplit));
   }
-  for (int b = 0; b < batch; ++b) {
-    auto& cb = cands[b];
-    std::vector<int> chosen(cb.size());
-    for (size_t i = 0; i < cb.size(); ++i) chosen[i] = (int)i;
-    std::stable_sort(chosen.begin(), chosen.end(), [&](int x, int y) { return cb[x].score > cb[y].score; });
-    chosen.resize(std::min<size_t>(chosen.size(), n_total));
-    std::vector<int> rank(cb.size(), -1);
-    for (size_t i = 0; i < chosen.size(); ++i) rank[chosen[i]] = (int)i;
-    std::vector<int> order = chosen;
-    std::stable_sort(order.begin(), order.end(), [&](int x, int y) {
-      return cb[x].depth != cb[y].depth ? cb[x].depth < cb[y].depth : rank[x] < rank[y];
-    });
-    std::vector<int> index(cb.size(), -1);
-    for (size_t i = 0; i < order.size(); ++i) index[order[i]] = (int)i + 1;
-    int32_t* to = tokens_out + (size_t)b * T;
-    int32_t* po = parents_out + (size_t)b * T;
-    n_nodes_out[b] = 1 + (int)order.size();
-    to[0] = root_tokens[b];
-    po[0] = -1;
-    if (scores_out) scores_out[(size_t)b * T] = 0.f;
-    for (size_t i = 0; i < order.size(); ++i) {
-      const Cand& q = cb[order[i]];
-      const int pc = p_cand[b][q.parent];
-      to[i + 1] = q.token;
-      po[i + 1] = pc < 0 ? 0 : index[pc];
-      if (scores_out) scores_out[(size_t)b * T + i + 1] = (float)q.score;
+  HIP_TRY(c, hipMemcpyAsync(c->meta_dev, h0, mb, hipMemcpyHostToDevice, c->stream));
+  if (depth > 1)
+    HIP_TRY(c, hipMemcpyAsync(dc->stage_dev, h0 + mb, tail * (depth - 1), hipMemcpyHostToDevice, c->stream));
+  HIP_TRY(c, hipEventRecord(dc->stage_ev, c->stream));
+  HIP_TRY(c, hipMemcpyAsync(dc->root_feat, root_features, sizeof(float) * batch * dc->d, hipMemcpyDeviceToDevice,
+                            c->stream));
+  c->batch = batch;
+  c->stepped = false;
+  c->accepted = nullptr;
+  const int rows = batch * T, MT = d.max_batch * T;
+  DraftSelectArgs sa{};
+  sa.k = k;
+  sa.depth = depth;
+  sa.n_total = n_total;
+  sa.max_tree = T;
+  sa.topk_tok = dc->topk_tok;
+  sa.topk_lp = dc->topk_lp;
+  sa.c_tok = dc->c_tok;
+  sa.c_node = dc->c_node;
+  sa.c_score = dc->c_score;
+  sa.n_cand = dc->n_cand;
+  sa.n_score = dc->n_score;
+  sa.m_token = reinterpret_cast<int32_t*>(c->meta_dev + c->off_token);
+  sa.m_parent = reinterpret_cast<int32_t*>(c->meta_dev + c->off_parent);
+  sa.m_anc = reinterpret_cast<uint64_t*>(c->meta_dev + c->off_anc);
+  sa.tail_dst = reinterpret_cast<uint4*>(c->meta_dev + c->off_prefix);
+  sa.o_nodes = dc->out_dev;
+  sa.o_tok = dc->out_dev + d.max_batch;
+  sa.o_par = sa.o_tok + MT;
+  sa.o_score = reinterpret_cast<float*>(sa.o_par + MT);
+  // the whole expansion, every pass with its top-k and selection, is one graph
+  TRY(run_graph(c, {batch, dc->logits, false, k, depth, n_total, nullptr}, [&]() -> int {
+    for (int t = 0; t < depth; ++t) {
+      TRY(enqueue_pass(c, dc->logits));
+      HIP_TRY(c, launch_draft_topk(dc->logits, d.vocab, d.vocab, c->meta, rows, T, k, dc->topk_tok, dc->topk_lp,
+                                   dc->topk_work, c->stream));
+      sa.t = t;
+      const bool more = t + 1 < depth;
+      sa.tail_src = more ? reinterpret_cast<const uint4*>(dc->stage_dev + tail * t) : nullptr;
+      sa.tail_words = more ? (int)(tail / 16) : 0;
+      HIP_TRY(c, launch_draft_select(sa, batch, c->stream));
     }
+    return GRIFFIN_OK;
+  }));
+  HIP_TRY(c, hipMemcpyAsync(dc->out_host, dc->out_dev, sizeof(int32_t) * (d.max_batch + 3LL * MT),
+                            hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  const int32_t* o_tok = dc->out_host + d.max_batch;
+  const int32_t* o_par = o_tok + MT;
+  const float* o_score = reinterpret_cast<const float*>(o_par + MT);
+  for (int b = 0; b < batch; ++b) {
+    const int n = dc->out_host[b];
+    n_nodes_out[b] = n;
+    memcpy(tokens_out + (size_t)b * T, o_tok + (size_t)b * T, sizeof(int32_t) * n);
+    memcpy(parents_out + (size_t)b * T, o_par + (size_t)b * T, sizeof(int32_t) * n);
+    if (scores_out) memcpy(scores_out + (size_t)b * T, o_score + (size_t)b * T, sizeof(float) * n);
   }
   return GRIFFIN_OK;
 }

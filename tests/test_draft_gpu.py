@@ -235,6 +235,83 @@ def test_drafted_tree_matches_oracle_expansion(name):
         dr.close()
 
 
+def _host_expansion(dm, prefix, roots, feat, k, D, N):
+    """The tree expansion written out on the host over single draft passes
+    (griffin_draft_step), in fp64 with Python's stable sorts: each pass's
+    frontier proposes its top-k, a candidate scores its parent's score plus
+    its log-probability, the k best new candidates (ties: the earlier one)
+    are the next frontier, and the tree is the N best candidates numbered by
+    depth, then rank.  The pass trees are those griffin_draft_tree builds on
+    the device, so both see the same top-k values."""
+    B = len(roots)
+    ptok = [[int(r)] for r in roots]
+    ppar = [[-1] for _ in roots]
+    pcand = [[-1] for _ in roots]
+    pscore = [[0.0] for _ in roots]
+    front = [[0] for _ in roots]
+    cands = [[] for _ in roots]  # (depth, proposing pass-tree node, token, score)
+    for t in range(D):
+        trees = [gen.Tree(np.asarray(ptok[b], np.int32), np.asarray(ppar[b], np.int32)) for b in range(B)]
+        ktok, klp = dm.step(prefix, trees, feat, k)
+        for b in range(B):
+            fresh = []
+            for r in front[b]:
+                for j in range(k):
+                    cands[b].append((t + 1, r, int(ktok[b, r, j]), pscore[b][r] + float(klp[b, r, j])))
+                    fresh.append(len(cands[b]) - 1)
+            if t + 1 == D:
+                continue
+            fresh.sort(key=lambda i, cb=cands[b]: -cb[i][3])
+            front[b] = []
+            for i in fresh[:k]:
+                _, r, tk, s = cands[b][i]
+                ptok[b].append(tk)
+                ppar[b].append(r)
+                pcand[b].append(i)
+                pscore[b].append(s)
+                front[b].append(len(ptok[b]) - 1)
+    out = []
+    for b in range(B):
+        cb = cands[b]
+        chosen = sorted(range(len(cb)), key=lambda i: -cb[i][3])[:N]
+        rank = {c: i for i, c in enumerate(chosen)}
+        order = sorted(chosen, key=lambda i: (cb[i][0], rank[i]))
+        index = {c: i + 1 for i, c in enumerate(order)}
+        tok = [int(roots[b])] + [cb[i][2] for i in order]
+        par = [-1] + [0 if pcand[b][cb[i][1]] < 0 else index[pcand[b][cb[i][1]]] for i in order]
+        sc = np.asarray([0.0] + [cb[i][3] for i in order]).astype(np.float32)
+        out.append((tok, par, sc))
+    return out
+
+
+@pytest.mark.parametrize("name,k,D,N", [("tiny", None, None, None), ("tiny-v20000", None, None, None),
+                                        ("tiny", 16, 4, 63), ("tiny", 3, 6, 10), ("tiny", 2, 3, 50),
+                                        ("tiny", 1, 5, 3)])
+def test_device_expansion_equals_host_expansion_of_its_passes(name, k, D, N):
+    """griffin_draft_tree selects on the device; written out on the host over
+    the same passes, the selection must give the same tree bit for bit
+    (tokens, parents, float32 scores), including n_total above the candidate
+    count, the largest k, k = 1 and the single-node frontier of the first pass."""
+    B = 3
+    dr = Draft(name, B, [20, 61, 90])
+    try:
+        ds = dr.ds
+        k, D, N = k or ds.k, D or ds.depth, N or ds.n_total
+        roots = [5, 17, 29]
+        feat = dr.feat.cuda()
+        say(f"draft {name}: device vs host expansion k={k} depth={D} n_total={N}")
+        n, tok, par, sc = dr.dm.tree(dr.prefix, roots, feat, k, D, N)
+        ref = _host_expansion(dr.dm, dr.prefix, roots, feat, k, D, N)
+        for b in range(B):
+            rt, rp, rs = ref[b]
+            assert n[b] == len(rt), (b, n[b], len(rt))
+            assert tok[b, : n[b]].tolist() == rt, b
+            assert par[b, : n[b]].tolist() == rp, b
+            assert np.array_equal(sc[b, : n[b]], rs), b
+    finally:
+        dr.close()
+
+
 def test_draft_errors():
     import paper_2502_11018_amd as P
     dr = Draft("tiny", 1, [30], max_tree=16)
