@@ -88,10 +88,14 @@ GemmPlan plan_gemm(int epi, int n_out, int K, int experts = 1, int m_tiles = 1) 
   const int n_wgs = cdiv(n_blocks, p.wn);
   if (epi == EPI_STORE) {
     // split K so that the launch has ~kTargetWaves waves, preferring splits
-    // that divide the K steps (little or no zero padding)
+    // that divide the K steps (little or no zero padding), and at most one
+    // workgroup per CU: a launch just past a multiple of 256 workgroups
+    // leaves some CUs twice the bytes to stream (measured on the draft's
+    // 11008 x 8192 matrix: 2 splits, 172 workgroups, beat 3 and 4)
     const double want = (double)kTargetWaves / ((double)n_wgs * p.wn * experts);
+    const int cap = std::max(1, 256 / (n_wgs * experts));
     double best_cost = 1e30;
-    for (int s = 1; s <= std::max(1, p.ks / 2) && s <= 16; ++s) {
+    for (int s = 1; s <= std::max(1, p.ks / 2) && s <= 16 && s <= cap; ++s) {
       const int len = cdiv(p.ks, s);
       const double pad = (double)(len * s - p.ks) / p.ks;
       const double cost = std::fabs(std::log((double)s / std::max(want, 1.0))) + 8.0 * pad;
