@@ -434,11 +434,29 @@ __device__ __forceinline__ bool sel_before(double sa, int a, double sb, int b) {
   return sa > sb || (sa == sb && a < b);
 }
 
-constexpr int SEL_T = 256;
+constexpr int SEL_T = 1024;  // one thread per candidate of the last pass (four waves per SIMD)
+constexpr int SEL_U = 16;    // candidates compared per batch of LDS reads
+
+// Rank of candidate q (key s) among the n candidates keyed sc[0, n): how many
+// rank before it.  The reads are batched so that their LDS latencies overlap.
+__device__ __forceinline__ int sel_rank(const double* sc, int n, double s, int q) {
+  int rk = 0, o = 0;
+  for (; o + SEL_U <= n; o += SEL_U) {
+    double v[SEL_U];
+#pragma unroll
+    for (int u = 0; u < SEL_U; ++u) v[u] = sc[o + u];
+#pragma unroll
+    for (int u = 0; u < SEL_U; ++u) rk += sel_before(v[u], o + u, s, q);
+  }
+  for (; o < n; ++o) rk += sel_before(sc[o], o, s, q);
+  return rk;
+}
 
 __global__ __launch_bounds__(SEL_T) void draft_select_kernel(DraftSelectArgs a) {
   __shared__ double sc[DRAFT_SEL_MAX];  // ranking keys of the candidates
-  __shared__ int rank[DRAFT_SEL_MAX], slot[DRAFT_SEL_MAX];
+  __shared__ int slot[DRAFT_SEL_MAX];   // last pass: output row - 1 of a kept candidate, else -1
+  __shared__ int dep[DRAFT_SEL_MAX];    // last pass: depth of a candidate
+  __shared__ int kept[64], kdep[64];    // last pass: kept candidates by rank, their depths
   const int b = blockIdx.x, tid = threadIdx.x, k = a.k, T = a.max_tree, t = a.t;
   // the frontier of pass t: the root, or the k nodes the previous pass added
   const int f0 = t == 0 ? 0 : 1 + k * (t - 1), nf = (t == 0 ? 1 : k) * k;
@@ -457,9 +475,7 @@ __global__ __launch_bounds__(SEL_T) void draft_select_kernel(DraftSelectArgs a) 
     __syncthreads();
     // the k best fresh candidates become pass-tree nodes 1 + k t + rank
     for (int q = tid; q < nf; q += SEL_T) {
-      const double s = sc[c0 + q];
-      int rk = 0;
-      for (int o = 0; o < nf; ++o) rk += sel_before(sc[c0 + o], o, s, q);
+      const int rk = sel_rank(sc + c0, nf, sc[c0 + q], q);
       if (rk < k) {
         const int node = 1 + k * t + rk, r = f0 + q / k;
         a.n_cand[nb + node] = c0 + q;
@@ -473,34 +489,30 @@ __global__ __launch_bounds__(SEL_T) void draft_select_kernel(DraftSelectArgs a) 
     return;
   }
   // last pass: the n_total best of all candidates, numbered by depth, then rank
-  const int nc = c0 + nf;
-  for (int q = tid; q < c0; q += SEL_T) sc[q] = sel_key(a.c_score[cb + q]);
-  __syncthreads();
+  const int nc = c0 + nf, keep = min(nc, a.n_total);
   for (int q = tid; q < nc; q += SEL_T) {
-    const double s = sc[q];
-    int rk = 0;
-    for (int o = 0; o < nc; ++o) rk += sel_before(sc[o], o, s, q);
-    rank[q] = rk;
+    if (q < c0) sc[q] = sel_key(a.c_score[cb + q]);
+    dep[q] = q < k ? 1 : 2 + (q - k) / (k * k);
+    slot[q] = -1;
   }
   __syncthreads();
-  const int keep = min(nc, a.n_total);
-  auto depth_of = [&](int q) { return q < k ? 1 : 2 + (q - k) / (k * k); };
   for (int q = tid; q < nc; q += SEL_T) {
-    int at = -1;
-    if (rank[q] < keep) {
-      const int dq = depth_of(q), rq = rank[q];
-      at = 0;
-      for (int o = 0; o < nc; ++o) {
-        const int ro = rank[o], dout = depth_of(o);
-        at += ro < keep && (dout < dq || (dout == dq && ro < rq));
-      }
+    const int rk = sel_rank(sc, nc, sc[q], q);
+    if (rk < keep) {  // ranks are distinct
+      kept[rk] = q;
+      kdep[rk] = dep[q];
     }
-    slot[q] = at;
   }
   __syncthreads();
-  for (int q = tid; q < nc; q += SEL_T) {
-    const int at = slot[q];
-    if (at < 0) continue;
+  if (tid < keep) {
+    const int dq = kdep[tid];
+    int at = 0;
+    for (int j = 0; j < keep; ++j) at += kdep[j] < dq || (kdep[j] == dq && j < tid);
+    slot[kept[tid]] = at;
+  }
+  __syncthreads();
+  if (tid < keep) {
+    const int q = kept[tid], at = slot[q];
     const int r = a.c_node[cb + q];
     const int pc = r == 0 ? -1 : a.n_cand[nb + r];
     a.o_tok[nb + at + 1] = a.c_tok[cb + q];
@@ -517,7 +529,7 @@ __global__ __launch_bounds__(SEL_T) void draft_select_kernel(DraftSelectArgs a) 
 
 hipError_t launch_draft_select(const DraftSelectArgs& a, int batch, hipStream_t s) {
   if (a.k < 1 || a.k > DK || a.t < 0 || a.t >= a.depth || a.max_tree > 64 || 1 + a.k * (a.depth - 1) > a.max_tree ||
-      a.k * (1 + a.k * (a.depth - 1)) > DRAFT_SEL_MAX || batch < 1)
+      a.k * (1 + a.k * (a.depth - 1)) > DRAFT_SEL_MAX || a.n_total < 1 || a.n_total > 63 || batch < 1)
     return hipErrorInvalidValue;
   hipLaunchKernelGGL(draft_select_kernel, dim3(batch), dim3(SEL_T), 0, s, a);
   return hipGetLastError();
