@@ -405,11 +405,11 @@ int griffin_draft_tree(griffin_draft *draft, int32_t batch, const int32_t *prefi
 #define GRIFFIN_KC_ROPE 1    /* rotary embedding + tree K/V write */
 #define GRIFFIN_KC_ATTN 2    /* prefix attention: split-KV partials */
 #define GRIFFIN_KC_O 3       /* output projection GEMM */
-#define GRIFFIN_KC_NORM 4    /* residual update + RMSNorm (and embedding) */
+#define GRIFFIN_KC_NORM 4    /* residual update + RMSNorm (and embedding; MoE: routing and dispatch) */
 #define GRIFFIN_KC_GATE_UP 5 /* gate/up GEMM with SwiGLU (MoE: routed experts) */
 #define GRIFFIN_KC_DOWN 6    /* down GEMM (MoE: routed experts) */
 #define GRIFFIN_KC_LM_HEAD 7 /* LM head GEMM with per-tile argmax */
-#define GRIFFIN_KC_OTHER 8   /* argmax reduction, acceptance walk, MoE routing */
+#define GRIFFIN_KC_OTHER 8   /* argmax reduction, acceptance walk */
 #define GRIFFIN_KC_MERGE 9   /* split merge + ancestor (tree-key) attention */
 #define GRIFFIN_KC_COUNT 10
 

@@ -92,13 +92,20 @@ __device__ __forceinline__ void route_row(const Router& rt, int r, const float4 
   constexpr int EC = ROUTE_EC;
   __shared__ float part[RN_THREADS / 64][EC];
   __shared__ float logit[64];
+  __shared__ int dest[4];  // dispatch: the row's place (expert tile row) for each kept expert
+  __shared__ int kept[4];  // kept experts by rank, and their unnormalised probabilities
+  __shared__ float kept_p[4];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int b = r / rt.max_tree, i = r % rt.max_tree;
-  if (r >= rt.rows) return;  // padding row (uniform)
+  if (r >= rt.rows) {  // padding row (uniform)
+    if (rt.count && r < rt.padded_rows && tid < rt.top_k) rt.slot[r * rt.top_k + tid] = -1;
+    return;
+  }
   if (i >= rt.n_nodes[b]) {  // absent node (uniform)
     if (tid < rt.top_k) {
       rt.ids[r * rt.top_k + tid] = -1;
       rt.weights[r * rt.top_k + tid] = 0.f;
+      if (rt.count) rt.slot[r * rt.top_k + tid] = -1;
     }
     return;
   }
@@ -136,28 +143,55 @@ __device__ __forceinline__ void route_row(const Router& rt, int r, const float4 
   }
   __syncthreads();
   if (tid < rt.n_experts) rt.logits[(long long)r * rt.n_experts + tid] = logit[tid];
+  if (tid < 4) {  // every kept slot defined, whatever the logits hold
+    kept[tid] = 0;
+    kept_p[tid] = 0.f;
+  }
   __syncthreads();
-  if (tid == 0) {
-    float mx = -INFINITY;
-    for (int e = 0; e < rt.n_experts; ++e) mx = fmaxf(mx, logit[e]);
-    float* p = logit;  // probabilities (unnormalised) in place
-    for (int e = 0; e < rt.n_experts; ++e) p[e] = __expf(logit[e] - mx);
-    int chosen[4];
-    float ps[4], tot = 0.f;
-    for (int k = 0; k < rt.top_k; ++k) {
-      int best = -1;
-      for (int e = 0; e < rt.n_experts; ++e) {
-        bool used = false;
-        for (int q = 0; q < k; ++q) used |= chosen[q] == e;
-        if (!used && (best < 0 || p[e] > p[best])) best = e;
-      }
-      chosen[k] = best;
-      ps[k] = p[best];
-      tot += p[best];
+  if (tid < 64) {  // wave 0: softmax and top-k, one lane per expert
+    const int n = rt.n_experts;
+    const float lg = tid < n ? logit[tid] : -INFINITY;
+    const float mx = wave_max(lg);
+    const float p = tid < n ? __expf(lg - mx) : -1.f;  // unnormalised probability; -1 is never kept
+    // place of this expert in (probability descending, id ascending)
+    int rank = 0;
+    for (int e = 0; e < n; ++e) {
+      const float pe = __shfl(p, e, 64);
+      rank += pe > p || (pe == p && e < tid);
     }
+    if (tid < n && rank < rt.top_k) {
+      kept[rank] = tid;
+      kept_p[rank] = p;
+    }
+  }
+  __syncthreads();
+  if (tid < rt.top_k) {
+    float tot = 0.f;
+    for (int k = 0; k < rt.top_k; ++k) tot += kept_p[k];  // rank order
+    const int e = min(max(kept[tid], 0), rt.n_experts - 1);
+    rt.ids[r * rt.top_k + tid] = e;
+    rt.weights[r * rt.top_k + tid] = kept_p[tid] / tot;
+    if (rt.count) {
+      const int place = __hip_atomic_fetch_add(rt.count + e, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      // place < cap unless NaN logits kept one expert twice (then dropped)
+      const int row = place < rt.cap ? e * rt.cap + place : -1;
+      rt.slot[r * rt.top_k + tid] = row;
+      dest[tid] = row;
+    }
+  }
+  if (rt.count) {  // the row's packed operand to its place in each kept expert's tiles (uniform branch)
+    __syncthreads();
     for (int k = 0; k < rt.top_k; ++k) {
-      rt.ids[r * rt.top_k + k] = chosen[k];
-      rt.weights[r * rt.top_k + k] = ps[k] / tot;
+      const int row = dest[k];
+      if (row < 0) continue;  // uniform
+#pragma unroll
+      for (int u = 0; u < GPT; ++u)
+        if (ok[u]) {
+          const Hilo2 p0 = pack_hilo2(h[u].x, h[u].y), p1 = pack_hilo2(h[u].z, h[u].w);
+          uint16_t* dst = rt.xe + xpack_off(row, 4 * gi[u], rt.xe_ks);
+          *reinterpret_cast<uint2*>(dst) = make_uint2(p0.hi, p1.hi);
+          *reinterpret_cast<uint2*>(dst + XPACK_LO) = make_uint2(p0.lo, p1.lo);
+        }
     }
   }
 }
@@ -170,6 +204,7 @@ __global__ __launch_bounds__(RN_THREADS) void residual_rmsnorm_kernel(float* __r
                                                                       Router rt) {
   __shared__ float red[16];
   const int r = blockIdx.x;
+  if (rt.clear && r == 0 && threadIdx.x < rt.n_clear) rt.clear[threadIdx.x] = 0;
   float* __restrict__ xr = x + (long long)r * d;
   const float* __restrict__ parts = add.parts;
   const int groups = d >> 2;
@@ -269,6 +304,9 @@ hipError_t launch_residual_rmsnorm(float* x, const ResidualAdd& add, const uint1
                                    int d, uint16_t* xn, int xn_ks, hipStream_t s, const Router& rt) {
   if (d % 4 != 0 || d > 8 * RN_THREADS || add.n_parts > RN_SPLITS) return hipErrorInvalidValue;
   if (rt.w && (rt.n_experts < 1 || rt.n_experts > 64 || rt.top_k < 1 || rt.top_k > 4)) return hipErrorInvalidValue;
+  if (rt.count && (!rt.w || !rt.slot || !rt.xe || rt.padded_rows < rows || rt.cap < rt.padded_rows))
+    return hipErrorInvalidValue;
+  if (rt.clear && (rt.n_clear < 0 || rt.n_clear > RN_THREADS)) return hipErrorInvalidValue;
   if (add.parts == nullptr) return launch_rn<0>(x, add, gain, eps, rows, d, xn, xn_ks, s, rt);
   if (add.slot != nullptr) return launch_rn<-1>(x, add, gain, eps, rows, d, xn, xn_ks, s, rt);
   switch (add.n_parts) {
@@ -571,79 +609,6 @@ __global__ __launch_bounds__(256) void gather_rows_kernel(const float* __restric
 
 hipError_t launch_gather_rows(const float* x, int d, const int32_t* rows, int n, float* out, hipStream_t s) {
   hipLaunchKernelGGL(gather_rows_kernel, dim3(n), dim3(256), 0, s, x, d, rows, out);
-  return hipGetLastError();
-}
-
-// ------------------------------------------------------------ MoE router ----
-// For a valid row: h = RMSNorm(x) (fp32, from the fp32 residual), router
-// logits h . w_e in fp32, softmax, keep the top_k experts (ties to the lower
-// id), renormalise their probabilities.  Absent rows get expert id -1.
-// Per-expert row lists and the gather of the routed rows, in one launch.  The
-// c-th row routed to expert e (rows in ascending order: deterministic) is
-// found by every workgroup (e, c) itself from wave ballots over the route
-// ids, and its packed split-bf16 activations are copied to row c of expert
-// e's tiles.  Workgroup (e, 0) also writes count[e] and, for every (row, k)
-// routed to e, slot[row][k] = e * cap + the row's place in the list; expert
-// 0's writes slot = -1 for absent entries and for the padding rows.
-__global__ __launch_bounds__(256) void moe_dispatch_kernel(const int32_t* __restrict__ route_ids, int rows,
-                                                           int padded_rows, int top_k, int cap,
-                                                           const uint16_t* __restrict__ xn, int ks, int d,
-                                                           uint16_t* __restrict__ xe, int xe_tiles, int32_t* count,
-                                                           int32_t* slot) {
-  __shared__ int src_row;
-  const int e = blockIdx.y, c = blockIdx.x, tid = threadIdx.x;
-  if (tid < 64) {
-    const int lane = tid;
-    int base = 0, found = -1;
-    for (int q0 = 0; q0 < padded_rows; q0 += 64) {
-      const int r = q0 + lane;
-      int hit_k = -1;
-      bool absent = false;
-      if (r < rows) {
-        for (int k = 0; k < top_k; ++k) {
-          const int id = route_ids[r * top_k + k];
-          if (id == e) hit_k = k;
-          if (id < 0) absent = true;
-        }
-      }
-      const uint64_t m = __ballot(hit_k >= 0);
-      const int n = __popcll(m);
-      if (c == 0) {
-        const int pos = base + __popcll(m & ((1ull << lane) - 1ull));
-        if (hit_k >= 0) slot[r * top_k + hit_k] = e * cap + pos;
-        if (e == 0 && r < padded_rows && (r >= rows || absent))
-          for (int k = 0; k < top_k; ++k) slot[r * top_k + k] = -1;
-      }
-      if (found < 0 && c >= base && c < base + n) {
-        // the (c - base)-th set bit of m
-        uint64_t mm = m;
-        for (int j = 0; j < c - base; ++j) mm &= mm - 1ull;
-        found = q0 + __ffsll((unsigned long long)mm) - 1;
-      }
-      base += n;
-    }
-    if (lane == 0) {
-      src_row = found;
-      if (c == 0) count[e] = base;
-    }
-  }
-  __syncthreads();
-  const int src = src_row;
-  if (src < 0) return;  // fewer than c + 1 rows routed to e (uniform)
-  const long long dst_row = (long long)e * xe_tiles * 64 + c;
-  for (int k = tid * 8; k < d; k += blockDim.x * 8) {
-    const long long o = xpack_off(dst_row, k, ks), i = xpack_off(src, k, ks);
-    *reinterpret_cast<u32x4*>(xe + o) = *reinterpret_cast<const u32x4*>(xn + i);
-    *reinterpret_cast<u32x4*>(xe + o + XPACK_LO) = *reinterpret_cast<const u32x4*>(xn + i + XPACK_LO);
-  }
-}
-
-hipError_t launch_moe_dispatch(const int32_t* route_ids, int rows, int padded_rows, int n_experts, int top_k,
-                               int cap, const uint16_t* xn, int xn_ks, int d, uint16_t* xe, int xe_tiles,
-                               int32_t* count, int32_t* slot, hipStream_t s) {
-  if (padded_rows > cap) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(moe_dispatch_kernel, dim3(cap, n_experts), dim3(256), 0, s, route_ids, rows, padded_rows,
-                     top_k, cap, xn, xn_ks, d, xe, xe_tiles, count, slot);
   return hipGetLastError();
 }
 

@@ -116,6 +116,20 @@ struct Router {
   int32_t* ids;              // [rows][top_k]
   float* weights;            // [rows][top_k]
   float* logits;             // [rows][n_experts], the fp32 router logits (diagnostic)
+  // Dispatch of the routed rows to the experts' GEMM operands (count non-null):
+  // each row takes place = atomicAdd(count[e], 1) for each kept expert e, in
+  // arrival order (a row's expert output does not depend on its place), sets
+  // slot[r][k] = e * cap + place and copies its packed operand to row `place`
+  // of expert e's tiles xe (xe_ks K steps per tile).  Absent rows and the
+  // padding rows up to padded_rows get slot -1.  count starts at zero.
+  int32_t* count;            // [n_experts]
+  int32_t* slot;             // [padded_rows][top_k]
+  uint16_t* xe;              // [n_experts][cap / 64 tiles] packed split bf16
+  int xe_ks, cap, padded_rows;
+  // Counters this launch sets to zero (the next routed norm's), or null; may
+  // be given without routing (w null).
+  int32_t* clear;
+  int n_clear;
 };
 
 // fp32 copies of the tree nodes' K (after rotation) and V for the layer being
@@ -180,9 +194,6 @@ hipError_t launch_accept(StepMeta meta, const int32_t* pred, const int32_t* nan_
                          int max_tree, int max_depth, int32_t* result, hipStream_t s);
 // Per-expert row lists (count[e], slot[row][k]) and the gather of the routed
 // rows' packed activations into each expert's tiles, in one launch.
-hipError_t launch_moe_dispatch(const int32_t* route_ids, int rows, int padded_rows, int n_experts, int top_k,
-                               int cap, const uint16_t* xn, int xn_ks, int d, uint16_t* xe, int xe_tiles,
-                               int32_t* count, int32_t* slot, hipStream_t s);
 
 // Result block written by the acceptance kernel, per sequence b:
 // [0] accept_len, [1] nan flag, [2 .. 2+max_depth] tokens_out (max_depth+1),

@@ -328,8 +328,13 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
   ResidualAdd add_down{};
   for (int l = 0; l < d.n_layers; ++l) {
     // ---- attention block
+    Router clear{};  // MoE: this layer's expert counters start at zero
+    if (c->E > 1) {
+      clear.clear = c->count;
+      clear.n_clear = c->E;
+    }
     LAUNCH(GRIFFIN_KC_NORM, launch_residual_rmsnorm(c->x, l == 0 ? none : add_down, c->attn_norm[l], d.rms_eps,
-                                                    Mpad, d.d_model, c->xn, c->xd_ks, s));
+                                                    Mpad, d.d_model, c->xn, c->xd_ks, s, clear));
     {
       GemmArgs a = gemm_args(c->p_qkv, c->xn, c->xd_ks, c->pk_qkv[l], m_tiles, !c->act_bf16);
       a.out = c->parts;
@@ -392,6 +397,12 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
       route.ids = c->route_ids;
       route.weights = c->route_w;
       route.logits = c->router_logits + (long long)l * rows * c->E;
+      route.count = c->count;
+      route.slot = c->slot;
+      route.xe = c->xe;
+      route.xe_ks = c->xd_ks;
+      route.cap = Mpad;
+      route.padded_rows = Mpad;
     }
     LAUNCH(GRIFFIN_KC_NORM, launch_residual_rmsnorm(c->x, add_o, c->mlp_norm[l], d.rms_eps, Mpad, d.d_model, c->xn,
                                                     c->xd_ks, s, route));
@@ -414,9 +425,7 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
       add_down.n_parts = c->p_down.out_splits();
       add_down.part_stride = ps * d.d_model;
     } else {
-      const int xe_tiles = Mpad / 64;
-      LAUNCH(GRIFFIN_KC_OTHER, launch_moe_dispatch(c->route_ids, rows, Mpad, c->E, c->topk, Mpad, c->xn, c->xd_ks,
-                                                   d.d_model, c->xe, xe_tiles, c->count, c->slot, s));
+      const int xe_tiles = Mpad / 64;  // the routing norm filled count, slot and the experts' tiles
       GemmArgs g = gemm_args(c->p_gu, c->xe, c->xd_ks, c->pk_gu[l], m_tiles, !c->act_bf16);
       g.x_etiles = xe_tiles;
       g.count = c->count;
