@@ -407,23 +407,30 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
   const int t = blockIdx.y * blockDim.x + threadIdx.x;
   if (t >= Hq * quads) return;  // whole heads at a time (quads divides the block size)
   const int h = t / quads, d = (t % quads) * 4;
-  float4 out = make_float4(0.f, 0.f, 0.f, 0.f);
-  if (i < meta.n_nodes[b]) {  // uniform over the workgroup
-    // the sequence's key splits fill the first of the MAXS slots; the
-    // attention kernel marks the rest empty (m = -inf, l = 0)
-    const long long base = ((long long)b * Hq + h) * MAXS;
-    float ms[MAXS], ls[MAXS];
-    float4 os[MAXS];
+  // Every load that does not wait on another is issued first: the row's
+  // metadata, its q and all split partials (row slots of absent nodes are
+  // allocated, so these loads stay unconditional).
+  const int n_nodes = meta.n_nodes[b];
+  const int P = meta.prefix_len[b];
+  const int ns = RAGGED ? meta.n_split[b] : MAXS;
+  uint64_t anc = meta.anc[r];
+  // the sequence's key splits fill the first of the MAXS slots; the
+  // attention kernel marks the rest empty (m = -inf, l = 0)
+  const long long base = ((long long)b * Hq + h) * MAXS;
+  float ms[MAXS], ls[MAXS];
+  float4 os[MAXS];
 #pragma unroll
-    for (int s = 0; s < MAXS; ++s) {
-      const long long row = (base + s) * qrows + i;
-      ms[s] = part_ml[row * 2];
-      ls[s] = part_ml[row * 2 + 1];
-      os[s] = *reinterpret_cast<const float4*>(part_o + row * dh + d);
-    }
+  for (int s = 0; s < MAXS; ++s) {
+    const long long row = (base + s) * qrows + i;
+    ms[s] = part_ml[row * 2];
+    ls[s] = part_ml[row * 2 + 1];
+    os[s] = *reinterpret_cast<const float4*>(part_o + row * dh + d);
+  }
+  const long long qo = ((long long)r * Hq + h) * dh + d;
+  const uint2 qh = *reinterpret_cast<const uint2*>(q + qo), ql = *reinterpret_cast<const uint2*>(q_lo + qo);
+  float4 out = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (i < n_nodes) {  // uniform over the workgroup
     const int hk = h / (Hq / Hkv);
-    const long long qo = ((long long)r * Hq + h) * dh + d;
-    const uint2 qh = *reinterpret_cast<const uint2*>(q + qo), ql = *reinterpret_cast<const uint2*>(q_lo + qo);
     const float q0 = bf16_to_f32(qh.x & 0xffff) + bf16_to_f32(ql.x & 0xffff);
     const float q1 = bf16_to_f32(qh.x >> 16) + bf16_to_f32(ql.x >> 16);
     const float q2 = bf16_to_f32(qh.y & 0xffff) + bf16_to_f32(ql.y & 0xffff);
@@ -432,8 +439,6 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
     // (m, l, o) over the split's prefix keys in fp32 from the bf16 cache, with
     // an exact running maximum
     {
-      const int P = meta.prefix_len[b];
-      const int ns = RAGGED ? meta.n_split[b] : MAXS;
       const int nblk = (P + 31) >> 5;
       const uint16_t* kh = prefix.k + ((long long)b * Hkv + hk) * prefix.kv_cap * dh + d;
       const uint16_t* vh = prefix.v + ((long long)b * Hkv + hk) * prefix.kv_cap * dh;
@@ -467,7 +472,6 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
     // tree keys
     const float* tk = tree.k + ((long long)b * Hkv + hk) * max_tree * dh + d;
     const float* tv = tree.v + ((long long)b * Hkv + hk) * max_tree * dh + d;
-    uint64_t anc = meta.anc[r];
     float mt = -INFINITY, lt = 0.f;
     float4 ot = make_float4(0.f, 0.f, 0.f, 0.f);
     constexpr int TB = 8;  // ancestors per batch: all their loads are issued before any is used

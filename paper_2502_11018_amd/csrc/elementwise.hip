@@ -218,6 +218,9 @@ __global__ __launch_bounds__(RN_THREADS) void residual_rmsnorm_kernel(float* __r
     gi[u] = ok[u] ? g : groups - 1;  // clamped: loads stay unconditional
     v[u] = reinterpret_cast<const float4*>(xr)[gi[u]];
   }
+  uint2 gg[GPT];  // gains, in flight with the row
+#pragma unroll
+  for (int u = 0; u < GPT; ++u) gg[u] = *reinterpret_cast<const uint2*>(gain + 4 * gi[u]);
   uint2 w0[ROUTE_EC][GPT];  // MoE: the first router weights, in flight during the norm
   if (rt.w) route_load<GPT>(rt, 0, d, gi, w0);
   if constexpr (NP > 0) {
@@ -266,10 +269,9 @@ __global__ __launch_bounds__(RN_THREADS) void residual_rmsnorm_kernel(float* __r
 #pragma unroll
   for (int u = 0; u < GPT; ++u) {
     if (ok[u]) {
-      const uint2 gg = *reinterpret_cast<const uint2*>(gain + 4 * gi[u]);
       const float4 a = v[u];
-      const Hilo2 p0 = pack_hilo2(a.x * rs * bf16_to_f32(gg.x & 0xffff), a.y * rs * bf16_to_f32(gg.x >> 16));
-      const Hilo2 p1 = pack_hilo2(a.z * rs * bf16_to_f32(gg.y & 0xffff), a.w * rs * bf16_to_f32(gg.y >> 16));
+      const Hilo2 p0 = pack_hilo2(a.x * rs * bf16_to_f32(gg[u].x & 0xffff), a.y * rs * bf16_to_f32(gg[u].x >> 16));
+      const Hilo2 p1 = pack_hilo2(a.z * rs * bf16_to_f32(gg[u].y & 0xffff), a.w * rs * bf16_to_f32(gg[u].y >> 16));
       uint16_t* dst = xn + xpack_off(r, 4 * gi[u], xn_ks);  // fragment-packed split-bf16 GEMM operand
       *reinterpret_cast<uint2*>(dst) = make_uint2(p0.hi, p1.hi);
       *reinterpret_cast<uint2*>(dst + XPACK_LO) = make_uint2(p0.lo, p1.lo);
@@ -278,11 +280,9 @@ __global__ __launch_bounds__(RN_THREADS) void residual_rmsnorm_kernel(float* __r
   if (rt.w) {  // MoE: route the row from its normed fp32 values (uniform branch)
     float4 h[GPT];
 #pragma unroll
-    for (int u = 0; u < GPT; ++u) {
-      const uint2 gg = *reinterpret_cast<const uint2*>(gain + 4 * gi[u]);
-      h[u] = make_float4(v[u].x * rs * bf16_to_f32(gg.x & 0xffff), v[u].y * rs * bf16_to_f32(gg.x >> 16),
-                         v[u].z * rs * bf16_to_f32(gg.y & 0xffff), v[u].w * rs * bf16_to_f32(gg.y >> 16));
-    }
+    for (int u = 0; u < GPT; ++u)
+      h[u] = make_float4(v[u].x * rs * bf16_to_f32(gg[u].x & 0xffff), v[u].y * rs * bf16_to_f32(gg[u].x >> 16),
+                         v[u].z * rs * bf16_to_f32(gg[u].y & 0xffff), v[u].w * rs * bf16_to_f32(gg[u].y >> 16));
     route_row<GPT>(rt, r, h, gi, ok, d, w0);
   }
 }
@@ -328,86 +328,90 @@ hipError_t launch_residual_rmsnorm(float* x, const ResidualAdd& add, const uint1
 // prefix_len[b] + i (k row-major per slot, v transposed: one row per dim),
 // and fp32 copies of the tree K/V for the attention merge.
 // q is kept as split bf16: q_out holds bf16(q), q_lo the bf16 residual.
+// The rotation angle pos * inv_freq[j] and its cosine and sine are evaluated
+// in fp64 and rounded to fp32 (inv_freq[j] = base^(-2j/dh), fp64), so no load
+// waits on the node's position; the row's metadata and partials are all
+// loaded before any is used.
 template <int NP>
-__global__ __launch_bounds__(256) void qkv_rope_kernel(const float* __restrict__ parts, int n_parts_unused,
-                                                       long long part_stride, StepMeta meta,
-                                                       const float* __restrict__ rcos,
-                                                       const float* __restrict__ rsin, int Hq, int Hkv,
-                                                       int dh, int max_tree, int kv_cap,
+__global__ __launch_bounds__(256) void qkv_rope_kernel(const float* __restrict__ parts, long long part_stride,
+                                                       StepMeta meta, const double* __restrict__ inv_freq,
+                                                       int Hq, int Hkv, int dh, int max_tree, int kv_cap,
                                                        uint16_t* __restrict__ q_out, uint16_t* __restrict__ q_lo,
                                                        uint16_t* __restrict__ kc, uint16_t* __restrict__ vc,
                                                        TreeKV32 tree) {
   const int r = blockIdx.x;
   const int b = r / max_tree, i = r % max_tree;
-  if (i >= meta.n_nodes[b]) return;
   const int half = dh >> 1;
   const int heads = Hq + 2 * Hkv;
   const int width = heads * dh;
+  const int t = blockIdx.y * blockDim.x + threadIdx.x;  // one (head, rotation pair) per thread
+  const bool live = t < heads * half;
+  const int tt = live ? t : 0;  // clamped: loads stay unconditional
+  const int h = tt / half, j = tt % half;
+  const int c1 = h * dh + j, c2 = c1 + half;
+  const int n_nodes = meta.n_nodes[b];
   const int pos = meta.pos[r];
   const int P = meta.prefix_len[b];
-  const int slot = P + i;
+  const double inv = inv_freq[j];
   const float* __restrict__ row = parts + (long long)r * width;
-  const int t = blockIdx.y * blockDim.x + threadIdx.x;  // one (head, rotation pair) per thread
-  if (t < heads * half) {
-    const int h = t / half, j = t % half;
-    const int c1 = h * dh + j, c2 = c1 + half;
-    (void)n_parts_unused;
-    float a1[NP], a2[NP];  // all K-split partials loaded before any is summed
+  float a1[NP], a2[NP];  // all K-split partials loaded before any is summed
 #pragma unroll
-    for (int s = 0; s < NP; ++s) {
-      a1[s] = row[s * part_stride + c1];
-      a2[s] = row[s * part_stride + c2];
-    }
-    float x1 = 0.f, x2 = 0.f;
+  for (int s = 0; s < NP; ++s) {
+    a1[s] = row[s * part_stride + c1];
+    a2[s] = row[s * part_stride + c2];
+  }
+  if (i >= n_nodes || !live) return;
+  const int slot = P + i;
+  float x1 = 0.f, x2 = 0.f;
 #pragma unroll
-    for (int s = 0; s < NP; ++s) {
-      x1 += a1[s];
-      x2 += a2[s];
-    }
-    if (h < Hq + Hkv) {
-      const float c = rcos[(long long)pos * half + j], sn = rsin[(long long)pos * half + j];
-      const float y1 = x1 * c - x2 * sn;
-      const float y2 = x2 * c + x1 * sn;
-      if (h < Hq) {
-        const long long o = ((long long)r * Hq + h) * dh;
-        const uint16_t h1 = f32_to_bf16(y1), h2 = f32_to_bf16(y2);
-        q_out[o + j] = h1;
-        q_out[o + j + half] = h2;
-        q_lo[o + j] = f32_to_bf16(y1 - bf16_to_f32(h1));
-        q_lo[o + j + half] = f32_to_bf16(y2 - bf16_to_f32(h2));
-      } else {
-        uint16_t* k = kc + (((long long)b * Hkv + (h - Hq)) * kv_cap + slot) * dh;
-        k[j] = f32_to_bf16(y1);
-        k[j + half] = f32_to_bf16(y2);
-        float* k32 = tree.k + (((long long)b * Hkv + (h - Hq)) * max_tree + i) * dh;
-        k32[j] = y1;
-        k32[j + half] = y2;
-      }
+  for (int s = 0; s < NP; ++s) {
+    x1 += a1[s];
+    x2 += a2[s];
+  }
+  if (h < Hq + Hkv) {
+    double sd, cd;
+    sincos((double)pos * inv, &sd, &cd);
+    const float c = (float)cd, sn = (float)sd;
+    const float y1 = x1 * c - x2 * sn;
+    const float y2 = x2 * c + x1 * sn;
+    if (h < Hq) {
+      const long long o = ((long long)r * Hq + h) * dh;
+      const uint16_t h1 = f32_to_bf16(y1), h2 = f32_to_bf16(y2);
+      q_out[o + j] = h1;
+      q_out[o + j + half] = h2;
+      q_lo[o + j] = f32_to_bf16(y1 - bf16_to_f32(h1));
+      q_lo[o + j + half] = f32_to_bf16(y2 - bf16_to_f32(h2));
     } else {
-      // 32-slot tiles, transposed within the tile: [tile][dim][32]
-      uint16_t* v = vc + ((long long)b * Hkv + (h - Hq - Hkv)) * dh * kv_cap + (long long)(slot >> 5) * dh * 32 +
-                    (slot & 31);
-      v[j * 32] = f32_to_bf16(x1);
-      v[(j + half) * 32] = f32_to_bf16(x2);
-      float* v32 = tree.v + (((long long)b * Hkv + (h - Hq - Hkv)) * max_tree + i) * dh;
-      v32[j] = x1;
-      v32[j + half] = x2;
+      uint16_t* k = kc + (((long long)b * Hkv + (h - Hq)) * kv_cap + slot) * dh;
+      k[j] = f32_to_bf16(y1);
+      k[j + half] = f32_to_bf16(y2);
+      float* k32 = tree.k + (((long long)b * Hkv + (h - Hq)) * max_tree + i) * dh;
+      k32[j] = y1;
+      k32[j + half] = y2;
     }
+  } else {
+    // 32-slot tiles, transposed within the tile: [tile][dim][32]
+    uint16_t* v = vc + ((long long)b * Hkv + (h - Hq - Hkv)) * dh * kv_cap + (long long)(slot >> 5) * dh * 32 +
+                  (slot & 31);
+    v[j * 32] = f32_to_bf16(x1);
+    v[(j + half) * 32] = f32_to_bf16(x2);
+    float* v32 = tree.v + (((long long)b * Hkv + (h - Hq - Hkv)) * max_tree + i) * dh;
+    v32[j] = x1;
+    v32[j + half] = x2;
   }
 }
 
 hipError_t launch_qkv_rope(const float* qkv_parts, int n_parts, long long part_stride, StepMeta meta,
-                           const float* rope_cos, const float* rope_sin, int Hq, int Hkv, int dh, int max_tree,
-                           int batch, int kv_cap, uint16_t* q_out, uint16_t* q_lo, uint16_t* k_cache_l,
-                           uint16_t* v_cache_l, TreeKV32 tree, hipStream_t s) {
+                           const double* inv_freq, int Hq, int Hkv, int dh, int max_tree, int batch, int kv_cap,
+                           uint16_t* q_out, uint16_t* q_lo, uint16_t* k_cache_l, uint16_t* v_cache_l, TreeKV32 tree,
+                           hipStream_t s) {
   const int items = (Hq + 2 * Hkv) * (dh / 2);
   const dim3 grid(batch * max_tree, (items + 255) / 256);
   switch (n_parts) {
-#define GRIFFIN_ROPE_CASE(n)                                                                                   \
-  case n:                                                                                                     \
-    hipLaunchKernelGGL(qkv_rope_kernel<n>, grid, dim3(256), 0, s, qkv_parts, n_parts, part_stride, meta, rope_cos, \
-                       rope_sin, Hq, Hkv, dh, max_tree, kv_cap, q_out, q_lo, k_cache_l, v_cache_l, \
-                       tree);                    \
+#define GRIFFIN_ROPE_CASE(n)                                                                                     \
+  case n:                                                                                                       \
+    hipLaunchKernelGGL(qkv_rope_kernel<n>, grid, dim3(256), 0, s, qkv_parts, part_stride, meta, inv_freq, Hq,     \
+                       Hkv, dh, max_tree, kv_cap, q_out, q_lo, k_cache_l, v_cache_l, tree);                     \
     break;
     GRIFFIN_ROPE_CASE(1) GRIFFIN_ROPE_CASE(2) GRIFFIN_ROPE_CASE(3) GRIFFIN_ROPE_CASE(4) GRIFFIN_ROPE_CASE(5)
     GRIFFIN_ROPE_CASE(6) GRIFFIN_ROPE_CASE(7) GRIFFIN_ROPE_CASE(8) GRIFFIN_ROPE_CASE(9) GRIFFIN_ROPE_CASE(10)

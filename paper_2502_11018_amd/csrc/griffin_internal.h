@@ -171,10 +171,11 @@ hipError_t launch_embed(const uint16_t* embed, const int32_t* token, int rows, i
 hipError_t launch_residual_rmsnorm(float* x, const ResidualAdd& add, const uint16_t* gain, float eps,
                                    int rows, int d, uint16_t* xn, int xn_ks, hipStream_t s,
                                    const Router& route = Router{});
+// inv_freq: [dh / 2] fp64 rotary frequencies base^(-2j/dh)
 hipError_t launch_qkv_rope(const float* qkv_parts, int n_parts, long long part_stride, StepMeta meta,
-                           const float* rope_cos, const float* rope_sin, int Hq, int Hkv, int dh,
-                           int max_tree, int batch, int kv_cap, uint16_t* q_out, uint16_t* q_lo,
-                           uint16_t* k_cache_l, uint16_t* v_cache_l, TreeKV32 tree, hipStream_t s);
+                           const double* inv_freq, int Hq, int Hkv, int dh, int max_tree, int batch, int kv_cap,
+                           uint16_t* q_out, uint16_t* q_lo, uint16_t* k_cache_l, uint16_t* v_cache_l, TreeKV32 tree,
+                           hipStream_t s);
 hipError_t launch_attention(const AttnArgs& a, int batch, hipStream_t s);
 constexpr int ATTN_RING = 4;  // 32-key K/V blocks in flight per attention workgroup
 int attn_waves(int group);    // waves (query heads) per attention workgroup

@@ -142,8 +142,8 @@ struct griffin_ctx {
 
   std::vector<void*> allocs;
   float *x = nullptr, *parts = nullptr, *attn_po = nullptr, *attn_pml = nullptr;
-  float *rope_cos = nullptr, *rope_sin = nullptr, *pmax = nullptr, *pmax2 = nullptr, *route_w = nullptr,
-        *yslots = nullptr;
+  float *pmax = nullptr, *pmax2 = nullptr, *route_w = nullptr, *yslots = nullptr;
+  double* rope_inv = nullptr;      // [head_dim / 2] rotary frequencies base^(-2j/dh), fp64
   float* margin = nullptr;         // [Mpad] top-2 logit margin of every row
   float* margin_host = nullptr;    // pinned copy for griffin_read_margins
   float* router_logits = nullptr;  // MoE: [n_layers][max_batch * max_tree][E] fp32, the last pass's
@@ -345,9 +345,9 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
     }
     uint16_t* kc = c->k_cache + (size_t)l * layer_kv;
     uint16_t* vc = c->v_cache + (size_t)l * layer_kv;
-    LAUNCH(GRIFFIN_KC_ROPE, launch_qkv_rope(c->parts, c->p_qkv.out_splits(), ps * c->qkv_n, c->meta, c->rope_cos,
-                                            c->rope_sin, d.n_q_heads, d.n_kv_heads, d.head_dim, d.max_tree, B,
-                                            d.kv_capacity, c->q, c->q_lo, kc, vc, c->tree, s));
+    LAUNCH(GRIFFIN_KC_ROPE, launch_qkv_rope(c->parts, c->p_qkv.out_splits(), ps * c->qkv_n, c->meta, c->rope_inv,
+                                            d.n_q_heads, d.n_kv_heads, d.head_dim, d.max_tree, B, d.kv_capacity,
+                                            c->q, c->q_lo, kc, vc, c->tree, s));
     if (c->kv_only && l == d.n_layers - 1) return GRIFFIN_OK;
     {
       AttnArgs a{};
@@ -788,8 +788,7 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
   ALLOC(c->samp_scratch, sampled_scratch_bytes(d.max_batch, d.max_tree, d.vocab));
   ALLOC(c->samp_u, 5LL * d.max_batch * d.max_tree);
   ALLOC(c->samp_result, (long long)d.max_batch * result_stride(d.max_depth));
-  ALLOC(c->rope_cos, (long long)d.kv_capacity * (d.head_dim / 2));
-  ALLOC(c->rope_sin, (long long)d.kv_capacity * (d.head_dim / 2));
+  ALLOC(c->rope_inv, d.head_dim / 2);
   if (moe) {
     ALLOC(c->route_ids, Mp * c->topk);
     ALLOC(c->route_w, Mp * c->topk);
@@ -839,20 +838,13 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
     }
   }
 
-  // rotary tables: angle pos * base^(-2j/dh) evaluated in double, stored fp32
+  // rotary frequencies base^(-2j/dh) in fp64; the kernel forms the angle
+  // pos * inv in fp64 and rounds its cosine and sine to fp32
   {
     const int half = d.head_dim / 2;
-    std::vector<float> cs((size_t)d.kv_capacity * half), sn((size_t)d.kv_capacity * half);
-    for (int j = 0; j < half; ++j) {
-      const double inv = std::pow(d.rope_base, -2.0 * j / d.head_dim);
-      for (int p = 0; p < d.kv_capacity; ++p) {
-        const double ang = (double)p * inv;
-        cs[(size_t)p * half + j] = (float)std::cos(ang);
-        sn[(size_t)p * half + j] = (float)std::sin(ang);
-      }
-    }
-    hipError_t e = hipMemcpy(c->rope_cos, cs.data(), cs.size() * sizeof(float), hipMemcpyHostToDevice);
-    if (e == hipSuccess) e = hipMemcpy(c->rope_sin, sn.data(), sn.size() * sizeof(float), hipMemcpyHostToDevice);
+    std::vector<double> inv(half);
+    for (int j = 0; j < half; ++j) inv[j] = std::pow(d.rope_base, -2.0 * j / d.head_dim);
+    hipError_t e = hipMemcpy(c->rope_inv, inv.data(), inv.size() * sizeof(double), hipMemcpyHostToDevice);
     if (e != hipSuccess) {
       griffin_verify_free(c);
       return GRIFFIN_EHIP;
