@@ -133,6 +133,7 @@ def write_prefix(k_cache: torch.Tensor, v_cache: torch.Tensor, shape, max_batch:
     P = k.shape[1]
     full, rem = divmod(P, 32)
     tiles = v_cache.view(shape.n_layers, max_batch, Hkv, kv_capacity // 32, dh, 32)[layer, seq]
+    stream.wait_stream(torch.cuda.current_stream(k.device))  # k, v may still be in flight on the caller's stream
     with torch.cuda.stream(stream):
         k_cache.view(shape.n_layers, max_batch, Hkv, kv_capacity, dh)[layer, seq, :, :P, :].copy_(k)
         if full:
@@ -186,6 +187,9 @@ class TreeVerifier:
                            cast(self._arrays["mlp_norm"]), cast(self._arrays["w_gate_up"]),
                            cast(self._arrays["w_down"]), cast(self._arrays["w_router"]))
         self.ctx = c_void_p()
+        # init repacks the weights on the library's stream: order it after the
+        # caller's stream, where the weights and caches were produced
+        self.stream.wait_stream(torch.cuda.current_stream(dev))
         rc = N.lib.griffin_verify_init(byref(self.desc), byref(self.w), k_cache.data_ptr(), v_cache.data_ptr(),
                                        c_void_p(self.stream.cuda_stream), byref(self.ctx))
         _check(rc, "griffin_verify_init")
@@ -221,6 +225,8 @@ class TreeVerifier:
                     logits_out.numel() < B * self.max_tree * self.shape.vocab:
                 raise ValueError("logits_out must be contiguous fp32 [B*max_tree, vocab]")
             lp = c_void_p(logits_out.data_ptr())
+            # the caller may have touched the buffer on its own stream
+            self.stream.wait_stream(torch.cuda.current_stream(logits_out.device))
         rc = N.lib.griffin_verify_step(self.ctx, B, _p32(pl), _p32(nn), _p32(tk), _p32(pa), lp)
         _check(rc, "griffin_verify_step", self.ctx)
         self._batch = B

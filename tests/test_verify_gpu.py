@@ -27,7 +27,7 @@ def _lib():
 class Setup:
     """Weights on both sides, prefix caches, oracle results and a verifier."""
 
-    def __init__(self, name, n_trees, max_tree=64, max_depth=None, kv_extra=0):
+    def __init__(self, name, n_trees, max_tree=64, max_depth=None, kv_extra=0, stream=None):
         P = _lib()
         self.w = get_workload(name)
         m = self.w.model
@@ -46,7 +46,7 @@ class Setup:
                       for i in range(n_trees)]
         say(f"{name}: init verifier cap={self.cap} max_tree={max_tree}")
         self.v = P.TreeVerifier(m, self.mw_gpu, max_batch=self.w.batch, max_tree=max_tree,
-                                max_depth=self.max_depth, kv_capacity=self.cap)
+                                max_depth=self.max_depth, kv_capacity=self.cap, stream=stream)
         for b, kv in enumerate(self.kvs):
             for l in range(m.n_layers):
                 self.v.write_prefix(l, b, torch.from_numpy(kv.K[l]).to(torch.bfloat16).to(self.dev),
@@ -342,7 +342,9 @@ def test_graph_replay_matches_plain_launches():
     launches, on every replay, with plain steps and synchronisations between
     the replays and two graph keys (batch sizes) in use."""
     name = "small-gqa"
-    s = Setup(name, n_trees=3)
+    # a stream of its own: the library captures and replays graphs only on a
+    # non-default stream
+    s = Setup(name, n_trees=3, stream=torch.cuda.Stream())
     try:
         m = s.w.model
         B = s.w.batch
