@@ -35,7 +35,7 @@ hipError_t launch_embed(const uint16_t* embed, const int32_t* token, int rows, i
 // of dense partials NP is a template parameter so that every load of the row
 // is issued before the first one is waited on (no branches between loads);
 // NP < 0 selects the MoE form (per-row expert slots).
-constexpr int RN_THREADS = 1024;
+constexpr int RN_THREADS = 1024;  // measured against 256 and 512 (one row per workgroup either way)
 constexpr int RN_SPLITS = 16;  // K-split partials per residual update
 
 __device__ __forceinline__ void add4(float4& a, const float4& p) {
@@ -290,19 +290,21 @@ __global__ __launch_bounds__(RN_THREADS) void residual_rmsnorm_kernel(float* __r
 template <int NP>
 static hipError_t launch_rn(float* x, const ResidualAdd& add, const uint16_t* gain, float eps, int rows, int d,
                             uint16_t* xn, int xn_ks, hipStream_t s, const Router& rt) {
-  const int groups = d / 4;
-  if (groups <= RN_THREADS)
-    hipLaunchKernelGGL((residual_rmsnorm_kernel<NP, 1>), dim3(rows), dim3(RN_THREADS), 0, s, x, add, gain, eps, d,
-                       xn, xn_ks, rt);
-  else
-    hipLaunchKernelGGL((residual_rmsnorm_kernel<NP, 2>), dim3(rows), dim3(RN_THREADS), 0, s, x, add, gain, eps, d,
-                       xn, xn_ks, rt);
+  const int gpt = (d / 4 + RN_THREADS - 1) / RN_THREADS;  // float4 groups per thread
+#define GRIFFIN_RN_LAUNCH(G)                                                                                    \
+  hipLaunchKernelGGL((residual_rmsnorm_kernel<NP, G>), dim3(rows), dim3(RN_THREADS), 0, s, x, add, gain, eps, d, \
+                     xn, xn_ks, rt)
+  if (gpt <= 1) GRIFFIN_RN_LAUNCH(1);
+  else if (gpt <= 2) GRIFFIN_RN_LAUNCH(2);
+  else if (gpt <= 4) GRIFFIN_RN_LAUNCH(4);
+  else GRIFFIN_RN_LAUNCH(8);
+#undef GRIFFIN_RN_LAUNCH
   return hipGetLastError();
 }
 
 hipError_t launch_residual_rmsnorm(float* x, const ResidualAdd& add, const uint16_t* gain, float eps, int rows,
                                    int d, uint16_t* xn, int xn_ks, hipStream_t s, const Router& rt) {
-  if (d % 4 != 0 || d > 8 * RN_THREADS || add.n_parts > RN_SPLITS) return hipErrorInvalidValue;
+  if (d % 4 != 0 || d > 32 * RN_THREADS || d > 32768 || add.n_parts > RN_SPLITS) return hipErrorInvalidValue;
   if (rt.w && (rt.n_experts < 1 || rt.n_experts > 64 || rt.top_k < 1 || rt.top_k > 4)) return hipErrorInvalidValue;
   if (rt.count && (!rt.w || !rt.slot || !rt.xe || rt.padded_rows < rows || rt.cap < rt.padded_rows))
     return hipErrorInvalidValue;
