@@ -90,21 +90,25 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, f32x16 (&acc)[N
                                                               acc[b][mb][4 * rg + 2], acc[b][mb][4 * rg + 3]);
         }
     } else if constexpr (EPI == EPI_SWIGLU) {
-      static_assert(EPI != EPI_SWIGLU || NB == 2, "SwiGLU pairs one gate and one up block");
+      // blocks [0, NB/2) hold gate rows, block b + NB/2 the up rows of block b
+      static_assert(EPI != EPI_SWIGLU || NB % 2 == 0, "SwiGLU pairs gate and up blocks");
+      constexpr int HB = NB / 2;
       if (!row_ok) continue;
 #pragma unroll
-      for (int rg = 0; rg < 4; ++rg) {
-        const int n = (wg * WN + wc) * 32 + 8 * rg + 4 * g;
-        if (n < a.N) {
-          float h[4];
+      for (int hb = 0; hb < HB; ++hb)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) h[i] = silu_f32(acc[0][mb][4 * rg + i]) * acc[NB - 1][mb][4 * rg + i];
-          uint16_t* dst = a.act + xpack_off(orow, n, a.act_ks);
-          const Hilo2 p0 = pack_hilo2(h[0], h[1]), p1 = pack_hilo2(h[2], h[3]);
-          *reinterpret_cast<uint2*>(dst) = make_uint2(p0.hi, p1.hi);
-          *reinterpret_cast<uint2*>(dst + XPACK_LO) = make_uint2(p0.lo, p1.lo);
+        for (int rg = 0; rg < 4; ++rg) {
+          const int n = ((wg * WN + wc) * HB + hb) * 32 + 8 * rg + 4 * g;
+          if (n < a.N) {
+            float h[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) h[i] = silu_f32(acc[hb][mb][4 * rg + i]) * acc[hb + HB][mb][4 * rg + i];
+            uint16_t* dst = a.act + xpack_off(orow, n, a.act_ks);
+            const Hilo2 p0 = pack_hilo2(h[0], h[1]), p1 = pack_hilo2(h[2], h[3]);
+            *reinterpret_cast<uint2*>(dst) = make_uint2(p0.hi, p1.hi);
+            *reinterpret_cast<uint2*>(dst + XPACK_LO) = make_uint2(p0.lo, p1.lo);
+          }
         }
-      }
     } else {  // EPI_ARGMAX: partial (max, argmax, second max, NaN count) over this wave's columns
       float best = -INFINITY, second = -INFINITY;
       int bidx = 0x7fffffff;
@@ -318,8 +322,9 @@ hipError_t launch_gemm(const GemmArgs& a, int experts, hipStream_t s) {
   GRIFFIN_GEMM_CASE(EPI_SWIGLU, 2, 2, 2, 1, 1)
   GRIFFIN_GEMM_CASE(EPI_ARGMAX, 2, 4, 4, 1, 1)
   GRIFFIN_GEMM_CASE(EPI_ARGMAX, 2, 4, 2, 1, 1)
-  // four row tiles per workgroup sharing each weight fragment (batched rows)
-  GRIFFIN_GEMM_CASE(EPI_SWIGLU, 2, 4, 2, 1, 4)
+  // two row tiles per workgroup sharing each weight fragment (batched rows)
+  GRIFFIN_GEMM_CASE(EPI_SWIGLU, 4, 4, 3, 1, 2)
+  GRIFFIN_GEMM_CASE(EPI_STORE, 4, 4, 2, 1, 2)
 #undef GRIFFIN_GEMM_CASE
   return hipErrorInvalidValue;
 }
@@ -348,10 +353,11 @@ __global__ __launch_bounds__(256) void pack_weight_kernel(const uint16_t* __rest
   const int r = lane & 31, gg = lane >> 5;
   long long row;
   bool ok;
-  if (p.swiglu) {  // nb == 2: block 0 gate rows, block 1 up rows of column block cb
-    const int c = (wg * p.wn + wave) * 32 + r;
+  if (p.swiglu) {  // blocks [0, nb/2): gate rows of the wave's column blocks; b + nb/2: their up rows
+    const int hb = p.nb / 2;
+    const int c = ((wg * p.wn + wave) * hb + b % hb) * 32 + r;
     ok = c < p.n_out;
-    row = c + (b ? p.n_out : 0);
+    row = c + (b >= hb ? p.n_out : 0);
   } else {
     row = ((long long)(wg * p.wn + wave) * p.nb + b) * 32 + r;
     ok = row < rows;

@@ -33,7 +33,8 @@ enum GemmEpilogue : int {
 // 64-wide K steps starting at split * len.
 struct PackShape {
   int nb, wn, splits, len, n_wgs;
-  int swiglu;   // 1: rows [0, n_out) are gate rows, [n_out, 2 n_out) up rows; nb == 2
+  int swiglu;   // 1: rows [0, n_out) are gate rows, [n_out, 2 n_out) up rows; a wave's blocks
+                // [0, nb/2) are gate blocks, block b + nb/2 the up rows of block b
   int n_out;    // SwiGLU output columns (d_ff)
 };
 

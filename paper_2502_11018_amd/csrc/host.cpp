@@ -45,29 +45,51 @@ struct GemmPlan {
   long long elems = 0;  // packed elements of one matrix (one expert)
 };
 
-// m_tiles: the most 64-row tiles a step of the context can have.  In a dense
-// context of several tiles the gate/up GEMM shares each weight fragment
-// between four tiles per workgroup (batched rows: re-streaming the weights
-// per tile, even from L2, bounds it).  The other GEMMs keep one tile per
-// workgroup: four tiles' activation stages leave LDS for only a two-stage
-// pipeline, which measured slower for them (down 129 -> 169 us, LM head
-// 0.90 -> 1.19 ms at 8 x 61 rows).
-GemmPlan plan_gemm(int epi, int n_out, int K, int experts = 1, int m_tiles = 1) {
+// m_tiles: the most 64-row tiles a step of the context can have.  With
+// several tiles (batched rows) the GEMMs approach the MFMA bound, and each
+// weight fragment is shared between two 64-row tiles per workgroup:
+//  * gate/up: every wave holds two gate and the matching two up blocks, so
+//    each activation fragment read from LDS feeds four weight blocks (the
+//    LDS reads, not HBM, bound these launches);
+//  * wide_tiles (O and down): four 32-column blocks per wave, same reason.
+// Measured at 8 x 61 rows (Llama-3-8B shapes, per launch): gate/up 254 ->
+// 222 us, down 128 -> 115 us, O 55 -> 50 us; QKV got slower (71 -> 109 us)
+// and the LM head gained little, so they keep one tile per workgroup.
+GemmPlan plan_gemm(int epi, int n_out, int K, int experts = 1, int m_tiles = 1, bool wide_tiles = false) {
   GemmPlan p;
   p.epi = epi;
   p.n_out = n_out;
   p.K = K;
   p.ks = cdiv(K, 64);
   if (m_tiles >= 2 && experts == 1 && epi == EPI_SWIGLU) {
-    p.tg = 4;
+    p.tg = 2;
     p.kslices = 1;
-    p.pf = 2;
-    p.nb = 2;
+    p.pf = 3;
+    p.nb = 4;
     p.wn = 4;
     p.rows = 2 * n_out;
-    const int n_wgs = cdiv(cdiv(n_out, 32), p.wn);
+    const int n_wgs = cdiv(cdiv(n_out, 32 * (p.nb / 2)), p.wn);
     p.ks_pad = p.ks;
     p.shape = PackShape{p.nb, p.wn, 1, p.ks, n_wgs, 1, n_out};
+    p.elems = packed_elems(p.shape);
+    return p;
+  }
+  if (m_tiles >= 2 && experts == 1 && epi == EPI_STORE && wide_tiles) {
+    p.tg = 2;
+    p.kslices = 1;
+    p.pf = 2;
+    p.nb = 4;
+    p.wn = 4;
+    p.rows = n_out;
+    const int n_wgs = cdiv(cdiv(n_out, 32 * p.nb), p.wn);
+    // K splits: about 256 workgroups in all (the grid holds round_up(n_wgs,
+    // 8) workgroups per pair of row tiles), at least 4 K steps per split;
+    // 512 measured slower for both matrices
+    const int per_split = round_up(n_wgs, 8) * cdiv(m_tiles, 2);
+    const int splits = std::max(1, std::min(16, std::min(p.ks / 4, 256 / per_split)));
+    const int len = cdiv(p.ks, splits);
+    p.ks_pad = len * splits;
+    p.shape = PackShape{p.nb, p.wn, splits, len, n_wgs, 0, n_out};
     p.elems = packed_elems(p.shape);
     return p;
   }
@@ -84,7 +106,7 @@ GemmPlan plan_gemm(int epi, int n_out, int K, int experts = 1, int m_tiles = 1) 
     p.wn = 4;
     p.rows = n_out;
   }
-  const int n_blocks = cdiv(n_out, 32 * (epi == EPI_SWIGLU ? 1 : p.nb));
+  const int n_blocks = cdiv(n_out, 32 * (epi == EPI_SWIGLU ? p.nb / 2 : p.nb));
   const int n_wgs = cdiv(n_blocks, p.wn);
   if (epi == EPI_STORE) {
     // split K so that the launch has ~kTargetWaves waves, preferring splits
@@ -740,9 +762,9 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
   }
   const int max_tiles = c->Mpad / 64;
   c->p_qkv = plan_gemm(EPI_STORE, c->qkv_n, d.d_model, 1, max_tiles);
-  c->p_o = plan_gemm(EPI_STORE, d.d_model, c->attn_w, 1, max_tiles);
+  c->p_o = plan_gemm(EPI_STORE, d.d_model, c->attn_w, 1, max_tiles, true);
   c->p_gu = plan_gemm(EPI_SWIGLU, d.d_ff, d.d_model, c->E, max_tiles);
-  c->p_down = plan_gemm(EPI_STORE, d.d_model, d.d_ff, c->E, max_tiles);
+  c->p_down = plan_gemm(EPI_STORE, d.d_model, d.d_ff, c->E, max_tiles, true);
   c->p_lm = plan_gemm(EPI_ARGMAX, d.vocab, d.d_model, 1, max_tiles);
   c->xd_ks = std::max({c->p_qkv.ks_pad, c->p_gu.ks_pad, c->p_lm.ks_pad});
   const long long Mp = c->Mpad;
