@@ -38,8 +38,13 @@
 
 namespace griffin {
 
-template <int DH, int NW, bool RAGGED>
-__global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
+// LEAN: two workgroups per CU (at most 256 registers per lane): no
+// cross-block software pipeline in a wave, K and V fragments read from LDS
+// half a block at a time; the second wave of each SIMD hides what the first
+// one waits on.  Chosen when a step has enough key-split units to fill two
+// workgroups per CU (long prefixes, several sequences).
+template <int DH, int NW, bool RAGGED, bool LEAN>
+__global__ __launch_bounds__(64 * NW, LEAN ? 2 : 1) void tree_attention_kernel(AttnArgs a) {
   constexpr int CH = DH / 64;          // 64-dim chunks of Q/K per lane pair
   constexpr int DB = DH / 32;          // 32-dim blocks of the output
   constexpr int KP = CH * 4;           // 1 KB pieces of a K block
@@ -166,21 +171,23 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
   // q = q_hi + q_lo.
   auto qk = [&](int slot) {
     // all K fragments are read before the first MFMA, so the LDS latency is
-    // paid once per block
-    u32x4 kf[CH * 4];
-#pragma unroll
-    for (int x = 0; x < CH * 4; ++x) kf[x] = ring[slot][x][lane];
+    // paid once per block (LEAN: once per 64-dim chunk)
+    constexpr int KR = LEAN ? 4 : CH * 4;  // K fragments held at once
     f32x16 sacc;
 #pragma unroll
     for (int r = 0; r < 16; ++r) sacc[r] = 0.f;
 #pragma unroll
-    for (int c = 0; c < CH; ++c)
+    for (int c0 = 0; c0 < CH * 4; c0 += KR) {
+      u32x4 kf[KR];
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
+      for (int x = 0; x < KR; ++x) kf[x] = ring[slot][c0 + x][lane];
+#pragma unroll
+      for (int x = 0; x < KR; ++x)
 #pragma unroll
         for (int h = 0; h < 2; ++h)
-          sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[c * 4 + j]), as_bf16x8(qf[h][c][j]), sacc, 0,
-                                                         0, 0);
+          sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[x]), as_bf16x8(qf[h][(c0 + x) / 4][(c0 + x) % 4]),
+                                                         sacc, 0, 0, 0);
+    }
     return sacc;
   };
 
@@ -214,14 +221,20 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
     l_run += psum + __shfl_xor(psum, 32, 64);
 
     // O^T += V^T P^T, P as split bf16 (p_hi + p_lo); all V fragments are
-    // read before the first MFMA
+    // read before the first MFMA (LEAN: those of each 16-key half)
+    constexpr int VT = LEAN ? 1 : 2;  // 16-key halves of V held at once
     u32x4 vfr[2][DB];
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
+    for (int t = 0; t < VT; ++t)
 #pragma unroll
       for (int d = 0; d < DB; ++d) vfr[t][d] = ring[slot][KP + d * 2 + t][lane];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
+      if (LEAN && t == 1) {
+#pragma unroll
+        for (int d = 0; d < DB; ++d) vfr[0][d] = ring[slot][KP + d * 2 + 1][lane];
+      }
+      const int tv = LEAN ? 0 : t;  // where this half's V fragments are held
       u32x4 pf[2];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -238,7 +251,7 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
       }
 #pragma unroll
       for (int d = 0; d < DB; ++d) {
-        u32x4 vf = vfr[t][d];
+        u32x4 vf = vfr[tv][d];
         if constexpr (TAIL) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) vf[q] &= keep[q];
@@ -270,7 +283,30 @@ __global__ __launch_bounds__(64 * NW) void tree_attention_kernel(AttnArgs a) {
   for (int d = 0; d < DB; ++d)
 #pragma unroll
     for (int r = 0; r < 16; ++r) oacc[d][r] = 0.f;
-  if (nb > 0) {
+  if (nb > 0 && LEAN) {
+    // one block per step: wait for block i (blocks i+1 .. i+D-2 stay in
+    // flight), publish it, refill the slot of block i - 1, then scores,
+    // softmax and P V of block i
+    auto step = [&](auto tail, int u, int i) {
+      wait_vmcnt_lds<(D - 2) * PPW>();
+      __builtin_amdgcn_s_barrier();
+      issue((u + D - 1) % D, kb0 + min(i + D - 1, nb - 1));
+      const f32x16 sc = qk(u);
+      sv(tail, sc, u, kb0 + i, i == 0);
+    };
+    int base = 0;
+    for (; base + D <= nfull; base += D) {
+#pragma unroll
+      for (int u = 0; u < D; ++u) step(std::false_type{}, u, base + u);
+    }
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+      const int i = base + u;
+      if (i < nfull) step(std::false_type{}, u, i);  // uniform
+      else if (i < nb) step(std::true_type{}, u, i);
+    }
+    wait_vmcnt_lds<0>();
+  } else if (nb > 0) {
     // Q (loaded before the first DMAs) and block 0
     wait_vmcnt_lds<(D - 2) * PPW>();
     __builtin_amdgcn_s_barrier();
@@ -356,10 +392,16 @@ int attn_waves(int group) { return group >= 4 ? 4 : group >= 2 ? 2 : 1; }
 
 template <int DH, int NW>
 static void launch_attn_nw(const AttnArgs& a, dim3 grid, hipStream_t s) {
-  if (a.meta.split_tab)
-    hipLaunchKernelGGL((tree_attention_kernel<DH, NW, true>), grid, dim3(64 * NW), 0, s, a);
-  else
-    hipLaunchKernelGGL((tree_attention_kernel<DH, NW, false>), grid, dim3(64 * NW), 0, s, a);
+  // two workgroups per CU pay off once the grid fills them (measured at 8
+  // sequences x 16384 keys); smaller grids keep the one-wave-per-SIMD form
+  const bool lean = grid.x >= 512;
+  if (a.meta.split_tab) {
+    if (lean) hipLaunchKernelGGL((tree_attention_kernel<DH, NW, true, true>), grid, dim3(64 * NW), 0, s, a);
+    else hipLaunchKernelGGL((tree_attention_kernel<DH, NW, true, false>), grid, dim3(64 * NW), 0, s, a);
+  } else {
+    if (lean) hipLaunchKernelGGL((tree_attention_kernel<DH, NW, false, true>), grid, dim3(64 * NW), 0, s, a);
+    else hipLaunchKernelGGL((tree_attention_kernel<DH, NW, false, false>), grid, dim3(64 * NW), 0, s, a);
+  }
 }
 
 template <int DH>

@@ -745,12 +745,13 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
   c->attn_w = d.n_q_heads * d.head_dim;
   c->qblocks = cdiv(d.max_tree, 32);
   {
-    // key splits: about 256 attention workgroups (one per CU: the kernel
-    // holds one wave per SIMD, so more workgroups only add rounds), at
-    // least two 32-key blocks per split
+    // key splits: about 512 attention workgroups, at least two 32-key
+    // blocks per split and at most 16 splits.  A grid of 512 or more runs
+    // the kernel's two-workgroups-per-CU form; smaller ones (a single
+    // sequence: 16 splits x 16 units) hold one wave per SIMD
     const int G = d.n_q_heads / d.n_kv_heads, nw = attn_waves(G);
     const int units = d.max_batch * d.n_kv_heads * cdiv(G, nw) * c->qblocks;
-    const int by_par = cdiv(256, units);
+    const int by_par = cdiv(512, units);
     const int by_len = std::max(1, d.kv_capacity / 64);
     c->attn_splits = std::max(1, std::min(std::min(by_len, by_par), 16));
     // With several sequences a step has batch * attn_splits split units,
