@@ -30,6 +30,22 @@ Degenerate inputs, read as: a child whose token has q(t) = 0 is accepted when
 p(t) > 0 and rejected otherwise (min(1, p/q) with p/0 = +inf); a rejection
 whose residual max(p - q, 0) sums to zero (p = q up to rounding, so the
 rejection had probability zero) leaves p unchanged.
+
+Deterministic drafts (q_draft None).  A tree built by ranking the draft's
+log-probabilities (the EAGLE-2 expansion the paper follows, App. "Draft Tree
+Structure") is a function of the draft's output, not a draw from it: given
+the draft, each child proposes its token with probability one.  The same rule
+with q the point mass at the child's own token then reads
+
+    accept the child with token t with probability p(t)
+    on rejection:  p <- p with t removed, renormalised
+
+and stays lossless for any such tree, however many children a node keeps and
+however they were chosen, as long as that choice does not see the target's
+uniforms (``tests/test_oracle_sampling.py`` pins it by exact enumeration).  A
+draw from q with the count of kept children depending on the draw's values
+would not: the kept children would no longer be distributed as q.  Duplicate
+sibling tokens are harmless (p(t) is already 0 at the second one).
 """
 
 from __future__ import annotations
@@ -69,13 +85,14 @@ def _children(parents: np.ndarray, n: int, u: int):
     return [c for c in range(1, n) if int(parents[c]) == u]
 
 
-def accept_sampled(tree, logits: np.ndarray, q_draft: np.ndarray, u_accept: Sequence[float],
+def accept_sampled(tree, logits: np.ndarray, q_draft: Optional[np.ndarray], u_accept: Sequence[float],
                    u_final: Sequence[float], temperature: float, trace: Optional[list] = None) -> AcceptResult:
     """Recursive rejection sampling down the tree (one sequence).
 
     tree: tokens [T], parents [T] (node 0 = root).  logits: [T, V] target
     logits at every node.  q_draft: [T, V], row u = the draft distribution
-    u's children were drawn from (rows of leaves are not read).  u_accept,
+    u's children were drawn from (rows of leaves are not read), or None for
+    a deterministic draft (each child a point mass at its own token).  u_accept,
     u_final: [T] uniforms in [0, 1).  Returns the accepted path (L draft
     tokens and their node ids) and the emitted token appended to the tokens.
     With a trace list, every decision appends its margin: ("accept", u - a)
@@ -86,6 +103,26 @@ def accept_sampled(tree, logits: np.ndarray, q_draft: np.ndarray, u_accept: Sequ
     node, path = 0, []
     while True:
         p = softmax_t(logits[node], temperature)
+        if q_draft is None:
+            nxt = None
+            for c in _children(parents, n, node):
+                t = int(tokens[c])
+                a = float(p[t])
+                if trace is not None:
+                    trace.append(("accept", float(u_accept[c]) - a))
+                if float(u_accept[c]) < a:
+                    nxt = c
+                    break
+                res = p.copy()
+                res[t] = 0.0
+                if np.sum(res) > 0:
+                    p = res / np.sum(res)
+            if nxt is None:
+                emitted = draw(p, u_final[node], trace)
+                break
+            path.append(nxt)
+            node = nxt
+            continue
         q = np.asarray(q_draft[node], dtype=np.float64).copy()
         q = q / np.sum(q) if np.sum(q) > 0 else q
         nxt = None

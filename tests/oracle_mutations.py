@@ -239,6 +239,47 @@ def sampling_ratio_inverted():
     _patch_sampled(_sampled_with(inverted=True))
 
 
+def _point_mass_with(kept=False, unnormalised=False):
+    """accept_sampled whose deterministic-draft (q_draft None) rule has one
+    mistake; drawn drafts keep the oracle's own rule."""
+    orig = osm.accept_sampled
+
+    def accept_sampled(tree, logits, q_draft, u_accept, u_final, temperature, trace=None):
+        if q_draft is not None:
+            return orig(tree, logits, q_draft, u_accept, u_final, temperature, trace)
+        tokens, parents = np.asarray(tree.tokens), np.asarray(tree.parents)
+        node, path = 0, []
+        while True:
+            p0 = osm.softmax_t(logits[node], temperature)
+            p = p0.copy()
+            nxt = None
+            for c in [c for c in range(1, len(tokens)) if int(parents[c]) == node]:
+                t = int(tokens[c])
+                a = (p0[t] if p[t] > 0 else 0.0) if unnormalised else p[t]
+                if float(u_accept[c]) < a:
+                    nxt = c
+                    break
+                if not kept:
+                    p = p.copy()
+                    p[t] = 0.0
+                    p = p / np.sum(p)
+            if nxt is None:
+                emitted = osm.draw(p, u_final[node])
+                break
+            path.append(nxt)
+            node = nxt
+        return oa.AcceptResult(len(path), [int(tokens[c]) for c in path] + [emitted], path)
+    return accept_sampled
+
+
+def sampling_point_mass_rejected_token_kept():
+    _patch_sampled(_point_mass_with(kept=True))
+
+
+def sampling_point_mass_residual_unnormalised():
+    _patch_sampled(_point_mass_with(unnormalised=True))
+
+
 def sampling_temperature_ignored():
     def softmax_t(logits, temperature):
         z = np.asarray(logits, dtype=np.float64)
@@ -338,6 +379,7 @@ MUTATIONS = {f.__name__: f for f in [
     moe_unnormalised, qkv_kv_swapped, accept_no_bonus, accept_first_child_only,
     argmax_last_on_ties, latency_missing_depth, sampling_rejected_token_kept_in_q,
     sampling_residual_unnormalised, sampling_ratio_inverted, sampling_temperature_ignored,
+    sampling_point_mass_rejected_token_kept, sampling_point_mass_residual_unnormalised,
     draft_tgf_no_residual, draft_layernorm_no_centring, draft_heads_swapped, draft_topk_probabilities,
     draft_frontier_by_local_probability,
 ]}

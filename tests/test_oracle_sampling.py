@@ -273,3 +273,154 @@ def test_draw_is_the_inverse_cdf():
                 want = v
                 break
         assert oracle.draw(p, r) == want
+
+
+# ---- deterministic drafts: every child a point mass at its own token ----------
+
+def _det_children(Q, prefix, depth_left, rule):
+    """Children tokens of a node, in node-id order, chosen from the draft's
+    table without any randomness (as a top-k expansion chooses them)."""
+    if depth_left == 0:
+        return []
+    q = Q[prefix]
+    order = [int(v) for v in np.argsort(-q, kind="stable")]
+    if rule == "top2":
+        return order[:2]
+    if rule == "dynamic":  # how many children depends on the draft's values
+        return [v for v in order if q[v] > 0.3] or order[:1]
+    if rule == "dup":      # a repeated sibling token
+        return [order[0], order[0], order[1]]
+    if rule == "all":
+        return order
+    raise ValueError(rule)
+
+
+def _exact_point(P, Q, prefix, depth_left, rule, mutation=None):
+    """Distribution of the emitted sequence below `prefix` when the children,
+    tested one after another, are accepted with probability p(t) of the
+    renormalised residual, which loses t on rejection (written out by
+    enumerating the outcomes of every test)."""
+    p = P[prefix].copy()
+    out = defaultdict(float)
+    reach = 1.0
+    for t in _det_children(Q, prefix, depth_left, rule):
+        if mutation == "draft ratio":       # as if the child had been drawn from q
+            a = min(1.0, p[t] / Q[prefix][t])
+        elif mutation == "residual not renormalised":
+            a = P[prefix][t] if p[t] > 0 else 0.0
+        else:
+            a = p[t]
+        for seq, pr in _exact_point(P, Q, prefix + (t,), depth_left - 1, rule, mutation).items():
+            out[(t,) + seq] += reach * a * pr
+        reach *= 1.0 - a
+        if mutation != "rejected token kept":
+            p = p.copy()
+            p[t] = 0.0
+            if p.sum() > 0:
+                p = p / p.sum()
+    for v in range(V):
+        out[(v,)] += reach * p[v]
+    return out
+
+
+def _target_err(P, dist, D):
+    ext = _extend(P, dist, D + 1)
+    assert abs(sum(ext.values()) - 1.0) < 1e-12
+    return max(abs(ext[s] - np.prod([P[s[:k]][s[k]] for k in range(D + 1)]))
+               for s in itertools.product(range(V), repeat=D + 1))
+
+
+@pytest.mark.parametrize("rule", ["top2", "dynamic", "dup", "all"])
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_point_mass_enumeration_is_lossless(rule, seed):
+    """Any tree chosen from the draft alone, with fixed or value-dependent
+    branching and with repeated sibling tokens, emits the target's own
+    distribution under the point-mass rule."""
+    P, Q = _tables(seed, 3)
+    assert _target_err(P, _exact_point(P, Q, (), 3, rule), 3) < 1e-12
+
+
+@pytest.mark.parametrize("mutation", ["draft ratio", "residual not renormalised", "rejected token kept"])
+def test_point_mass_enumeration_detects_near_misses(mutation):
+    """Testing a deterministic child against the draft's ratio min(1, p/q), not
+    renormalising the residual, or leaving a rejected token in it, each
+    change the emitted distribution."""
+    P, Q = _tables(3, 2)
+    assert _target_err(P, _exact_point(P, Q, (), 2, "top2", mutation), 2) > 1e-3
+
+
+def _det_tree(Q, root, depth, rule):
+    """A concrete tree (BFS ids) of _det_children's choices below `root`."""
+    tokens, parents, prefixes = [root], [-1], [()]
+    frontier = [0]
+    for d in range(depth, 0, -1):
+        nxt = []
+        for node in frontier:
+            for t in _det_children(Q, prefixes[node], d, rule):
+                tokens.append(t)
+                parents.append(node)
+                prefixes.append(prefixes[node] + (t,))
+                nxt.append(len(tokens) - 1)
+        frontier = nxt
+    return gen.Tree(np.array(tokens, np.int32), np.array(parents, np.int32)), prefixes
+
+
+@pytest.mark.parametrize("rule", ["dynamic", "dup"])
+def test_point_mass_oracle_monte_carlo_matches_exact_distribution(rule):
+    D = 2
+    P, Q = _tables(6, D)
+    exact = _extend(P, _exact_point(P, Q, (), D, rule), D + 1)
+    tree, prefixes = _det_tree(Q, 0, D, rule)
+    logits = np.stack([np.log(P[pre]) for pre in prefixes])
+    rng = np.random.default_rng(12)
+    n = 20000
+    counts = defaultdict(int)
+    for _ in range(n):
+        res = oracle.accept_sampled(tree, logits, None, rng.random(tree.n), rng.random(tree.n), 1.0)
+        seq = tuple(res.tokens)
+        while len(seq) < D + 1:
+            seq = seq + (oracle.draw(P[seq], rng.random()),)
+        counts[seq] += 1
+    chi2 = sum((counts[s] - n * e) ** 2 / (n * e) for s, e in exact.items() if e > 0)
+    dof = sum(1 for e in exact.values() if e > 0) - 1
+    assert chi2 < dof + 6 * np.sqrt(2 * dof), (chi2, dof)
+
+
+def test_point_mass_on_chains_equals_one_hot_draft_rows():
+    """On a chain every node has one child, whose point mass is the one-hot
+    row at its token: both forms of the rule take the same decisions."""
+    rng = np.random.default_rng(13)
+    Vb = 30
+    for trial in range(40):
+        n = 1 + int(rng.integers(1, 7))
+        tree = gen.Tree(rng.integers(0, Vb, n).astype(np.int32), np.arange(-1, n - 1, dtype=np.int32))
+        logits = rng.normal(size=(n, Vb)) * 2.0
+        qd = np.zeros((n, Vb))
+        for c in range(1, n):
+            qd[c - 1, tree.tokens[c]] = 1.0
+        ua, uf = rng.random(n), rng.random(n)
+        a = oracle.accept_sampled(tree, logits, None, ua, uf, 0.7)
+        b = oracle.accept_sampled(tree, logits, qd, ua, uf, 0.7)
+        assert a.tokens == b.tokens and a.path == b.path
+
+
+def test_point_mass_small_temperature_reduces_to_greedy_walk():
+    rng = np.random.default_rng(14)
+    Vb = 40
+    for trial in range(30):
+        tree, _ = gen.random_tree((3, 2, 3), Vb, 300 + trial)
+        logits = rng.normal(size=(tree.n, Vb)) * 3.0
+        # distinct sibling tokens, one child of some nodes carrying the parent's argmax
+        toks = tree.tokens.copy()
+        for u in range(tree.n):
+            kids = [c for c in range(1, tree.n) if tree.parents[c] == u]
+            best = int(np.argmax(logits[u]))
+            others = [v for v in range(Vb) if v != best]
+            for j, c in enumerate(kids):
+                toks[c] = others[(u * 5 + j) % len(others)]
+            if kids and rng.random() < 0.7:
+                toks[kids[int(rng.integers(len(kids)))]] = best
+        tree = gen.Tree(toks, tree.parents)
+        res = oracle.accept_sampled(tree, logits, None, rng.random(tree.n), rng.random(tree.n), 1e-4)
+        ref = oracle.accept_dfs(tree, oracle.argmax_first(logits))
+        assert res.tokens == ref.tokens and res.length == ref.length
