@@ -176,7 +176,7 @@ def main():
     log(f"weights {weights.nbytes() / 1e9:.2f} GB generated in {time.time() - t0:.1f} s")
     max_tree = w.max_tree
     prefix = w.prefixes()
-    cycle_room = 128  # positions the draft leg's speculative cycles append to the prefix
+    cycle_room = 192  # positions the draft leg's speculative cycles append to the prefix
     v = P.TreeVerifier(m, weights, max_batch=w.batch, max_tree=max_tree, max_depth=w.depth,
                        kv_capacity=w.kv_capacity() + cycle_room)
     v.set_graphs(not args.no_graphs)
@@ -329,12 +329,20 @@ def main():
         for i in range(ns):
             v.accept_sampled(logits, qd, *uniforms(), 1.0)
         t_acc = (time.perf_counter() - t0) / ns
+        t0 = time.perf_counter()
+        for i in range(ns):
+            v.accept_sampled(logits, None, *uniforms(), 1.0)
+        t_acc_pm = (time.perf_counter() - t0) / ns
         sampled = {"temperature": 1.0, "steps": ns, "ms_per_step": round(t_cycle * 1e3, 4),
                    "accept_sampled_us": round(t_acc * 1e6, 1),
+                   "accept_deterministic_draft_us": round(t_acc_pm * 1e6, 1),
                    "synthetic_mean_accept_len": round(float(np.mean(lens)) + 1.0, 3),
                    "note": "step writing all logits + stochastic acceptance; draft distributions are "
-                           "seeded random rows, so acceptance is synthetic"}
-        log(f"T=1 cycle {t_cycle * 1e3:.3f} ms/step, stochastic acceptance {t_acc * 1e6:.1f} us")
+                           "seeded random rows, so acceptance is synthetic; accept_deterministic_draft_us: the "
+                           "acceptance of the same trees as a deterministic draft (q_draft NULL), as the "
+                           "drafted trees of the temperature-1 cycle are accepted"}
+        log(f"T=1 cycle {t_cycle * 1e3:.3f} ms/step, stochastic acceptance {t_acc * 1e6:.1f} us "
+            f"(deterministic draft {t_acc_pm * 1e6:.1f} us)")
 
     # draft model of the same target: one pass (t-bar of the paper's latency
     # model) and a whole 60-token depth-6 tree, then the modelled speedup
@@ -366,23 +374,28 @@ def main():
         t_tree = (time.perf_counter() - t0) * 1e3 / nd
         # whole cycles: draft tree, verify, accept, commit, the target's
         # features, the draft's catch-up (random weights: about one token each)
-        t_cycle, cycle_tokens = None, None
+        t_cycle, cycle_tokens, t_cycle_t1, cycle_tokens_t1 = None, None, None, None
         if not args.no_cycle and max_tree >= ds.n_total + 1 and w.depth >= ds.depth:
             from paper_2502_11018_amd.cycle import SpeculativeCycle
-            cyc = SpeculativeCycle(v, dm, ds.k, ds.depth, ds.n_total)
-            cyc.start(prefix, roots, feat)
             n_cyc = min(args.steps, 10)
-            assert (n_cyc + 2) * (ds.depth + 1) <= cycle_room
-            for _ in range(2):
-                cyc.cycle()
-            torch.cuda.synchronize()
-            emitted = 0
-            t0 = time.perf_counter()
-            for _ in range(n_cyc):
-                emitted += sum(len(t) for t in cyc.cycle())
-            torch.cuda.synchronize()
-            t_cycle = (time.perf_counter() - t0) * 1e3 / n_cyc
-            cycle_tokens = emitted / n_cyc
+            assert 2 * (n_cyc + 2) * (ds.depth + 1) <= cycle_room
+
+            def run_cycles(temperature, start_prefix):
+                # greedy, then T = 1 from where the greedy cycles left the caches
+                cyc = SpeculativeCycle(v, dm, ds.k, ds.depth, ds.n_total, temperature=temperature, seed=5)
+                cyc.start(start_prefix, roots, feat)
+                for _ in range(2):
+                    cyc.cycle()
+                torch.cuda.synchronize()
+                emitted = 0
+                t0 = time.perf_counter()
+                for _ in range(n_cyc):
+                    emitted += sum(len(t) for t in cyc.cycle())
+                torch.cuda.synchronize()
+                return (time.perf_counter() - t0) * 1e3 / n_cyc, emitted / n_cyc, cyc.prefix
+
+            t_cycle, cycle_tokens, after = run_cycles(0.0, prefix)
+            t_cycle_t1, cycle_tokens_t1, _ = run_cycles(1.0, after)
         dm.close()
         sr = {str(tau): round(tau * ms_per_step / (ms_per_step + ds.depth * t_pass), 3) for tau in (4, 5, 6)}
         cycle = {str(tau): round(tau * root_ms / (ms_per_step + t_tree), 3) for tau in (4, 5, 6)}
@@ -391,6 +404,8 @@ def main():
                  "speedup_model": sr, "speedup_vs_plain_decoding": cycle,
                  "cycle_ms": None if t_cycle is None else round(t_cycle, 4),
                  "cycle_tokens_measured": cycle_tokens,
+                 "cycle_t1_ms": None if t_cycle_t1 is None else round(t_cycle_t1, 4),
+                 "cycle_t1_tokens_measured": cycle_tokens_t1,
                  "speedup_from_measured_cycle": None if t_cycle is None else
                  {str(tau): round(tau * root_ms / t_cycle, 3) for tau in (4, 5, 6)},
                  "note": "pass_ms = one draft pass over the largest expansion (1 + k (depth - 1) nodes), host "
@@ -399,13 +414,15 @@ def main():
                          "+ tree_ms); tau (tokens per cycle, bonus included) needs trained drafts and is a free "
                          "parameter here; cycle_ms = one whole draft-and-verify cycle (SpeculativeCycle: tree, "
                          "verify step, accept, commit, target features, draft catch-up) on the same context, "
-                         "cycle_tokens_measured its emitted tokens with random weights, "
+                         "cycle_tokens_measured its emitted tokens with random weights, cycle_t1_ms the same "
+                         "cycle at temperature 1 (logits written, stochastic acceptance of the drafted tree), "
                          "speedup_from_measured_cycle = tau root_only_ms / cycle_ms"}
         log(f"draft: pass {t_pass:.3f} ms ({biggest[0].n} nodes), tree {t_tree:.3f} ms, "
             f"modelled speedup at tau 5: {sr['5']}x")
         if t_cycle is not None:
             log(f"cycle: {t_cycle:.3f} ms, {cycle_tokens:.2f} tokens per cycle measured (random weights); "
-                f"at tau 5: {5 * root_ms / t_cycle:.3f}x plain decoding")
+                f"at tau 5: {5 * root_ms / t_cycle:.3f}x plain decoding; T=1 cycle {t_cycle_t1:.3f} ms, "
+                f"{cycle_tokens_t1:.2f} tokens")
 
     gc.enable()
     gc.unfreeze()

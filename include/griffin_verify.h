@@ -164,13 +164,21 @@ int griffin_accept(griffin_ctx *ctx, int32_t *accept_len, int32_t *tokens_out, i
  *             griffin_verify_step filled (logits_out must have been given)
  *   q_draft   device fp32 [batch*max_tree][vocab]: row b*max_tree+u = the
  *             draft distribution u's children were drawn from (finite, >= 0,
- *             any positive scale; rows of leaves are not read)
+ *             any positive scale; rows of leaves are not read); or NULL for a
+ *             deterministic draft, such as the top-k expansion of
+ *             griffin_draft_tree (App. "Draft Tree Structure"), whose children
+ *             are a function of the draft rather than draws from it: each
+ *             child is then the point mass at its own token, accepted with
+ *             probability p(t) / D (D = mass of p left after the node's
+ *             earlier rejections), and a rejection removes t from p (nothing
+ *             for a token already removed, or when no mass would be left).
+ *             Lossless for any such tree.
  *   u_accept  host [batch][max_tree], u_final host [batch][max_tree]:
  *             uniform draws in [0, 1) (entries of absent nodes are checked
  *             but not used)
  * Outputs as for griffin_accept: L accepted draft tokens, then the emitted
- * token.  Synchronises the context's stream.  Errors: EINVAL (NULL input,
- * T <= 0 or not finite, a uniform outside [0, 1)), EORDER (no step yet),
+ * token.  Synchronises the context's stream.  Errors: EINVAL (NULL logits or
+ * uniforms, T <= 0 or not finite, a uniform outside [0, 1)), EORDER (no step yet),
  * EHIP, ENUMERIC (a NaN logit at a node the walk visited). */
 int griffin_accept_sampled(griffin_ctx *ctx, const float *logits, const float *q_draft,
                            const float *u_accept, const float *u_final, float temperature,
@@ -280,7 +288,8 @@ int griffin_accept_walk(void *hip_stream, int32_t batch, int32_t max_tree, int32
 /* The stochastic acceptance of griffin_accept_sampled for trees given
  * directly: n_nodes, tokens, parents and the uniforms are host arrays laid
  * out as for griffin_verify_step / griffin_accept_sampled; logits and q_draft
- * are device fp32 [batch*max_tree][vocab].  Allocates and frees its own
+ * are device fp32 [batch*max_tree][vocab] (q_draft NULL: a deterministic
+ * draft, as for griffin_accept_sampled).  Allocates and frees its own
  * device buffers and synchronises hip_stream.  Errors: EINVAL, ETREE, ETOKEN,
  * ENOMEM, EHIP, ENUMERIC (outputs still written). */
 int griffin_accept_sampled_walk(void *hip_stream, int32_t batch, int32_t max_tree, int32_t max_depth,

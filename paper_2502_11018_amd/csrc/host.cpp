@@ -1046,8 +1046,8 @@ int griffin_accept_sampled(griffin_ctx* c, const float* logits, const float* q_d
                            const float* u_final, float temperature, int32_t* accept_len, int32_t* tokens_out,
                            int32_t* path_nodes) {
   if (!c) return GRIFFIN_EINVAL;
-  if (!logits || !q_draft || !u_accept || !u_final)
-    return set_err(c, GRIFFIN_EINVAL, "logits, q_draft and both uniform arrays are required");
+  if (!logits || !u_accept || !u_final)
+    return set_err(c, GRIFFIN_EINVAL, "logits and both uniform arrays are required");
   if (!(temperature > 0.f) || !std::isfinite(temperature))
     return set_err(c, GRIFFIN_EINVAL, "temperature must be finite and > 0");
   if (!c->stepped) return set_err(c, GRIFFIN_EORDER, "no verification step has been enqueued");
@@ -1325,7 +1325,7 @@ static int sampled_walk(void* hip_stream, int32_t batch, int32_t max_tree, int32
                         int32_t* accept_len, int32_t* tokens_out, int32_t* path_nodes, char* fixed,
                         size_t fixed_bytes) {
   if (batch < 1 || max_tree < 1 || max_tree > kMaxTree || max_depth < 0 || max_depth >= max_tree || vocab < 1 ||
-      !n_nodes || !tokens || !parents || !logits || !q_draft || !u_accept || !u_final)
+      !n_nodes || !tokens || !parents || !logits || !u_accept || !u_final)
     return GRIFFIN_EINVAL;
   if (!(temperature > 0.f) || !std::isfinite(temperature)) return GRIFFIN_EINVAL;
   const int rows = batch * max_tree;

@@ -39,6 +39,16 @@
 //   sampled_pick_kernel: the inverse CDF: the slice that holds u * total,
 //     then an exact in-order scan inside it.
 // Kernel boundaries order every hand-over; no counters, fences or atomics.
+//
+// Deterministic drafts (q == nullptr): a tree ranked from the draft's
+// log-probabilities is a function of the draft, so each child is the point
+// mass at its own token: accepted with probability p(t) / D, D the mass of p
+// left after the node's earlier rejections; a rejection removes t from p (no
+// change for a token already removed, or when nothing would be left).  No
+// vocabulary pass per rejection: the step launches are skipped and the walk
+// itself tests every child of the nodes it visits.  The final node's
+// residual is p without its rejected tokens, which the draw kernels take as
+// the q-free residual (a = 0) with each rejected token frozen at 0.
 
 #include <algorithm>
 #include <mutex>
@@ -225,7 +235,7 @@ __global__ __launch_bounds__(SA_THREADS) void sampled_norm_kernel(SampledArgs a,
   const SampScratch sc = sa_carve(a.scratch, a.scratch_batch, a.max_tree, nslice);
   const int s = blockIdx.x, row = a.order[blockIdx.y], tid = threadIdx.x, V = a.vocab;
   const float* lg = a.logits + (size_t)row * V;
-  const float* qd = a.q + (size_t)row * V;
+  const float* qd = a.q ? a.q + (size_t)row * V : nullptr;
   const float inv_t = a.inv_t;
   int lo, hi;
   slice_range(V, nslice, s, lo, hi);
@@ -240,7 +250,7 @@ __global__ __launch_bounds__(SA_THREADS) void sampled_norm_kernel(SampledArgs a,
     se = (mn == m ? se : se * expf((m - mn) * inv_t)) + (x > -INFINITY ? expf((x - mn) * inv_t) : 0.f);
     m = mn;
   };
-  if ((int)blockIdx.y < n_parents)  // rows of `order` with children come first
+  if (qd && (int)blockIdx.y < n_parents)  // rows of `order` with children come first
     for_slice<VEC, true>(lg, qd, lo, hi, f);
   else
     for_slice<VEC, false>(lg, qd, lo, hi, f);
@@ -314,7 +324,61 @@ struct WalkEnd {
   RmEntry e;                // this lane's rejected-token entry of the final node
 };
 
+// Walk of a deterministic draft's tree: every child a point mass at its token.
+__device__ __forceinline__ WalkEnd walk_tree_point_mass(const SampledArgs& a, const SampScratch& sc, int nslice,
+                                                        int b) {
+  const int lane = threadIdx.x & 63, n = a.n_nodes[b];
+  const size_t row0 = (size_t)b * a.max_tree;
+  const bool in = lane < n;
+  const int ln = min(lane, n - 1);
+  const int par = (in && lane >= 1) ? a.parent[row0 + ln] : -1;
+  const int tok = in ? a.token[row0 + ln] : 0;
+  const float ua = in ? a.u_accept[row0 + ln] : 1.f;
+  WalkEnd w;
+  w.node = 0;
+  w.L = 0;
+  w.nan = 0;
+  w.pathv = -1;
+  for (int it = 0;; ++it) {
+    const size_t fr = row0 + w.node;
+    const float4 pp = lane < nslice ? sc.npart[fr * nslice + lane] : make_float4(-INFINITY, 0.f, 0.f, 0.f);
+    SampState st = state_from_norm(pp, a.inv_t);  // D = 1: all of p left
+    w.e = RmEntry{-1, 0.f, 0.f, 0.f};
+    w.st = st;
+    if (st.bad) {
+      w.nan = 1;
+      return w;
+    }
+    const Norm nm = norm_of(st, a.inv_t);
+    const bool kid = par == w.node;
+    const float pt = kid ? p_of(a.logits[fr * a.vocab + tok], nm) : 0.f;
+    int nxt = -1;
+    for (uint64_t rest = __ballot(kid); rest && it < a.max_depth; rest &= rest - 1) {
+      const int c = __ffsll((unsigned long long)rest) - 1;
+      const int t = __shfl(tok, c, 64);
+      const float ptc = __shfl(pt, c, 64);
+      const bool dup = __ballot(lane < st.n_rm && w.e.tok == t) != 0;
+      const float acc = dup ? 0.f : fminf(1.f, ptc / st.D);
+      if (__shfl(ua, c, 64) < acc) {
+        nxt = c;
+        break;
+      }
+      if (!dup && st.D - ptc > 0.f) {
+        if (lane == st.n_rm) w.e = RmEntry{t, 0.f, ptc, 0.f};
+        st.D -= ptc;
+        ++st.n_rm;
+      }
+    }
+    w.st = st;
+    if (nxt < 0) return w;
+    if (lane == w.L) w.pathv = nxt;
+    ++w.L;
+    w.node = nxt;
+  }
+}
+
 __device__ __forceinline__ WalkEnd walk_tree(const SampledArgs& a, const SampScratch& sc, int nslice, int b) {
+  if (!a.q) return walk_tree_point_mass(a, sc, nslice, b);
   const int lane = threadIdx.x & 63, n = a.n_nodes[b];
   const size_t row0 = (size_t)b * a.max_tree, rows = (size_t)a.scratch_batch * a.max_tree;
   const bool in = lane < n;
@@ -389,11 +453,12 @@ __global__ __launch_bounds__(SA_THREADS) void sampled_draw_sums_kernel(SampledAr
     int lo, hi;
     slice_range(V, nslice, s, lo, hi);
     const float af = st.a;
+    const float* qd = a.q ? a.q + fr * V : nullptr;
     auto f = [&](float x, float y) { g += resid(x, y, af, nm); };
-    if (st.n_rm > 0)  // a node without children (or rejections) draws from p alone
-      for_slice<VEC, true>(a.logits + fr * V, a.q + fr * V, lo, hi, f);
+    if (st.n_rm > 0 && qd)  // a node without children (or rejections) draws from p alone
+      for_slice<VEC, true>(a.logits + fr * V, qd, lo, hi, f);
     else
-      for_slice<VEC, false>(a.logits + fr * V, a.q + fr * V, lo, hi, f);
+      for_slice<VEC, false>(a.logits + fr * V, qd, lo, hi, f);
     if (tid < st.n_rm) {  // rejected tokens in this slice: frozen value instead
       const RmEntry e = rml[tid];
       if (e.tok >= lo && e.tok < hi) g += e.f - resid_pq(e.p, e.q, af);
@@ -450,7 +515,7 @@ __global__ __launch_bounds__(SA_THREADS) void sampled_pick_kernel(SampledArgs a,
       const Norm nm = norm_of(st, a.inv_t);
       const size_t fr = row0 + sh_node;
       const float* lg = a.logits + fr * V;
-      const float* qd = a.q + fr * V;
+      const float* qd = a.q ? a.q + fr * V : nullptr;
       // exact residual inside slice si, thread ranges in order
       int clo, chi;
       slice_range(V, nslice, si, clo, chi);
@@ -459,7 +524,7 @@ __global__ __launch_bounds__(SA_THREADS) void sampled_pick_kernel(SampledArgs a,
       const int nrm = st.n_rm;
       const float af = st.a;
       auto r_at = [&](int v) {
-        float r = resid(lg[v], nrm > 0 ? qd[v] : 0.f, af, nm);
+        float r = resid(lg[v], (nrm > 0 && qd) ? qd[v] : 0.f, af, nm);
         for (int j = 0; j < nrm; ++j) r = rml[j].tok == v ? rml[j].f : r;
         return r;
       };
@@ -505,9 +570,11 @@ __global__ __launch_bounds__(SA_THREADS) void sampled_pick_kernel(SampledArgs a,
 
 template <bool VEC>
 static void launch_all(const SampledArgs& a, const int* rows_with, int max_children, int ns, hipStream_t s) {
+  // a deterministic draft's walk tests the children itself: no step launches
+  const int steps = a.q ? max_children : 0;
   hipLaunchKernelGGL(sampled_norm_kernel<VEC>, dim3(ns, rows_with[0]), dim3(SA_THREADS), 0, s, a, ns,
-                     max_children > 0 ? rows_with[1] : 0);
-  for (int k = 0, base = 0, prev = 0; k < max_children; prev = base, base += rows_with[++k])
+                     steps > 0 ? rows_with[1] : 0);
+  for (int k = 0, base = 0, prev = 0; k < steps; prev = base, base += rows_with[++k])
     hipLaunchKernelGGL(sampled_step_kernel<VEC>, dim3(ns, rows_with[k + 1]), dim3(SA_THREADS), 0, s, a, ns, k, base,
                        prev);
   hipLaunchKernelGGL(sampled_draw_sums_kernel<VEC>, dim3(ns, a.batch), dim3(SA_THREADS), 0, s, a, ns);

@@ -9,6 +9,11 @@ Every compute step is a library call; this class only sequences them:
    token before it.
 2. ``TreeVerifier.step`` / ``accept`` / ``commit``: the target scores the tree
    in one pass, walks it, and moves the accepted path's K/V into its cache.
+   At temperature T > 0 (the paper evaluates T = 1 beside greedy decoding,
+   Sec. 5) the walk is ``accept_sampled`` over the step's logits with the
+   tree as a deterministic draft (each child a point mass at its token: the
+   expansion ranks the draft's log-probabilities, it draws nothing), which
+   keeps the emitted tokens distributed as sampling the target itself.
 3. ``TreeVerifier.features``: the target's features of the root and of the
    accepted nodes.
 4. ``DraftModel.extend``: the draft layer's K/V of the root and the accepted
@@ -37,22 +42,37 @@ class _Tree:
 
 
 class SpeculativeCycle:
-    """Greedy (temperature 0) speculative decoding with a draft model.
+    """Speculative decoding with a draft model, greedy (temperature 0) or
+    sampled (temperature > 0).
 
     verifier: a ``TreeVerifier`` of the target; draft: a ``DraftModel`` of the
     same target, both on one stream, whose caches hold the same prefix;
-    k, depth, n_total: the expansion (the paper's: 10, 6, 60)."""
+    k, depth, n_total: the expansion (the paper's: 10, 6, 60); temperature:
+    the target's sampling temperature; seed: the generator of the acceptance
+    uniforms when a cycle is not handed its own."""
 
-    def __init__(self, verifier, draft, k: int, depth: int, n_total: int):
+    def __init__(self, verifier, draft, k: int, depth: int, n_total: int, temperature: float = 0.0,
+                 seed: int = 0):
         if draft.max_tree < max(n_total + 1, depth + 1):
             raise ValueError("the draft's max_tree must hold n_total + 1 nodes and a chain of depth + 1 tokens")
+        if verifier.max_tree < n_total + 1:
+            raise ValueError("the verifier's max_tree must hold n_total + 1 nodes")
+        if not (temperature >= 0.0 and np.isfinite(temperature)):
+            raise ValueError("temperature must be finite and >= 0")
         self.v, self.d = verifier, draft
         self.k, self.depth, self.n_total = k, depth, n_total
+        self.temperature = float(temperature)
+        self.rng = np.random.default_rng(seed)
+        self.logits = None
+        if self.temperature > 0:
+            self.logits = torch.empty((verifier.max_batch * verifier.max_tree, verifier.shape.vocab),
+                                      dtype=torch.float32, device=verifier.k_cache.device)
         self.prefix: List[int] = []
         self.roots: List[int] = []
         self.root_features = None
         self.last_tree_nodes: List[int] = []
         self.last_accepted: List[int] = []
+        self.last_trees: List[_Tree] = []
 
     def start(self, prefix_len: Sequence[int], roots: Sequence[int], root_features: torch.Tensor):
         """prefix_len[b] tokens cached by both models, roots[b] the next token
@@ -62,14 +82,25 @@ class SpeculativeCycle:
         self.roots = [int(r) for r in roots]
         self.root_features = root_features.contiguous()
 
-    def cycle(self) -> List[List[int]]:
+    def cycle(self, uniforms=None) -> List[List[int]]:
         """One cycle; returns the tokens emitted per sequence (the accepted
-        drafts, then the target's token after them)."""
+        drafts, then the target's token after them).  uniforms: at
+        temperature > 0, the acceptance's (u_accept, u_final), each
+        [B, verifier.max_tree] in [0, 1); drawn from the cycle's generator
+        when None."""
         B, T, dm = len(self.roots), self.d.max_tree, self.d.shape.d_model
         n, tok, par, _ = self.d.tree(self.prefix, self.roots, self.root_features, self.k, self.depth, self.n_total)
         trees = [_Tree(tok[b, : n[b]].copy(), par[b, : n[b]].copy()) for b in range(B)]
-        self.v.step(self.prefix, trees)
-        acc = self.v.accept()
+        self.last_trees = trees
+        if self.temperature > 0:
+            self.v.step(self.prefix, trees, logits_out=self.logits)
+            if uniforms is None:
+                shape = (B, self.v.max_tree)
+                uniforms = (self.rng.random(shape, dtype=np.float32), self.rng.random(shape, dtype=np.float32))
+            acc = self.v.accept_sampled(self.logits, None, uniforms[0], uniforms[1], self.temperature)
+        else:
+            self.v.step(self.prefix, trees)
+            acc = self.v.accept()
         self.v.commit()
         seqs = [acc.sequence(b) for b in range(B)]
         width = max(L for L, _, _ in seqs) + 1

@@ -95,17 +95,20 @@ def _pf32(a: np.ndarray):
     return a.ctypes.data_as(POINTER(c_float))
 
 
-def _device_rows(t: torch.Tensor, rows: int, vocab: int, what: str):
-    if not (t.is_cuda and t.dtype == torch.float32 and t.is_contiguous() and t.numel() >= rows * vocab):
+def _device_rows(t: Optional[torch.Tensor], rows: int, vocab: int, what: str, optional: bool = False):
+    if t is None and optional:
+        return c_void_p(None)
+    if t is None or not (t.is_cuda and t.dtype == torch.float32 and t.is_contiguous() and t.numel() >= rows * vocab):
         raise ValueError(f"{what} must be a contiguous fp32 CUDA tensor with [B*max_tree, vocab] elements")
     return c_void_p(t.data_ptr())
 
 
-def accept_sampled_walk(trees: Sequence, logits: torch.Tensor, q_draft: torch.Tensor, u_accept, u_final,
+def accept_sampled_walk(trees: Sequence, logits: torch.Tensor, q_draft: Optional[torch.Tensor], u_accept, u_final,
                         temperature: float, max_tree: int, max_depth: int, vocab: int,
                         stream: Optional[torch.cuda.Stream] = None, noalloc: bool = False) -> AcceptResult:
     """Device stochastic acceptance (temperature > 0) on given logits and
-    draft distributions, both fp32 [B*max_tree, vocab] CUDA tensors; the
+    draft distributions, both fp32 [B*max_tree, vocab] CUDA tensors (q_draft
+    None: a deterministic draft, each child a point mass at its token); the
     uniforms are [B, max_tree] arrays in [0, 1).  noalloc: the entry point
     that uses the library's fixed device block instead of allocating."""
     n, tok, par = pack_trees(trees, max_tree)
@@ -118,7 +121,8 @@ def accept_sampled_walk(trees: Sequence, logits: torch.Tensor, q_draft: torch.Te
     name = "griffin_accept_sampled_walk_noalloc" if noalloc else "griffin_accept_sampled_walk"
     rc = getattr(N.lib, name)(
         c_void_p(s), B, max_tree, max_depth, vocab, _p32(n), _p32(tok), _p32(par),
-        _device_rows(logits, B * max_tree, vocab, "logits"), _device_rows(q_draft, B * max_tree, vocab, "q_draft"),
+        _device_rows(logits, B * max_tree, vocab, "logits"),
+        _device_rows(q_draft, B * max_tree, vocab, "q_draft", optional=True),
         _pf32(ua), _pf32(uf), float(temperature), _p32(L), _p32(out), _p32(path))
     _check(rc, name)
     return AcceptResult(L, out, path[:, :max_depth])
@@ -241,12 +245,13 @@ class TreeVerifier:
             _check(rc, "griffin_accept", self.ctx)
         return AcceptResult(L[:B], out[:B], path[:B, :D], rc)
 
-    def accept_sampled(self, logits: torch.Tensor, q_draft: torch.Tensor, u_accept, u_final,
+    def accept_sampled(self, logits: torch.Tensor, q_draft: Optional[torch.Tensor], u_accept, u_final,
                        temperature: float = 1.0, check: bool = True) -> AcceptResult:
         """Stochastic acceptance (temperature > 0) of the last step: logits is
         the logits_out tensor that step filled, q_draft the draft distributions
-        (fp32 [B*max_tree, vocab] CUDA tensor), u_accept / u_final uniforms
-        [B, max_tree] in [0, 1)."""
+        (fp32 [B*max_tree, vocab] CUDA tensor) or None for a deterministic
+        draft such as DraftModel.tree's top-k expansion, u_accept / u_final
+        uniforms [B, max_tree] in [0, 1)."""
         B, D, T = self._batch, self.max_depth, self.max_tree
         V = self.shape.vocab
         ua, uf = _f32(u_accept).reshape(B, T), _f32(u_final).reshape(B, T)
@@ -254,7 +259,8 @@ class TreeVerifier:
         out = np.zeros((max(B, 1), D + 1), dtype=np.int32)
         path = np.zeros((max(B, 1), max(D, 1)), dtype=np.int32)
         rc = N.lib.griffin_accept_sampled(self.ctx, _device_rows(logits, B * T, V, "logits"),
-                                          _device_rows(q_draft, B * T, V, "q_draft"), _pf32(ua), _pf32(uf),
+                                          _device_rows(q_draft, B * T, V, "q_draft", optional=True),
+                                          _pf32(ua), _pf32(uf),
                                           float(temperature), _p32(L), _p32(out), _p32(path))
         if rc != N.CODES["GRIFFIN_ENUMERIC"] or check:
             _check(rc, "griffin_accept_sampled", self.ctx)

@@ -223,3 +223,100 @@ def test_cycle_with_a_draft_equal_to_the_target_accepts_its_greedy_path():
         assert rate >= 2.0
     finally:
         pr.close()
+
+
+# ---- temperature > 0: the drafted tree accepted as a deterministic draft --------
+
+ACCEPT_MARGIN_T = 2e-3  # |u - a| below which the fp64 and device tests may differ (logits differ by rounding)
+DRAW_MARGIN_T = 1e-3    # distance of u * sum from a cumulative boundary, as a fraction of the sum
+DRAW_TOL_T = 2e-3
+
+
+def _oracle_tree_logits(pr, b, history, tree):
+    """fp64 target logits of the nodes of `tree`, whose root follows the
+    cached prefix and `history` (the tokens emitted before the root, starting
+    with the first root): one oracle pass over the chain with the tree hung
+    below it."""
+    m = len(history)
+    toks = [int(t) for t in history] + [int(t) for t in tree.tokens]
+    par = list(range(-1, m)) + [m + int(p) for p in tree.parents[1:]]
+    big = gen.Tree(np.asarray(toks, np.int32), np.asarray(par, np.int32))
+    return oracle.verify_tree(pr.ow, pr.kv[b].fn(), big, pr.prefixes[b]).logits[m:]
+
+
+def _run_sampled_cycles(pr, ds, roots, n_cycles, root_features, T, seed):
+    """Cycles at temperature T with seeded uniforms; every cycle's emitted
+    tokens against the oracle's walk of the same drafted tree over its own
+    fp64 logits, with the same uniforms.  A sequence stops being compared at
+    its first accept test within ACCEPT_MARGIN_T of its boundary; a draw
+    within DRAW_MARGIN_T of a boundary must be a valid draw within
+    DRAW_TOL_T, and the comparison goes on from the device's token."""
+    from paper_2502_11018_amd.cycle import SpeculativeCycle
+    B = len(roots)
+    cyc = SpeculativeCycle(pr.v, pr.d, ds.k, ds.depth, ds.n_total, temperature=T)
+    cyc.start(pr.prefixes, roots, root_features.cuda())
+    rng = np.random.default_rng(seed)
+    hist, cur, live = [[] for _ in roots], [int(r) for r in roots], [True] * B
+    compared, accepted, draws_checked = 0, 0, 0
+    for c in range(n_cycles):
+        shape = (B, pr.v.max_tree)
+        ua, uf = rng.random(shape, dtype=np.float32), rng.random(shape, dtype=np.float32)
+        say(f"{pr.m.name} T={T}: sampled cycle {c} prefix {cyc.prefix}")
+        emitted = cyc.cycle(uniforms=(ua, uf))
+        assert all(n == ds.n_total + 1 for n in cyc.last_tree_nodes)
+        for b in range(B):
+            if not live[b]:
+                continue
+            t = cyc.last_trees[b]
+            tree = gen.Tree(np.asarray(t.tokens, np.int32), np.asarray(t.parents, np.int32))
+            tr = []
+            r = oracle.accept_sampled(tree, _oracle_tree_logits(pr, b, hist[b], tree), None, ua[b, : tree.n],
+                                      uf[b, : tree.n], T, tr)
+            if any(e[0] == "accept" and abs(e[1]) <= ACCEPT_MARGIN_T for e in tr):
+                live[b] = False
+                continue
+            L = r.length
+            assert emitted[b][:-1] == r.tokens[:-1], (c, b, emitted[b], r.tokens)
+            _, margin, rr, cdf = [e for e in tr if e[0] == "draw"][0]
+            g = emitted[b][-1]
+            if margin > DRAW_MARGIN_T:
+                assert g == r.tokens[-1], (c, b, g, r.tokens[-1], margin)
+            else:
+                lo = cdf[g - 1] if g > 0 else 0.0
+                assert lo - DRAW_TOL_T <= rr <= cdf[g] + DRAW_TOL_T, (c, b, g, rr, lo, cdf[g])
+                draws_checked += 1
+            compared += 1
+            accepted += L
+            hist[b] += [cur[b]] + r.tokens[:-1]
+            cur[b] = g
+    say(f"{pr.m.name} T={T}: compared {compared} cycles ({draws_checked} boundary draws), {accepted} drafts accepted")
+    return compared, accepted
+
+
+def test_sampled_cycle_with_a_random_draft_matches_oracle():
+    ds = DRAFTS["tiny"]
+    mw = gen.make_weights(ds.target, 0)
+    pr = Pair(ds, mw, gen.make_draft_weights(ds, 3), [40, 75], synthetic_draft_kv(ds))
+    try:
+        compared, _ = _run_sampled_cycles(pr, ds, [6, 17], 8, gen.draft_root_features(ds.target.d_model, 2, 11),
+                                          1.0, 41)
+        assert compared >= 8
+    finally:
+        pr.close()
+
+
+@pytest.mark.parametrize("T", [1.0, 0.6])
+def test_sampled_cycle_with_a_draft_equal_to_the_target_accepts_paths(T):
+    """A draft equal to a one-layer target (LM head scaled so that the
+    target's distributions stay peaked at T = 1) proposes the target's likely
+    tokens, so sampled cycles accept several drafts each, and every emitted
+    token follows the oracle's walk."""
+    ds, mw, dw = self_draft(lm_scale=32.0)
+    pr = Pair(ds, mw, dw, [40], target_layer0_kv)
+    try:
+        compared, accepted = _run_sampled_cycles(pr, ds, [7], 8, gen.draft_root_features(ds.target.d_model, 1, 11),
+                                                 T, 43)
+        assert compared >= 4
+        assert accepted >= 1.5 * compared
+    finally:
+        pr.close()

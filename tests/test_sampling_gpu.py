@@ -52,10 +52,12 @@ def _pack(cases, max_tree, V):
     for b, c in enumerate(cases):
         n = c.tree.n
         lg[b * max_tree: b * max_tree + n] = c.logits
-        q[b * max_tree: b * max_tree + n] = c.q
+        if c.q is not None:
+            q[b * max_tree: b * max_tree + n] = c.q
         ua[b, :n] = c.u_accept
         uf[b, :n] = c.u_final
-    return torch.from_numpy(lg).cuda(), torch.from_numpy(q).cuda(), ua, uf
+    qd = None if all(c.q is None for c in cases) else torch.from_numpy(q).cuda()
+    return torch.from_numpy(lg).cuda(), qd, ua, uf
 
 
 def _compare(tree, logits, q, ua, uf, T, dev, b, accept_margin=ACCEPT_MARGIN, draw_margin=DRAW_MARGIN,
@@ -64,7 +66,8 @@ def _compare(tree, logits, q, ua, uf, T, dev, b, accept_margin=ACCEPT_MARGIN, dr
     result): False when an accept test on the oracle's path is within
     accept_margin of its boundary (nothing asserted)."""
     tr = []
-    r = oracle.accept_sampled(tree, np.asarray(logits, np.float64), np.asarray(q, np.float64), ua, uf, T, tr)
+    r = oracle.accept_sampled(tree, np.asarray(logits, np.float64), None if q is None else np.asarray(q, np.float64),
+                              ua, uf, T, tr)
     if any(abs(e[1]) <= accept_margin for e in tr if e[0] == "accept"):
         return False, r
     L = int(dev.length[b])
@@ -96,6 +99,64 @@ def test_sampled_walk_matches_oracle(V, T, B):
         lengths.append(r.length)
     say(f"sampled walk V={V} T={T}: compared {compared}/{B}, oracle lengths {lengths}")
     assert compared >= B - 1
+
+
+@pytest.mark.parametrize("V,T,B", [(3000, 1.0, 8), (128256, 1.0, 3), (3000, 0.7, 8), (4001, 1.0, 4)])
+def test_point_mass_walk_matches_oracle(V, T, B):
+    """Deterministic drafts (q_draft NULL): trees whose children are the
+    draft's ranked tokens, some repeated, under confident targets so that
+    paths are accepted; the odd vocabulary takes the unvectorised loads."""
+    P = _lib()
+    max_tree, D = 64, 6
+    cases = [gen.deterministic_case((10,) * 6, V, 900 + 13 * i, temperature=T) for i in range(B)]
+    lg, q, ua, uf = _pack(cases, max_tree, V)
+    assert q is None
+    say(f"point-mass walk V={V} T={T} B={B}")
+    res = P.accept_sampled_walk([c.tree for c in cases], lg, None, ua, uf, T, max_tree, D, V)
+    compared, lengths = 0, []
+    for b, c in enumerate(cases):
+        ok, r = _compare(c.tree, c.logits, None, c.u_accept, c.u_final, T, res, b)
+        compared += ok
+        lengths.append(r.length)
+    say(f"point-mass walk V={V} T={T}: compared {compared}/{B}, oracle lengths {lengths}")
+    assert compared >= B - 1
+    assert max(lengths) >= 2  # the cases do accept paths
+
+
+@pytest.mark.parametrize("rule", ["dynamic", "dup"])
+def test_point_mass_walk_is_lossless_on_gpu(rule):
+    """One deterministic tree (value-dependent branching, or a repeated
+    sibling token), accepted 20000 times on the device with fresh uniforms:
+    the emitted sequences, extended by target sampling, follow the exact
+    enumeration of tests/test_oracle_sampling.py (which equals target
+    sampling)."""
+    P = _lib()
+    D = 2
+    Ptab, Qtab = S._tables(6, D)
+    exact = S._extend(Ptab, S._exact_point(Ptab, Qtab, (), D, rule), D + 1)
+    tree, prefixes = S._det_tree(Qtab, 0, D, rule)
+    n, max_tree = 20000, 16
+    assert tree.n <= max_tree
+    lg = np.zeros((n * max_tree, S.V), np.float32)
+    rows = np.stack([np.log(Ptab[pre]) for pre in prefixes]).astype(np.float32)
+    for i in range(n):
+        lg[i * max_tree: i * max_tree + tree.n] = rows
+    rng = np.random.default_rng(31)
+    ua = rng.random((n, max_tree)).astype(np.float32)
+    uf = rng.random((n, max_tree)).astype(np.float32)
+    say(f"point-mass walk losslessness ({rule}): {n} walks of a {tree.n}-node tree")
+    res = P.accept_sampled_walk([tree] * n, torch.from_numpy(lg).cuda(), None, ua, uf, 1.0, max_tree, D, S.V)
+    counts = defaultdict(int)
+    for i in range(n):
+        L = int(res.length[i])
+        seq = tuple(int(t) for t in res.tokens[i, : L + 1])
+        while len(seq) < D + 1:
+            seq = seq + (int(rng.choice(S.V, p=Ptab[seq])),)
+        counts[seq] += 1
+    chi2 = sum((counts[s] - n * e) ** 2 / (n * e) for s, e in exact.items() if e > 0)
+    dof = sum(1 for e in exact.values() if e > 0) - 1
+    say(f"point-mass walk losslessness ({rule}): chi2 {chi2:.1f} dof {dof}")
+    assert chi2 < dof + 6 * np.sqrt(2 * dof), (chi2, dof)
 
 
 def test_sampled_walk_is_lossless_on_gpu():

@@ -316,7 +316,7 @@ class SampledCase:
     """Inputs of the stochastic (temperature > 0) acceptance for one tree."""
     tree: Tree
     logits: np.ndarray    # float32 [T, V] target logits at every node
-    q: np.ndarray         # float32 [T, V] draft distribution of each node's children
+    q: Optional[np.ndarray]  # float32 [T, V] draft distribution of each node's children (None: deterministic)
     u_accept: np.ndarray  # float32 [T] uniform for the test at each child
     u_final: np.ndarray   # float32 [T] uniform for the token drawn at each node
 
@@ -345,6 +345,40 @@ def sampled_case(widths: Sequence[int], vocab: int, seed: int, temperature: floa
             for c, t in zip(kids, draws):
                 tokens[c] = int(t)
     return SampledCase(Tree(tokens, shape.parents.copy()), logits.astype(np.float32), q.astype(np.float32),
+                       rng.random(T).astype(np.float32), rng.random(T).astype(np.float32))
+
+
+def deterministic_case(widths: Sequence[int], vocab: int, seed: int, temperature: float = 1.0,
+                       logit_std: float = 2.0, peak: Optional[float] = None, peak_rate: float = 0.8,
+                       draft_noise: float = 1.0, dup_rate: float = 0.1) -> SampledCase:
+    """A draft tree chosen without drawing, as a top-k expansion chooses it,
+    with the inputs the stochastic acceptance reads (q is None).
+
+    Target logits are i.i.d. N(0, logit_std^2), and at a share peak_rate of
+    the nodes one random token gets `peak` added (default log(vocab) + 5: a
+    confident target, so that children are accepted).  A node's children take, in order, the tokens of
+    largest logits / temperature + N(0, draft_noise^2) (a drafter correlated
+    with the target); each child after the first repeats its previous
+    sibling's token with probability dup_rate.  The shape is `random_tree`'s."""
+    shape, rng = random_tree(widths, vocab, seed)
+    T = shape.n
+    peak = math.log(vocab) + 5.0 if peak is None else peak
+    logits = rng.normal(0.0, logit_std, size=(T, vocab))
+    for u in range(T):
+        if rng.random() < peak_rate:
+            logits[u, int(rng.integers(0, vocab))] += peak
+    z = logits / temperature + rng.normal(0.0, draft_noise, size=(T, vocab))
+    tokens = np.zeros(T, dtype=np.int32)
+    tokens[0] = rng.integers(0, vocab)
+    for u in range(T):
+        kids = [c for c in range(1, T) if shape.parents[c] == u]
+        if kids:
+            order = np.argsort(-z[u], kind="stable")
+            for j, c in enumerate(kids):
+                tokens[c] = int(order[j])
+                if j > 0 and rng.random() < dup_rate:
+                    tokens[c] = tokens[kids[j - 1]]
+    return SampledCase(Tree(tokens, shape.parents.copy()), logits.astype(np.float32), None,
                        rng.random(T).astype(np.float32), rng.random(T).astype(np.float32))
 
 
