@@ -216,13 +216,17 @@ __global__ __launch_bounds__(64 * WN * KS) void gemm_kernel(GemmArgs a) {
   // Stage t: this wave's weight blocks into registers, its share of the
   // activation stage of every tile straight into LDS slot t % PF (lane l's 16
   // bytes land at the piece base + 16 l, which is the fragment order).
+  // Non-temporal weight loads where they measured faster: the LM head
+  // (189 -> 182 us) and the two-slice store form (down); the one-slice store
+  // and the SwiGLU forms measured slower with them.
+  constexpr bool NT_W = EPI == EPI_ARGMAX || (EPI == EPI_STORE && KS == 2);
   u32x4 wb[PF][NB][4];
   auto issue = [&](u32x4 (&wv)[NB][4], int slot, int t) {
     const uint16_t* wp = W + t * wstep;
 #pragma unroll
     for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int b = 0; b < NB; ++b) wv[b][j] = ld_u4(wp + b * 2048 + j * 512);
+      for (int b = 0; b < NB; ++b) wv[b][j] = NT_W ? ld_u4_nt(wp + b * 2048 + j * 512) : ld_u4(wp + b * 2048 + j * 512);
 #pragma unroll
     for (int g = 0; g < TG; ++g)
 #pragma unroll
@@ -317,6 +321,7 @@ hipError_t launch_gemm(const GemmArgs& a, int experts, hipStream_t s) {
   // one 64-row tile per workgroup
   GRIFFIN_GEMM_CASE(EPI_STORE, 1, 4, 4, 1, 1)
   GRIFFIN_GEMM_CASE(EPI_STORE, 1, 4, 2, 1, 1)
+  GRIFFIN_GEMM_CASE(EPI_STORE, 1, 4, 3, 2, 1)
   GRIFFIN_GEMM_CASE(EPI_SWIGLU, 2, 2, 3, 2, 1)
   GRIFFIN_GEMM_CASE(EPI_SWIGLU, 2, 2, 2, 2, 1)
   GRIFFIN_GEMM_CASE(EPI_SWIGLU, 2, 2, 2, 1, 1)

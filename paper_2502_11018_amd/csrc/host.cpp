@@ -127,6 +127,15 @@ GemmPlan plan_gemm(int epi, int n_out, int K, int experts = 1, int m_tiles = 1, 
       }
     }
   }
+  if (epi == EPI_STORE && experts == 1 && p.ks >= 16 * splits) {
+    // long K ranges (the down projection): two waves per column block take
+    // the two halves of each split's range and merge in LDS, eight waves per
+    // workgroup, each with three stages in flight (down 34.3 -> 30.3 us per
+    // launch with the non-temporal loads of this form; the shorter QKV and O
+    // ranges measured slower so, with one stage in flight)
+    p.kslices = 2;
+    splits *= 2;
+  }
   if (epi == EPI_SWIGLU && p.ks >= 4) {
     // one column block per wave gives too few waves to keep the matrix cores
     // of every SIMD busy with split-bf16 operands: two waves per column block
