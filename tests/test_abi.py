@@ -130,3 +130,19 @@ def test_init_and_step_reject_bad_arguments_before_any_device_work():
     assert N.lib.griffin_accept(None, None, None, None) == N.CODES["GRIFFIN_EINVAL"]
     assert N.lib.griffin_kv_cache_bytes(byref(desc)) == 2 * 1 * 4 * 192 * 64 * 2
     N.lib.griffin_verify_free(None)
+
+
+def test_sampled_cycle_rejects_bad_temperatures():
+    """SpeculativeCycle validates its temperature before touching the GPU."""
+    from paper_2502_11018_amd.cycle import SpeculativeCycle
+
+    class _Stub:
+        max_tree, max_batch = 64, 1
+
+    for bad in (-1.0, float("nan"), float("inf")):
+        with pytest.raises(ValueError):
+            SpeculativeCycle(_Stub(), _Stub(), 10, 6, 60, temperature=bad)
+    with pytest.raises(ValueError):     # the verifier cannot hold n_total + 1 nodes
+        small = _Stub()
+        small.max_tree = 16
+        SpeculativeCycle(small, _Stub(), 10, 6, 60)
