@@ -218,9 +218,10 @@ def test_scores_past_the_attention_cap_match_oracle():
     """Prefix keys after the first 32 are scaled by 2^14, so inside the first
     key split (two 32-key blocks: 1024 keys over 16 splits) the second block's
     scores exceed the first block's maximum by thousands of log2 units, far
-    past the attention kernel's 2^64 cap on unnormalised probabilities.  That
-    split is flagged and the merge recomputes it exactly; the rest of the
-    pass is unchanged.  The softmax then concentrates on a few keys, on both
+    past the 2^64 bound the attention kernel allows its unnormalised
+    probabilities (they overflow to inf there).  That split is flagged and
+    the merge recomputes it exactly, ignoring its overflowed partial; the
+    rest of the pass is unchanged.  The softmax then concentrates on a few keys, on both
     sides."""
     P = _lib()
     w = get_workload("small-gqa")
@@ -245,7 +246,7 @@ def test_scores_past_the_attention_cap_match_oracle():
         out = torch.empty((16, m.vocab), device="cuda")
         v.step([plen], [tree], out)
         acc = v.accept()
-        # the merge recomputes the capped splits from the bf16 cache: a larger, bounded error
+        # the merge recomputes the flagged splits from the bf16 cache: a larger, bounded error
         st = H.check_parity(os_, out[: tree.n].cpu().numpy(), v.predictions()[0], acc.sequence(0),
                             regress_tol=5e-3)
     say(f"scores past the attention cap: max rel err {st['max_rel']:.2e}")
