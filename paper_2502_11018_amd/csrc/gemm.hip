@@ -329,7 +329,7 @@ hipError_t launch_gemm(const GemmArgs& a, int experts, hipStream_t s) {
   GRIFFIN_GEMM_CASE(EPI_ARGMAX, 2, 4, 2, 1, 1)
   // two row tiles per workgroup sharing each weight fragment (batched rows)
   GRIFFIN_GEMM_CASE(EPI_SWIGLU, 4, 4, 3, 1, 2)
-  GRIFFIN_GEMM_CASE(EPI_STORE, 4, 4, 2, 1, 2)
+  GRIFFIN_GEMM_CASE(EPI_STORE, 2, 4, 3, 1, 2)
 #undef GRIFFIN_GEMM_CASE
   return hipErrorInvalidValue;
 }

@@ -51,10 +51,11 @@ struct GemmPlan {
 //  * gate/up: every wave holds two gate and the matching two up blocks, so
 //    each activation fragment read from LDS feeds four weight blocks (the
 //    LDS reads, not HBM, bound these launches);
-//  * wide_tiles (O and down): four 32-column blocks per wave, same reason.
+//  * wide_tiles (QKV, O and down): two 32-column blocks per wave with three
+//    pipeline stages.
 // Measured at 8 x 61 rows (Llama-3-8B shapes, per launch): gate/up 254 ->
-// 222 us, down 128 -> 115 us, O 55 -> 50 us; QKV got slower (71 -> 109 us)
-// and the LM head gained little, so they keep one tile per workgroup.
+// 222 us; with the wide form down 122 -> 113 us, O 56 -> 45 us, QKV about
+// 70 -> 60 us.  The LM head gained little and keeps one tile per workgroup.
 GemmPlan plan_gemm(int epi, int n_out, int K, int experts = 1, int m_tiles = 1, bool wide_tiles = false) {
   GemmPlan p;
   p.epi = epi;
@@ -75,10 +76,14 @@ GemmPlan plan_gemm(int epi, int n_out, int K, int experts = 1, int m_tiles = 1, 
     return p;
   }
   if (m_tiles >= 2 && experts == 1 && epi == EPI_STORE && wide_tiles) {
+    // two row tiles per workgroup, two column blocks per wave and three
+    // pipeline stages: four blocks with two stages (the register budget's
+    // other choice) wait a full memory latency at every step (long-context
+    // step 27.1 -> 26.1 ms for O and down, 25.3 ms with QKV in this form)
     p.tg = 2;
     p.kslices = 1;
-    p.pf = 2;
-    p.nb = 4;
+    p.pf = 3;
+    p.nb = 2;
     p.wn = 4;
     p.rows = n_out;
     const int n_wgs = cdiv(cdiv(n_out, 32 * p.nb), p.wn);
@@ -771,7 +776,7 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
     c->attn_sp = d.max_batch > 1 ? std::min(16, 2 * c->attn_splits) : c->attn_splits;
   }
   const int max_tiles = c->Mpad / 64;
-  c->p_qkv = plan_gemm(EPI_STORE, c->qkv_n, d.d_model, 1, max_tiles);
+  c->p_qkv = plan_gemm(EPI_STORE, c->qkv_n, d.d_model, 1, max_tiles, true);
   c->p_o = plan_gemm(EPI_STORE, d.d_model, c->attn_w, 1, max_tiles, true);
   c->p_gu = plan_gemm(EPI_SWIGLU, d.d_ff, d.d_model, c->E, max_tiles);
   c->p_down = plan_gemm(EPI_STORE, d.d_model, d.d_ff, c->E, max_tiles, true);
