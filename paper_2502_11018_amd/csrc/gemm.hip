@@ -154,7 +154,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, f32x16 (&acc)[N
   }
 }
 
-template <int EPI, int NB, int WN, int PF, int KS, bool XLO, int TG>
+template <int EPI, int NB, int WN, int PF, int KS, bool XLO, int TG, bool NT_W>
 __global__ __launch_bounds__(64 * WN * KS) void gemm_kernel(GemmArgs a) {
   // per step: {hi, lo} (XLO) or {hi} x {rows 0-31, 32-63} x 4 pieces of 1 KB,
   // for each of the TG 64-row tiles of the workgroup
@@ -216,17 +216,21 @@ __global__ __launch_bounds__(64 * WN * KS) void gemm_kernel(GemmArgs a) {
   // Stage t: this wave's weight blocks into registers, its share of the
   // activation stage of every tile straight into LDS slot t % PF (lane l's 16
   // bytes land at the piece base + 16 l, which is the fragment order).
-  // Non-temporal weight loads where they measured faster: the LM head
-  // (189 -> 182 us) and the two-slice store form (down); the one-slice store
-  // and the SwiGLU forms measured slower with them.
-  constexpr bool NT_W = EPI == EPI_ARGMAX || (EPI == EPI_STORE && KS == 2);
+  // NT_W: non-temporal weight loads (see launch_gemm for where they are used)
   u32x4 wb[PF][NB][4];
   auto issue = [&](u32x4 (&wv)[NB][4], int slot, int t) {
     const uint16_t* wp = W + t * wstep;
+    if constexpr (NT_W) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+      for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int b = 0; b < NB; ++b) wv[b][j] = NT_W ? ld_u4_nt(wp + b * 2048 + j * 512) : ld_u4(wp + b * 2048 + j * 512);
+        for (int b = 0; b < NB; ++b) wv[b][j] = ld_u4_nt(wp + b * 2048 + j * 512);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int b = 0; b < NB; ++b) wv[b][j] = ld_u4(wp + b * 2048 + j * 512);
+    }
 #pragma unroll
     for (int g = 0; g < TG; ++g)
 #pragma unroll
@@ -301,12 +305,12 @@ __global__ __launch_bounds__(64 * WN * KS) void gemm_kernel(GemmArgs a) {
   stamp_end(a.stamp);
 }
 
-template <int EPI, int NB, int WN, int PF, int KS, bool XLO, int TG>
+template <int EPI, int NB, int WN, int PF, int KS, bool XLO, int TG, bool NT_W>
 static hipError_t launch_one(const GemmArgs& a, int experts, hipStream_t s) {
   const int groups = (a.m_tiles + TG - 1) / TG;
   const int gx = groups > 1 ? (a.n_wgs + 7) / 8 * 8 * groups : a.n_wgs;
   dim3 grid(gx, experts, a.splits / KS);
-  hipLaunchKernelGGL((gemm_kernel<EPI, NB, WN, PF, KS, XLO, TG>), grid, dim3(64 * WN * KS), 0, s, a);
+  hipLaunchKernelGGL((gemm_kernel<EPI, NB, WN, PF, KS, XLO, TG, NT_W>), grid, dim3(64 * WN * KS), 0, s, a);
   return hipGetLastError();
 }
 
@@ -314,10 +318,21 @@ hipError_t launch_gemm(const GemmArgs& a, int experts, hipStream_t s) {
   const int epi = a.epi, nb = a.nb, wn = a.wn, pf = a.pf, ks = a.kslices;
   if (ks < 1 || a.splits % ks != 0) return hipErrorInvalidValue;
   const int tg = a.tg < 1 ? 1 : a.tg;
+  // Non-temporal weight loads where they measured faster: the two-slice store
+  // form (down) and the LM head over one row tile (a.nt; 189 -> 182 us, while
+  // over eight tiles, whose re-reads L2 serves, they took it 891 -> 1217 us).
+  // The one-slice store and the SwiGLU forms measured slower with them.
 #define GRIFFIN_GEMM_CASE(E, B, N_, P, K_, T_)                                                         \
-  if (epi == (E) && nb == (B) && wn == (N_) && pf == (P) && ks == (K_) && tg == (T_))                 \
-    return a.xlo ? launch_one<E, B, N_, P, K_, true, T_>(a, experts, s)                               \
-                 : launch_one<E, B, N_, P, K_, false, T_>(a, experts, s);
+  if (epi == (E) && nb == (B) && wn == (N_) && pf == (P) && ks == (K_) && tg == (T_)) {               \
+    constexpr bool nts = (E) == EPI_STORE && (K_) == 2;                                               \
+    if constexpr ((E) == EPI_ARGMAX) {                                                                \
+      if (a.nt)                                                                                       \
+        return a.xlo ? launch_one<E, B, N_, P, K_, true, T_, true>(a, experts, s)                     \
+                     : launch_one<E, B, N_, P, K_, false, T_, true>(a, experts, s);                   \
+    }                                                                                                 \
+    return a.xlo ? launch_one<E, B, N_, P, K_, true, T_, nts>(a, experts, s)                          \
+                 : launch_one<E, B, N_, P, K_, false, T_, nts>(a, experts, s);                        \
+  }
   // one 64-row tile per workgroup
   GRIFFIN_GEMM_CASE(EPI_STORE, 1, 4, 4, 1, 1)
   GRIFFIN_GEMM_CASE(EPI_STORE, 1, 4, 2, 1, 1)

@@ -67,6 +67,7 @@ struct GemmArgs {
   const uint16_t* X;         // packed activations
   int x_ks;                  // K steps per activation tile
   int xlo;                   // 1: activations as bf16 hi + lo (fp32-grade); 0: the bf16 hi part alone
+  int nt;                    // LM head: 1 = non-temporal weight loads (one row tile: each weight read once)
   int x_etiles;              // MoE: activation tiles per expert (0 for dense)
   const int32_t* count;      // MoE: [E] valid rows per expert; NULL = m_tiles * 64
   const uint16_t* W;         // packed weights (+ e * w_estride)

@@ -299,6 +299,9 @@ GemmArgs gemm_args(const GemmPlan& p, const uint16_t* X, int x_ks, const uint16_
   a.len = p.shape.len;
   a.N = p.n_out;
   a.m_tiles = m_tiles;
+  // each weight read once (one row tile): stream the LM head past the caches;
+  // with several tiles their re-reads of a fragment are served by L2
+  a.nt = p.epi == EPI_ARGMAX && m_tiles == 1 ? 1 : 0;
   a.X = X;
   a.x_ks = x_ks;
   a.xlo = xlo ? 1 : 0;
