@@ -159,13 +159,13 @@ __global__ __launch_bounds__(64 * NW, LEAN ? 2 : 1) void tree_attention_kernel(A
   // domain), the maximum of its scores in the split's first block, so the
   // output accumulators are never rescaled inside the block loop (a rescale
   // there would make the compiler shuttle them between register files every
-  // block).  Later scores may exceed m_ref, and m_true tracks the real
-  // maximum.  A row whose scores rise more than kExpCap (log2 domain) above
-  // its reference within one split is flagged, and the merge recomputes that
-  // split exactly, so p = 2^(s - m_ref) needs no clamp: only flagged rows can
-  // overflow, and a NaN score stays NaN (a clamp cost 0.8 us per launch).
-  constexpr float kExpCap = 64.f;
-  float m_ref = -INFINITY, m_true = -INFINITY, l_run = 0.f;
+  // block), and later blocks compute no maximum at all.  Later scores may
+  // exceed m_ref: a row whose sum of p = 2^(s - m_ref) passes 2^64 (which
+  // every row with a key more than 64 above its reference does) is flagged,
+  // and the merge recomputes that split exactly.  So p needs no clamp: only
+  // flagged rows can overflow, and a NaN score stays NaN (a clamp cost 0.8 us
+  // per launch, the running maximum 10 us at 16384 keys per sequence).
+  float m_ref = -INFINITY, l_run = 0.f;
   f32x16 oacc[DB];
 
   // QK: S^T = K Q^T for the block in `slot` (rows: keys, cols: queries),
@@ -208,12 +208,12 @@ __global__ __launch_bounds__(64 * NW, LEAN ? 2 : 1) void tree_attention_kernel(A
       s[r] = sacc[r];
       if constexpr (TAIL) s[r] = (key0 + 16 * hh + r < P) ? s[r] : -INFINITY;
     }
-    float mx = fmaxf(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])), fmaxf(fmaxf(s[4], s[5]), fmaxf(s[6], s[7])));
-    mx = fmaxf(mx, fmaxf(fmaxf(fmaxf(s[8], s[9]), fmaxf(s[10], s[11])),
-                         fmaxf(fmaxf(s[12], s[13]), fmaxf(s[14], s[15]))));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * a.scale_log2;
-    m_ref = first ? mx : m_ref;
-    m_true = fmaxf(m_true, mx);
+    if (first) {  // wave-uniform
+      float mx = fmaxf(fmaxf(fmaxf(s[0], s[1]), fmaxf(s[2], s[3])), fmaxf(fmaxf(s[4], s[5]), fmaxf(s[6], s[7])));
+      mx = fmaxf(mx, fmaxf(fmaxf(fmaxf(s[8], s[9]), fmaxf(s[10], s[11])),
+                           fmaxf(fmaxf(s[12], s[13]), fmaxf(s[14], s[15]))));
+      m_ref = fmaxf(mx, __shfl_xor(mx, 32, 64)) * a.scale_log2;
+    }
     float p[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) p[r] = __builtin_amdgcn_exp2f(fmaf(s[r], a.scale_log2, -m_ref));
@@ -341,9 +341,9 @@ __global__ __launch_bounds__(64 * NW, LEAN ? 2 : 1) void tree_attention_kernel(A
     }
     wait_vmcnt_lds<0>();
   }
-  // a row whose scores went past the cap marks its partial invalid (l < 0);
-  // the merge recomputes that split exactly
-  if (m_true > m_ref + kExpCap) l_run = -1.f;
+  // a row whose probabilities went past the cap marks its partial invalid
+  // (l < 0); the merge recomputes that split exactly
+  if (l_run > 0x1p64f) l_run = -1.f;
 
   // ---- partials, row-major [32 rows][DH].  The accumulators hold O^T (lane:
   // query col, dims 32 d + 8 (r/4) + 4 hh + r%4), so each wave transposes its
@@ -478,8 +478,8 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
     const float q1 = bf16_to_f32(qh.x >> 16) + bf16_to_f32(ql.x >> 16);
     const float q2 = bf16_to_f32(qh.y & 0xffff) + bf16_to_f32(ql.y & 0xffff);
     const float q3 = bf16_to_f32(qh.y >> 16) + bf16_to_f32(ql.y >> 16);
-    // splits flagged by the attention kernel (scores more than 2^64 above its
-    // reference, where p may have overflowed): recompute
+    // splits flagged by the attention kernel (their p = 2^(s - m_ref) summed
+    // past 2^64, where p may have overflowed): recompute
     // (m, l, o) over the split's prefix keys in fp32 from the bf16 cache, with
     // an exact running maximum
     {
