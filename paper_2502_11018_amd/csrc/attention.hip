@@ -434,12 +434,15 @@ hipError_t launch_attention(const AttnArgs& a, int batch, hipStream_t s) {
 // (sum_s 2^(m_s - M) l_s + 2^(m_t - M) l_t).  Absent rows get zeros.  One
 // workgroup per row, one thread per (head, 4 dims); the dot products of a
 // tree key reduce over the head's dh/4 threads with xor shuffles (a fixed
-// order).  The merged rows are written fragment-packed split bf16 (o_ks K
+// order).  It reads the first MAXS of the sp partial slots of each (sequence,
+// head): the step's largest split count rounded up, so that a batch whose
+// sequences all hold the even share does not read the slots kept for
+// uneven ones.  The merged rows are written fragment-packed split bf16 (o_ks K
 // steps per tile) as the activation operand of the output projection.
 template <int MAXS, bool RAGGED>
 __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restrict__ part_o,
                                                            const float* __restrict__ part_ml, StepMeta meta,
-                                                           int Hq, int Hkv, int dh, int qrows, int max_tree,
+                                                           int Hq, int Hkv, int dh, int sp, int qrows, int max_tree,
                                                            const uint16_t* __restrict__ q,
                                                            const uint16_t* __restrict__ q_lo, TreeKV32 tree,
                                                            PrefixKV prefix, float scale_log2,
@@ -459,7 +462,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
   uint64_t anc = meta.anc[r];
   // the sequence's key splits fill the first of the MAXS slots; the
   // attention kernel marks the rest empty (m = -inf, l = 0)
-  const long long base = ((long long)b * Hq + h) * MAXS;
+  const long long base = ((long long)b * Hq + h) * sp;
   float ms[MAXS], ls[MAXS];
   float4 os[MAXS];
 #pragma unroll
@@ -584,22 +587,22 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
 }
 
 hipError_t launch_attn_combine(const float* part_o, const float* part_ml, StepMeta meta, int Hq, int Hkv, int dh,
-                               int splits, int qrows, int max_tree, int batch, const uint16_t* q,
+                               int slots, int sp, int qrows, int max_tree, int batch, const uint16_t* q,
                                const uint16_t* q_lo, TreeKV32 tree, PrefixKV prefix, float scale_log2,
                                uint16_t* o_out, int o_ks, hipStream_t s) {
   const int quads = dh / 4;
-  if (256 % quads != 0) return hipErrorInvalidValue;
+  if (256 % quads != 0 || slots < 1 || slots > sp) return hipErrorInvalidValue;
   const int items = Hq * quads;
   const dim3 grid(batch * max_tree, (items + 255) / 256);
-  switch (splits) {
+  switch (slots) {
 #define GRIFFIN_COMB_CASE(n)                                                                                   \
   case n:                                                                                                     \
     if (meta.split_tab)                                                                                       \
       hipLaunchKernelGGL((attn_combine_kernel<n, true>), grid, dim3(256), 0, s, part_o, part_ml, meta, Hq, Hkv,   \
-                         dh, qrows, max_tree, q, q_lo, tree, prefix, scale_log2, o_out, o_ks);                \
+                         dh, sp, qrows, max_tree, q, q_lo, tree, prefix, scale_log2, o_out, o_ks);                \
     else                                                                                                      \
       hipLaunchKernelGGL((attn_combine_kernel<n, false>), grid, dim3(256), 0, s, part_o, part_ml, meta, Hq, Hkv,  \
-                         dh, qrows, max_tree, q, q_lo, tree, prefix, scale_log2, o_out, o_ks);                \
+                         dh, sp, qrows, max_tree, q, q_lo, tree, prefix, scale_log2, o_out, o_ks);                \
     break;
     GRIFFIN_COMB_CASE(1) GRIFFIN_COMB_CASE(2) GRIFFIN_COMB_CASE(3) GRIFFIN_COMB_CASE(4) GRIFFIN_COMB_CASE(5)
     GRIFFIN_COMB_CASE(6) GRIFFIN_COMB_CASE(7) GRIFFIN_COMB_CASE(8) GRIFFIN_COMB_CASE(9) GRIFFIN_COMB_CASE(10)

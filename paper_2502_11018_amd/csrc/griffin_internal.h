@@ -182,7 +182,7 @@ hipError_t launch_attention(const AttnArgs& a, int batch, hipStream_t s);
 constexpr int ATTN_RING = 4;  // 32-key K/V blocks in flight per attention workgroup
 int attn_waves(int group);    // waves (query heads) per attention workgroup
 hipError_t launch_attn_combine(const float* part_o, const float* part_ml, StepMeta meta, int Hq, int Hkv, int dh,
-                               int splits, int qrows, int max_tree, int batch, const uint16_t* q,
+                               int slots, int sp, int qrows, int max_tree, int batch, const uint16_t* q,
                                const uint16_t* q_lo, TreeKV32 tree, PrefixKV prefix, float scale_log2,
                                uint16_t* o_out, int o_ks, hipStream_t s);
 hipError_t launch_argmax_reduce(const float* pmax, const float* pmax2, const int32_t* pidx, const int32_t* pnan,

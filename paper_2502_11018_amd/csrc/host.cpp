@@ -166,6 +166,7 @@ struct griffin_ctx {
   hipStream_t stream = nullptr;
 
   int R = 0, Mpad = 0, qkv_n = 0, attn_w = 0, attn_splits = 1, attn_sp = 1, qblocks = 1;
+  int comb_slots = 1;  // partial slots the merge reads this step (<= attn_sp)
   int E = 1, topk = 1;
   long long parts_elems = 0;
 
@@ -216,6 +217,7 @@ struct griffin_ctx {
     float* logits;
     bool kv_only;
     int tree_k, tree_depth, tree_n;  // 0: one pass
+    int slots;                       // partial slots the merge reads
     hipGraphExec_t exec;
   };
   std::vector<GraphEntry> graphs;
@@ -410,9 +412,9 @@ int enqueue_pass(griffin_ctx* c, float* logits_out) {
       LAUNCH(GRIFFIN_KC_ATTN, launch_attention(a, B, s));
     }
     LAUNCH(GRIFFIN_KC_MERGE, launch_attn_combine(c->attn_po, c->attn_pml, c->meta, d.n_q_heads, d.n_kv_heads,
-                                                d.head_dim, c->attn_sp, c->qblocks * 32, d.max_tree, B, c->q,
-                                                c->q_lo, c->tree, PrefixKV{kc, vc, d.kv_capacity}, scale_log2, c->o,
-                                                c->p_o.ks_pad, s));
+                                                d.head_dim, c->comb_slots, c->attn_sp, c->qblocks * 32, d.max_tree,
+                                                B, c->q, c->q_lo, c->tree, PrefixKV{kc, vc, d.kv_capacity},
+                                                scale_log2, c->o, c->p_o.ks_pad, s));
     {
       GemmArgs a = gemm_args(c->p_o, c->o, c->p_o.ks_pad, c->pk_o[l], m_tiles, !c->act_bf16);
       a.out = c->parts;
@@ -532,7 +534,7 @@ int run_graph(griffin_ctx* c, const griffin_ctx::GraphEntry& key, Body body) {
   if (!c->use_graphs || c->prof_mask != 0 || c->stream == nullptr) return body();
   for (auto& g : c->graphs)
     if (g.batch == key.batch && g.logits == key.logits && g.kv_only == key.kv_only && g.tree_k == key.tree_k &&
-        g.tree_depth == key.tree_depth && g.tree_n == key.tree_n) {
+        g.tree_depth == key.tree_depth && g.tree_n == key.tree_n && g.slots == key.slots) {
       HIP_TRY(c, hipGraphLaunch(g.exec, c->stream));
       return GRIFFIN_OK;
     }
@@ -562,7 +564,7 @@ int run_graph(griffin_ctx* c, const griffin_ctx::GraphEntry& key, Body body) {
 
 // One pass (batch, logits_out, kv_only from the context).
 int run_pass(griffin_ctx* c, float* logits_out) {
-  return run_graph(c, {c->batch, logits_out, c->kv_only, 0, 0, 0, nullptr},
+  return run_graph(c, {c->batch, logits_out, c->kv_only, 0, 0, 0, c->comb_slots, nullptr},
                    [&]() { return enqueue_pass(c, logits_out); });
 }
 
@@ -778,6 +780,7 @@ int griffin_verify_init(const griffin_model_desc* desc, const griffin_weights* w
     // single-sequence context gives its sequence all attn_splits, no table.
     c->attn_sp = d.max_batch > 1 ? std::min(16, 2 * c->attn_splits) : c->attn_splits;
   }
+  c->comb_slots = c->attn_sp;
   const int max_tiles = c->Mpad / 64;
   c->p_qkv = plan_gemm(EPI_STORE, c->qkv_n, d.d_model, 1, max_tiles, true);
   c->p_o = plan_gemm(EPI_STORE, d.d_model, c->attn_w, 1, max_tiles, true);
@@ -998,6 +1001,8 @@ int griffin_verify_step(griffin_ctx* c, int32_t batch, const int32_t* prefix_len
   }
   attn_split_plan(batch, prefix_len, n_nodes, c->attn_splits, c->attn_sp,
                   reinterpret_cast<int32_t*>(h + c->off_split), reinterpret_cast<int32_t*>(h + c->off_nsplit));
+  c->comb_slots = c->meta.split_tab ? merge_slots(reinterpret_cast<const int32_t*>(h + c->off_nsplit), batch, c->attn_sp)
+                                    : c->attn_sp;
   HIP_TRY(c, hipMemcpyAsync(c->meta_dev, h, c->meta_bytes, hipMemcpyHostToDevice, c->stream));
   HIP_TRY(c, hipEventRecord(c->meta_ev[k], c->stream));
   c->meta_cur = k;
@@ -1758,7 +1763,9 @@ int griffin_draft_tree(griffin_draft* dc, int32_t batch, const int32_t* prefix_l
   sa.o_par = sa.o_tok + MT;
   sa.o_score = reinterpret_cast<float*>(sa.o_par + MT);
   // the whole expansion, every pass with its top-k and selection, is one graph
-  TRY(run_graph(c, {batch, dc->logits, false, k, depth, n_total, nullptr}, [&]() -> int {
+  // the passes' split plans differ, so the merge reads every slot
+  c->comb_slots = c->attn_sp;
+  TRY(run_graph(c, {batch, dc->logits, false, k, depth, n_total, c->comb_slots, nullptr}, [&]() -> int {
     for (int t = 0; t < depth; ++t) {
       TRY(enqueue_pass(c, dc->logits));
       HIP_TRY(c, launch_draft_topk(dc->logits, d.vocab, d.vocab, c->meta, rows, T, k, dc->topk_tok, dc->topk_lp,

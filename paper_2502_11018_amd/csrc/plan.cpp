@@ -89,6 +89,14 @@ void attn_split_plan(int batch, const int32_t* prefix_len, const int32_t* n_node
   }
 }
 
+int merge_slots(const int32_t* nsplit, int batch, int sp) {
+  int most = 1;
+  for (int b = 0; b < batch; ++b) most = std::max(most, (int)nsplit[b]);
+  int slots = 1;
+  while (slots < most) slots *= 2;
+  return std::min(slots, sp);
+}
+
 int validate_desc(const griffin_model_desc* d, std::string* why) {
   auto bad = [&](const char* m) {
     if (why) *why = m;

@@ -25,6 +25,11 @@ int prepare_tree(int32_t n, const int32_t* tokens, const int32_t* parents, int32
 void attn_split_plan(int batch, const int32_t* prefix_len, const int32_t* n_nodes, int splits, int sp,
                      int32_t* tab, int32_t* nsplit);
 
+// Partial slots the merge reads for a plan: the largest split count of the
+// batch rounded up to a power of two (few distinct values, so few captured
+// step graphs), at most sp.
+int merge_slots(const int32_t* nsplit, int batch, int sp);
+
 // GRIFFIN_OK or GRIFFIN_ESHAPE for a model shape the kernels do not support.
 int validate_desc(const griffin_model_desc* d, std::string* why);
 

@@ -65,7 +65,7 @@ int main() {
       attn_split_plan(batch, prefix.data(), nodes.data(), splits, sp, tab.data(), nsplit.data());
       put(tab);
       put(nsplit);
-      std::cout << '\n';
+      std::cout << ' ' << merge_slots(nsplit.data(), batch, sp) << '\n';
     } else if (op == 'D') {
       griffin_model_desc d{};
       in >> d.n_layers >> d.d_model >> d.n_q_heads >> d.n_kv_heads >> d.head_dim >> d.d_ff >> d.vocab >>

@@ -118,8 +118,11 @@ def test_split_plan_invariants(driver):
     for (batch, splits, sp, prefix, nodes), res in zip(cases, out):
         v = [int(x) for x in res.split()]
         tab = np.array(v[: 4 * batch * splits]).reshape(-1, 4)
-        nsplit = v[4 * batch * splits:]
+        nsplit, slots = v[4 * batch * splits:-1], v[-1]
         assert len(nsplit) == batch and sum(nsplit) <= batch * splits
+        # the merge reads the first `slots` partial slots: every split, within the allocation
+        assert max(nsplit) <= slots <= sp
+        assert slots == sp or (slots & (slots - 1)) == 0 and slots < 2 * max(nsplit)
         j = 0
         for b in range(batch):
             cap = max(1, min(sp, ((prefix[b] + 31) // 32) // 2))
