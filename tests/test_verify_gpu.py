@@ -341,7 +341,11 @@ def test_gpu_prefill_by_chain_steps_matches_oracle_prefill():
 def test_graph_replay_matches_plain_launches():
     """Steps replayed from captured HIP graphs give the same bits as plain
     launches, on every replay, with plain steps and synchronisations between
-    the replays and two graph keys (batch sizes) in use."""
+    the replays and several graph keys in use: two batch sizes, and prefix
+    lengths that change the key-split plan (one full prefix beside a short
+    one: the same merge slot count as equal prefixes, with another split
+    table) or the merge's slot count itself (all prefixes short: one split
+    each, one slot instead of four), so a new graph."""
     name = "small-gqa"
     # a stream of its own: the library captures and replays graphs only on a
     # non-default stream
@@ -352,17 +356,31 @@ def test_graph_replay_matches_plain_launches():
         trees = [[c.tree for c in s.cases[i]] for i in range(3)]
         out = torch.empty((B * s.max_tree, m.vocab), device=s.dev)
 
-        def step(ts):
+        other = {"uneven": [s.w.prefix_len] + [40] * (B - 1), "short": [40] * B}
+        # a step writes its tree's K/V at slots prefix + i: a short step
+        # overwrites prefix slots that the full-prefix steps read, so the
+        # cache is restored after it
+        torch.cuda.synchronize()
+        kc0, vc0 = s.v.k_cache.clone(), s.v.v_cache.clone()
+
+        def step(ts, prefixes=None):
             out.fill_(float("nan"))
-            s.v.step([s.w.prefix_len] * len(ts), ts, out)
+            s.v.step(prefixes or [s.w.prefix_len] * len(ts), ts, out)
             acc = s.v.accept(check=False)
-            return out[: len(ts) * s.max_tree].cpu().numpy().copy(), s.v.predictions(), \
+            res = out[: len(ts) * s.max_tree].cpu().numpy().copy(), s.v.predictions(), \
                 [acc.sequence(b) for b in range(len(ts))]
+            if prefixes is not None:
+                torch.cuda.synchronize()
+                s.v.k_cache.copy_(kc0)
+                s.v.v_cache.copy_(vc0)
+                torch.cuda.synchronize()
+            return res
 
         say(f"{name}: plain launches")
         s.v.set_graphs(False)
         ref = [step(t) for t in trees]
         ref1 = step(trees[0][:1])
+        ref_o = {k: step(trees[0], pl) for k, pl in other.items()}
         s.v.set_graphs(True)
         for rep in range(3):
             for i, t in enumerate(trees):
@@ -370,6 +388,11 @@ def test_graph_replay_matches_plain_launches():
                 lg, pred, acc = step(t)
                 assert np.array_equal(lg.view(np.uint32), ref[i][0].view(np.uint32))
                 assert np.array_equal(pred, ref[i][1]) and acc == ref[i][2]
+                if i == 0:  # the other prefix patterns between the equal ones
+                    for k, pl in other.items():
+                        lg, pred, acc = step(t, pl)
+                        assert np.array_equal(lg.view(np.uint32), ref_o[k][0].view(np.uint32)), k
+                        assert np.array_equal(pred, ref_o[k][1]) and acc == ref_o[k][2], k
             lg1, pred1, acc1 = step(trees[0][:1])  # batch 1: a second graph
             assert np.array_equal(lg1.view(np.uint32), ref1[0].view(np.uint32)) and acc1 == ref1[2]
             s.v.set_graphs(False)            # plain step between replays
