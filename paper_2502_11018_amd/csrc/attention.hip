@@ -460,8 +460,9 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(const float* __restri
   const int P = meta.prefix_len[b];
   const int ns = RAGGED ? meta.n_split[b] : MAXS;
   uint64_t anc = meta.anc[r];
-  // the sequence's key splits fill the first of the MAXS slots; the
-  // attention kernel marks the rest empty (m = -inf, l = 0)
+  // the sequence's key splits fill the first of its sp slots and the
+  // attention kernel marks the rest empty (m = -inf, l = 0), so the first
+  // MAXS (at least the step's largest split count) hold every split
   const long long base = ((long long)b * Hq + h) * sp;
   float ms[MAXS], ls[MAXS];
   float4 os[MAXS];
