@@ -67,8 +67,13 @@ __global__ __launch_bounds__(64 * NW, LEAN ? 2 : 1) void tree_attention_kernel(A
   const int per_unit = chunks * a.qblocks;
   const int id = blockIdx.x;
   const int rest = id >> 3;
-  const int u = (rest / per_unit) * 8 + (id & 7);
-  if (u >= a.units * a.Hkv) return;  // uniform over the workgroup
+  const int u_raw = (rest / per_unit) * 8 + (id & 7);
+  // a workgroup past the last unit (the grid is rounded up) runs the
+  // prologue's loads for unit 0 and leaves with the workgroups without live
+  // rows: no branch before the loads, so the kernel arguments are fetched at
+  // once
+  const bool unit_live = u_raw < a.units * a.Hkv;  // uniform over the workgroup
+  const int u = unit_live ? u_raw : 0;
   const int within = rest % per_unit;
   const int qb = within % a.qblocks;
   const int chunk = within / a.qblocks;
@@ -150,7 +155,7 @@ __global__ __launch_bounds__(64 * NW, LEAN ? 2 : 1) void tree_attention_kernel(A
 #pragma unroll
     for (int i = 0; i < D - 1; ++i) issue(i, kb0 + min(i, nb - 1));
   }
-  if (qb * 32 >= n_nodes) {  // no live query rows in this block (uniform)
+  if (!unit_live || qb * 32 >= n_nodes) {  // no unit, or no live query rows in this block (uniform)
     wait_vmcnt_lds<0>();
     return;
   }
